@@ -1,0 +1,230 @@
+"""CPU oracle for the DenseNet conv5 descriptor-pyramid path (arXiv 1404.1869).
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The GPU library never imports, links or
+calls it, and it never imports the GPU library.
+
+The arithmetic lives in ``oracle.cpp`` (plain C++17 + OpenMP, fp64); this module only marshals numpy
+arrays through ctypes.  Array conventions are the natural ones of the paper's description: images and
+planes are channel-major ``[C][H][W]``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.cpp into liboracle.so with g++ (no HIP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fopenmp", "-ffp-contract=off", "-fPIC",
+                               "-shared", _SRC, "-o", tmp])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, f64 = ctypes.c_int, ctypes.c_double
+        L.oracle_plan.argtypes = [i32, i32, i32, i32, f64, i32, i32, i32, i32, P, P]
+        L.oracle_plan.restype = i32
+        L.oracle_resize_center.argtypes = [P, i32, i32, i32, i32, P, P]
+        L.oracle_resize_center.restype = None
+        L.oracle_build_planes.argtypes = [P, i32, i32, i32, P, P, i32, i32, P, i32, i32, i32, P]
+        L.oracle_build_planes.restype = None
+        L.oracle_conv2d.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, i32, i32, i32, P]
+        L.oracle_conv2d.restype = i32
+        L.oracle_lrn.argtypes = [P, i32, i32, i32, i32, f64, f64, f64, P]
+        L.oracle_lrn.restype = i32
+        L.oracle_maxpool.argtypes = [P, i32, i32, i32, i32, i32, P]
+        L.oracle_maxpool.restype = i32
+        L.oracle_net.argtypes = [P, i32, i32, P, P, f64, f64, f64, i32, i32, P, P]
+        L.oracle_net.restype = i32
+        L.oracle_region_windows.argtypes = [P, P, P, P, i32, i32, P, P, i32, P, P, i32, f64, i32,
+                                            P, P, P, P]
+        L.oracle_region_windows.restype = i32
+        for name in ("oracle_conv5_side", "oracle_pool_side"):
+            getattr(L, name).argtypes = [i32]
+            getattr(L, name).restype = i32
+        L.oracle_conv_side.argtypes = [i32, i32, i32, i32]
+        L.oracle_conv_side.restype = i32
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ----------------------------------------------------------------------------------------------
+# Geometry
+# ----------------------------------------------------------------------------------------------
+GI_FIELDS = ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0", "r1", "c0", "c1", "plane_h",
+             "plane_w")
+
+
+@dataclass
+class Plan:
+    gi: np.ndarray          # [K][16] int32, fields GI_FIELDS
+    gd: np.ndarray          # [K][3] float64: s, sy, sx
+    n_planes: int
+    pad: int
+    plane_sizes: list       # [(PH, PW)] per plane
+
+    def field(self, name):
+        return self.gi[:, GI_FIELDS.index(name)]
+
+
+def plan(H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, plane_w=0) -> Plan:
+    """Scales, sizes, rectangles, stitching and conv5 windows (Sec. 3.1)."""
+    gi = np.zeros((K, 16), np.int32)
+    gd = np.zeros((K, 3), np.float64)
+    n = lib().oracle_plan(H, W, K, spo, float(base_scale), base_longest_side, pad, plane_h, plane_w,
+                          _p(gi), _p(gd))
+    if n < 0:
+        raise ValueError(f"oracle_plan failed with {n}")
+    sizes = [None] * n
+    for k in range(K):
+        sizes[gi[k, 3]] = (int(gi[k, 12]), int(gi[k, 13]))
+    return Plan(gi, gd, n, pad, sizes)
+
+
+def conv5_side(n: int) -> int:
+    return lib().oracle_conv5_side(n)
+
+
+def pool_side(n: int) -> int:
+    return lib().oracle_pool_side(n)
+
+
+def conv_side(n: int, R: int, s: int, p: int) -> int:
+    return lib().oracle_conv_side(n, R, s, p)
+
+
+# ----------------------------------------------------------------------------------------------
+# Pyramid
+# ----------------------------------------------------------------------------------------------
+def resize_center(img: np.ndarray, h: int, w: int, mean) -> np.ndarray:
+    """Bilinear half-pixel resize of a uint8 [3][H][W] image to h x w, minus the mean pixel (fp64)."""
+    img = np.ascontiguousarray(img, np.uint8)
+    _, H, W = img.shape
+    m = np.ascontiguousarray(mean, np.float64)
+    out = np.zeros((3, h, w), np.float64)
+    lib().oracle_resize_center(_p(img), H, W, h, w, _p(m), _p(out))
+    return out
+
+
+def build_planes(img: np.ndarray, pl: Plan, pad_mode: int, mean) -> list:
+    """Stitched, centred, padded planes of one image, as a list of fp64 [3][PH][PW] arrays."""
+    img = np.ascontiguousarray(img, np.uint8)
+    _, H, W = img.shape
+    PHm = max(s[0] for s in pl.plane_sizes)
+    PWm = max(s[1] for s in pl.plane_sizes)
+    m = np.ascontiguousarray(mean, np.float64)
+    buf = np.zeros((pl.n_planes, 3, PHm, PWm), np.float64)
+    lib().oracle_build_planes(_p(img), H, W, pl.gi.shape[0], _p(pl.gi), _p(pl.gd), pl.pad, pad_mode,
+                              _p(m), pl.n_planes, PHm, PWm, _p(buf))
+    return [np.ascontiguousarray(buf[i, :, :ph, :pw]) for i, (ph, pw) in enumerate(pl.plane_sizes)]
+
+
+# ----------------------------------------------------------------------------------------------
+# Layers
+# ----------------------------------------------------------------------------------------------
+def conv2d(x: np.ndarray, w: np.ndarray, b: np.ndarray, stride=1, pad=0, groups=1, relu=True):
+    x = np.ascontiguousarray(x, np.float32)
+    w = np.ascontiguousarray(w, np.float32)
+    b = np.ascontiguousarray(b, np.float32)
+    C, Hi, Wi = x.shape
+    M, _, R, _ = w.shape
+    Ho, Wo = conv_side(Hi, R, stride, pad), conv_side(Wi, R, stride, pad)
+    out = np.zeros((M, Ho, Wo), np.float32)
+    rc = lib().oracle_conv2d(_p(x), C, Hi, Wi, _p(w), _p(b), M, R, stride, pad, groups, int(relu),
+                             _p(out))
+    if rc:
+        raise ValueError("oracle_conv2d: bad arguments")
+    return out
+
+
+def lrn(x: np.ndarray, n=5, alpha=1e-4, beta=0.75, k=1.0):
+    x = np.ascontiguousarray(x, np.float32)
+    C, H, W = x.shape
+    out = np.zeros_like(x)
+    if lib().oracle_lrn(_p(x), C, H, W, n, alpha, beta, k, _p(out)):
+        raise ValueError("oracle_lrn: bad arguments")
+    return out
+
+
+def maxpool(x: np.ndarray, R=3, s=2):
+    x = np.ascontiguousarray(x, np.float32)
+    C, H, W = x.shape
+    Ho, Wo = pool_side(H) if (R, s) == (3, 2) else None, pool_side(W) if (R, s) == (3, 2) else None
+    if Ho is None:
+        raise ValueError("only 3x3/2 pooling has a size helper")
+    out = np.zeros((C, Ho, Wo), np.float32)
+    if lib().oracle_maxpool(_p(x), C, H, W, R, s, _p(out)):
+        raise ValueError("oracle_maxpool: bad arguments")
+    return out
+
+
+def net(plane: np.ndarray, weights, lrn_params=(1e-4, 0.75, 1.0, 5), lrn_before_pool=True,
+        pool5=False):
+    """conv1..conv5 (+pool5) on one [3][PH][PW] plane.  weights = [(w1,b1),...,(w5,b5)] fp32."""
+    plane = np.ascontiguousarray(plane, np.float32)
+    _, PH, PW = plane.shape
+    Hc, Wc = conv5_side(PH), conv5_side(PW)
+    if Hc <= 0 or Wc <= 0:
+        raise ValueError("plane too small for the network")
+    ws = [np.ascontiguousarray(w, np.float32) for w, _ in weights]
+    bs = [np.ascontiguousarray(b, np.float32) for _, b in weights]
+    wp = (ctypes.c_void_p * 5)(*[w.ctypes.data for w in ws])
+    bp = (ctypes.c_void_p * 5)(*[b.ctypes.data for b in bs])
+    c5 = np.zeros((256, Hc, Wc), np.float32)
+    p5 = np.zeros((256, pool_side(Hc), pool_side(Wc)), np.float32) if pool5 else None
+    a, be, k, n = lrn_params
+    rc = lib().oracle_net(_p(plane), PH, PW, wp, bp, a, be, k, n, int(lrn_before_pool), _p(c5),
+                          _p(p5) if pool5 else None)
+    if rc:
+        raise ValueError("oracle_net failed")
+    return (c5, p5) if pool5 else c5
+
+
+# ----------------------------------------------------------------------------------------------
+# Region windows
+# ----------------------------------------------------------------------------------------------
+def region_windows(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None, T=227.0, S=6):
+    """conv5_planes: list over (image, plane) of fp32 [256][Hc][Wc]; returns desc, scale, idx, lam."""
+    flat = np.concatenate([np.ascontiguousarray(c, np.float32).ravel() for c in conv5_planes])
+    offs = np.cumsum([0] + [c.size for c in conv5_planes[:-1]]).astype(np.int64)
+    Hcs = np.array([c.shape[1] for c in conv5_planes], np.int32)
+    Wcs = np.array([c.shape[2] for c in conv5_planes], np.int32)
+    boxes = np.ascontiguousarray(boxes, np.float32)
+    n = boxes.shape[0]
+    bi = None if box_img is None else np.ascontiguousarray(box_img, np.int32)
+    desc = np.zeros((n, 256 * S * S), np.float32)
+    scale = np.zeros(n, np.int32)
+    idx = np.zeros((n, S, S, 2), np.int32)
+    lam = np.zeros((n, S, S, 2), np.float64)
+    rc = lib().oracle_region_windows(_p(flat), _p(offs), _p(Hcs), _p(Wcs), pl.n_planes,
+                                     pl.gi.shape[0], _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
+                                     _p(bi) if bi is not None else None, n, float(T), S, _p(desc),
+                                     _p(scale), _p(idx), _p(lam))
+    if rc:
+        raise ValueError("oracle_region_windows: bad arguments")
+    return desc, scale, idx, lam
