@@ -1,0 +1,188 @@
+/* densenet.h — C ABI of the DenseNet conv5 descriptor-pyramid library for one MI355X (gfx950).
+ *
+ * Method: Iandola et al., "DenseNet: Implementing Efficient ConvNet Descriptor Pyramids",
+ * arXiv 1404.1869.  An image is resampled to a multiscale pyramid (Sec. 3.1), centred on one mean
+ * pixel (Sec. 3.2), each scale is padded by a 16-px border and the scales are stitched onto large
+ * planes (Sec. 3.1, Bottom-Left Fill); conv1..conv5 of the AlexNet topology then run on every plane,
+ * and the conv5 maps are unpacked per scale (Sec. 3.1) and read out as fixed-size region windows
+ * ("crop after", Sec. 4).  The paper's own interface is pyra = convnet_featpyramid(image) (Sec. 3.5):
+ * image in, per-scale feature maps plus the scale-to-plane geometry out.
+ *
+ * Conventions for every entry point:
+ *  - Return value: a dn_status.  Arguments are validated on the host before any device work; no
+ *    C++ exception crosses the ABI.  densenet_last_error() returns a thread-local message for the
+ *    last failing call on this thread.
+ *  - Ownership: the caller owns every buffer.  d_* pointers are device pointers (256-byte aligned,
+ *    as returned by hipMalloc or the torch caching allocator); other pointers are host memory.
+ *    The library allocates no device memory and keeps no device state.
+ *  - Size queries: where an output or workspace pointer may be NULL, the call only writes the
+ *    required byte count to *_needed and returns DN_OK.  A buffer that is too small returns
+ *    DN_E_BUFFER_TOO_SMALL (the needed size is still written).
+ *  - Streams: `stream` is a hipStream_t passed as void* (NULL = the default stream).  Device work is
+ *    enqueued asynchronously on it; outputs are valid once the stream reaches that point.
+ *  - dtypes: DN_F32, DN_F16, DN_BF16 select the storage and MFMA input type of planes and
+ *    activations; accumulation is always fp32.  Region descriptors are always fp32.
+ *  - Layouts: images are uint8 [n_img][3][H][W].  Planes are channel-major [3][PH][PW] per plane,
+ *    packed back to back.  Activations and conv5 maps are channels-last [Hc][Wc][C] per plane, packed
+ *    back to back.
+ */
+#ifndef DENSENET_H
+#define DENSENET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DN_OK = 0,
+  DN_E_INVALID_ARG = -1,      /* null pointer, non-positive size, inconsistent parameters */
+  DN_E_TOO_LARGE = -2,        /* a padded scale does not fit the stitching plane, or a limit below */
+  DN_E_BUFFER_TOO_SMALL = -3, /* caller buffer shorter than *_needed */
+  DN_E_UNSUPPORTED = -4,      /* dtype or mode not implemented */
+  DN_E_HIP = -5,              /* a HIP runtime call or kernel launch failed */
+  DN_E_INTERNAL = -6
+} dn_status;
+
+typedef enum { DN_F32 = 0, DN_F16 = 1, DN_BF16 = 2 } dn_dtype;
+typedef enum { DN_PAD_ZERO = 0, DN_PAD_RAMP = 1 } dn_pad_mode;
+
+#define DN_MAX_SCALES 64
+#define DN_MAX_PLANES_PER_IMAGE 64
+
+/* Pyramid recipe (Sec. 3.1, 3.2).
+ *  scales: s_k = base * 2^(-k / steps_per_octave), k = 0 .. n_scales-1, where base = base_scale, or
+ *          base_longest_side / max(H, W) when base_longest_side > 0; scaled sides round half up
+ *          (minimum 1).
+ *  pad:    border width p around every scale (the paper uses 16).  pad_mode RAMP blends linearly
+ *          from the edge pixel to the mean pixel: weight (p+1-d)/(p+1) at distance d, product of the
+ *          row and column weights at corners; ZERO fills the border with the mean pixel.
+ *  plane_h, plane_w: 0,0 => every padded scale is its own plane; otherwise the scales, padded and
+ *          rounded up to multiples of 16 px, are stitched onto planes of this size by Bottom-Left
+ *          Fill (largest first; first plane, then topmost, then leftmost candidate corner).
+ *  mean:   the mean pixel subtracted from input channels 0, 1, 2 (the background of every plane
+ *          is the mean pixel, i.e. 0 after centring). */
+typedef struct {
+  int32_t n_scales;
+  int32_t steps_per_octave;
+  double base_scale;
+  int32_t base_longest_side;
+  int32_t pad;
+  int32_t pad_mode;
+  int32_t plane_h, plane_w;
+  float mean[3];
+} dn_pyramid_params;
+
+/* Geometry of scale k, identical for every image of a batch (Sec. 3.1 unpacking).
+ *  (h, w): scaled image size; sy = h/H, sx = w/W are the effective factors.
+ *  plane:  index of the scale's plane within one image's planes.
+ *  (y, x, rh, rw): padded rectangle on that plane; the real pixels start at (y+pad, x+pad).
+ *  [r0, r1] x [c0, c1]: conv5 cells of that plane whose receptive-field centre (16 i + 17.5 in
+ *          continuous plane coordinates) lies on a real pixel of the scale; the scale's feature map
+ *          is that window of the plane's conv5 map.  Empty when r1 < r0 or c1 < c0. */
+typedef struct {
+  int32_t k, h, w, plane;
+  int32_t y, x, rh, rw;
+  int32_t r0, r1, c0, c1;
+  double s, sy, sx;
+} dn_scale_geom;
+
+/* One plane or map: h x w pixels at `offset` elements from the start of its buffer. */
+typedef struct {
+  int32_t h, w;
+  int64_t offset;
+} dn_plane_desc;
+
+/* Network options (Sec. 3: conv1..conv5 of the AlexNet topology, with ReLU, cross-channel LRN and
+ * 3x3/2 max-pooling after conv1 and conv2).  LRN: b_c = a_c (k + alpha/n sum_{|j-c|<=n/2} a_j^2)^-beta
+ * over all channels of the layer; pooling uses ceil-mode sizes with windows clipped to the input.
+ * lrn_before_pool = 1 applies LRN then pool, 0 pool then LRN.  pool5 = 1 also emits 3x3/2 max-pooled
+ * conv5 maps. */
+typedef struct {
+  float lrn_alpha, lrn_beta, lrn_k;
+  int32_t lrn_n;
+  int32_t lrn_before_pool;
+  int32_t pool5;
+} dn_net_params;
+
+/* Geometry only (host, no device work): scales, sizes, stitching and conv5 windows for an H x W image.
+ * geom: [n_scales] out.  planes: [max_planes] out, the planes of ONE image, offsets in elements of the
+ * packed [3][PH][PW] planes; *image_elems = elements per image.  Returns DN_E_TOO_LARGE when a padded
+ * scale exceeds the stitching plane or the plane count exceeds max_planes. */
+int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_scale_geom* geom,
+                          dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                          int64_t* image_elems);
+
+/* Image(s) in -> centred, padded, stitched planes out (Sec. 3.1, 3.2), one fused kernel.
+ * d_images: uint8 [n_img][3][H][W].  d_planes: n_img consecutive blocks of *image_elems elements of
+ * `dtype`, image b's plane j at b * image_elems + planes[j].offset, or NULL for a size query.
+ * geom/planes/n_planes/image_elems as densenet_plan_pyramid. */
+int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                           const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
+                           size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
+                           dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                           int64_t* image_elems, void* stream);
+
+/* Repack conv1..conv5 weights for the kernels.  d_w[l]: device fp32 OIHW weights of layer l
+ * (96x3x11x11, 256x48x5x5, 384x256x3x3, 384x192x3x3, 256x192x3x3); d_b[l]: device fp32 biases.
+ * d_packed: output blob in `dtype` (biases stay fp32), or NULL for a size query. */
+int densenet_pack_weights(const float* const* d_w, const float* const* d_b, dn_dtype dtype,
+                          void* d_packed, size_t packed_bytes, size_t* bytes_needed, void* stream);
+
+/* Planes -> conv5 maps (+ pool5), the whole conv stack (Sec. 3).  planes: [n_planes] descriptors of
+ * the planes to run (offsets into d_planes, elements of `dtype`); consecutive planes of equal size
+ * whose offsets are evenly spaced run in one launch per layer.  d_packed from densenet_pack_weights
+ * with the same dtype.  d_workspace: scratch of ws_bytes (NULL => size query into *ws_needed).
+ * d_conv5: out, per plane [Hc][Wc][256] packed back to back (descs in conv5_desc[n_planes]).
+ * d_pool5: nullable; when net->pool5 it receives [Hp][Wp][256] per plane (descs in pool5_desc).
+ * *conv5_needed / *pool5_needed receive the output sizes in bytes (size query when d_conv5 == NULL). */
+int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, int32_t n_planes,
+                           dn_dtype dtype, const void* d_packed, const dn_net_params* net,
+                           void* d_workspace, size_t ws_bytes, size_t* ws_needed, void* d_conv5,
+                           size_t conv5_bytes, size_t* conv5_needed, dn_plane_desc* conv5_desc,
+                           void* d_pool5, size_t pool5_bytes, size_t* pool5_needed,
+                           dn_plane_desc* pool5_desc, void* stream);
+
+/* Region windows ("crop after", Sec. 4).  For each box (x1, y1, x2, y2) of original-image pixel-edge
+ * coordinates (fp32), the scale k whose scaled box area (sy bh)(sx bw) is closest to target^2 in log
+ * ratio (ties to the smaller k; scales with an empty window skipped) is chosen, and S x S bilinear
+ * samples at the bin centres of the box are read from that scale's conv5 window (coordinates clamped
+ * to the window), all 256 channels: d_out[n][256 * S * S] fp32, flattened (channel, row, column).
+ * conv5_desc: [n_img * planes_per_img] maps from densenet_conv_features (image b's plane j at index
+ * b * planes_per_img + j).  d_box_img: nullable [n] image index per box (NULL => image 0).
+ * d_scale: [n] chosen scale, -1 for a box with a non-finite or non-positive side (its row is 0).
+ * d_idx: nullable [n][S][S][2] int32 (i0, j0) conv5 cell of each sample's top-left neighbour.
+ * Index arithmetic is fp64 with + - * / only, so scales and indices are reproducible bit for bit. */
+int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                            dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,
+                            int32_t pad, int32_t planes_per_img, const float* d_boxes,
+                            const int32_t* d_box_img, int32_t n, float target, int32_t S,
+                            float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream);
+
+/* Single layers of the conv stack, for callers composing their own schedule.  All on channels-last
+ * maps of n planes of equal size, packed back to back.
+ * densenet_conv_layer: layer 1..5 with bias and ReLU.  Layer 1 reads channel-major planes
+ * [n][3][H][W]; layers 2..5 read [n][H][W][C].  Output [n][Ho][Wo][M].
+ * densenet_lrn_pool: LRN + 3x3/2 ceil max-pool (order per net->lrn_before_pool), [n][H][W][C] ->
+ * [n][Hp][Wp][C].  densenet_maxpool: 3x3/2 ceil max-pool only. */
+int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, int32_t W,
+                        dn_dtype dtype, const void* d_packed, void* d_out, void* stream);
+int densenet_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, dn_dtype dtype,
+                      const dn_net_params* net, void* d_out, void* stream);
+int densenet_maxpool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, dn_dtype dtype,
+                     void* d_out, void* stream);
+
+/* Output sizes of the conv stack for an H x W plane: conv1, pool1, conv2, pool2, conv3..5, pool5
+ * (8 pairs written to hw[16]).  Returns DN_E_INVALID_ARG when the plane is too small for conv5. */
+int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw);
+
+/* Thread-local message describing the last error on this thread ("" if none). */
+const char* densenet_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DENSENET_H */

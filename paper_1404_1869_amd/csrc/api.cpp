@@ -1,0 +1,409 @@
+// C ABI entry points: argument validation, size queries, workspace layout and kernel dispatch.
+// Every check happens on the host before any device work is enqueued; launch failures surface as
+// DN_E_HIP with the HIP error string in densenet_last_error().
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <sstream>
+
+#include "common.h"
+
+namespace dn {
+
+static thread_local std::string g_error;
+
+void set_error(const std::string& msg) { g_error = msg; }
+
+int fail(int status, const std::string& msg) {
+  g_error = msg;
+  return status;
+}
+
+static int hip_status(int err, const char* what) {
+  if (err == 0) return DN_OK;
+  std::ostringstream os;
+  os << what << ": " << hipGetErrorString((hipError_t)err);
+  return fail(DN_E_HIP, os.str());
+}
+
+static bool valid_dtype(dn_dtype dt) { return dt == DN_F32 || dt == DN_F16 || dt == DN_BF16; }
+
+// Sizes of the stack for one plane size; false if conv5 would be empty.
+struct StackShape {
+  int64_t h[8], w[8];
+};
+static bool stack_shape(int32_t H, int32_t W, StackShape& s) {
+  stack_sides(H, s.h);
+  stack_sides(W, s.w);
+  return s.h[6] > 0 && s.w[6] > 0;
+}
+
+// Planes grouped into runs of equal size and evenly spaced offsets (one launch per layer per run).
+struct Run {
+  int32_t first, count, h, w;
+  int64_t stride;  // elements between consecutive planes (0 for a run of one)
+};
+static std::vector<Run> make_runs(const dn_plane_desc* planes, int32_t n) {
+  std::vector<Run> runs;
+  for (int32_t i = 0; i < n;) {
+    Run r{i, 1, planes[i].h, planes[i].w, 0};
+    int32_t j = i + 1;
+    if (j < n && planes[j].h == r.h && planes[j].w == r.w) {
+      r.stride = planes[j].offset - planes[i].offset;
+      while (j < n && planes[j].h == r.h && planes[j].w == r.w &&
+             planes[j].offset - planes[j - 1].offset == r.stride && r.stride > 0)
+        ++j;
+      r.count = j - i;
+      if (r.count == 1) r.stride = 0;
+    }
+    runs.push_back(r);
+    i += r.count;
+  }
+  return runs;
+}
+
+}  // namespace dn
+
+using namespace dn;
+
+extern "C" {
+
+const char* densenet_last_error(void) { return g_error.c_str(); }
+
+int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw) {
+  if (!hw) return fail(DN_E_INVALID_ARG, "hw is NULL");
+  if (H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "plane sides must be positive");
+  StackShape s;
+  const bool ok = stack_shape(H, W, s);
+  for (int i = 0; i < 8; ++i) {
+    hw[2 * i] = (int32_t)s.h[i];
+    hw[2 * i + 1] = (int32_t)s.w[i];
+  }
+  if (!ok) return fail(DN_E_INVALID_ARG, "plane too small: conv5 would be empty");
+  return DN_OK;
+}
+
+int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_scale_geom* geom,
+                          dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                          int64_t* image_elems) {
+  try {
+    if (!p || !geom || !planes || !n_planes || !image_elems)
+      return fail(DN_E_INVALID_ARG, "null pointer argument");
+    Plan plan;
+    int st = make_plan(H, W, *p, plan);
+    if (st != DN_OK) return st;
+    const int32_t np = (int32_t)plan.planes.size();
+    *n_planes = np;
+    if (np > max_planes) return fail(DN_E_TOO_LARGE, "more planes than max_planes");
+    std::copy(plan.scales.begin(), plan.scales.end(), geom);
+    int64_t off = 0;
+    for (int32_t j = 0; j < np; ++j) {
+      planes[j].h = plan.planes[j].h;
+      planes[j].w = plan.planes[j].w;
+      planes[j].offset = off;
+      off += 3LL * plan.planes[j].h * plan.planes[j].w;
+    }
+    *image_elems = off;
+    return DN_OK;
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                           const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
+                           size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
+                           dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                           int64_t* image_elems, void* stream) {
+  try {
+    if (!bytes_needed) return fail(DN_E_INVALID_ARG, "bytes_needed is NULL");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_img <= 0) return fail(DN_E_INVALID_ARG, "n_img must be positive");
+    int st = densenet_plan_pyramid(H, W, p, geom, planes, max_planes, n_planes, image_elems);
+    if (st != DN_OK) return st;
+    const size_t need = (size_t)n_img * (size_t)*image_elems * dtype_size(dtype);
+    *bytes_needed = need;
+    if (!d_planes) return DN_OK;
+    if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
+    if (!d_images) return fail(DN_E_INVALID_ARG, "d_images is NULL");
+    if ((int64_t)n_img * *n_planes > 65535) return fail(DN_E_TOO_LARGE, "too many planes in one call");
+    PyrArgs a{};
+    a.n_scales = p->n_scales;
+    a.H = H;
+    a.W = W;
+    a.pad = p->pad;
+    a.ramp = p->pad_mode == DN_PAD_RAMP;
+    for (int c = 0; c < 3; ++c) a.mean[c] = p->mean[c];
+    for (int k = 0; k < p->n_scales; ++k)
+      a.s[k] = PyrScale{geom[k].plane, geom[k].y, geom[k].x, geom[k].rh, geom[k].rw, geom[k].h,
+                        geom[k].w};
+    PyrPlanes pl{};
+    pl.n = *n_planes;
+    pl.image_elems = *image_elems;
+    int32_t mh = 0, mw = 0;
+    for (int j = 0; j < pl.n; ++j) {
+      pl.p[j] = PyrPlane{planes[j].h, planes[j].w, planes[j].offset};
+      mh = std::max(mh, planes[j].h);
+      mw = std::max(mw, planes[j].w);
+    }
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, mh, mw, dtype, d_planes, stream),
+                      "build_planes launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_pack_weights(const float* const* d_w, const float* const* d_b, dn_dtype dtype,
+                          void* d_packed, size_t packed_bytes, size_t* bytes_needed, void* stream) {
+  try {
+    if (!bytes_needed) return fail(DN_E_INVALID_ARG, "bytes_needed is NULL");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    const PackedLayout L = packed_layout(dtype);
+    *bytes_needed = L.total;
+    if (!d_packed) return DN_OK;
+    if (packed_bytes < L.total) return fail(DN_E_BUFFER_TOO_SMALL, "packed buffer too small");
+    if (!d_w || !d_b) return fail(DN_E_INVALID_ARG, "weight pointer arrays are NULL");
+    for (int l = 0; l < 5; ++l)
+      if (!d_w[l] || !d_b[l]) return fail(DN_E_INVALID_ARG, "a layer's weight or bias is NULL");
+    return hip_status(launch_pack_weights(d_w, d_b, dtype, d_packed, stream), "pack launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, int32_t W,
+                        dn_dtype dtype, const void* d_packed, void* d_out, void* stream) {
+  try {
+    if (layer < 1 || layer > 5) return fail(DN_E_INVALID_ARG, "layer must be 1..5");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (!d_in || !d_out || !d_packed) return fail(DN_E_INVALID_ARG, "null device pointer");
+    if (n <= 0 || H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "sizes must be positive");
+    static const int Cs[5] = {3, 96, 256, 384, 384}, Ms[5] = {96, 256, 384, 384, 256};
+    int64_t Ho = H, Wo = W;
+    if (layer == 1) {
+      if (H < 11 || W < 11) return fail(DN_E_INVALID_ARG, "conv1 needs at least 11 x 11 input");
+      Ho = (H - 11) / 4 + 1;
+      Wo = (W - 11) / 4 + 1;
+    }
+    const int64_t in_stride = (int64_t)Cs[layer - 1] * H * W;
+    const int64_t out_stride = (int64_t)Ms[layer - 1] * Ho * Wo;
+    return hip_status(launch_conv(layer, d_in, n, H, W, in_stride, dtype, d_packed, d_out,
+                                  out_stride, stream),
+                      "conv launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, dn_dtype dtype,
+                      const dn_net_params* net, void* d_out, void* stream) {
+  try {
+    if (!net) return fail(DN_E_INVALID_ARG, "net is NULL");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (!d_in || !d_out) return fail(DN_E_INVALID_ARG, "null device pointer");
+    if (n <= 0 || H < 2 || W < 2 || C <= 0) return fail(DN_E_INVALID_ARG, "bad sizes");
+    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0) return fail(DN_E_INVALID_ARG, "lrn_n must be odd");
+    if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
+    const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
+    return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, true,
+                                      net->lrn_before_pool != 0, net->lrn_alpha, net->lrn_beta,
+                                      net->lrn_k, net->lrn_n, d_out, (int64_t)C * Ho * Wo, stream),
+                      "lrn_pool launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_maxpool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, dn_dtype dtype,
+                     void* d_out, void* stream) {
+  try {
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (!d_in || !d_out) return fail(DN_E_INVALID_ARG, "null device pointer");
+    if (n <= 0 || H < 2 || W < 2 || C <= 0) return fail(DN_E_INVALID_ARG, "bad sizes");
+    const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
+    return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, false, false, 0,
+                                      0, 1, 1, d_out, (int64_t)C * Ho * Wo, stream),
+                      "maxpool launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, int32_t n_planes,
+                           dn_dtype dtype, const void* d_packed, const dn_net_params* net,
+                           void* d_workspace, size_t ws_bytes, size_t* ws_needed, void* d_conv5,
+                           size_t conv5_bytes, size_t* conv5_needed, dn_plane_desc* conv5_desc,
+                           void* d_pool5, size_t pool5_bytes, size_t* pool5_needed,
+                           dn_plane_desc* pool5_desc, void* stream) {
+  try {
+    if (!planes || !net || !ws_needed || !conv5_needed || !conv5_desc)
+      return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_planes <= 0) return fail(DN_E_INVALID_ARG, "n_planes must be positive");
+    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0) return fail(DN_E_INVALID_ARG, "lrn_n must be odd");
+    if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
+    if (net->pool5 && (!pool5_needed || !pool5_desc))
+      return fail(DN_E_INVALID_ARG, "pool5 requested without pool5_needed / pool5_desc");
+    const size_t es = dtype_size(dtype);
+    // Output layout and workspace: two ping-pong buffers sized for the largest run.
+    int64_t c5_off = 0, p5_off = 0;
+    size_t ws_a = 0, ws_b = 0;
+    for (int32_t i = 0; i < n_planes; ++i) {
+      StackShape s;
+      if (planes[i].h <= 0 || planes[i].w <= 0 || planes[i].offset < 0)
+        return fail(DN_E_INVALID_ARG, "bad plane descriptor");
+      if (!stack_shape(planes[i].h, planes[i].w, s)) {
+        std::ostringstream os;
+        os << "plane " << i << " (" << planes[i].h << "x" << planes[i].w
+           << ") is too small for conv5";
+        return fail(DN_E_INVALID_ARG, os.str());
+      }
+      conv5_desc[i] = dn_plane_desc{(int32_t)s.h[6], (int32_t)s.w[6], c5_off};
+      c5_off += 256 * s.h[6] * s.w[6];
+      if (net->pool5) {
+        if (s.h[6] < 2 || s.w[6] < 2) return fail(DN_E_INVALID_ARG, "conv5 too small for pool5");
+        pool5_desc[i] = dn_plane_desc{(int32_t)s.h[7], (int32_t)s.w[7], p5_off};
+        p5_off += 256 * s.h[7] * s.w[7];
+      }
+    }
+    const std::vector<Run> runs = make_runs(planes, n_planes);
+    for (const Run& r : runs) {
+      StackShape s;
+      stack_shape(r.h, r.w, s);
+      const size_t a = std::max({96 * s.h[0] * s.w[0], 256 * s.h[2] * s.w[2], 384 * s.h[4] * s.w[4]});
+      const size_t b = std::max({96 * s.h[1] * s.w[1], 256 * s.h[3] * s.w[3], 384 * s.h[5] * s.w[5]});
+      ws_a = std::max(ws_a, (size_t)r.count * a * es);
+      ws_b = std::max(ws_b, (size_t)r.count * b * es);
+    }
+    ws_a = (ws_a + 255) & ~(size_t)255;
+    *ws_needed = ws_a + ws_b;
+    *conv5_needed = (size_t)c5_off * es;
+    if (net->pool5) *pool5_needed = (size_t)p5_off * es;
+    if (!d_conv5) return DN_OK;
+    if (!d_planes || !d_packed) return fail(DN_E_INVALID_ARG, "null device pointer");
+    if (!d_workspace || ws_bytes < *ws_needed)
+      return fail(DN_E_BUFFER_TOO_SMALL, "workspace too small");
+    if (conv5_bytes < *conv5_needed) return fail(DN_E_BUFFER_TOO_SMALL, "conv5 buffer too small");
+    if (net->pool5 && (!d_pool5 || pool5_bytes < *pool5_needed))
+      return fail(DN_E_BUFFER_TOO_SMALL, "pool5 buffer too small");
+
+    char* A = (char*)d_workspace;
+    char* B = A + ws_a;
+    const bool lf = net->lrn_before_pool != 0;
+    for (const Run& r : runs) {
+      StackShape s;
+      stack_shape(r.h, r.w, s);
+      const int n = r.count;
+      const char* in = (const char*)d_planes + planes[r.first].offset * es;
+      const int64_t sp = r.count > 1 ? r.stride : 3LL * r.h * r.w;
+      const int64_t H0 = r.h, W0 = r.w;
+      const int64_t s1 = 96 * s.h[0] * s.w[0], p1 = 96 * s.h[1] * s.w[1];
+      const int64_t s2 = 256 * s.h[2] * s.w[2], p2 = 256 * s.h[3] * s.w[3];
+      const int64_t s3 = 384 * s.h[4] * s.w[4], s4 = 384 * s.h[5] * s.w[5];
+      const int64_t s5 = 256 * s.h[6] * s.w[6], q5 = 256 * s.h[7] * s.w[7];
+      char* c5 = (char*)d_conv5 + conv5_desc[r.first].offset * es;
+      int st;
+      st = hip_status(launch_conv(1, in, n, (int)H0, (int)W0, sp, dtype, d_packed, A, s1, stream),
+                      "conv1 launch");
+      if (st) return st;
+      st = hip_status(launch_lrn_pool(A, n, (int)s.h[0], (int)s.w[0], 96, s1, dtype, true, lf,
+                                      net->lrn_alpha, net->lrn_beta, net->lrn_k, net->lrn_n, B, p1,
+                                      stream),
+                      "lrn_pool1 launch");
+      if (st) return st;
+      st = hip_status(launch_conv(2, B, n, (int)s.h[1], (int)s.w[1], p1, dtype, d_packed, A, s2,
+                                  stream),
+                      "conv2 launch");
+      if (st) return st;
+      st = hip_status(launch_lrn_pool(A, n, (int)s.h[2], (int)s.w[2], 256, s2, dtype, true, lf,
+                                      net->lrn_alpha, net->lrn_beta, net->lrn_k, net->lrn_n, B, p2,
+                                      stream),
+                      "lrn_pool2 launch");
+      if (st) return st;
+      st = hip_status(launch_conv(3, B, n, (int)s.h[3], (int)s.w[3], p2, dtype, d_packed, A, s3,
+                                  stream),
+                      "conv3 launch");
+      if (st) return st;
+      st = hip_status(launch_conv(4, A, n, (int)s.h[4], (int)s.w[4], s3, dtype, d_packed, B, s4,
+                                  stream),
+                      "conv4 launch");
+      if (st) return st;
+      st = hip_status(launch_conv(5, B, n, (int)s.h[5], (int)s.w[5], s4, dtype, d_packed, c5, s5,
+                                  stream),
+                      "conv5 launch");
+      if (st) return st;
+      if (net->pool5) {
+        char* p5 = (char*)d_pool5 + pool5_desc[r.first].offset * es;
+        st = hip_status(launch_lrn_pool(c5, n, (int)s.h[6], (int)s.w[6], 256, s5, dtype, false, false,
+                                        0, 0, 1, 1, p5, q5, stream),
+                        "pool5 launch");
+        if (st) return st;
+      }
+    }
+    return DN_OK;
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                            dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,
+                            int32_t pad, int32_t planes_per_img, const float* d_boxes,
+                            const int32_t* d_box_img, int32_t n, float target, int32_t S,
+                            float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream) {
+  try {
+    if (!d_conv5 || !conv5_desc || !geom || !d_boxes || !d_out || !d_scale)
+      return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (!valid_dtype(conv5_dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_scales <= 0 || n_scales > DN_MAX_SCALES) return fail(DN_E_INVALID_ARG, "bad n_scales");
+    if (planes_per_img <= 0 || planes_per_img > DN_MAX_PLANES_PER_IMAGE || n_maps < planes_per_img ||
+        n_maps % planes_per_img)
+      return fail(DN_E_INVALID_ARG, "n_maps must be a positive multiple of planes_per_img");
+    if (S <= 0 || S > 8) return fail(DN_E_UNSUPPORTED, "S must be in 1..8");
+    if (!(target > 0)) return fail(DN_E_INVALID_ARG, "target must be positive");
+    if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
+    if (n == 0) return DN_OK;
+    RegArgs a{};
+    a.n_scales = n_scales;
+    a.pad = pad;
+    a.planes_per_img = planes_per_img;
+    a.S = S;
+    a.C = 256;
+    a.target = (double)target;
+    for (int32_t j = 0; j < planes_per_img; ++j) {
+      a.map_off[j] = conv5_desc[j].offset - conv5_desc[0].offset;
+      a.map_w[j] = conv5_desc[j].w;
+    }
+    const int n_img = n_maps / planes_per_img;
+    a.n_img = n_img;
+    a.image_stride = 0;
+    if (n_img > 1) {
+      a.image_stride = conv5_desc[planes_per_img].offset - conv5_desc[0].offset;
+      for (int b = 1; b < n_img; ++b)
+        for (int j = 0; j < planes_per_img; ++j) {
+          const dn_plane_desc& d = conv5_desc[b * planes_per_img + j];
+          if (d.offset - conv5_desc[0].offset != b * a.image_stride + a.map_off[j] ||
+              d.w != conv5_desc[j].w || d.h != conv5_desc[j].h)
+            return fail(DN_E_INVALID_ARG, "images' conv5 maps must be laid out identically");
+        }
+    }
+    for (int k = 0; k < n_scales; ++k) {
+      const dn_scale_geom& g = geom[k];
+      if (g.plane < 0 || g.plane >= planes_per_img) return fail(DN_E_INVALID_ARG, "bad geom plane");
+      const dn_plane_desc& d = conv5_desc[g.plane];
+      const bool empty = g.r1 < g.r0 || g.c1 < g.c0;
+      if (!empty && (g.r0 < 0 || g.c0 < 0 || g.r1 >= d.h || g.c1 >= d.w))
+        return fail(DN_E_INVALID_ARG, "scale window outside its conv5 map");
+      a.s[k] = RegScale{g.plane, g.y, g.x, g.r0, g.r1, g.c0, g.c1, empty ? 1 : 0, g.sy, g.sx};
+    }
+    const char* base = (const char*)d_conv5 + conv5_desc[0].offset * dtype_size(conv5_dtype);
+    return hip_status(launch_region_windows(base, conv5_dtype, a, d_boxes, d_box_img, n, d_out,
+                                            d_scale, d_idx, stream),
+                      "region_windows launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+// Internal declarations shared by the library's translation units: status helpers, the host plan,
+// device type traits for the three storage types and the MFMA tiles of gfx950, and the launchers.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "densenet.h"
+
+#if defined(__HIPCC__)
+#include <hip/hip_runtime.h>
+#endif
+
+namespace dn {
+
+// ---------------------------------------------------------------------------------------------
+// Errors
+// ---------------------------------------------------------------------------------------------
+void set_error(const std::string& msg);
+int fail(int status, const std::string& msg);
+
+// ---------------------------------------------------------------------------------------------
+// Host geometry (plan.cpp)
+// ---------------------------------------------------------------------------------------------
+struct PlaneSize {
+  int32_t h, w;
+};
+
+struct Plan {
+  std::vector<dn_scale_geom> scales;
+  std::vector<PlaneSize> planes;  // planes of one image
+};
+
+// Sizes after conv1, pool1, conv2, pool2, conv3, conv4, conv5, pool5 of an n-px side (0 = empty).
+void stack_sides(int64_t n, int64_t out[8]);
+
+// Scale list, rectangles, stitching and conv5 windows.  Returns DN_OK or an error status (message
+// set).
+int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan);
+
+// ---------------------------------------------------------------------------------------------
+// Launchers (device code in the .hip files).  Every launcher enqueues on `stream` and returns
+// hipGetLastError() as an int (0 = success).
+// ---------------------------------------------------------------------------------------------
+struct PyrScale {  // per-scale parameters of the plane builder, passed by value
+  int32_t plane, y, x, rh, rw, h, w;
+};
+struct PyrArgs {
+  int32_t n_scales;
+  int32_t H, W, pad, ramp;
+  float mean[3];
+  PyrScale s[DN_MAX_SCALES];
+};
+struct PyrPlane {
+  int32_t h, w;
+  int64_t offset;
+};
+struct PyrPlanes {
+  int32_t n;
+  int64_t image_elems;
+  PyrPlane p[DN_MAX_PLANES_PER_IMAGE];
+};
+
+int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
+                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, void* stream);
+
+// Packed weight blob: offsets in bytes of each layer's weights and fp32 biases.
+struct PackedLayout {
+  size_t w_off[5], b_off[5], total;
+};
+PackedLayout packed_layout(dn_dtype dt);
+int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dtype dt, void* d_packed,
+                        void* stream);
+
+// One conv layer (1..5) with bias and ReLU over n equal planes spaced in_stride / out_stride elements.
+int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
+                dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride, void* stream);
+
+// LRN + pool (order by lrn_first), or plain pool when lrn == false.  Channels-last maps.
+int launch_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in_stride,
+                    dn_dtype dt, bool lrn, bool lrn_first, float alpha, float beta, float k,
+                    int32_t lrn_n, void* d_out, int64_t out_stride, void* stream);
+
+struct RegScale {
+  int32_t plane, y, x, r0, r1, c0, c1;
+  int32_t empty;
+  double sy, sx;
+};
+struct RegArgs {
+  int32_t n_scales, pad, planes_per_img, S, C, n_img;
+  double target;
+  RegScale s[DN_MAX_SCALES];
+  int64_t map_off[DN_MAX_PLANES_PER_IMAGE];  // offset of plane j's map within an image's maps
+  int32_t map_w[DN_MAX_PLANES_PER_IMAGE];
+  int64_t image_stride;                       // elements between images' maps
+};
+int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
+                          const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
+                          int32_t* d_idx, void* stream);
+
+inline size_t dtype_size(dn_dtype dt) { return dt == DN_F32 ? 4 : 2; }
+
+}  // namespace dn
+
+#if defined(__HIPCC__)
+namespace dn {
+// ---------------------------------------------------------------------------------------------
+// Device side: storage types and the gfx950 MFMA tiles used by the conv kernels.
+//   32x32x16 f16 / bf16: each lane holds 8 consecutive k of row (lane % 32) of A and column
+//   (lane % 32) of B, k offset 8 * (lane / 32); 32x32x2 f32: one k, offset lane / 32.  The
+//   accumulator register r of lane l holds D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+// ---------------------------------------------------------------------------------------------
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T>
+struct Mfma;
+template <>
+struct Mfma<_Float16> {
+  static constexpr int KPL = 8, KS = 16;
+  typedef f16x8 frag;
+  typedef f16x4 half_frag;
+  __device__ static inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+template <>
+struct Mfma<__bf16> {
+  static constexpr int KPL = 8, KS = 16;
+  typedef bf16x8 frag;
+  typedef bf16x4 half_frag;
+  __device__ static inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <>
+struct Mfma<float> {
+  static constexpr int KPL = 1, KS = 2;
+  typedef float frag;
+  typedef float half_frag;
+  __device__ static inline f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+template <typename T>
+__device__ inline T from_f32(float x) {
+  return (T)x;  // round to nearest even for _Float16 and __bf16
+}
+template <typename T>
+__device__ inline float to_f32(T x) {
+  return (float)x;
+}
+
+}  // namespace dn
+#endif

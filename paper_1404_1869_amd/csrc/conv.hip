@@ -1,0 +1,434 @@
+// Convolution engine for conv1..conv5 of the AlexNet topology (the bulk of the path's work, Sec. 3),
+// as implicit GEMMs on gfx950 MFMA: fp16 / bf16 inputs with fp32 accumulation (32x32x16 tiles) or an
+// fp32 path (32x32x2 tiles).  Bias and ReLU are applied in the epilogue.
+//
+// GEMM view: rows = output pixels of a 2-D spatial tile, columns = output channels of one group,
+// k = (input channel, kernel tap).  A workgroup stages the input tile with its halo in LDS once per
+// chunk of 16 input channels and reuses it for every kernel tap, so each input element is read from
+// L2 once per output-channel block instead of once per tap.
+//
+//  conv1 (11x11, stride 4, 3 channels) reads channel-major planes.  Its k index runs over
+//  (channel, row ky in 0..11, column group of 4 in 0..2, column in group): each lane's 8 k values
+//  are two runs of 4 consecutive input pixels of one row, read as two 8-byte LDS loads; taps with
+//  ky = 11 or kx = 11 carry zero weights (144 k per channel instead of 121).
+//  conv2..conv5 (stride 1, R x R, pad (R-1)/2, groups) read channels-last maps; k = (tap, channel),
+//  each lane's 8 k values are 8 consecutive channels of one pixel (one 16-byte LDS load).
+#include <type_traits>
+
+#include "common.h"
+
+namespace dn {
+namespace {
+
+// ------------------------------------------------------------------------------------------------
+// Packed weight layout
+//   conv1: [96][3][144] in dtype, k = (ky * 3 + kx / 4) * 4 + kx % 4 (ky, kx in 0..11, zero beyond 10)
+//   conv2..5: [M][R*R][C/G] in dtype (tap-major, channels contiguous)
+//   biases: fp32 [M]
+// ------------------------------------------------------------------------------------------------
+constexpr int L_M[5] = {96, 256, 384, 384, 256};
+constexpr int L_C[5] = {3, 96, 256, 384, 384};
+constexpr int L_R[5] = {11, 5, 3, 3, 3};
+constexpr int L_G[5] = {1, 2, 1, 2, 2};
+constexpr int K1 = 144;  // conv1 packed k per input channel
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+template <typename T>
+__global__ void pack_conv1_kernel(const float* __restrict__ w, T* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 96 * 3 * K1) return;
+  const int k = i % K1, mc = i / K1;  // mc = m * 3 + c
+  const int q = k >> 2, kx = (q % 3) * 4 + (k & 3), ky = q / 3;
+  float v = 0.f;
+  if (ky < 11 && kx < 11) v = w[(mc * 11 + ky) * 11 + kx];
+  out[i] = from_f32<T>(v);
+}
+
+template <typename T>
+__global__ void pack_conv_kernel(const float* __restrict__ w, T* __restrict__ out, int M, int Cg,
+                                 int RR) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)M * Cg * RR) return;
+  const int c = (int)(i % Cg);
+  const int t = (int)((i / Cg) % RR);
+  const int m = (int)(i / ((int64_t)Cg * RR));
+  out[i] = from_f32<T>(w[((int64_t)m * Cg + c) * RR + t]);
+}
+
+__global__ void copy_f32_kernel(const float* __restrict__ a, float* __restrict__ b, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) b[i] = a[i];
+}
+
+// ------------------------------------------------------------------------------------------------
+// LDS fragment loads
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+__device__ inline typename Mfma<T>::frag lds_frag16(const T* p) {  // 8 consecutive halves, 16 B
+  return *(const typename Mfma<T>::frag*)p;
+}
+template <>
+__device__ inline float lds_frag16<float>(const float* p) {
+  return *p;
+}
+
+// ------------------------------------------------------------------------------------------------
+// conv1: 11x11 / stride 4 / no padding, 3 -> 96 channels, channel-major input planes.
+// Workgroup: 16 x 16 output pixels x all 96 output channels, 4 waves of 96 channels x 64 pixels.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+struct Conv1Cfg {
+  static constexpr int TH = 16, TW = 16;
+  static constexpr int HR = 72;                                       // halo rows / cols (4*15+12)
+  static constexpr int HS = std::is_same<T, float>::value ? 72 : 80;  // halo row stride
+  static constexpr int WS = K1 + (std::is_same<T, float>::value ? 1 : 8);
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T* __restrict__ out,
+                                                    const T* __restrict__ wp,
+                                                    const float* __restrict__ bias, int H, int W,
+                                                    int Ho, int Wo, int64_t in_stride,
+                                                    int64_t out_stride, int tiles_x, int tiles_y) {
+  using C = Conv1Cfg<T>;
+  using Op = Mfma<T>;
+  __shared__ T s_in[C::HR * C::HS];
+  __shared__ T s_w[96 * C::WS];
+
+  int bid = blockIdx.x;
+  const int tx = bid % tiles_x;
+  bid /= tiles_x;
+  const int ty = bid % tiles_y;
+  const int plane = bid / tiles_y;
+  const int oy0 = ty * C::TH, ox0 = tx * C::TW;
+  const int iy0 = oy0 * 4, ix0 = ox0 * 4;
+  const T* src = in + plane * in_stride;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  int prow[2], pcol[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int idx = wave * 64 + t * 32 + l32;
+    prow[t] = idx / C::TW;
+    pcol[t] = idx % C::TW;
+  }
+  f32x16 acc[3][2];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) acc[a][t] = f32x16{};
+
+  for (int c = 0; c < 3; ++c) {
+    __syncthreads();
+    const T* sc = src + (int64_t)c * H * W;
+    for (int e = threadIdx.x; e < C::HR * C::HR; e += 256) {
+      const int hy = e / C::HR, hx = e % C::HR;
+      const int iy = iy0 + hy, ix = ix0 + hx;
+      T v = from_f32<T>(0.f);
+      if (iy < H && ix < W) v = sc[(int64_t)iy * W + ix];
+      s_in[hy * C::HS + hx] = v;
+    }
+    for (int e = threadIdx.x; e < 96 * K1; e += 256) {
+      const int m = e / K1, k = e % K1;
+      s_w[m * C::WS + k] = wp[(m * 3 + c) * K1 + k];
+    }
+    __syncthreads();
+#pragma unroll 3
+    for (int ks = 0; ks < K1 / Op::KS; ++ks) {
+      typename Op::frag a[2], b[3];
+      if constexpr (std::is_same<T, float>::value) {
+        const int k = ks * 2 + half;
+        const int q = k >> 2, ky = q / 3, kx = (q % 3) * 4 + (k & 3);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) a[t] = s_in[(4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx];
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt) b[mt] = s_w[(mt * 32 + l32) * C::WS + k];
+      } else {
+        // two groups of 4 columns: q0 = 4 ks + 2 half and q0 + 1
+        const int q0 = 4 * ks + 2 * half;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          typename Op::half_frag lo, hi;
+          {
+            const int ky = q0 / 3, kx = (q0 % 3) * 4;
+            lo = *(const typename Op::half_frag*)(s_in + (4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx);
+          }
+          {
+            const int q1 = q0 + 1, ky = q1 / 3, kx = (q1 % 3) * 4;
+            hi = *(const typename Op::half_frag*)(s_in + (4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx);
+          }
+          a[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt)
+          b[mt] = lds_frag16<T>(s_w + (mt * 32 + l32) * C::WS + ks * Op::KS + half * 8);
+      }
+#pragma unroll
+      for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) acc[mt][t] = Op::mma(a[t], b[mt], acc[mt][t]);
+    }
+  }
+
+  T* dst = out + plane * out_stride;
+#pragma unroll
+  for (int mt = 0; mt < 3; ++mt) {
+    const int m = mt * 32 + l32;
+    const float bv = bias[m];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = 8 * (r >> 2) + 4 * half + (r & 3);
+        const int idx = wave * 64 + t * 32 + i;
+        const int oy = oy0 + idx / C::TW, ox = ox0 + idx % C::TW;
+        if (oy < Ho && ox < Wo)
+          dst[((int64_t)oy * Wo + ox) * 96 + m] = from_f32<T>(fmaxf(acc[mt][t][r] + bv, 0.f));
+      }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Stride-1 R x R conv with zero padding (R-1)/2, grouped, channels-last.
+// Workgroup: TH x TW = 16 x 16 output pixels x BM output channels of one group.  Waves: BM/64 along
+// channels x 2 along pixels; each wave owns 64 channels x 128 pixels (2 x 4 MFMA tiles).
+// LDS: input halo (TH+R-1) x (TW+R-1) x 16 channels, and the weights of one kernel row
+// (R taps x BM channels x 16 input channels).
+// ------------------------------------------------------------------------------------------------
+template <typename T, int R, int BM>
+struct ConvCfg {
+  static constexpr int TH = 16, TW = 16, CC = 16;
+  static constexpr int HH = TH + R - 1, HW = TW + R - 1;
+  static constexpr int CS = CC + (std::is_same<T, float>::value ? 1 : 8);  // LDS stride (elements)
+  static constexpr int WM = BM / 64, WN = (TH * TW) / 128;
+  static constexpr int NT = 64 * WM * WN;
+  static_assert(NT == 2 * BM, "launch bounds assume two pixel waves per 64 channels");
+};
+
+template <typename T, int R, int BM>
+__global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
+    const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
+    const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
+    int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
+  using Cf = ConvCfg<T, R, BM>;
+  using Op = Mfma<T>;
+  constexpr int pad = (R - 1) / 2;
+  constexpr bool F32 = std::is_same<T, float>::value;
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int VPP = Cf::CC / VEC;
+  typedef T vec_t __attribute__((ext_vector_type(VEC)));
+  __shared__ T s_in[Cf::HH * Cf::HW * Cf::CS];
+  __shared__ T s_w[R * BM * Cf::CS];
+
+  int bid = blockIdx.x;
+  const int tx = bid % tiles_x;
+  bid /= tiles_x;
+  const int ty = bid % tiles_y;
+  bid /= tiles_y;
+  const int mb = bid % mblocks;
+  const int plane = bid / mblocks;
+  const int mpg = Mg / BM;
+  const int g = mb / mpg, m0 = (mb % mpg) * BM;
+  const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
+  const T* src = in + plane * in_stride;
+  const T* wg = wp + ((int64_t)g * Mg + m0) * R * R * Cg;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave % Cf::WM, wn = wave / Cf::WM;
+  const int half = lane >> 5, l32 = lane & 31;
+  int prow[4], pcol[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int idx = wn * 128 + t * 32 + l32;
+    prow[t] = idx / Cf::TW;
+    pcol[t] = idx % Cf::TW;
+  }
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[a][t] = f32x16{};
+
+  for (int c0 = 0; c0 < Cg; c0 += Cf::CC) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < Cf::HH * Cf::HW * VPP; e += Cf::NT) {
+      const int v = e % VPP, p = e / VPP;
+      const int hy = p / Cf::HW, hx = p % Cf::HW;
+      const int iy = oy0 - pad + hy, ix = ox0 - pad + hx;
+      vec_t val = vec_t{};
+      if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+        val = *(const vec_t*)(src + ((int64_t)iy * W + ix) * C + g * Cg + c0 + v * VEC);
+      if constexpr (F32) {
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) s_in[p * Cf::CS + v * VEC + q] = val[q];
+      } else {
+        *(vec_t*)(s_in + p * Cf::CS + v * VEC) = val;
+      }
+    }
+    for (int ky = 0; ky < R; ++ky) {
+      if (ky) __syncthreads();
+      for (int e = threadIdx.x; e < R * BM * VPP; e += Cf::NT) {
+        const int v = e % VPP, t = e / VPP;
+        const int m = t % BM, kx = t / BM;
+        const vec_t val = *(const vec_t*)(wg + ((int64_t)m * R * R + ky * R + kx) * Cg + c0 + v * VEC);
+        if constexpr (F32) {
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) s_w[(kx * BM + m) * Cf::CS + v * VEC + q] = val[q];
+        } else {
+          *(vec_t*)(s_w + (kx * BM + m) * Cf::CS + v * VEC) = val;
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int kx = 0; kx < R; ++kx) {
+#pragma unroll
+        for (int kk = 0; kk < Cf::CC / Op::KS; ++kk) {
+          const int koff = kk * Op::KS + half * Op::KPL;
+          typename Op::frag a[4], b[2];
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            a[t] = lds_frag16<T>(s_in + ((prow[t] + ky) * Cf::HW + pcol[t] + kx) * Cf::CS + koff);
+#pragma unroll
+          for (int mt = 0; mt < 2; ++mt)
+            b[mt] = lds_frag16<T>(s_w + (kx * BM + wm * 64 + mt * 32 + l32) * Cf::CS + koff);
+#pragma unroll
+          for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[mt][t] = Op::mma(a[t], b[mt], acc[mt][t]);
+        }
+      }
+    }
+  }
+
+  T* dst = out + plane * out_stride;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int m = g * Mg + m0 + wm * 64 + mt * 32 + l32;
+    const float bv = bias[m];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = 8 * (r >> 2) + 4 * half + (r & 3);
+        const int idx = wn * 128 + t * 32 + i;
+        const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+        if (oy < H && ox < W)
+          dst[((int64_t)oy * W + ox) * M + m] = from_f32<T>(fmaxf(acc[mt][t][r] + bv, 0.f));
+      }
+  }
+}
+
+template <typename T, int R, int BM>
+int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int H, int W, int C,
+                int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
+  using Cf = ConvCfg<T, R, BM>;
+  const int Cg = C / G, Mg = M / G;
+  const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
+  const int mblocks = G * (Mg / BM);
+  const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
+  if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+  conv_s1_kernel<T, R, BM><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+      in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+  return (int)hipGetLastError();
+}
+
+template <typename T>
+int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
+                  const void* d_packed, void* d_out, int64_t out_stride, const PackedLayout& L,
+                  hipStream_t s) {
+  const T* in = (const T*)d_in;
+  T* out = (T*)d_out;
+  const T* wp = (const T*)((const char*)d_packed + L.w_off[layer - 1]);
+  const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
+  if (layer == 1) {
+    const int Ho = (H - 11) / 4 + 1, Wo = (W - 11) / 4 + 1;
+    const int tiles_x = (Wo + 15) / 16, tiles_y = (Ho + 15) / 16;
+    const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
+    if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+                                                    out_stride, tiles_x, tiles_y);
+    return (int)hipGetLastError();
+  }
+  const int li = layer - 1;
+  switch (layer) {
+    case 2:
+      return run_conv_s1<T, 5, 128>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
+                                    out_stride, s);
+    case 3:
+    case 5:
+      return run_conv_s1<T, 3, 128>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
+                                    out_stride, s);
+    case 4:
+      return run_conv_s1<T, 3, 192>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
+                                    out_stride, s);
+  }
+  return (int)hipErrorInvalidValue;
+}
+
+}  // namespace
+
+PackedLayout packed_layout(dn_dtype dt) {
+  PackedLayout L{};
+  const size_t es = dtype_size(dt);
+  size_t off = 0;
+  for (int l = 0; l < 5; ++l) {
+    L.w_off[l] = off;
+    const size_t n = l == 0 ? (size_t)96 * 3 * K1
+                            : (size_t)L_M[l] * (L_C[l] / L_G[l]) * L_R[l] * L_R[l];
+    off = align256(off + n * es);
+  }
+  for (int l = 0; l < 5; ++l) {
+    L.b_off[l] = off;
+    off = align256(off + (size_t)L_M[l] * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dtype dt, void* d_packed,
+                        void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  const PackedLayout L = packed_layout(dt);
+  char* base = (char*)d_packed;
+  for (int l = 0; l < 5; ++l) {
+    void* dst = base + L.w_off[l];
+    if (l == 0) {
+      const int n = 96 * 3 * K1;
+      if (dt == DN_F32) pack_conv1_kernel<float><<<(n + 255) / 256, 256, 0, s>>>(d_w[0], (float*)dst);
+      if (dt == DN_F16)
+        pack_conv1_kernel<_Float16><<<(n + 255) / 256, 256, 0, s>>>(d_w[0], (_Float16*)dst);
+      if (dt == DN_BF16) pack_conv1_kernel<__bf16><<<(n + 255) / 256, 256, 0, s>>>(d_w[0], (__bf16*)dst);
+    } else {
+      const int Cg = L_C[l] / L_G[l], RR = L_R[l] * L_R[l];
+      const int64_t n = (int64_t)L_M[l] * Cg * RR;
+      const unsigned nb = (unsigned)((n + 255) / 256);
+      if (dt == DN_F32) pack_conv_kernel<float><<<nb, 256, 0, s>>>(d_w[l], (float*)dst, L_M[l], Cg, RR);
+      if (dt == DN_F16)
+        pack_conv_kernel<_Float16><<<nb, 256, 0, s>>>(d_w[l], (_Float16*)dst, L_M[l], Cg, RR);
+      if (dt == DN_BF16)
+        pack_conv_kernel<__bf16><<<nb, 256, 0, s>>>(d_w[l], (__bf16*)dst, L_M[l], Cg, RR);
+    }
+    copy_f32_kernel<<<(L_M[l] + 255) / 256, 256, 0, s>>>(d_b[l], (float*)(base + L.b_off[l]), L_M[l]);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
+                dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride, void* stream) {
+  const PackedLayout L = packed_layout(dt);
+  hipStream_t s = (hipStream_t)stream;
+  switch (dt) {
+    case DN_F32:
+      return conv_dispatch<float>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L, s);
+    case DN_F16:
+      return conv_dispatch<_Float16>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L,
+                                     s);
+    case DN_BF16:
+      return conv_dispatch<__bf16>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L, s);
+  }
+  return (int)hipErrorInvalidValue;
+}
+
+}  // namespace dn

@@ -1,0 +1,181 @@
+// Host geometry of the pyramid (Sec. 3.1): scale list, scaled sizes, padded rectangles, Bottom-Left
+// Fill stitching onto planes, and each scale's window of conv5 cells.  Integer and fp64 arithmetic
+// only; no device code.
+//
+// Stitching works on a 16-px occupancy grid: in stitched mode every rectangle side is a multiple of
+// 16 px (the conv5 stride), so every corner a rectangle can take is a grid point and a fit test is a
+// scan of grid cells.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <sstream>
+
+#include "common.h"
+
+namespace dn {
+
+static int64_t div_floor(int64_t a, int64_t b) {  // b > 0
+  return a >= 0 ? a / b : -((-a + b - 1) / b);
+}
+static int64_t div_ceil(int64_t a, int64_t b) { return -div_floor(-a, b); }
+
+void stack_sides(int64_t n, int64_t out[8]) {
+  auto conv = [](int64_t v, int64_t R, int64_t s, int64_t p) -> int64_t {
+    return v + 2 * p >= R ? (v + 2 * p - R) / s + 1 : 0;
+  };
+  // 3x3/2 pooling, ceil mode: ceil((v-3)/2)+1 windows, the last one starting inside the input.
+  auto pool = [](int64_t v) -> int64_t { return v >= 2 ? (v - 2) / 2 + 1 : 0; };
+  out[0] = conv(n, 11, 4, 0);
+  out[1] = pool(out[0]);
+  out[2] = conv(out[1], 5, 1, 2);
+  out[3] = pool(out[2]);
+  out[4] = conv(out[3], 3, 1, 1);
+  out[5] = conv(out[4], 3, 1, 1);
+  out[6] = conv(out[5], 3, 1, 1);
+  out[7] = pool(out[6]);
+}
+
+namespace {
+
+struct Grid {  // occupancy of one plane in 16 x 16 px cells
+  int gh, gw;
+  std::vector<uint8_t> used;
+  std::vector<int> tops, lefts;  // candidate corner coordinates in cells
+  Grid(int h, int w) : gh(h), gw(w), used((size_t)h * w, 0), tops{0}, lefts{0} {}
+  bool free_at(int cy, int cx, int nh, int nw) const {
+    if (cy + nh > gh || cx + nw > gw) return false;
+    for (int r = cy; r < cy + nh; ++r) {
+      const uint8_t* row = used.data() + (size_t)r * gw;
+      for (int c = cx; c < cx + nw; ++c)
+        if (row[c]) return false;
+    }
+    return true;
+  }
+  void occupy(int cy, int cx, int nh, int nw) {
+    for (int r = cy; r < cy + nh; ++r) std::memset(used.data() + (size_t)r * gw + cx, 1, nw);
+    tops.insert(std::upper_bound(tops.begin(), tops.end(), cy + nh), cy + nh);
+    lefts.insert(std::upper_bound(lefts.begin(), lefts.end(), cx + nw), cx + nw);
+  }
+  // First corner in (top, left) order where an nh x nw block fits, or false.
+  bool place(int nh, int nw, int& cy, int& cx) const {
+    for (size_t i = 0; i < tops.size(); ++i) {
+      if (i && tops[i] == tops[i - 1]) continue;
+      for (size_t j = 0; j < lefts.size(); ++j) {
+        if (j && lefts[j] == lefts[j - 1]) continue;
+        if (free_at(tops[i], lefts[j], nh, nw)) {
+          cy = tops[i];
+          cx = lefts[j];
+          return true;
+        }
+      }
+    }
+    return false;
+  }
+};
+
+}  // namespace
+
+int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan) {
+  if (H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "image sides must be positive");
+  if (p.n_scales <= 0 || p.n_scales > DN_MAX_SCALES) {
+    std::ostringstream os;
+    os << "n_scales must be in 1.." << DN_MAX_SCALES;
+    return fail(DN_E_INVALID_ARG, os.str());
+  }
+  if (p.steps_per_octave <= 0) return fail(DN_E_INVALID_ARG, "steps_per_octave must be positive");
+  if (p.pad < 0 || p.pad > 1024) return fail(DN_E_INVALID_ARG, "pad must be in 0..1024");
+  if (p.pad_mode != DN_PAD_ZERO && p.pad_mode != DN_PAD_RAMP)
+    return fail(DN_E_INVALID_ARG, "pad_mode must be DN_PAD_ZERO or DN_PAD_RAMP");
+  if ((p.plane_h == 0) != (p.plane_w == 0) || p.plane_h < 0 || p.plane_w < 0)
+    return fail(DN_E_INVALID_ARG, "plane_h and plane_w must both be 0 or both positive");
+  const double base = p.base_longest_side > 0 ? (double)p.base_longest_side / (double)std::max(H, W)
+                                               : p.base_scale;
+  if (!(base > 0.0) || !std::isfinite(base)) return fail(DN_E_INVALID_ARG, "base scale must be > 0");
+
+  const int K = p.n_scales;
+  const bool stitched = p.plane_h > 0;
+  plan.scales.assign(K, dn_scale_geom{});
+  plan.planes.clear();
+  for (int k = 0; k < K; ++k) {
+    dn_scale_geom& g = plan.scales[k];
+    g.k = k;
+    g.s = base * std::pow(2.0, -(double)k / (double)p.steps_per_octave);
+    const double fh = std::floor((double)H * g.s + 0.5), fw = std::floor((double)W * g.s + 0.5);
+    if (!(fh < 1e6) || !(fw < 1e6)) return fail(DN_E_TOO_LARGE, "scaled image side exceeds 1e6 px");
+    g.h = std::max(1, (int)fh);
+    g.w = std::max(1, (int)fw);
+    g.sy = (double)g.h / (double)H;
+    g.sx = (double)g.w / (double)W;
+    g.rh = g.h + 2 * p.pad;
+    g.rw = g.w + 2 * p.pad;
+    if (stitched) {
+      g.rh = (int)(div_ceil(g.rh, 16) * 16);
+      g.rw = (int)(div_ceil(g.rw, 16) * 16);
+      if (g.rh > p.plane_h || g.rw > p.plane_w) {
+        std::ostringstream os;
+        os << "scale " << k << " needs a " << g.rh << "x" << g.rw << " rectangle, larger than the "
+           << p.plane_h << "x" << p.plane_w << " stitching plane";
+        return fail(DN_E_TOO_LARGE, os.str());
+      }
+    }
+  }
+
+  if (!stitched) {
+    for (int k = 0; k < K; ++k) {
+      dn_scale_geom& g = plan.scales[k];
+      g.plane = k;
+      g.y = g.x = 0;
+      plan.planes.push_back({g.rh, g.rw});
+    }
+  } else {
+    // Largest rectangles first: by height, then width, then scale index.
+    std::vector<int> order(K);
+    for (int k = 0; k < K; ++k) order[k] = k;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+      const dn_scale_geom &A = plan.scales[a], &B = plan.scales[b];
+      if (A.rh != B.rh) return A.rh > B.rh;
+      if (A.rw != B.rw) return A.rw > B.rw;
+      return a < b;
+    });
+    std::vector<Grid> grids;
+    for (int k : order) {
+      dn_scale_geom& g = plan.scales[k];
+      const int nh = g.rh / 16, nw = g.rw / 16;
+      int cy = 0, cx = 0;
+      size_t pi = 0;
+      for (; pi < grids.size(); ++pi)
+        if (grids[pi].place(nh, nw, cy, cx)) break;
+      if (pi == grids.size()) {
+        if ((int)grids.size() >= DN_MAX_PLANES_PER_IMAGE)
+          return fail(DN_E_TOO_LARGE, "more planes than DN_MAX_PLANES_PER_IMAGE");
+        grids.emplace_back(p.plane_h / 16, p.plane_w / 16);
+        cy = cx = 0;
+      }
+      grids[pi].occupy(cy, cx, nh, nw);
+      g.plane = (int32_t)pi;
+      g.y = cy * 16;
+      g.x = cx * 16;
+    }
+    plan.planes.assign(grids.size(), PlaneSize{p.plane_h, p.plane_w});
+  }
+  if ((int)plan.planes.size() > DN_MAX_PLANES_PER_IMAGE)
+    return fail(DN_E_TOO_LARGE, "more planes than DN_MAX_PLANES_PER_IMAGE");
+
+  // conv5 windows: cell i is centred at 16 i + 17.5; keep cells centred on rows [y+p, y+p+h).
+  for (int k = 0; k < K; ++k) {
+    dn_scale_geom& g = plan.scales[k];
+    const PlaneSize ps = plan.planes[g.plane];
+    int64_t sh[8], sw[8];
+    stack_sides(ps.h, sh);
+    stack_sides(ps.w, sw);
+    const int64_t top = g.y + p.pad, left = g.x + p.pad;
+    // first i with 32 i + 35 >= 2 top; last i with 32 i + 35 <= 2 (top + h) - 1
+    g.r0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * top - 35, 32));
+    g.r1 = (int32_t)std::min<int64_t>(sh[6] - 1, div_floor(2 * (top + g.h) - 36, 32));
+    g.c0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * left - 35, 32));
+    g.c1 = (int32_t)std::min<int64_t>(sw[6] - 1, div_floor(2 * (left + g.w) - 36, 32));
+  }
+  return DN_OK;
+}
+
+}  // namespace dn

@@ -1,0 +1,145 @@
+// Region windows ("crop after", Sec. 4): a box of the original image is read out of the conv5
+// pyramid at the scale whose scaled area is closest to target^2, as S x S bilinear samples at the
+// bin centres of the box, all channels.
+//
+// One workgroup per box, one thread per channel.  The scale choice and the sample positions are
+// computed in fp64 with + - * / only and FP contraction off, in the same order as the definition, so
+// the chosen scale and cell indices are reproducible bit for bit on any IEEE fp64 implementation.
+// Samples of one bin read 4 cells x C contiguous channels (coalesced); the descriptor row is staged
+// in LDS and written out contiguously.
+#include "common.h"
+
+namespace dn {
+namespace {
+
+constexpr int MAX_S = 8;
+
+template <typename T>
+__global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict__ maps, RegArgs a,
+                                                             const float* __restrict__ boxes,
+                                                             const int32_t* __restrict__ box_img,
+                                                             float* __restrict__ out,
+                                                             int32_t* __restrict__ scale_out,
+                                                             int32_t* __restrict__ idx_out) {
+#pragma clang fp contract(off)
+  extern __shared__ float s_row[];  // C * S * S
+  __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
+  __shared__ float s_ly[MAX_S], s_lx[MAX_S];
+  const int r = blockIdx.x;
+  const int S = a.S, C = a.C, SS = S * S;
+  const int tid = threadIdx.x;
+  const double x1 = boxes[4 * r + 0], y1 = boxes[4 * r + 1], x2 = boxes[4 * r + 2],
+               y2 = boxes[4 * r + 3];
+  const double bw = x2 - x1, bh = y2 - y1;
+  const int img = box_img ? box_img[r] : 0;
+  int best = -1;
+  if (img >= 0 && img < a.n_img && isfinite(x1) && isfinite(y1) && isfinite(x2) && isfinite(y2) && bw > 0 && bh > 0) {
+    const double T2 = a.target * a.target;
+    double best_cost = 0;
+    for (int k = 0; k < a.n_scales; ++k) {
+      if (a.s[k].empty) continue;
+      const double area = (a.s[k].sy * bh) * (a.s[k].sx * bw);
+      const double p = area / T2, q = T2 / area;
+      const double cost = p < q ? q : p;
+      if (best < 0 || cost < best_cost) {
+        best = k;
+        best_cost = cost;
+      }
+    }
+  }
+  float* dst = out + (int64_t)r * C * SS;
+  if (best < 0) {
+    for (int e = tid; e < C * SS; e += blockDim.x) dst[e] = 0.f;
+    if (tid == 0) scale_out[r] = -1;
+    if (idx_out)
+      for (int e = tid; e < 2 * SS; e += blockDim.x) idx_out[(int64_t)r * 2 * SS + e] = 0;
+    return;
+  }
+  const RegScale sc = a.s[best];
+  if (tid < 2 * S) {
+    // tid < S: row sample a = tid; S <= tid < 2S: column sample b = tid - S
+    const bool row = tid < S;
+    const int t = row ? tid : tid - S;
+    const double f = ((double)t + 0.5) / (double)S;
+    double lo, hi, cmin, cmax;
+    if (row) {
+      lo = y1 * sc.sy + (double)sc.y + (double)a.pad;
+      hi = y2 * sc.sy + (double)sc.y + (double)a.pad;
+      cmin = sc.r0;
+      cmax = sc.r1;
+    } else {
+      lo = x1 * sc.sx + (double)sc.x + (double)a.pad;
+      hi = x2 * sc.sx + (double)sc.x + (double)a.pad;
+      cmin = sc.c0;
+      cmax = sc.c1;
+    }
+    double g = ((lo + f * (hi - lo)) - 17.5) * 0.0625;
+    g = g < cmin ? cmin : (g > cmax ? cmax : g);
+    const int i0 = (int)floor(g);
+    const int i1 = min(i0 + 1, (int)cmax);
+    const float lam = (float)(g - (double)i0);
+    if (row) {
+      s_i0[t] = i0;
+      s_i1[t] = i1;
+      s_ly[t] = lam;
+    } else {
+      s_j0[t] = i0;
+      s_j1[t] = i1;
+      s_lx[t] = lam;
+    }
+  }
+  __syncthreads();
+  const T* F = maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
+  const int Wc = a.map_w[sc.plane];
+  for (int c = tid; c < C; c += blockDim.x) {
+    for (int u = 0; u < S; ++u) {
+      const int i0 = s_i0[u], i1 = s_i1[u];
+      const float ly = s_ly[u];
+      for (int v = 0; v < S; ++v) {
+        const int j0 = s_j0[v], j1 = s_j1[v];
+        const float lx = s_lx[v];
+        const float v00 = to_f32(F[((int64_t)i0 * Wc + j0) * C + c]);
+        const float v01 = to_f32(F[((int64_t)i0 * Wc + j1) * C + c]);
+        const float v10 = to_f32(F[((int64_t)i1 * Wc + j0) * C + c]);
+        const float v11 = to_f32(F[((int64_t)i1 * Wc + j1) * C + c]);
+        const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
+        s_row[c * SS + u * S + v] = top + ly * (bot - top);
+      }
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < C * SS; e += blockDim.x) dst[e] = s_row[e];
+  if (tid == 0) scale_out[r] = best;
+  if (idx_out)
+    for (int e = tid; e < SS; e += blockDim.x) {
+      idx_out[((int64_t)r * SS + e) * 2 + 0] = s_i0[e / S];
+      idx_out[((int64_t)r * SS + e) * 2 + 1] = s_j0[e % S];
+    }
+}
+
+}  // namespace
+
+int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
+                          const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
+                          int32_t* d_idx, void* stream) {
+  if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
+  hipStream_t s = (hipStream_t)stream;
+  const size_t lds = sizeof(float) * (size_t)a.C * a.S * a.S;
+  switch (dt) {
+    case DN_F32:
+      region_windows_kernel<float><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes, d_box_img,
+                                                       d_out, d_scale, d_idx);
+      break;
+    case DN_F16:
+      region_windows_kernel<_Float16><<<n, 256, lds, s>>>((const _Float16*)d_conv5, a, d_boxes,
+                                                          d_box_img, d_out, d_scale, d_idx);
+      break;
+    case DN_BF16:
+      region_windows_kernel<__bf16><<<n, 256, lds, s>>>((const __bf16*)d_conv5, a, d_boxes,
+                                                        d_box_img, d_out, d_scale, d_idx);
+      break;
+  }
+  return (int)hipGetLastError();
+}
+
+}  // namespace dn

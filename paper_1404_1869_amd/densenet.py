@@ -1,0 +1,353 @@
+"""ctypes binding of libdensenet.so: the C ABI of include/densenet.h, same names, argument marshalling
+only.  Device memory comes from torch tensors and the stream from torch.cuda.current_stream(); every
+step of the computation runs in the library's HIP kernels.  There is no fallback: if the library or a
+GPU is missing the calls raise.
+
+On top of the raw entry points, ``convnet_featpyramid`` mirrors the paper's interface
+(``pyra = convnet_featpyramid(image)``, Sec. 3.5): image(s) in, per-scale conv5 maps plus geometry out.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdensenet.so")
+
+DN_OK, DN_E_INVALID_ARG, DN_E_TOO_LARGE, DN_E_BUFFER_TOO_SMALL = 0, -1, -2, -3
+DN_E_UNSUPPORTED, DN_E_HIP, DN_E_INTERNAL = -4, -5, -6
+DN_F32, DN_F16, DN_BF16 = 0, 1, 2
+DN_PAD_ZERO, DN_PAD_RAMP = 0, 1
+DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE = 64, 64
+DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
+
+EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
+           "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
+           "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_last_error")
+
+
+class dn_pyramid_params(ctypes.Structure):
+    _fields_ = [("n_scales", ctypes.c_int32), ("steps_per_octave", ctypes.c_int32),
+                ("base_scale", ctypes.c_double), ("base_longest_side", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("pad_mode", ctypes.c_int32), ("plane_h", ctypes.c_int32),
+                ("plane_w", ctypes.c_int32), ("mean", ctypes.c_float * 3)]
+
+
+class dn_scale_geom(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
+                                              "r1", "c0", "c1")] + \
+               [(n, ctypes.c_double) for n in ("s", "sy", "sx")]
+
+
+class dn_plane_desc(ctypes.Structure):
+    _fields_ = [("h", ctypes.c_int32), ("w", ctypes.c_int32), ("offset", ctypes.c_int64)]
+
+
+class dn_net_params(ctypes.Structure):
+    _fields_ = [("lrn_alpha", ctypes.c_float), ("lrn_beta", ctypes.c_float),
+                ("lrn_k", ctypes.c_float), ("lrn_n", ctypes.c_int32),
+                ("lrn_before_pool", ctypes.c_int32), ("pool5", ctypes.c_int32)]
+
+
+class DenseNetError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"densenet error {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libdensenet.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+        pp, pg, pd = ctypes.POINTER(dn_pyramid_params), ctypes.POINTER(dn_scale_geom), ctypes.POINTER(dn_plane_desc)
+        pn = ctypes.POINTER(dn_net_params)
+        psz, pi32, pi64 = ctypes.POINTER(sz), ctypes.POINTER(i32), ctypes.POINTER(i64)
+        sig = {
+            "densenet_plan_pyramid": [i32, i32, pp, pg, pd, i32, pi32, pi64],
+            "densenet_build_pyramid": [P, i32, i32, i32, pp, i32, P, sz, psz, pg, pd, i32, pi32, pi64, P],
+            "densenet_pack_weights": [P, P, i32, P, sz, psz, P],
+            "densenet_conv_features": [P, pd, i32, i32, P, pn, P, sz, psz, P, sz, psz, pd, P, sz, psz,
+                                       pd, P],
+            "densenet_region_windows": [P, pd, i32, i32, pg, i32, i32, i32, P, P, i32, f32, i32, P, P,
+                                        P, P],
+            "densenet_conv_layer": [i32, P, i32, i32, i32, i32, P, P, P],
+            "densenet_lrn_pool": [P, i32, i32, i32, i32, i32, pn, P, P],
+            "densenet_maxpool": [P, i32, i32, i32, i32, i32, P, P],
+            "densenet_layer_sizes": [i32, i32, pi32],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.densenet_last_error.argtypes = []
+        L.densenet_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().densenet_last_error().decode()
+
+
+def check(status: int):
+    if status != DN_OK:
+        raise DenseNetError(status, last_error())
+    return status
+
+
+# ------------------------------------------------------------------------------------------------
+# torch plumbing: device memory and streams only
+# ------------------------------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    assert t.is_cuda and t.is_contiguous(), "device tensors must be contiguous CUDA/HIP tensors"
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _tdtype(dt: int):
+    torch = _torch()
+    return {DN_F32: torch.float32, DN_F16: torch.float16, DN_BF16: torch.bfloat16}[dt]
+
+
+def pyramid_params(n_scales, steps_per_octave, base_scale=1.0, base_longest_side=0, pad=0,
+                   pad_mode=DN_PAD_ZERO, plane_h=0, plane_w=0, mean=(0.0, 0.0, 0.0)):
+    p = dn_pyramid_params()
+    p.n_scales, p.steps_per_octave, p.base_scale = n_scales, steps_per_octave, base_scale
+    p.base_longest_side, p.pad, p.pad_mode = base_longest_side, pad, pad_mode
+    p.plane_h, p.plane_w = plane_h, plane_w
+    p.mean = (ctypes.c_float * 3)(*mean)
+    return p
+
+
+def params_for(w):
+    """dn_pyramid_params of a configs.Workload."""
+    return pyramid_params(w.n_scales, w.steps_per_octave, w.base_scale, w.base_longest_side, w.pad,
+                          w.pad_mode, w.plane_h, w.plane_w, w.mean)
+
+
+def net_params(alpha=1e-4, beta=0.75, k=1.0, n=5, lrn_before_pool=True, pool5=False):
+    q = dn_net_params()
+    q.lrn_alpha, q.lrn_beta, q.lrn_k, q.lrn_n = alpha, beta, k, n
+    q.lrn_before_pool, q.pool5 = int(lrn_before_pool), int(pool5)
+    return q
+
+
+# ------------------------------------------------------------------------------------------------
+# Entry points
+# ------------------------------------------------------------------------------------------------
+@dataclass
+class PlanResult:
+    geom: list            # dn_scale_geom per scale
+    planes: list          # dn_plane_desc per plane of one image
+    image_elems: int
+
+    def geom_array(self) -> np.ndarray:
+        """[K][12] int32: k, h, w, plane, y, x, rh, rw, r0, r1, c0, c1."""
+        return np.array([[getattr(g, f) for f in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
+                                                   "r1", "c0", "c1")] for g in self.geom], np.int32)
+
+    def scale_array(self) -> np.ndarray:
+        return np.array([[g.s, g.sy, g.sx] for g in self.geom], np.float64)
+
+
+def densenet_plan_pyramid(H: int, W: int, p: dn_pyramid_params) -> PlanResult:
+    geom = (dn_scale_geom * p.n_scales)()
+    planes = (dn_plane_desc * DN_MAX_PLANES_PER_IMAGE)()
+    n = ctypes.c_int32()
+    e = ctypes.c_int64()
+    check(lib().densenet_plan_pyramid(H, W, ctypes.byref(p), geom, planes, DN_MAX_PLANES_PER_IMAGE,
+                                      ctypes.byref(n), ctypes.byref(e)))
+    return PlanResult(list(geom), list(planes[:n.value]), e.value)
+
+
+def densenet_build_pyramid(images, p: dn_pyramid_params, dtype: int, out=None):
+    """images: uint8 device tensor [n][3][H][W] (or [3][H][W]).  Returns (planes tensor, PlanResult)."""
+    torch = _torch()
+    if images.dim() == 3:
+        images = images[None]
+    n_img, _, H, W = images.shape
+    geom = (dn_scale_geom * p.n_scales)()
+    planes = (dn_plane_desc * DN_MAX_PLANES_PER_IMAGE)()
+    n = ctypes.c_int32()
+    e = ctypes.c_int64()
+    need = ctypes.c_size_t()
+    L = lib()
+    check(L.densenet_build_pyramid(None, n_img, H, W, ctypes.byref(p), dtype, None, 0,
+                                   ctypes.byref(need), geom, planes, DN_MAX_PLANES_PER_IMAGE,
+                                   ctypes.byref(n), ctypes.byref(e), None))
+    es = 4 if dtype == DN_F32 else 2
+    if out is None:
+        out = torch.empty(need.value // es, dtype=_tdtype(dtype), device=images.device)
+    check(L.densenet_build_pyramid(_ptr(images), n_img, H, W, ctypes.byref(p), dtype, _ptr(out),
+                                   out.numel() * out.element_size(), ctypes.byref(need), geom, planes,
+                                   DN_MAX_PLANES_PER_IMAGE, ctypes.byref(n), ctypes.byref(e),
+                                   _stream()))
+    return out, PlanResult(list(geom), list(planes[:n.value]), e.value)
+
+
+def densenet_pack_weights(weights, dtype: int):
+    """weights: [(w, b)] conv1..conv5 as fp32 device tensors (OIHW).  Returns the packed blob."""
+    torch = _torch()
+    ws = [w.contiguous().float() for w, _ in weights]
+    bs = [b.contiguous().float() for _, b in weights]
+    wp = (ctypes.c_void_p * 5)(*[w.data_ptr() for w in ws])
+    bp = (ctypes.c_void_p * 5)(*[b.data_ptr() for b in bs])
+    need = ctypes.c_size_t()
+    L = lib()
+    check(L.densenet_pack_weights(wp, bp, dtype, None, 0, ctypes.byref(need), None))
+    blob = torch.empty(need.value, dtype=torch.uint8, device=ws[0].device)
+    check(L.densenet_pack_weights(wp, bp, dtype, _ptr(blob), need.value, ctypes.byref(need),
+                                  _stream()))
+    return blob
+
+
+class ConvFeatures:
+    """Reusable buffers for densenet_conv_features over a fixed plane list."""
+
+    def __init__(self, planes_desc, dtype: int, net: dn_net_params, device="cuda"):
+        torch = _torch()
+        self.n = len(planes_desc)
+        self.pd = (dn_plane_desc * self.n)(*planes_desc)
+        self.dtype, self.net = dtype, net
+        self.c5d = (dn_plane_desc * self.n)()
+        self.p5d = (dn_plane_desc * self.n)()
+        ws, c5, p5 = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+        check(lib().densenet_conv_features(None, self.pd, self.n, dtype, None, ctypes.byref(net), None,
+                                           0, ctypes.byref(ws), None, 0, ctypes.byref(c5), self.c5d,
+                                           None, 0, ctypes.byref(p5), self.p5d, None))
+        es = 4 if dtype == DN_F32 else 2
+        self.workspace = torch.empty(max(ws.value, 1), dtype=torch.uint8, device=device)
+        self.conv5 = torch.empty(c5.value // es, dtype=_tdtype(dtype), device=device)
+        self.pool5 = torch.empty(p5.value // es, dtype=_tdtype(dtype), device=device) if net.pool5 else None
+
+    def __call__(self, planes_tensor, packed):
+        check(lib().densenet_conv_features(
+            _ptr(planes_tensor), self.pd, self.n, self.dtype, _ptr(packed), ctypes.byref(self.net),
+            _ptr(self.workspace), self.workspace.numel(), ctypes.byref(ctypes.c_size_t()),
+            _ptr(self.conv5), self.conv5.numel() * self.conv5.element_size(),
+            ctypes.byref(ctypes.c_size_t()), self.c5d, _ptr(self.pool5),
+            0 if self.pool5 is None else self.pool5.numel() * self.pool5.element_size(),
+            ctypes.byref(ctypes.c_size_t()), self.p5d, _stream()))
+        return self.conv5, self.pool5
+
+    def conv5_maps(self):
+        """Per-plane [Hc][Wc][256] views of the conv5 buffer."""
+        return [self.conv5[d.offset:d.offset + d.h * d.w * 256].view(d.h, d.w, 256) for d in self.c5d]
+
+    def pool5_maps(self):
+        return [self.pool5[d.offset:d.offset + d.h * d.w * 256].view(d.h, d.w, 256) for d in self.p5d]
+
+
+def densenet_conv_features(planes_tensor, planes_desc, dtype: int, packed, net: dn_net_params):
+    cf = ConvFeatures(planes_desc, dtype, net, device=planes_tensor.device)
+    cf(planes_tensor, packed)
+    return cf
+
+
+def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad: int, planes_per_img,
+                            boxes, box_img=None, target=227.0, S=6, want_idx=False):
+    torch = _torch()
+    n = boxes.shape[0]
+    out = torch.empty((n, 256 * S * S), dtype=torch.float32, device=boxes.device)
+    scale = torch.empty(n, dtype=torch.int32, device=boxes.device)
+    idx = torch.empty((n, S, S, 2), dtype=torch.int32, device=boxes.device) if want_idx else None
+    geom = (dn_scale_geom * len(plan.geom))(*plan.geom)
+    cd = (dn_plane_desc * len(conv5_desc))(*conv5_desc)
+    check(lib().densenet_region_windows(_ptr(conv5), cd, len(conv5_desc), dtype, geom, len(plan.geom),
+                                        pad, planes_per_img, _ptr(boxes), _ptr(box_img), n, target, S,
+                                        _ptr(out), _ptr(scale), _ptr(idx), _stream()))
+    return out, scale, idx
+
+
+def densenet_conv_layer(layer: int, x, n: int, H: int, W: int, dtype: int, packed):
+    torch = _torch()
+    hw = layer_sizes(H, W, strict=False) if layer == 1 else None
+    M = (96, 256, 384, 384, 256)[layer - 1]
+    Ho, Wo = (hw[0] if layer == 1 else (H, W))
+    out = torch.empty((n, Ho, Wo, M), dtype=_tdtype(dtype), device=x.device)
+    check(lib().densenet_conv_layer(layer, _ptr(x), n, H, W, dtype, _ptr(packed), _ptr(out), _stream()))
+    return out
+
+
+def _pool_side(v):
+    return (v - 2) // 2 + 1 if v >= 2 else 0
+
+
+def densenet_lrn_pool(x, dtype: int, net: dn_net_params):
+    torch = _torch()
+    n, H, W, C = x.shape
+    out = torch.empty((n, _pool_side(H), _pool_side(W), C), dtype=_tdtype(dtype), device=x.device)
+    check(lib().densenet_lrn_pool(_ptr(x), n, H, W, C, dtype, ctypes.byref(net), _ptr(out), _stream()))
+    return out
+
+
+def densenet_maxpool(x, dtype: int):
+    torch = _torch()
+    n, H, W, C = x.shape
+    out = torch.empty((n, _pool_side(H), _pool_side(W), C), dtype=_tdtype(dtype), device=x.device)
+    check(lib().densenet_maxpool(_ptr(x), n, H, W, C, dtype, _ptr(out), _stream()))
+    return out
+
+
+def layer_sizes(H: int, W: int, strict=True):
+    hw = (ctypes.c_int32 * 16)()
+    st = lib().densenet_layer_sizes(H, W, hw)
+    if strict:
+        check(st)
+    return [(hw[2 * i], hw[2 * i + 1]) for i in range(8)]
+
+
+# ------------------------------------------------------------------------------------------------
+# The paper's interface: pyra = convnet_featpyramid(image)
+# ------------------------------------------------------------------------------------------------
+@dataclass
+class Pyramid:
+    feat: list            # per scale: [rows][cols][256] view of its plane's conv5 map
+    scales: np.ndarray    # [K] scale factors s_k
+    plan: PlanResult
+    planes: object        # the stitched planes tensor
+    conv: ConvFeatures
+    n_img: int
+
+
+def convnet_featpyramid(images, p: dn_pyramid_params, packed, dtype: int, net=None) -> Pyramid:
+    """Image(s) (uint8 device tensor [n][3][H][W]) -> per-scale conv5 maps (views) + geometry."""
+    if images.dim() == 3:
+        images = images[None]
+    net = net or net_params()
+    planes, plan = densenet_build_pyramid(images, p, dtype)
+    n_img = images.shape[0]
+    desc = []
+    for b in range(n_img):
+        for d in plan.planes:
+            q = dn_plane_desc()
+            q.h, q.w, q.offset = d.h, d.w, b * plan.image_elems + d.offset
+            desc.append(q)
+    cf = densenet_conv_features(planes, desc, dtype, packed, net)
+    maps = cf.conv5_maps()
+    feat = []
+    npl = len(plan.planes)
+    for b in range(n_img):
+        for g in plan.geom:
+            feat.append(maps[b * npl + g.plane][g.r0:g.r1 + 1, g.c0:g.c1 + 1])
+    return Pyramid(feat, np.array([g.s for g in plan.geom]), plan, planes, cf, n_img)

@@ -1,0 +1,103 @@
+"""GPU parity, layer by layer and teacher-forced: each HIP layer kernel, called through the C ABI, is
+compared with the oracle on the same (storage-rounded) input, element by element, at sizes that span
+several tiles with ragged tails."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1404_1869_amd import synth
+from tests.parity import assert_layer_close, chw, hwc, round_to
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DTS = {"f32": 0, "f16": 1, "bf16": 2}
+TORCH_DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+W7 = synth.weights(7)
+LAYERS = [(96, 3, 11, 4, 0, 1), (256, 96, 5, 1, 2, 2), (384, 256, 3, 1, 1, 1), (384, 384, 3, 1, 1, 2),
+          (256, 384, 3, 1, 1, 2)]
+
+
+@pytest.fixture(scope="module")
+def D():
+    from paper_1404_1869_amd import densenet
+    assert torch.cuda.is_available()
+    densenet.lib()
+    return densenet
+
+
+_packed = {}
+
+
+def packed(D, dt):
+    if dt not in _packed:
+        ws = [(torch.from_numpy(w).cuda(), torch.from_numpy(b).cuda()) for w, b in W7]
+        _packed[dt] = D.densenet_pack_weights(ws, DTS[dt])
+    return _packed[dt]
+
+
+def oracle_weights(dt):
+    """Weights as the GPU path holds them: rounded to the storage type."""
+    return [(round_to(w, dt), b) for w, b in W7]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 227, 227), (1, 300, 263), (1, 83, 51)])
+def test_conv1(D, dt, shape):
+    n, H, W = shape
+    rng = np.random.default_rng(H * 7 + W)
+    x = round_to(rng.normal(0, 50, (n, 3, H, W)), dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_conv_layer(1, xg, n, H, W, DTS[dt], packed(D, dt)).float().cpu().numpy()
+    w, b = oracle_weights(dt)[0]
+    for i in range(n):
+        ref = oracle.conv2d(x[i], w, b, 4, 0, 1, True)
+        assert out[i].shape == hwc(ref).shape
+        assert_layer_close(chw(out[i]), ref, dt, f"conv1 {shape}[{i}]")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("layer,shape", [(2, (2, 37, 45)), (2, (1, 16, 16)), (3, (2, 21, 35)),
+                                         (4, (1, 33, 17)), (5, (2, 19, 40)), (3, (1, 74, 74))])
+def test_conv_s1(D, dt, layer, shape):
+    n, H, W = shape
+    M, C, R, s, p, G = LAYERS[layer - 1]
+    rng = np.random.default_rng(layer * 1000 + H)
+    x = round_to(np.abs(rng.normal(0, 3, (n, H, W, C))), dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_conv_layer(layer, xg, n, H, W, DTS[dt], packed(D, dt)).float().cpu().numpy()
+    w, b = oracle_weights(dt)[layer - 1]
+    for i in range(n):
+        ref = oracle.conv2d(chw(x[i]), w, b, s, p, G, True)
+        assert_layer_close(chw(out[i]), ref, dt, f"conv{layer} {shape}[{i}]")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("C,shape", [(96, (2, 55, 55)), (256, (1, 27, 26)), (96, (1, 298, 31)),
+                                     (256, (2, 4, 3))])
+@pytest.mark.parametrize("lrn_first", [True, False])
+def test_lrn_pool(D, dt, C, shape, lrn_first):
+    n, H, W = shape
+    rng = np.random.default_rng(C + H + W)
+    x = round_to(np.abs(rng.normal(0, 30, (n, H, W, C))), dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_lrn_pool(xg, DTS[dt], D.net_params(lrn_before_pool=lrn_first)).float().cpu().numpy()
+    for i in range(n):
+        if lrn_first:
+            ref = oracle.maxpool(oracle.lrn(chw(x[i])))
+        else:
+            ref = oracle.lrn(oracle.maxpool(chw(x[i])))
+        assert_layer_close(chw(out[i]), ref, dt, f"lrn_pool {C} {shape}[{i}]")
+        if dt == "f32":
+            # fp32 output of an fp32 computation: well inside the bar
+            assert np.max(np.abs(chw(out[i]) - ref) / np.maximum(np.abs(ref), 1e-3)) < 2e-5
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_maxpool_exact(D, dt):
+    rng = np.random.default_rng(5)
+    x = round_to(rng.normal(0, 1, (3, 13, 14, 256)), dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_maxpool(xg, DTS[dt]).float().cpu().numpy()
+    for i in range(3):
+        np.testing.assert_array_equal(chw(out[i]), oracle.maxpool(chw(x[i])))

@@ -1,0 +1,38 @@
+"""The library's host geometry (written independently of the oracle) equals the oracle's plan bit for
+bit: sizes, factors, planes, rectangles, offsets and conv5 windows (Sec. 3.1)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1404_1869_amd import configs as C
+from paper_1404_1869_amd import densenet as D
+
+CASES = list(C.ALL) + [
+    C.Workload("odd_small", 37, 53, (1,), 6, 3, pad=16, pad_mode=1, plane_h=400, plane_w=480),
+    C.Workload("upsampled", 300, 200, (1,), 12, 5, base_scale=2.0, pad=16, pad_mode=1, plane_h=2000,
+               plane_w=2000),
+    C.Workload("tiny", 1, 1, (1,), 1, 1, pad=16),
+    C.Workload("wide", 64, 1000, (1,), 9, 3, pad=8, plane_h=600, plane_w=1200),
+    C.Workload("many_small", 120, 160, (1,), 40, 10, pad=16, pad_mode=1, plane_h=480, plane_w=480),
+]
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_plan_bit_exact_vs_oracle(w):
+    lib = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w))
+    ref = oracle.plan(w.H, w.W, w.n_scales, w.steps_per_octave, w.base_scale, w.base_longest_side,
+                      w.pad, w.plane_h, w.plane_w)
+    assert len(lib.planes) == ref.n_planes
+    np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, :12])
+    np.testing.assert_array_equal(lib.scale_array(), ref.gd)   # bitwise equal fp64
+    assert [(p.h, p.w) for p in lib.planes] == ref.plane_sizes
+    off = np.cumsum([0] + [3 * h * w for h, w in ref.plane_sizes])
+    assert [p.offset for p in lib.planes] == list(off[:-1])
+    assert lib.image_elems == off[-1]
+
+
+def test_plan_is_deterministic():
+    w = C.XGA_25SCALE
+    a = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w)).geom_array()
+    b = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w)).geom_array()
+    np.testing.assert_array_equal(a, b)
