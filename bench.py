@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Throughput of the DenseNet conv5 descriptor-pyramid path on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic input already resident in HBM:
+fused pyramid build (resize, centring, padding, stitching) -> conv1..conv5 with ReLU, LRN and pooling
+on every stitched plane -> per-scale conv5 windows -> region windows for 2000 boxes per image.
+The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
+1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
+
+Prints one JSON line: throughput in 25-scale pyramids/s, the roofline of the dominant kernel (its
+average duration measured live with events on its own stream during the timed steps), the conv
+MFMA utilisation, and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "25-scale conv5 pyramids/sec on 1 GPU + conv MFMA util % of peak"
+PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+CONV_NAMES = ("conv1", "conv2", "conv3", "conv4", "conv5")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=("batch16", "single"), default="batch16",
+                    help="batch16: 16 images, bf16 (default); single: one image, fp16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-planes", type=int, default=2,
+                    help="planes of image 0 the oracle's conv stack runs on for the CPU baseline")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after the timed steps, run one plain device copy of this many MiB "
+                         "(a known-size reference for hardware byte counters)")
+    ap.add_argument("--kernels", action="store_true", help="also print the per-kernel breakdown")
+    return ap.parse_args()
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1404_1869_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str, digest: str):
+    """Per-launch HBM bytes of `kernel` from the committed counter summary, if taken on this source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_digest") != digest:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build runs the whole path on a single MI355X and has "
+              "no multi-GPU mode (--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1404_1869_amd import configs as C
+    from paper_1404_1869_amd import densenet as D
+    from paper_1404_1869_amd import synth, workmodel
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = C.XGA_25SCALE_B16 if args.workload == "batch16" else C.XGA_25SCALE
+    dtn = w.dtypes[0]
+    dt = D.DTYPES[dtn]
+    n_img = w.n_img
+    boxes_per_img = 2000
+
+    # ---- inputs resident in HBM before the timed region
+    imgs = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).to(dev)
+    weights = [(torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev)) for a, b in synth.weights(7)]
+    packed = D.densenet_pack_weights(weights, dt)
+    boxes = torch.from_numpy(np.concatenate([synth.boxes(105 + b, boxes_per_img, w.H, w.W)
+                                             for b in range(n_img)])).to(dev)
+    box_img = torch.arange(n_img, dtype=torch.int32, device=dev).repeat_interleave(boxes_per_img)
+    params = D.params_for(w)
+    planes, plan = D.densenet_build_pyramid(imgs, params, dt)
+    ppi = len(plan.planes)
+    desc = []
+    for b in range(n_img):
+        for d in plan.planes:
+            q = D.dn_plane_desc()
+            q.h, q.w, q.offset = d.h, d.w, b * plan.image_elems + d.offset
+            desc.append(q)
+    net = D.net_params(pool5=False)
+    cf = D.ConvFeatures(desc, dt, net, device=dev)
+    c5d = list(cf.c5d)
+    n_boxes = boxes.shape[0]
+    out_desc = torch.empty((n_boxes, 256 * 36), dtype=torch.float32, device=dev)
+    out_scale = torch.empty(n_boxes, dtype=torch.int32, device=dev)
+
+    def step():
+        D.densenet_build_pyramid(imgs, params, dt, out=planes)
+        cf(planes, packed)
+        D.densenet_region_windows(cf.conv5, c5d, dt, plan, w.pad, ppi, boxes, box_img, out=out_desc,
+                                  scale=out_scale)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- per-kernel breakdown (untimed pass, every launch traced) picks the dominant kernel
+    D.profile_start()
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    breakdown = D.profile_stop()
+    dominant = max(breakdown, key=lambda k: breakdown[k][1])
+
+    # ---- timed region: K steps, only the dominant kernel bracketed by events on its stream
+    D.profile_start([dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    live = D.profile_stop()
+    elapsed = t1 - t0
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = n_img * args.steps / elapsed
+
+    if args.copy_mib > 0:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    # ---- algorithmic work per launch (whole planes, MFMA padding not counted)
+    n_planes = len(desc)
+    PH, PW = plan.planes[0].h, plan.planes[0].w
+    fl = workmodel.conv_flops(PH, PW)
+    es = 4 if dtn == "f32" else 2
+    sd = workmodel.sides(PH)
+    work = {f"conv{i + 1}": ("mfma", fl[i] * n_planes) for i in range(5)}
+    work["lrn_pool1"] = ("hbm", (sd[0] ** 2 + sd[1] ** 2) * 96 * es * n_planes)
+    work["lrn_pool2"] = ("hbm", (sd[2] ** 2 + sd[3] ** 2) * 256 * es * n_planes)
+    work["build_planes"] = ("hbm", 3 * w.H * w.W * n_img + 3 * PH * PW * es * n_planes)
+    work["region_windows"] = ("hbm", n_boxes * (256 * 36 * 4 + 36 * 4 * 256 * es))
+    kind, units = work[dominant]
+    launches, tot_ms = live[dominant]
+    avg_s = tot_ms / launches / 1e3
+    digest = source_digest()
+    if kind == "mfma":
+        achieved = units / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[dtn],
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[dtn], 4)}
+    else:
+        achieved = units / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dominant
+    roof["avg_launch_ms"] = round(avg_s * 1e3, 4)
+    roof["algorithmic_per_launch"] = units
+    roof["traffic"] = load_traffic(dominant, w.name, digest)
+
+    conv_ms = sum(breakdown[k][1] / breakdown[k][0] for k in CONV_NAMES if k in breakdown)
+    conv_flops = sum(fl) * n_planes
+    conv_util = conv_flops / (conv_ms / 1e3) / 1e12 / PEAK_TFLOPS[dtn]
+
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "pyramids/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtn,
+        "data": "synthetic (seeded uniform uint8 images, N(0,0.01) weights, log-uniform boxes)",
+        "config": {"workload": w.name, "images": n_img, "image": f"{w.H}x{w.W}",
+                   "scales": w.n_scales, "steps_per_octave": w.steps_per_octave,
+                   "plane": f"{PH}x{PW}", "planes": n_planes, "boxes_per_image": boxes_per_img,
+                   "region_window": "6x6x256"},
+        "conv_mfma_util": round(conv_util, 4),
+        "conv_tflops": round(conv_flops / (conv_ms / 1e3) / 1e12, 2),
+        "roofline": roof,
+        "source_digest": digest,
+    }
+    if args.kernels:
+        result["kernels_ms"] = {k: round(v[1] / v[0], 4) for k, v in breakdown.items()}
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(w, n_planes_sample):
+    """The oracle, as it stands, on a bounded sample of the workload: image 0's planes and its 2000
+    region windows in full, its conv stack on `n_planes_sample` of its planes (a plane's cost depends
+    only on its size), extrapolated to one 25-scale pyramid."""
+    import numpy as np
+
+    import oracle
+    from paper_1404_1869_amd import synth
+
+    img = synth.image(w.seeds[0], w.H, w.W)
+    W7 = synth.weights(7)
+    t0 = time.perf_counter()
+    p = oracle.plan(w.H, w.W, w.n_scales, w.steps_per_octave, w.base_scale, w.base_longest_side,
+                    w.pad, w.plane_h, w.plane_w)
+    planes = oracle.build_planes(img, p, w.pad_mode, w.mean)
+    t_build = time.perf_counter() - t0
+    c5 = {}
+    t0 = time.perf_counter()
+    for j in range(n_planes_sample):
+        c5[j] = oracle.net(planes[j].astype(np.float32), W7)
+    t_plane = (time.perf_counter() - t0) / n_planes_sample
+    maps = [c5.get(j, np.zeros((256, oracle.conv5_side(h), oracle.conv5_side(wd)), np.float32))
+            for j, (h, wd) in enumerate(p.plane_sizes)]
+    boxes = synth.boxes(105, 2000, w.H, w.W)
+    t0 = time.perf_counter()
+    oracle.region_windows(maps, p, boxes)
+    t_reg = time.perf_counter() - t0
+    per_pyr = t_build + p.n_planes * t_plane + t_reg
+    return {"value": round(1.0 / per_pyr, 5), "unit": "pyramids/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": (f"image 0 of the workload: planes and 2000 region windows in full, conv stack "
+                       f"on {n_planes_sample} of its {p.n_planes} 1200x1200 planes, extrapolated to "
+                       f"{p.n_planes} planes ({per_pyr:.1f} s per pyramid)")}
+
+
+if __name__ == "__main__":
+    main()

@@ -178,6 +178,20 @@ int densenet_maxpool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t 
  * (8 pairs written to hw[16]).  Returns DN_E_INVALID_ARG when the plane is too small for conv5. */
 int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw);
 
+/* Launch tracing.  While tracing is on, every kernel launch whose name matches `filter` (a
+ * comma-separated list of names; NULL or "" = all) is bracketed by two hipEvents recorded on the
+ * launch's own stream.  densenet_profile_stop() waits for the recorded events, writes per-name
+ * totals (launches, summed elapsed ms) to out[max_entries] (*n_entries = number of names) and turns
+ * tracing off.  Kernel names: build_planes, conv1..conv5, lrn_pool1, lrn_pool2, pool5,
+ * region_windows, pack_weights.  Events come from a pool owned by the library (no device memory). */
+typedef struct {
+  char name[32];
+  int32_t launches;
+  double total_ms;
+} dn_profile_entry;
+int densenet_profile_start(const char* filter);
+int densenet_profile_stop(dn_profile_entry* out, int32_t max_entries, int32_t* n_entries);
+
 /* Thread-local message describing the last error on this thread ("" if none). */
 const char* densenet_last_error(void);
 

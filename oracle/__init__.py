@@ -62,6 +62,8 @@ def lib():
         for name in ("oracle_conv5_side", "oracle_pool_side"):
             getattr(L, name).argtypes = [i32]
             getattr(L, name).restype = i32
+        L.oracle_threads.argtypes = []
+        L.oracle_threads.restype = i32
         L.oracle_conv_side.argtypes = [i32, i32, i32, i32]
         L.oracle_conv_side.restype = i32
         _lib = L
@@ -104,6 +106,11 @@ def plan(H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, pl
     for k in range(K):
         sizes[gi[k, 3]] = (int(gi[k, 12]), int(gi[k, 13]))
     return Plan(gi, gd, n, pad, sizes)
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return lib().oracle_threads()
 
 
 def conv5_side(n: int) -> int:

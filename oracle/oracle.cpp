@@ -26,7 +26,20 @@
 #include <cstring>
 #include <vector>
 
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
 extern "C" {
+
+// Threads the OpenMP loops of this library use.
+int oracle_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
 
 // ------------------------------------------------------------------------------------------------
 // Geometry (Sec. 3.1): scale selection, scale sizes, padded rectangles, Bottom-Left-Fill stitching,

@@ -27,6 +27,13 @@ static int hip_status(int err, const char* what) {
   return fail(DN_E_HIP, os.str());
 }
 
+// One traced launch: the launcher's HIP status mapped to a dn_status naming the step.
+template <typename F>
+static int run_step(const char* name, void* stream, F&& launch) {
+  TraceScope trace(name, stream);
+  return hip_status(launch(), name);
+}
+
 static bool valid_dtype(dn_dtype dt) { return dt == DN_F32 || dt == DN_F16 || dt == DN_BF16; }
 
 // Sizes of the stack for one plane size; false if conv5 would be empty.
@@ -147,6 +154,7 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
       mh = std::max(mh, planes[j].h);
       mw = std::max(mw, planes[j].w);
     }
+    TraceScope trace("build_planes", stream);
     return hip_status(launch_build_planes(d_images, n_img, a, pl, mh, mw, dtype, d_planes, stream),
                       "build_planes launch");
   } catch (...) {
@@ -166,6 +174,7 @@ int densenet_pack_weights(const float* const* d_w, const float* const* d_b, dn_d
     if (!d_w || !d_b) return fail(DN_E_INVALID_ARG, "weight pointer arrays are NULL");
     for (int l = 0; l < 5; ++l)
       if (!d_w[l] || !d_b[l]) return fail(DN_E_INVALID_ARG, "a layer's weight or bias is NULL");
+    TraceScope trace("pack_weights", stream);
     return hip_status(launch_pack_weights(d_w, d_b, dtype, d_packed, stream), "pack launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
@@ -188,6 +197,8 @@ int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, i
     }
     const int64_t in_stride = (int64_t)Cs[layer - 1] * H * W;
     const int64_t out_stride = (int64_t)Ms[layer - 1] * Ho * Wo;
+    static const char* names[5] = {"conv1", "conv2", "conv3", "conv4", "conv5"};
+    TraceScope trace(names[layer - 1], stream);
     return hip_status(launch_conv(layer, d_in, n, H, W, in_stride, dtype, d_packed, d_out,
                                   out_stride, stream),
                       "conv launch");
@@ -206,6 +217,7 @@ int densenet_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t
     if (net->lrn_n <= 0 || net->lrn_n % 2 == 0) return fail(DN_E_INVALID_ARG, "lrn_n must be odd");
     if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
     const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
+    TraceScope trace(C == 96 ? "lrn_pool1" : "lrn_pool2", stream);
     return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, true,
                                       net->lrn_before_pool != 0, net->lrn_alpha, net->lrn_beta,
                                       net->lrn_k, net->lrn_n, d_out, (int64_t)C * Ho * Wo, stream),
@@ -222,6 +234,7 @@ int densenet_maxpool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t 
     if (!d_in || !d_out) return fail(DN_E_INVALID_ARG, "null device pointer");
     if (n <= 0 || H < 2 || W < 2 || C <= 0) return fail(DN_E_INVALID_ARG, "bad sizes");
     const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
+    TraceScope trace("pool5", stream);
     return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, false, false, 0,
                                       0, 1, 1, d_out, (int64_t)C * Ho * Wo, stream),
                       "maxpool launch");
@@ -303,42 +316,49 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       const int64_t s3 = 384 * s.h[4] * s.w[4], s4 = 384 * s.h[5] * s.w[5];
       const int64_t s5 = 256 * s.h[6] * s.w[6], q5 = 256 * s.h[7] * s.w[7];
       char* c5 = (char*)d_conv5 + conv5_desc[r.first].offset * es;
+      const int h0 = (int)s.h[0], w0 = (int)s.w[0], h1 = (int)s.h[1], w1 = (int)s.w[1];
+      const int h2 = (int)s.h[2], w2 = (int)s.w[2], h3 = (int)s.h[3], w3 = (int)s.w[3];
+      const int h4 = (int)s.h[4], w4 = (int)s.w[4], h6 = (int)s.h[6], w6 = (int)s.w[6];
+      const float al = net->lrn_alpha, be = net->lrn_beta, kk = net->lrn_k;
+      const int ln = net->lrn_n;
       int st;
-      st = hip_status(launch_conv(1, in, n, (int)H0, (int)W0, sp, dtype, d_packed, A, s1, stream),
-                      "conv1 launch");
-      if (st) return st;
-      st = hip_status(launch_lrn_pool(A, n, (int)s.h[0], (int)s.w[0], 96, s1, dtype, true, lf,
-                                      net->lrn_alpha, net->lrn_beta, net->lrn_k, net->lrn_n, B, p1,
-                                      stream),
-                      "lrn_pool1 launch");
-      if (st) return st;
-      st = hip_status(launch_conv(2, B, n, (int)s.h[1], (int)s.w[1], p1, dtype, d_packed, A, s2,
-                                  stream),
-                      "conv2 launch");
-      if (st) return st;
-      st = hip_status(launch_lrn_pool(A, n, (int)s.h[2], (int)s.w[2], 256, s2, dtype, true, lf,
-                                      net->lrn_alpha, net->lrn_beta, net->lrn_k, net->lrn_n, B, p2,
-                                      stream),
-                      "lrn_pool2 launch");
-      if (st) return st;
-      st = hip_status(launch_conv(3, B, n, (int)s.h[3], (int)s.w[3], p2, dtype, d_packed, A, s3,
-                                  stream),
-                      "conv3 launch");
-      if (st) return st;
-      st = hip_status(launch_conv(4, A, n, (int)s.h[4], (int)s.w[4], s3, dtype, d_packed, B, s4,
-                                  stream),
-                      "conv4 launch");
-      if (st) return st;
-      st = hip_status(launch_conv(5, B, n, (int)s.h[5], (int)s.w[5], s4, dtype, d_packed, c5, s5,
-                                  stream),
-                      "conv5 launch");
-      if (st) return st;
+      if ((st = run_step("conv1", stream, [&] {
+             return launch_conv(1, in, n, (int)H0, (int)W0, sp, dtype, d_packed, A, s1, stream);
+           })))
+        return st;
+      if ((st = run_step("lrn_pool1", stream, [&] {
+             return launch_lrn_pool(A, n, h0, w0, 96, s1, dtype, true, lf, al, be, kk, ln, B, p1,
+                                    stream);
+           })))
+        return st;
+      if ((st = run_step("conv2", stream, [&] {
+             return launch_conv(2, B, n, h1, w1, p1, dtype, d_packed, A, s2, stream);
+           })))
+        return st;
+      if ((st = run_step("lrn_pool2", stream, [&] {
+             return launch_lrn_pool(A, n, h2, w2, 256, s2, dtype, true, lf, al, be, kk, ln, B, p2,
+                                    stream);
+           })))
+        return st;
+      if ((st = run_step("conv3", stream, [&] {
+             return launch_conv(3, B, n, h3, w3, p2, dtype, d_packed, A, s3, stream);
+           })))
+        return st;
+      if ((st = run_step("conv4", stream, [&] {
+             return launch_conv(4, A, n, h4, w4, s3, dtype, d_packed, B, s4, stream);
+           })))
+        return st;
+      if ((st = run_step("conv5", stream, [&] {
+             return launch_conv(5, B, n, h4, w4, s4, dtype, d_packed, c5, s5, stream);
+           })))
+        return st;
       if (net->pool5) {
         char* p5 = (char*)d_pool5 + pool5_desc[r.first].offset * es;
-        st = hip_status(launch_lrn_pool(c5, n, (int)s.h[6], (int)s.w[6], 256, s5, dtype, false, false,
-                                        0, 0, 1, 1, p5, q5, stream),
-                        "pool5 launch");
-        if (st) return st;
+        if ((st = run_step("pool5", stream, [&] {
+               return launch_lrn_pool(c5, n, h6, w6, 256, s5, dtype, false, false, 0, 0, 1, 1, p5,
+                                      q5, stream);
+             })))
+          return st;
       }
     }
     return DN_OK;
@@ -398,6 +418,7 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
       a.s[k] = RegScale{g.plane, g.y, g.x, g.r0, g.r1, g.c0, g.c1, empty ? 1 : 0, g.sy, g.sx};
     }
     const char* base = (const char*)d_conv5 + conv5_desc[0].offset * dtype_size(conv5_dtype);
+    TraceScope trace("region_windows", stream);
     return hip_status(launch_region_windows(base, conv5_dtype, a, d_boxes, d_box_img, n, d_out,
                                             d_scale, d_idx, stream),
                       "region_windows launch");

@@ -101,6 +101,19 @@ int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, co
 
 inline size_t dtype_size(dn_dtype dt) { return dt == DN_F32 ? 4 : 2; }
 
+// Brackets one kernel launch with trace events when tracing is on and the name is selected.
+class TraceScope {
+ public:
+  TraceScope(const char* name, void* stream);
+  ~TraceScope();
+  TraceScope(const TraceScope&) = delete;
+  TraceScope& operator=(const TraceScope&) = delete;
+
+ private:
+  int idx_;
+  void* stream_;
+};
+
 }  // namespace dn
 
 #if defined(__HIPCC__)

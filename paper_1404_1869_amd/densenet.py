@@ -26,7 +26,8 @@ DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
            "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
-           "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_last_error")
+           "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_profile_start",
+           "densenet_profile_stop", "densenet_last_error")
 
 
 class dn_pyramid_params(ctypes.Structure):
@@ -50,6 +51,10 @@ class dn_net_params(ctypes.Structure):
     _fields_ = [("lrn_alpha", ctypes.c_float), ("lrn_beta", ctypes.c_float),
                 ("lrn_k", ctypes.c_float), ("lrn_n", ctypes.c_int32),
                 ("lrn_before_pool", ctypes.c_int32), ("pool5", ctypes.c_int32)]
+
+
+class dn_profile_entry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
 class DenseNetError(RuntimeError):
@@ -84,6 +89,8 @@ def lib():
             "densenet_lrn_pool": [P, i32, i32, i32, i32, i32, pn, P, P],
             "densenet_maxpool": [P, i32, i32, i32, i32, i32, P, P],
             "densenet_layer_sizes": [i32, i32, pi32],
+            "densenet_profile_start": [ctypes.c_char_p],
+            "densenet_profile_stop": [ctypes.POINTER(dn_profile_entry), i32, pi32],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -265,11 +272,14 @@ def densenet_conv_features(planes_tensor, planes_desc, dtype: int, packed, net: 
 
 
 def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad: int, planes_per_img,
-                            boxes, box_img=None, target=227.0, S=6, want_idx=False):
+                            boxes, box_img=None, target=227.0, S=6, want_idx=False, out=None,
+                            scale=None):
     torch = _torch()
     n = boxes.shape[0]
-    out = torch.empty((n, 256 * S * S), dtype=torch.float32, device=boxes.device)
-    scale = torch.empty(n, dtype=torch.int32, device=boxes.device)
+    if out is None:
+        out = torch.empty((n, 256 * S * S), dtype=torch.float32, device=boxes.device)
+    if scale is None:
+        scale = torch.empty(n, dtype=torch.int32, device=boxes.device)
     idx = torch.empty((n, S, S, 2), dtype=torch.int32, device=boxes.device) if want_idx else None
     geom = (dn_scale_geom * len(plan.geom))(*plan.geom)
     cd = (dn_plane_desc * len(conv5_desc))(*conv5_desc)
@@ -315,6 +325,19 @@ def layer_sizes(H: int, W: int, strict=True):
     if strict:
         check(st)
     return [(hw[2 * i], hw[2 * i + 1]) for i in range(8)]
+
+
+def profile_start(names=None):
+    """Trace launches (all, or those named in `names`) with events on their own streams."""
+    check(lib().densenet_profile_start(",".join(names).encode() if names else None))
+
+
+def profile_stop():
+    """Stop tracing; returns {name: (launches, total_ms)} (waits for the traced launches)."""
+    out = (dn_profile_entry * 64)()
+    n = ctypes.c_int32()
+    check(lib().densenet_profile_stop(out, 64, ctypes.byref(n)))
+    return {out[i].name.decode(): (out[i].launches, out[i].total_ms) for i in range(min(n.value, 64))}
 
 
 # ------------------------------------------------------------------------------------------------
