@@ -98,7 +98,7 @@ typedef struct {
 /* Network options (Sec. 3: conv1..conv5 of the AlexNet topology, with ReLU, cross-channel LRN and
  * 3x3/2 max-pooling after conv1 and conv2).  LRN: b_c = a_c (k + alpha/n sum_{|j-c|<=n/2} a_j^2)^-beta
  * over all channels of the layer; pooling uses ceil-mode sizes with windows clipped to the input.
- * lrn_before_pool = 1 applies LRN then pool, 0 pool then LRN.  pool5 = 1 also emits 3x3/2 max-pooled
+ * lrn_n must be odd and at most 9.  lrn_before_pool = 1 applies LRN then pool, 0 pool then LRN.  pool5 = 1 also emits 3x3/2 max-pooled
  * conv5 maps. */
 typedef struct {
   float lrn_alpha, lrn_beta, lrn_k;
@@ -108,6 +108,7 @@ typedef struct {
 } dn_net_params;
 
 /* Geometry only (host, no device work): scales, sizes, stitching and conv5 windows for an H x W image.
+ * Image sides are limited to 32768 px and scaled sides to 65535 px (DN_E_TOO_LARGE beyond).
  * geom: [n_scales] out.  planes: [max_planes] out, the planes of ONE image, offsets in elements of the
  * packed [3][PH][PW] planes; *image_elems = elements per image.  Returns DN_E_TOO_LARGE when a padded
  * scale exceeds the stitching plane or the plane count exceeds max_planes. */
@@ -151,7 +152,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
  * samples at the bin centres of the box are read from that scale's conv5 window (coordinates clamped
  * to the window), all 256 channels: d_out[n][256 * S * S] fp32, flattened (channel, row, column).
  * conv5_desc: [n_img * planes_per_img] maps from densenet_conv_features (image b's plane j at index
- * b * planes_per_img + j).  d_box_img: nullable [n] image index per box (NULL => image 0).
+ * b * planes_per_img + j), channels-last with 256 channels, offsets multiples of 16 bytes.  d_box_img: nullable [n] image index per box (NULL => image 0).
  * d_scale: [n] chosen scale, -1 for a box with a non-finite or non-positive side (its row is 0).
  * d_idx: nullable [n][S][S][2] int32 (i0, j0) conv5 cell of each sample's top-left neighbour.
  * Index arithmetic is fp64 with + - * / only, so scales and indices are reproducible bit for bit. */

@@ -214,7 +214,8 @@ int densenet_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t
     if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
     if (!d_in || !d_out) return fail(DN_E_INVALID_ARG, "null device pointer");
     if (n <= 0 || H < 2 || W < 2 || C <= 0) return fail(DN_E_INVALID_ARG, "bad sizes");
-    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0) return fail(DN_E_INVALID_ARG, "lrn_n must be odd");
+    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0 || net->lrn_n > 9)
+      return fail(DN_E_INVALID_ARG, "lrn_n must be odd and at most 9");
     if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
     const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
     TraceScope trace(C == 96 ? "lrn_pool1" : "lrn_pool2", stream);
@@ -254,7 +255,8 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       return fail(DN_E_INVALID_ARG, "null pointer argument");
     if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
     if (n_planes <= 0) return fail(DN_E_INVALID_ARG, "n_planes must be positive");
-    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0) return fail(DN_E_INVALID_ARG, "lrn_n must be odd");
+    if (net->lrn_n <= 0 || net->lrn_n % 2 == 0 || net->lrn_n > 9)
+      return fail(DN_E_INVALID_ARG, "lrn_n must be odd and at most 9");
     if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
     if (net->pool5 && (!pool5_needed || !pool5_desc))
       return fail(DN_E_INVALID_ARG, "pool5 requested without pool5_needed / pool5_desc");
@@ -391,6 +393,10 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
     a.S = S;
     a.C = 256;
     a.target = (double)target;
+    const int64_t vec = 16 / (int64_t)dtype_size(conv5_dtype);
+    for (int32_t i = 0; i < n_maps; ++i)
+      if (conv5_desc[i].offset < 0 || conv5_desc[i].offset % vec)
+        return fail(DN_E_INVALID_ARG, "conv5 map offsets must be multiples of 16 bytes");
     for (int32_t j = 0; j < planes_per_img; ++j) {
       a.map_off[j] = conv5_desc[j].offset - conv5_desc[0].offset;
       a.map_w[j] = conv5_desc[j].w;

@@ -193,17 +193,27 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
 // ------------------------------------------------------------------------------------------------
 // Stride-1 R x R conv with zero padding (R-1)/2, grouped, channels-last.
 // Workgroup: TH x TW = 16 x 16 output pixels x BM output channels of one group.  Waves: BM/64 along
-// channels x 2 along pixels; each wave owns 64 channels x 128 pixels (2 x 4 MFMA tiles).
-// LDS: input halo (TH+R-1) x (TW+R-1) x 16 channels, and the weights of one kernel row
-// (R taps x BM channels x 16 input channels).
+// channels x 2 along pixels; each wave owns 64 channels x 128 pixels (2 x 4 MFMA tiles).  The MFMA
+// A operand is the weights and B the pixels, so each lane's accumulator holds 4 consecutive output
+// channels of one pixel per register group and the epilogue stores 4 channels at a time.
+// Pipeline: a stage is (chunk of 16 input channels, kernel row ky).  LDS holds two halo buffers
+// ((TH+R-1) x (TW+R-1) x 16 channels, one per chunk) and two weight-row buffers (R taps x BM x 16).
+// While a stage computes from LDS, the next stage's weight row (and, during a chunk's first row, the
+// next chunk's halo) is already in flight into registers; it is written to the other buffers after
+// the stage's MFMAs, and one barrier per stage publishes it.
 // ------------------------------------------------------------------------------------------------
 template <typename T, int R, int BM>
 struct ConvCfg {
   static constexpr int TH = 16, TW = 16, CC = 16;
   static constexpr int HH = TH + R - 1, HW = TW + R - 1;
-  static constexpr int CS = CC + (std::is_same<T, float>::value ? 1 : 8);  // LDS stride (elements)
+  static constexpr bool F32 = std::is_same<T, float>::value;
+  static constexpr int CS = CC + (F32 ? 1 : 8);  // LDS stride of one pixel / channel row (elements)
   static constexpr int WM = BM / 64, WN = (TH * TW) / 128;
   static constexpr int NT = 64 * WM * WN;
+  static constexpr int VEC = 16 / sizeof(T);  // elements per 16-byte global load
+  static constexpr int VPP = CC / VEC;
+  static constexpr int HALO_V = HH * HW * VPP, HALO_PER = (HALO_V + NT - 1) / NT;
+  static constexpr int W_V = R * BM * VPP, W_PER = (W_V + NT - 1) / NT;
   static_assert(NT == 2 * BM, "launch bounds assume two pixel waves per 64 channels");
 };
 
@@ -215,12 +225,11 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
   using Cf = ConvCfg<T, R, BM>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
-  constexpr bool F32 = std::is_same<T, float>::value;
-  constexpr int VEC = 16 / sizeof(T);
-  constexpr int VPP = Cf::CC / VEC;
+  constexpr int VEC = Cf::VEC, VPP = Cf::VPP, CS = Cf::CS, NT = Cf::NT;
   typedef T vec_t __attribute__((ext_vector_type(VEC)));
-  __shared__ T s_in[Cf::HH * Cf::HW * Cf::CS];
-  __shared__ T s_w[R * BM * Cf::CS];
+  typedef T out4_t __attribute__((ext_vector_type(4)));
+  __shared__ __align__(16) T s_in[2][Cf::HH * Cf::HW * CS];
+  __shared__ __align__(16) T s_w[2][R * BM * CS];
 
   int bid = blockIdx.x;
   const int tx = bid % tiles_x;
@@ -232,18 +241,18 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
   const int mpg = Mg / BM;
   const int g = mb / mpg, m0 = (mb % mpg) * BM;
   const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
-  const T* src = in + plane * in_stride;
+  const T* src = in + plane * in_stride + g * Cg;
   const T* wg = wp + ((int64_t)g * Mg + m0) * R * R * Cg;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave % Cf::WM, wn = wave / Cf::WM;
   const int half = lane >> 5, l32 = lane & 31;
-  int prow[4], pcol[4];
+  int pix[4];  // LDS pixel index (row * HW + col) of this lane's pixel in each pixel tile
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int idx = wn * 128 + t * 32 + l32;
-    prow[t] = idx / Cf::TW;
-    pcol[t] = idx % Cf::TW;
+    pix[t] = (idx / Cf::TW) * Cf::HW + idx % Cf::TW;
   }
   f32x16 acc[2][4];
 #pragma unroll
@@ -251,73 +260,125 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[a][t] = f32x16{};
 
-  for (int c0 = 0; c0 < Cg; c0 += Cf::CC) {
-    __syncthreads();
-    for (int e = threadIdx.x; e < Cf::HH * Cf::HW * VPP; e += Cf::NT) {
-      const int v = e % VPP, p = e / VPP;
-      const int hy = p / Cf::HW, hx = p % Cf::HW;
-      const int iy = oy0 - pad + hy, ix = ox0 - pad + hx;
-      vec_t val = vec_t{};
-      if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-        val = *(const vec_t*)(src + ((int64_t)iy * W + ix) * C + g * Cg + c0 + v * VEC);
-      if constexpr (F32) {
+  vec_t hreg[Cf::HALO_PER], wreg[Cf::W_PER];
+  auto load_halo = [&](int c0) {
 #pragma unroll
-        for (int q = 0; q < VEC; ++q) s_in[p * Cf::CS + v * VEC + q] = val[q];
-      } else {
-        *(vec_t*)(s_in + p * Cf::CS + v * VEC) = val;
+    for (int i = 0; i < Cf::HALO_PER; ++i) {
+      const int e = tid + i * NT;
+      vec_t val = vec_t{};
+      if (e < Cf::HALO_V) {
+        const int v = e % VPP, p = e / VPP;
+        const int iy = oy0 - pad + p / Cf::HW, ix = ox0 - pad + p % Cf::HW;
+        if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+          val = *(const vec_t*)(src + ((int64_t)iy * W + ix) * C + c0 + v * VEC);
+      }
+      hreg[i] = val;
+    }
+  };
+  auto store_halo = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < Cf::HALO_PER; ++i) {
+      const int e = tid + i * NT;
+      if (e < Cf::HALO_V) {
+        T* d = &s_in[buf][(e / VPP) * CS + (e % VPP) * VEC];
+        if constexpr (Cf::F32) {
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) d[q] = hreg[i][q];
+        } else {
+          *(vec_t*)d = hreg[i];
+        }
       }
     }
-    for (int ky = 0; ky < R; ++ky) {
-      if (ky) __syncthreads();
-      for (int e = threadIdx.x; e < R * BM * VPP; e += Cf::NT) {
+  };
+  auto load_w = [&](int c0, int ky) {
+#pragma unroll
+    for (int i = 0; i < Cf::W_PER; ++i) {
+      const int e = tid + i * NT;
+      vec_t val = vec_t{};
+      if (e < Cf::W_V) {
         const int v = e % VPP, t = e / VPP;
         const int m = t % BM, kx = t / BM;
-        const vec_t val = *(const vec_t*)(wg + ((int64_t)m * R * R + ky * R + kx) * Cg + c0 + v * VEC);
-        if constexpr (F32) {
-#pragma unroll
-          for (int q = 0; q < VEC; ++q) s_w[(kx * BM + m) * Cf::CS + v * VEC + q] = val[q];
-        } else {
-          *(vec_t*)(s_w + (kx * BM + m) * Cf::CS + v * VEC) = val;
-        }
+        val = *(const vec_t*)(wg + ((int64_t)m * R * R + ky * R + kx) * Cg + c0 + v * VEC);
       }
-      __syncthreads();
+      wreg[i] = val;
+    }
+  };
+  auto store_w = [&](int buf) {
 #pragma unroll
-      for (int kx = 0; kx < R; ++kx) {
+    for (int i = 0; i < Cf::W_PER; ++i) {
+      const int e = tid + i * NT;
+      if (e < Cf::W_V) {
+        const int v = e % VPP, t = e / VPP;
+        const int m = t % BM, kx = t / BM;
+        T* d = &s_w[buf][(kx * BM + m) * CS + v * VEC];
+        if constexpr (Cf::F32) {
 #pragma unroll
-        for (int kk = 0; kk < Cf::CC / Op::KS; ++kk) {
-          const int koff = kk * Op::KS + half * Op::KPL;
-          typename Op::frag a[4], b[2];
-#pragma unroll
-          for (int t = 0; t < 4; ++t)
-            a[t] = lds_frag16<T>(s_in + ((prow[t] + ky) * Cf::HW + pcol[t] + kx) * Cf::CS + koff);
-#pragma unroll
-          for (int mt = 0; mt < 2; ++mt)
-            b[mt] = lds_frag16<T>(s_w + (kx * BM + wm * 64 + mt * 32 + l32) * Cf::CS + koff);
-#pragma unroll
-          for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) acc[mt][t] = Op::mma(a[t], b[mt], acc[mt][t]);
+          for (int q = 0; q < VEC; ++q) d[q] = wreg[i][q];
+        } else {
+          *(vec_t*)d = wreg[i];
         }
       }
     }
+  };
+  auto compute = [&](int hb, int wb, int ky) {
+    const T* hs = s_in[hb];
+    const T* ws = s_w[wb];
+#pragma unroll
+    for (int kx = 0; kx < R; ++kx) {
+#pragma unroll
+      for (int kk = 0; kk < Cf::CC / Op::KS; ++kk) {
+        const int koff = kk * Op::KS + half * Op::KPL;
+        typename Op::frag x[4], w[2];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) x[t] = lds_frag16<T>(hs + (pix[t] + ky * Cf::HW + kx) * CS + koff);
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          w[mt] = lds_frag16<T>(ws + (kx * BM + wm * 64 + mt * 32 + l32) * CS + koff);
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
+      }
+    }
+  };
+
+  const int nchunks = Cg / Cf::CC, nst = nchunks * R;
+  load_halo(0);
+  load_w(0, 0);
+  store_halo(0);
+  store_w(0);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int chunk = st / R, ky = st - chunk * R;
+    const bool more = st + 1 < nst, next_chunk = chunk + 1 < nchunks;
+    if (more) load_w(((st + 1) / R) * Cf::CC, (st + 1) % R);
+    if (ky == 0 && next_chunk) load_halo((chunk + 1) * Cf::CC);
+    compute(chunk & 1, st & 1, ky);
+    if (more) store_w((st + 1) & 1);
+    if (ky == R - 1 && next_chunk) store_halo((chunk + 1) & 1);
+    __syncthreads();
   }
 
+  // Epilogue: D[m][pixel]; register group q holds channels 8 q + 4 half + 0..3 of pixel l32.
   T* dst = out + plane * out_stride;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-    const int m = g * Mg + m0 + wm * 64 + mt * 32 + l32;
-    const float bv = bias[m];
+  for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int q = 0; q < 4; ++q) {
+      const int m = g * Mg + m0 + wm * 64 + mt * 32 + 8 * q + 4 * half;
+      const f32x4 bv = *(const f32x4*)(bias + m);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = 8 * (r >> 2) + 4 * half + (r & 3);
-        const int idx = wn * 128 + t * 32 + i;
+      for (int t = 0; t < 4; ++t) {
+        const int idx = wn * 128 + t * 32 + l32;
         const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
-        if (oy < H && ox < W)
-          dst[((int64_t)oy * W + ox) * M + m] = from_f32<T>(fmaxf(acc[mt][t][r] + bv, 0.f));
+        if (oy < H && ox < W) {
+          out4_t r;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+          *(out4_t*)(dst + ((int64_t)oy * W + ox) * M + m) = r;
+        }
       }
-  }
+    }
 }
 
 template <typename T, int R, int BM>

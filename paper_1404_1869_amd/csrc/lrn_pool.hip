@@ -1,12 +1,22 @@
 // Cross-channel LRN and 3x3 / stride-2 max-pooling with ceil-mode output size and clipped windows,
 // on channels-last maps (the normalisation and pooling that follow conv1 and conv2 of the AlexNet
-// topology, and the optional pool after conv5).
+// topology, and the optional pool after conv5).  Bandwidth-bound: every input element should cross
+// HBM once and every output once.
 //
-// One thread per output element, channels fastest, so a wave reads and writes 64 consecutive
-// channels of one pixel.  LRN of the pooling window's pixels is recomputed per output: inputs come
-// from L1/L2 (each is reused by neighbouring windows and channels), and HBM sees each input once.
-// (k + alpha/n * s)^-beta is evaluated as exp2(-beta * log2(.)) with the hardware transcendental
-// units; the argument is >= k > 0.
+// Tiled kernel (LRN then pool, or pool only): a workgroup owns TPH x TPW pooled outputs and all C
+// channels.  Phase 1 reads the (2 TPH + 1) x (2 TPW + 1) input pixels of its windows with 16-byte
+// channel vectors, computes the LRN of each input element once (the channel window is taken from
+// the neighbouring vectors, zero beyond the channel range, which equals clipping the window), and
+// stores the results in LDS in the storage type.  Phase 2 takes the max over each clipped window
+// from LDS and writes 16-byte vectors.  Rounding to the storage type before the max gives the same
+// result as after it, since rounding is monotone.
+//
+// (k + alpha/n * s)^-beta is evaluated as exp2(-beta * log2(.)) on the hardware transcendental units;
+// the argument is >= k > 0.
+//
+// The pool-then-LRN order uses a simple kernel with one thread per output element.
+#include <type_traits>
+
 #include "common.h"
 
 namespace dn {
@@ -16,8 +26,110 @@ __device__ inline float lrn_scale(float s, float alpha_n, float beta, float k) {
   return __builtin_amdgcn_exp2f(-beta * __builtin_amdgcn_logf(k + alpha_n * s));
 }
 
-template <typename T, bool LRN, bool LRN_FIRST>
-__global__ __launch_bounds__(256) void lrn_pool_kernel(const T* __restrict__ in, T* __restrict__ out,
+constexpr int VECB = 16;  // bytes per channel vector
+constexpr int MAX_HALF = 8;
+
+template <typename T>
+struct Vec {
+  static constexpr int N = VECB / sizeof(T);
+  typedef T type __attribute__((ext_vector_type(N)));
+};
+
+template <typename T, bool LRN, int HN>
+__global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict__ in,
+                                                            T* __restrict__ out, int H, int W, int C,
+                                                            int Ho, int Wo, int TPH, int TPW,
+                                                            int tiles_x, int tiles_y,
+                                                            int64_t in_stride, int64_t out_stride,
+                                                            float alpha_n, float beta, float k) {
+  constexpr int N = Vec<T>::N;
+  static_assert(HN <= N && HN <= MAX_HALF, "the channel window must fit one neighbouring vector");
+  typedef typename Vec<T>::type vec_t;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* s = (T*)smem;
+  const int CS = C + N;  // LDS pixel stride (elements), keeps 16-byte alignment
+  const int G = C / N;   // channel vectors per pixel
+
+  int bid = blockIdx.x;
+  const int tx = bid % tiles_x;
+  bid /= tiles_x;
+  const int ty = bid % tiles_y;
+  const int plane = bid / tiles_y;
+  const int oy0 = ty * TPH, ox0 = tx * TPW;
+  const int iy0 = 2 * oy0, ix0 = 2 * ox0;
+  const int IH = 2 * TPH + 1, IW = 2 * TPW + 1;
+  const T* src = in + plane * in_stride;
+
+  // Phase 1: LRN of every input element of the tile's windows, into LDS.
+  for (int e = threadIdx.x; e < IH * IW * G; e += blockDim.x) {
+    const int g = e % G, p = e / G;
+    const int hy = p / IW, hx = p % IW;
+    const int y = iy0 + hy, x = ix0 + hx;
+    if (y >= H || x >= W) continue;  // outside the map: never inside a clipped window
+    const T* px = src + ((int64_t)y * W + x) * C;
+    const vec_t v = *(const vec_t*)(px + g * N);
+    vec_t r;
+    if constexpr (LRN) {
+      float f[N + 2 * MAX_HALF];
+#pragma unroll
+      for (int i = 0; i < N + 2 * MAX_HALF; ++i) f[i] = 0.f;
+#pragma unroll
+      for (int i = 0; i < N; ++i) f[MAX_HALF + i] = to_f32(v[i]);
+      if (g > 0) {
+        const vec_t l = *(const vec_t*)(px + (g - 1) * N);
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+          if (i >= N - MAX_HALF) f[MAX_HALF - N + i] = to_f32(l[i]);
+      }
+      if (g + 1 < G) {
+        const vec_t q = *(const vec_t*)(px + (g + 1) * N);
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+          if (i < MAX_HALF) f[MAX_HALF + N + i] = to_f32(q[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        float sq = 0.f;
+#pragma unroll
+        for (int j = -HN; j <= HN; ++j) {
+          const float a = f[MAX_HALF + i + j];
+          sq += a * a;
+        }
+        r[i] = from_f32<T>(f[MAX_HALF + i] * lrn_scale(sq, alpha_n, beta, k));
+      }
+    } else {
+      r = v;
+    }
+    *(vec_t*)(s + p * CS + g * N) = r;
+  }
+  __syncthreads();
+
+  // Phase 2: max over each clipped 3x3 window.
+  for (int e = threadIdx.x; e < TPH * TPW * G; e += blockDim.x) {
+    const int g = e % G, q = e / G;
+    const int qy = q / TPW, qx = q % TPW;
+    const int oy = oy0 + qy, ox = ox0 + qx;
+    if (oy >= Ho || ox >= Wo) continue;
+    const int y1 = min(2 * oy + 3, H) - iy0, x1 = min(2 * ox + 3, W) - ix0;
+    float m[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) m[i] = -INFINITY;
+    for (int hy = 2 * qy; hy < y1; ++hy)
+      for (int hx = 2 * qx; hx < x1; ++hx) {
+        const vec_t v = *(const vec_t*)(s + (hy * IW + hx) * CS + g * N);
+#pragma unroll
+        for (int i = 0; i < N; ++i) m[i] = fmaxf(m[i], to_f32(v[i]));
+      }
+    vec_t r;
+#pragma unroll
+    for (int i = 0; i < N; ++i) r[i] = from_f32<T>(m[i]);
+    *(vec_t*)(out + plane * out_stride + ((int64_t)oy * Wo + ox) * C + g * N) = r;
+  }
+}
+
+// Pool first, then LRN of the pooled vector: one thread per output element.
+template <typename T>
+__global__ __launch_bounds__(256) void pool_lrn_kernel(const T* __restrict__ in, T* __restrict__ out,
                                                        int H, int W, int C, int Ho, int Wo,
                                                        int64_t in_stride, int64_t out_stride,
                                                        int64_t total, float alpha_n, float beta,
@@ -33,33 +145,32 @@ __global__ __launch_bounds__(256) void lrn_pool_kernel(const T* __restrict__ in,
   const T* src = in + plane * in_stride;
   const int y0 = 2 * oy, y1 = min(y0 + 3, H), x0 = 2 * ox, x1 = min(x0 + 3, W);
   const int clo = max(0, c - half_n), chi = min(C - 1, c + half_n);
-  float best = -INFINITY;
-  if (!LRN) {
+  float s = 0.f, mine = 0.f;
+  for (int j = clo; j <= chi; ++j) {
+    float m = -INFINITY;
     for (int y = y0; y < y1; ++y)
-      for (int x = x0; x < x1; ++x) best = fmaxf(best, to_f32(src[((int64_t)y * W + x) * C + c]));
-  } else if (LRN_FIRST) {
-    for (int y = y0; y < y1; ++y)
-      for (int x = x0; x < x1; ++x) {
-        const T* px = src + ((int64_t)y * W + x) * C;
-        float s = 0.f;
-        for (int j = clo; j <= chi; ++j) {
-          const float v = to_f32(px[j]);
-          s += v * v;
-        }
-        best = fmaxf(best, to_f32(px[c]) * lrn_scale(s, alpha_n, beta, k));
-      }
-  } else {
-    float s = 0.f, mine = 0.f;
-    for (int j = clo; j <= chi; ++j) {
-      float m = -INFINITY;
-      for (int y = y0; y < y1; ++y)
-        for (int x = x0; x < x1; ++x) m = fmaxf(m, to_f32(src[((int64_t)y * W + x) * C + j]));
-      s += m * m;
-      if (j == c) mine = m;
-    }
-    best = mine * lrn_scale(s, alpha_n, beta, k);
+      for (int x = x0; x < x1; ++x) m = fmaxf(m, to_f32(src[((int64_t)y * W + x) * C + j]));
+    s += m * m;
+    if (j == c) mine = m;
   }
-  out[plane * out_stride + ((int64_t)oy * Wo + ox) * C + c] = from_f32<T>(best);
+  out[plane * out_stride + ((int64_t)oy * Wo + ox) * C + c] =
+      from_f32<T>(mine * lrn_scale(s, alpha_n, beta, k));
+}
+
+// Output tile so that the LDS tile stays within 64 KB.
+template <typename T>
+void pick_tile(int C, int& TPH, int& TPW) {
+  const size_t es = sizeof(T), cs = (size_t)C + VECB / es;
+  const int cand[][2] = {{8, 8}, {4, 8}, {4, 6}, {4, 4}, {2, 4}, {2, 2}, {1, 2}, {1, 1}};
+  for (auto& c : cand) {
+    const size_t bytes = (size_t)(2 * c[0] + 1) * (2 * c[1] + 1) * cs * es;
+    if (bytes <= 65536) {
+      TPH = c[0];
+      TPW = c[1];
+      return;
+    }
+  }
+  TPH = TPW = 0;
 }
 
 template <typename T>
@@ -67,23 +178,42 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
         bool lrn_first, float alpha, float beta, float k, int32_t lrn_n, void* d_out,
         int64_t out_stride, hipStream_t s) {
   const int Ho = H >= 2 ? (H - 2) / 2 + 1 : 0, Wo = W >= 2 ? (W - 2) / 2 + 1 : 0;
-  const int64_t total = (int64_t)n * Ho * Wo * C;
-  if (total <= 0) return (int)hipErrorInvalidValue;
-  const int64_t blocks = (total + 255) / 256;
-  if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+  if (n <= 0 || Ho <= 0 || Wo <= 0) return (int)hipErrorInvalidValue;
   const float an = alpha / (float)lrn_n;
   const int hn = lrn_n / 2;
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
-  if (!lrn)
-    lrn_pool_kernel<T, false, false><<<(unsigned)blocks, 256, 0, s>>>(
-        in, out, H, W, C, Ho, Wo, in_stride, out_stride, total, an, beta, k, hn);
-  else if (lrn_first)
-    lrn_pool_kernel<T, true, true><<<(unsigned)blocks, 256, 0, s>>>(
-        in, out, H, W, C, Ho, Wo, in_stride, out_stride, total, an, beta, k, hn);
-  else
-    lrn_pool_kernel<T, true, false><<<(unsigned)blocks, 256, 0, s>>>(
-        in, out, H, W, C, Ho, Wo, in_stride, out_stride, total, an, beta, k, hn);
+  if (lrn && !lrn_first) {
+    const int64_t total = (int64_t)n * Ho * Wo * C;
+    const int64_t blocks = (total + 255) / 256;
+    if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    pool_lrn_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, H, W, C, Ho, Wo, in_stride,
+                                                       out_stride, total, an, beta, k, hn);
+    return (int)hipGetLastError();
+  }
+  constexpr int N = Vec<T>::N;
+  if (C % N || hn > 4) return (int)hipErrorInvalidValue;
+  int TPH, TPW;
+  pick_tile<T>(C, TPH, TPW);
+  if (!TPH) return (int)hipErrorInvalidValue;
+  const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
+  const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
+  if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+  const size_t lds = (size_t)(2 * TPH + 1) * (2 * TPW + 1) * (C + N) * sizeof(T);
+#define DN_TILE_ARGS in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k
+  if (!lrn) {
+    lrn_pool_tile_kernel<T, false, 0><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS);
+  } else {
+    switch (hn) {
+      case 0: lrn_pool_tile_kernel<T, true, 0><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS); break;
+      case 1: lrn_pool_tile_kernel<T, true, 1><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS); break;
+      case 2: lrn_pool_tile_kernel<T, true, 2><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS); break;
+      case 3: lrn_pool_tile_kernel<T, true, 3><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS); break;
+      case 4: lrn_pool_tile_kernel<T, true, 4><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS); break;
+      default: return (int)hipErrorInvalidValue;
+    }
+  }
+#undef DN_TILE_ARGS
   return (int)hipGetLastError();
 }
 

@@ -77,6 +77,7 @@ struct Grid {  // occupancy of one plane in 16 x 16 px cells
 
 int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan) {
   if (H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "image sides must be positive");
+  if (H > 32768 || W > 32768) return fail(DN_E_TOO_LARGE, "image sides are limited to 32768");
   if (p.n_scales <= 0 || p.n_scales > DN_MAX_SCALES) {
     std::ostringstream os;
     os << "n_scales must be in 1.." << DN_MAX_SCALES;
@@ -101,7 +102,8 @@ int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan) {
     g.k = k;
     g.s = base * std::pow(2.0, -(double)k / (double)p.steps_per_octave);
     const double fh = std::floor((double)H * g.s + 0.5), fw = std::floor((double)W * g.s + 0.5);
-    if (!(fh < 1e6) || !(fw < 1e6)) return fail(DN_E_TOO_LARGE, "scaled image side exceeds 1e6 px");
+    if (!(fh <= 65535.0) || !(fw <= 65535.0))
+      return fail(DN_E_TOO_LARGE, "scaled image sides are limited to 65535 px");
     g.h = std::max(1, (int)fh);
     g.w = std::max(1, (int)fw);
     g.sy = (double)g.h / (double)H;

@@ -2,11 +2,11 @@
 // pyramid at the scale whose scaled area is closest to target^2, as S x S bilinear samples at the
 // bin centres of the box, all channels.
 //
-// One workgroup per box, one thread per channel.  The scale choice and the sample positions are
+// One workgroup per box; each thread blends one 16-byte vector of channels of one bin at a time.  The scale choice and the sample positions are
 // computed in fp64 with + - * / only and FP contraction off, in the same order as the definition, so
 // the chosen scale and cell indices are reproducible bit for bit on any IEEE fp64 implementation.
 // Samples of one bin read 4 cells x C contiguous channels (coalesced); the descriptor row is staged
-// in LDS and written out contiguously.
+// in LDS and written out with 16-byte stores.
 #include "common.h"
 
 namespace dn {
@@ -22,7 +22,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
                                                              int32_t* __restrict__ scale_out,
                                                              int32_t* __restrict__ idx_out) {
 #pragma clang fp contract(off)
-  extern __shared__ float s_row[];  // C * S * S
+  extern __shared__ __align__(16) float s_row[];  // C * S * S
   __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
   __shared__ float s_ly[MAX_S], s_lx[MAX_S];
   const int r = blockIdx.x;
@@ -91,24 +91,35 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   __syncthreads();
   const T* F = maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
   const int Wc = a.map_w[sc.plane];
-  for (int c = tid; c < C; c += blockDim.x) {
-    for (int u = 0; u < S; ++u) {
-      const int i0 = s_i0[u], i1 = s_i1[u];
-      const float ly = s_ly[u];
-      for (int v = 0; v < S; ++v) {
-        const int j0 = s_j0[v], j1 = s_j1[v];
-        const float lx = s_lx[v];
-        const float v00 = to_f32(F[((int64_t)i0 * Wc + j0) * C + c]);
-        const float v01 = to_f32(F[((int64_t)i0 * Wc + j1) * C + c]);
-        const float v10 = to_f32(F[((int64_t)i1 * Wc + j0) * C + c]);
-        const float v11 = to_f32(F[((int64_t)i1 * Wc + j1) * C + c]);
+  // Each thread blends VT consecutive channels (one 16-byte vector per neighbour cell); C / VT
+  // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.
+  constexpr int VT = 16 / sizeof(T);
+  typedef T vec_t __attribute__((ext_vector_type(VT)));
+  const int per_bin = C / VT, groups = blockDim.x / per_bin;
+  const int lt = tid % per_bin, grp = tid / per_bin;
+  if (grp < groups) {
+    const int c0 = lt * VT;
+    for (int bin = grp; bin < SS; bin += groups) {
+      const int u = bin / S, v = bin - u * S;
+      const int i0 = s_i0[u], i1 = s_i1[u], j0 = s_j0[v], j1 = s_j1[v];
+      const float ly = s_ly[u], lx = s_lx[v];
+      const vec_t a00 = *(const vec_t*)(F + ((int64_t)i0 * Wc + j0) * C + c0);
+      const vec_t a01 = *(const vec_t*)(F + ((int64_t)i0 * Wc + j1) * C + c0);
+      const vec_t a10 = *(const vec_t*)(F + ((int64_t)i1 * Wc + j0) * C + c0);
+      const vec_t a11 = *(const vec_t*)(F + ((int64_t)i1 * Wc + j1) * C + c0);
+#pragma unroll
+      for (int q = 0; q < VT; ++q) {
+        const float v00 = to_f32(a00[q]), v01 = to_f32(a01[q]);
+        const float v10 = to_f32(a10[q]), v11 = to_f32(a11[q]);
         const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
-        s_row[c * SS + u * S + v] = top + ly * (bot - top);
+        s_row[(c0 + q) * SS + bin] = top + ly * (bot - top);
       }
     }
   }
   __syncthreads();
-  for (int e = tid; e < C * SS; e += blockDim.x) dst[e] = s_row[e];
+  const int n4 = (C * SS) / 4;
+  for (int e = tid; e < n4; e += blockDim.x) ((f32x4*)dst)[e] = ((const f32x4*)s_row)[e];
+  for (int e = n4 * 4 + tid; e < C * SS; e += blockDim.x) dst[e] = s_row[e];
   if (tid == 0) scale_out[r] = best;
   if (idx_out)
     for (int e = tid; e < SS; e += blockDim.x) {
