@@ -13,6 +13,7 @@
 //  ky = 11 or kx = 11 carry zero weights (144 k per channel instead of 121).
 //  conv2..conv5 (stride 1, R x R, pad (R-1)/2, groups) read channels-last maps; k = (tap, channel),
 //  each lane's 8 k values are 8 consecutive channels of one pixel (one 16-byte LDS load).
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -188,6 +189,165 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
           dst[((int64_t)oy * Wo + ox) * 96 + m] = from_f32<T>(fmaxf(acc[mt][t][r] + bv, 0.f));
       }
   }
+}
+
+// ------------------------------------------------------------------------------------------------
+// conv1 for 16-bit storage: persistent workgroups (one per CU).  All 96 x 432 packed weights stay in
+// LDS for the whole launch; each workgroup walks output tiles of 16 x 16 pixels, and while it
+// computes one tile the next tile's 3 x 72 x 72 input halo is already loading into registers (16-byte
+// loads of plane rows), to be written to the other LDS halo buffer after the tile's MFMAs.
+// Waves: 4 x (96 channels x 64 pixels); A = weights, B = pixels, so each lane stores 4 consecutive
+// output channels of one pixel per store.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+struct Conv1P {
+  static constexpr int TH = 16, TW = 16, HR = 72, HS = 80;
+  static constexpr int KT = 3 * K1, WS = KT + 8;
+  static constexpr int HV = 3 * HR * (HR / 8);  // 16-byte vectors per halo
+  static constexpr int HPER = (HV + 255) / 256;
+  static constexpr size_t LDS = sizeof(T) * (96 * WS + 2 * 3 * HR * HS);
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void conv1_persistent_kernel(
+    const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
+    const float* __restrict__ bias, int H, int W, int Ho, int Wo, int64_t in_stride,
+    int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
+  using P = Conv1P<T>;
+  using Op = Mfma<T>;
+  typedef T vec8 __attribute__((ext_vector_type(8)));
+  typedef T out4_t __attribute__((ext_vector_type(4)));
+  __shared__ __align__(16) T s_w[96 * P::WS];
+  __shared__ __align__(16) T s_in[2][3 * P::HR * P::HS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  for (int e = tid; e < 96 * (P::KT / 8); e += 256) {
+    const int m = e / (P::KT / 8), v = e % (P::KT / 8);
+    *(vec8*)(s_w + m * P::WS + v * 8) = *(const vec8*)(wp + (int64_t)m * P::KT + v * 8);
+  }
+  int lpix[2];  // LDS offset of this lane's pixel (row 4 * prow, column 4 * pcol) per pixel tile
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int idx = wave * 64 + t * 32 + l32;
+    lpix[t] = 4 * (idx / P::TW) * P::HS + 4 * (idx % P::TW);
+  }
+  const bool vec_ok = (W % 8) == 0;
+  vec8 hreg[P::HPER];
+  auto load_halo = [&](int t) {
+    const int tx = t % tiles_x, r = t / tiles_x, ty = r % tiles_y, plane = r / tiles_y;
+    const T* src = in + plane * in_stride;
+    const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
+#pragma unroll
+    for (int i = 0; i < P::HPER; ++i) {
+      const int e = tid + i * 256;
+      vec8 val = vec8{};
+      if (e < P::HV) {
+        const int c = e / (P::HR * 9), rem = e % (P::HR * 9);
+        const int iy = iy0 + rem / 9, ix = ix0 + 8 * (rem % 9);
+        if (iy < H) {
+          const T* rowp = src + ((int64_t)c * H + iy) * W;
+          if (vec_ok && ix + 8 <= W) {
+            val = *(const vec8*)(rowp + ix);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+              if (ix + q < W) val[q] = rowp[ix + q];
+          }
+        }
+      }
+      hreg[i] = val;
+    }
+  };
+  auto store_halo = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < P::HPER; ++i) {
+      const int e = tid + i * 256;
+      if (e < P::HV) {
+        const int c = e / (P::HR * 9), rem = e % (P::HR * 9);
+        *(vec8*)(s_in[buf] + (c * P::HR + rem / 9) * P::HS + 8 * (rem % 9)) = hreg[i];
+      }
+    }
+  };
+
+  int t = blockIdx.x;
+  if (t < ntiles) {
+    load_halo(t);
+    store_halo(0);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (; t < ntiles; t += gridDim.x) {
+    const int tn = t + gridDim.x;
+    if (tn < ntiles) load_halo(tn);
+    f32x16 acc[3][2];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+    const T* hs = s_in[buf];
+#pragma unroll 1
+    for (int c = 0; c < 3; ++c) {
+#pragma unroll
+      for (int ks = 0; ks < K1 / 16; ++ks) {
+        // k-step ks of channel c: column groups q0 = 4 ks + 2 half and q0 + 1 (q = ky * 3 + kx / 4)
+        const int q0 = 4 * ks + 2 * half, q1 = q0 + 1;
+        const int o0 = (c * P::HR + q0 / 3) * P::HS + 4 * (q0 % 3);
+        const int o1 = (c * P::HR + q1 / 3) * P::HS + 4 * (q1 % 3);
+        typename Op::frag x[2], w[3];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const typename Op::half_frag lo = *(const typename Op::half_frag*)(hs + lpix[b] + o0);
+          const typename Op::half_frag hi = *(const typename Op::half_frag*)(hs + lpix[b] + o1);
+          x[b] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt)
+          w[mt] = *(const typename Op::frag*)(s_w + (mt * 32 + l32) * P::WS + c * K1 + ks * 16 + half * 8);
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(w[mt], x[b], acc[mt][b]);
+      }
+    }
+    if (tn < ntiles) store_halo(buf ^ 1);
+    // epilogue: bias + ReLU, 4 consecutive channels per store
+    const int tx = t % tiles_x, r = t / tiles_x, ty = r % tiles_y, plane = r / tiles_y;
+    T* dst = out + plane * out_stride;
+#pragma unroll
+    for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = mt * 32 + 8 * q + 4 * half;
+        const f32x4 bv = *(const f32x4*)(bias + m);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int idx = wave * 64 + b * 32 + l32;
+          const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
+          if (oy < Ho && ox < Wo) {
+            out4_t v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
+            *(out4_t*)(dst + ((int64_t)oy * Wo + ox) * 96 + m) = v;
+          }
+        }
+      }
+    __syncthreads();
+    buf ^= 1;
+  }
+}
+
+int device_cu_count() {
+  static int n = 0;
+  if (!n) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -408,8 +568,14 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
     const int tiles_x = (Wo + 15) / 16, tiles_y = (Ho + 15) / 16;
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
     if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-    conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
-                                                    out_stride, tiles_x, tiles_y);
+    if constexpr (std::is_same<T, float>::value) {
+      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+                                                      out_stride, tiles_x, tiles_y);
+    } else {
+      const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
+      conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+                                                     out_stride, tiles_x, tiles_y, (int)blocks);
+    }
     return (int)hipGetLastError();
   }
   const int li = layer - 1;
