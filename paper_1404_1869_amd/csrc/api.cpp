@@ -142,9 +142,15 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     a.pad = p->pad;
     a.ramp = p->pad_mode == DN_PAD_RAMP;
     for (int c = 0; c < 3; ++c) a.mean[c] = p->mean[c];
-    for (int k = 0; k < p->n_scales; ++k)
-      a.s[k] = PyrScale{geom[k].plane, geom[k].y, geom[k].x, geom[k].rh, geom[k].rw, geom[k].h,
-                        geom[k].w};
+    int e = 0;
+    for (int j = 0; j < *n_planes; ++j) {
+      a.plane_first[j] = (uint8_t)e;
+      for (int k = 0; k < p->n_scales; ++k)
+        if (geom[k].plane == j)
+          a.s[e++] = PyrScale{geom[k].plane, geom[k].y, geom[k].x, geom[k].rh, geom[k].rw, geom[k].h,
+                              geom[k].w};
+      a.plane_count[j] = (uint8_t)(e - a.plane_first[j]);
+    }
     PyrPlanes pl{};
     pl.n = *n_planes;
     pl.image_elems = *image_elems;

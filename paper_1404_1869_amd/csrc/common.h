@@ -50,7 +50,9 @@ struct PyrArgs {
   int32_t n_scales;
   int32_t H, W, pad, ramp;
   float mean[3];
-  PyrScale s[DN_MAX_SCALES];
+  PyrScale s[DN_MAX_SCALES];                    // grouped by plane
+  uint8_t plane_first[DN_MAX_PLANES_PER_IMAGE];  // first entry of s[] on each plane
+  uint8_t plane_count[DN_MAX_PLANES_PER_IMAGE];  // entries of s[] on each plane
 };
 struct PyrPlane {
   int32_t h, w;

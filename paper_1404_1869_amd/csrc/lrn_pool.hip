@@ -127,6 +127,99 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
   }
 }
 
+// LRN then pool for C = CPT * TPP channels (96 = 96 x 1, 256 = 128 x 2): every thread owns one
+// input pixel's CPT consecutive channels.  It issues all of their 16-byte loads at once (plus one
+// neighbouring vector on each inner side when a pixel is split over two threads), computes the
+// channel-window sums from registers, and stores the LRN result to LDS; then the tile is pooled from
+// LDS as in the generic kernel.
+template <typename T, int CPT, int HN>
+__global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict__ in,
+                                                             T* __restrict__ out, int H, int W,
+                                                             int C, int Ho, int Wo, int TPH, int TPW,
+                                                             int tiles_x, int tiles_y,
+                                                             int64_t in_stride, int64_t out_stride,
+                                                             float alpha_n, float beta, float k) {
+  constexpr int N = Vec<T>::N;
+  constexpr int NV = CPT / N;
+  static_assert(CPT % N == 0 && HN <= N, "channel split must be whole vectors");
+  typedef typename Vec<T>::type vec_t;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* s = (T*)smem;
+  const int CS = C + N;
+  const int TPP = C / CPT;
+
+  int bid = blockIdx.x;
+  const int tx = bid % tiles_x;
+  bid /= tiles_x;
+  const int ty = bid % tiles_y;
+  const int plane = bid / tiles_y;
+  const int oy0 = ty * TPH, ox0 = tx * TPW;
+  const int iy0 = 2 * oy0, ix0 = 2 * ox0;
+  const int IW = 2 * TPW + 1, NP = (2 * TPH + 1) * IW;
+
+  const int p = threadIdx.x / TPP, part = threadIdx.x % TPP;
+  if (p < NP) {
+    const int y = iy0 + p / IW, x = ix0 + p % IW;
+    if (y < H && x < W) {
+      const T* px = in + plane * in_stride + ((int64_t)y * W + x) * C + part * CPT;
+      vec_t v[NV], lv = vec_t{}, rv = vec_t{};
+#pragma unroll
+      for (int i = 0; i < NV; ++i) v[i] = *(const vec_t*)(px + i * N);
+      if (part > 0) lv = *(const vec_t*)(px - N);
+      if (part + 1 < TPP) rv = *(const vec_t*)(px + CPT);
+      float sq[CPT + 2 * HN];
+#pragma unroll
+      for (int i = 0; i < HN; ++i) {
+        const float a = to_f32(lv[N - HN + i]), b = to_f32(rv[i]);
+        sq[i] = a * a;
+        sq[HN + CPT + i] = b * b;
+      }
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const float a = to_f32(v[i / N][i % N]);
+        sq[HN + i] = a * a;
+      }
+      T* d = s + p * CS + part * CPT;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        vec_t r;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          const int c = i * N + e;
+          float sum = 0.f;
+#pragma unroll
+          for (int j = 0; j <= 2 * HN; ++j) sum += sq[c + j];
+          r[e] = from_f32<T>(to_f32(v[i][e]) * lrn_scale(sum, alpha_n, beta, k));
+        }
+        *(vec_t*)(d + i * N) = r;
+      }
+    }
+  }
+  __syncthreads();
+
+  const int G = C / N;
+  for (int e = threadIdx.x; e < TPH * TPW * G; e += blockDim.x) {
+    const int g = e % G, q = e / G;
+    const int qy = q / TPW, qx = q % TPW;
+    const int oy = oy0 + qy, ox = ox0 + qx;
+    if (oy >= Ho || ox >= Wo) continue;
+    const int y1 = min(2 * oy + 3, H) - iy0, x1 = min(2 * ox + 3, W) - ix0;
+    float m[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) m[i] = -INFINITY;
+    for (int hy = 2 * qy; hy < y1; ++hy)
+      for (int hx = 2 * qx; hx < x1; ++hx) {
+        const vec_t v = *(const vec_t*)(s + (hy * IW + hx) * CS + g * N);
+#pragma unroll
+        for (int i = 0; i < N; ++i) m[i] = fmaxf(m[i], to_f32(v[i]));
+      }
+    vec_t r;
+#pragma unroll
+    for (int i = 0; i < N; ++i) r[i] = from_f32<T>(m[i]);
+    *(vec_t*)(out + plane * out_stride + ((int64_t)oy * Wo + ox) * C + g * N) = r;
+  }
+}
+
 // Pool first, then LRN of the pooled vector: one thread per output element.
 template <typename T>
 __global__ __launch_bounds__(256) void pool_lrn_kernel(const T* __restrict__ in, T* __restrict__ out,
@@ -193,6 +286,31 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
   }
   constexpr int N = Vec<T>::N;
   if (C % N || hn > 4) return (int)hipErrorInvalidValue;
+  // Per-pixel kernel for the two channel counts of the network with the default window (n = 5).
+  if (lrn && hn == 2 && (C == 96 || C == 256)) {
+    const int cpt = C == 96 ? 96 : 128, tpp = C / cpt;
+    int TPH = 0, TPW = 0;
+    const int cand[][2] = {{8, 7}, {4, 7}, {4, 6}, {2, 6}, {2, 5}, {2, 3}, {1, 3}, {1, 1}};
+    for (auto& c : cand) {
+      const int np = (2 * c[0] + 1) * (2 * c[1] + 1);
+      if (np * tpp <= 256 && (size_t)np * (C + N) * sizeof(T) <= 65536) {
+        TPH = c[0];
+        TPW = c[1];
+        break;
+      }
+    }
+    const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
+    const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
+    if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    const size_t lds = (size_t)(2 * TPH + 1) * (2 * TPW + 1) * (C + N) * sizeof(T);
+    if (C == 96)
+      lrn_pool_pixel_kernel<T, 96, 2><<<(unsigned)blocks, 256, lds, s>>>(
+          in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+    else
+      lrn_pool_pixel_kernel<T, 128, 2><<<(unsigned)blocks, 256, lds, s>>>(
+          in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+    return (int)hipGetLastError();
+  }
   int TPH, TPW;
   pick_tile<T>(C, TPH, TPW);
   if (!TPH) return (int)hipErrorInvalidValue;

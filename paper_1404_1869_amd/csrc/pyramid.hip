@@ -14,57 +14,36 @@ namespace {
 
 constexpr int PX = 4;  // consecutive plane pixels per thread
 
-// Value of plane pixel (y, x) of plane j: owner scale lookup, border weight, bilinear sample.
-// Writes the three centred channel values; 0 for background and alignment slack.
-__device__ inline void plane_pixel(const uint8_t* __restrict__ I, const PyrArgs& a, int j, int y,
-                                   int x, float v[3]) {
-  v[0] = v[1] = v[2] = 0.f;
-  int owner = -1;
-  for (int k = 0; k < a.n_scales; ++k) {
-    if (a.s[k].plane != j) continue;  // uniform across the workgroup
-    const PyrScale& s = a.s[k];
-    if (y >= s.y && y < s.y + s.rh && x >= s.x && x < s.x + s.rw) {
-      owner = k;
-      break;
-    }
-  }
-  if (owner < 0) return;
-  const PyrScale s = a.s[owner];
-  const int vy = y - s.y - a.pad, ux = x - s.x - a.pad;
-  const int dy = max(0, max(-vy, vy - (s.h - 1)));
-  const int dx = max(0, max(-ux, ux - (s.w - 1)));
-  if (dy > a.pad || dx > a.pad) return;
-  float wgt = 1.f;
-  if (dy | dx) {
-    if (!a.ramp) return;
-    const float den = (float)(a.pad + 1);
-    const float wy = dy ? (float)(a.pad + 1 - dy) / den : 1.f;
-    const float wx = dx ? (float)(a.pad + 1 - dx) / den : 1.f;
-    wgt = wy * wx;
-  }
-  const int yc = min(max(vy, 0), s.h - 1), xc = min(max(ux, 0), s.w - 1);
-  // half-pixel source coordinate ((2 yc + 1) H - h) / (2 h), clamped at 0; exact in 32 bits
-  // (sides are limited so that (2 h + 1) H < 2^32)
-  const uint32_t dh = 2u * (uint32_t)s.h, dw = 2u * (uint32_t)s.w;
-  const int64_t nys = (int64_t)(2 * yc + 1) * a.H - s.h, nxs = (int64_t)(2 * xc + 1) * a.W - s.w;
-  const uint32_t ny = nys > 0 ? (uint32_t)nys : 0u, nx = nxs > 0 ? (uint32_t)nxs : 0u;
-  const uint32_t y0 = ny / dh, x0 = nx / dw;
-  const float ly = (float)(ny - y0 * dh) / (float)dh;
-  const float lx = (float)(nx - x0 * dw) / (float)dw;
-  const int y1 = min((int)y0 + 1, a.H - 1), x1 = min((int)x0 + 1, a.W - 1);
-  const int64_t HW = (int64_t)a.H * a.W;
-  const int r0 = (int)y0 * a.W, r1 = y1 * a.W;
-#pragma unroll
-  for (int c = 0; c < 3; ++c) {
-    const uint8_t* P = I + c * HW;
-    const float i00 = P[r0 + (int)x0], i01 = P[r0 + x1];
-    const float i10 = P[r1 + (int)x0], i11 = P[r1 + x1];
-    const float top = i00 + lx * (i01 - i00), bot = i10 + lx * (i11 - i10);
-    v[c] = (top + ly * (bot - top) - a.mean[c]) * wgt;
-  }
+// floor(n / d) and the remainder for n, d < 2^32 with d > 0: a double-precision reciprocal estimate,
+// corrected to the exact quotient with integer arithmetic.
+__device__ inline uint32_t udiv_exact(uint32_t n, uint32_t d, double inv_d, uint32_t& rem) {
+  uint32_t q = (uint32_t)((double)n * inv_d);
+  if ((uint64_t)q * d > n) --q;
+  else if ((uint64_t)(q + 1) * d <= n) ++q;
+  rem = n - q * d;
+  return q;
 }
 
-// One thread per PX consecutive pixels of a plane row; a wave covers 64 * PX columns.
+// Source row (or column) of output index o of a scale of size h out of H: the half-pixel coordinate
+// ((2 o + 1) H - h) / (2 h), clamped at 0, split into the integer part and the fraction.
+__device__ inline void src_coord(int o, int H, int h, double inv2h, int& i0, int& i1, float& frac) {
+  const int64_t num = (int64_t)(2 * o + 1) * H - h;
+  const uint32_t n = num > 0 ? (uint32_t)num : 0u, d = 2u * (uint32_t)h;
+  uint32_t rem;
+  i0 = (int)udiv_exact(n, d, inv2h, rem);
+  i1 = min(i0 + 1, H - 1);
+  frac = (float)((double)rem * inv2h);
+}
+
+__device__ inline float border_weight(int d, int pad, bool ramp) {
+  if (d == 0) return 1.f;
+  if (!ramp || d > pad) return 0.f;
+  return (float)(pad + 1 - d) / (float)(pad + 1);
+}
+
+// One thread per PX consecutive pixels of a plane row; a wave covers 64 * PX columns.  In stitched
+// planes every rectangle edge is a multiple of 16 px, and a per-scale plane is its scale's rectangle,
+// so an aligned group of PX pixels has a single owner (or none), found among the plane's own scales.
 template <typename T>
 __global__ __launch_bounds__(256) void build_planes_kernel(const uint8_t* __restrict__ img,
                                                            PyrArgs a, PyrPlanes pl,
@@ -76,14 +55,51 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint8_t* __rest
   const int x0 = (blockIdx.x * 64 + (threadIdx.x & 63)) * PX;
   const int y = blockIdx.y * 4 + (threadIdx.x >> 6);
   if (x0 >= PW || y >= PH) return;
-  const uint8_t* I = img + (int64_t)b * 3 * a.H * a.W;
+
   float v[PX][3];
 #pragma unroll
-  for (int i = 0; i < PX; ++i) {
-    if (x0 + i < PW) {
-      plane_pixel(I, a, j, y, x0 + i, v[i]);
-    } else {
-      v[i][0] = v[i][1] = v[i][2] = 0.f;
+  for (int i = 0; i < PX; ++i) v[i][0] = v[i][1] = v[i][2] = 0.f;
+
+  int owner = -1;
+  const int f0 = a.plane_first[j], f1 = f0 + a.plane_count[j];
+  for (int e = f0; e < f1; ++e) {
+    const PyrScale& s = a.s[e];
+    if (y >= s.y && y < s.y + s.rh && x0 >= s.x && x0 < s.x + s.rw) {
+      owner = e;
+      break;
+    }
+  }
+  if (owner >= 0) {
+    const PyrScale s = a.s[owner];
+    const int vy = y - s.y - a.pad;
+    const int dy = max(0, max(-vy, vy - (s.h - 1)));
+    const float wy = border_weight(dy, a.pad, a.ramp);
+    if (wy != 0.f) {
+      const uint8_t* I = img + (int64_t)b * 3 * a.H * a.W;
+      const int64_t HW = (int64_t)a.H * a.W;
+      int sy0, sy1;
+      float ly;
+      src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, 1.0 / (2.0 * s.h), sy0, sy1, ly);
+      const double inv2w = 1.0 / (2.0 * s.w);
+      const int r0 = sy0 * a.W, r1 = sy1 * a.W;
+#pragma unroll
+      for (int i = 0; i < PX; ++i) {
+        const int ux = x0 + i - s.x - a.pad;
+        const int dx = max(0, max(-ux, ux - (s.w - 1)));
+        const float wgt = wy * border_weight(dx, a.pad, a.ramp);
+        if (wgt == 0.f || x0 + i >= PW) continue;
+        int sx0, sx1;
+        float lx;
+        src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, inv2w, sx0, sx1, lx);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+          const uint8_t* P = I + c * HW;
+          const float i00 = P[r0 + sx0], i01 = P[r0 + sx1];
+          const float i10 = P[r1 + sx0], i11 = P[r1 + sx1];
+          const float top = i00 + lx * (i01 - i00), bot = i10 + lx * (i11 - i10);
+          v[i][c] = (top + ly * (bot - top) - a.mean[c]) * wgt;
+        }
+      }
     }
   }
   T* o = out + (int64_t)b * pl.image_elems + pl.p[j].offset;
