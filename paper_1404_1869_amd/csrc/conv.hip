@@ -352,8 +352,8 @@ int device_cu_count() {
 
 // ------------------------------------------------------------------------------------------------
 // Stride-1 R x R conv with zero padding (R-1)/2, grouped, channels-last.
-// Workgroup: TH x TW = 16 x 16 output pixels x BM output channels of one group.  Waves: BM/64 along
-// channels x 2 along pixels; each wave owns 64 channels x 128 pixels (2 x 4 MFMA tiles).  The MFMA
+// Workgroup: TH x TW = 16 x 16 output pixels x BM output channels of one group.  Waves: BM/(32 TM)
+// along channels x 2 along pixels; each wave owns 32 TM channels x 128 pixels (TM x 4 MFMA tiles).  The MFMA
 // A operand is the weights and B the pixels, so each lane's accumulator holds 4 consecutive output
 // channels of one pixel per register group and the epilogue stores 4 channels at a time.
 // Pipeline: a stage is (chunk of 16 input channels, kernel row ky).  LDS holds two halo buffers
@@ -362,42 +362,51 @@ int device_cu_count() {
 // next chunk's halo) is already in flight into registers; it is written to the other buffers after
 // the stage's MFMAs, and one barrier per stage publishes it.
 // ------------------------------------------------------------------------------------------------
-template <typename T, int R, int BM>
+template <typename T, int R, int BM, int TM, int PAD>
 struct ConvCfg {
   static constexpr int TH = 16, TW = 16, CC = 16;
+  static constexpr int TN = 4;                     // 32-pixel MFMA tiles per wave (128 pixels)
   static constexpr int HH = TH + R - 1, HW = TW + R - 1;
   static constexpr bool F32 = std::is_same<T, float>::value;
-  static constexpr int CS = CC + (F32 ? 1 : 8);  // LDS stride of one pixel / channel row (elements)
-  static constexpr int WM = BM / 64, WN = (TH * TW) / 128;
+  static constexpr int CS = CC + (F32 ? 1 : PAD);  // LDS stride of a pixel / channel row (elements)
+  static constexpr int WM = BM / (32 * TM), WN = (TH * TW) / (32 * TN);
   static constexpr int NT = 64 * WM * WN;
   static constexpr int VEC = 16 / sizeof(T);  // elements per 16-byte global load
   static constexpr int VPP = CC / VEC;
   static constexpr int HALO_V = HH * HW * VPP, HALO_PER = (HALO_V + NT - 1) / NT;
   static constexpr int W_V = R * BM * VPP, W_PER = (W_V + NT - 1) / NT;
-  static_assert(NT == 2 * BM, "launch bounds assume two pixel waves per 64 channels");
+  static_assert(WM * 32 * TM == BM, "channel block must be whole wave tiles");
 };
 
-template <typename T, int R, int BM>
-__global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
+constexpr int conv_threads(int BM, int TM) { return 64 * (BM / (32 * TM)) * 2; }
+
+template <typename T, int R, int BM, int TM, int OCC, int PAD>
+__global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
-  using Cf = ConvCfg<T, R, BM>;
+  using Cf = ConvCfg<T, R, BM, TM, PAD>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
-  constexpr int VEC = Cf::VEC, VPP = Cf::VPP, CS = Cf::CS, NT = Cf::NT;
+  constexpr int VEC = Cf::VEC, VPP = Cf::VPP, CS = Cf::CS, NT = Cf::NT, TN = Cf::TN;
   typedef T vec_t __attribute__((ext_vector_type(VEC)));
   typedef T out4_t __attribute__((ext_vector_type(4)));
-  __shared__ __align__(16) T s_in[2][Cf::HH * Cf::HW * CS];
-  __shared__ __align__(16) T s_w[2][R * BM * CS];
+  constexpr int HALO_E = Cf::HH * Cf::HW * CS, W_E = R * BM * CS;
+  __shared__ __align__(16) T s_mem[2 * HALO_E + 2 * W_E];
+  auto halo_buf = [&](int b) { return s_mem + b * HALO_E; };
+  auto wrow_buf = [&](int b) { return s_mem + 2 * HALO_E + b * W_E; };
 
-  int bid = blockIdx.x;
+  // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs, so the i-th block of XCD
+  // x takes logical index x * (blocks per XCD) + i; consecutive logical blocks (the channel blocks of
+  // one tile first, then neighbouring tiles) then share that XCD's L2.
+  const int nb = gridDim.x, xcd = blockIdx.x % 8, per = nb / 8, rem = nb % 8;
+  int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int mb = bid % mblocks;
+  bid /= mblocks;
   const int tx = bid % tiles_x;
   bid /= tiles_x;
   const int ty = bid % tiles_y;
-  bid /= tiles_y;
-  const int mb = bid % mblocks;
-  const int plane = bid / mblocks;
+  const int plane = bid / tiles_y;
   const int mpg = Mg / BM;
   const int g = mb / mpg, m0 = (mb % mpg) * BM;
   const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
@@ -408,17 +417,17 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave % Cf::WM, wn = wave / Cf::WM;
   const int half = lane >> 5, l32 = lane & 31;
-  int pix[4];  // LDS pixel index (row * HW + col) of this lane's pixel in each pixel tile
+  int pix[TN];  // LDS pixel index (row * HW + col) of this lane's pixel in each pixel tile
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int idx = wn * 128 + t * 32 + l32;
+  for (int t = 0; t < TN; ++t) {
+    const int idx = wn * 32 * TN + t * 32 + l32;
     pix[t] = (idx / Cf::TW) * Cf::HW + idx % Cf::TW;
   }
-  f32x16 acc[2][4];
+  f32x16 acc[TM][TN];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TM; ++a)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[a][t] = f32x16{};
+    for (int t = 0; t < TN; ++t) acc[a][t] = f32x16{};
 
   vec_t hreg[Cf::HALO_PER], wreg[Cf::W_PER];
   auto load_halo = [&](int c0) {
@@ -440,7 +449,7 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
     for (int i = 0; i < Cf::HALO_PER; ++i) {
       const int e = tid + i * NT;
       if (e < Cf::HALO_V) {
-        T* d = &s_in[buf][(e / VPP) * CS + (e % VPP) * VEC];
+        T* d = halo_buf(buf) + (e / VPP) * CS + (e % VPP) * VEC;
         if constexpr (Cf::F32) {
 #pragma unroll
           for (int q = 0; q < VEC; ++q) d[q] = hreg[i][q];
@@ -470,7 +479,7 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
       if (e < Cf::W_V) {
         const int v = e % VPP, t = e / VPP;
         const int m = t % BM, kx = t / BM;
-        T* d = &s_w[buf][(kx * BM + m) * CS + v * VEC];
+        T* d = wrow_buf(buf) + (kx * BM + m) * CS + v * VEC;
         if constexpr (Cf::F32) {
 #pragma unroll
           for (int q = 0; q < VEC; ++q) d[q] = wreg[i][q];
@@ -481,23 +490,23 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
     }
   };
   auto compute = [&](int hb, int wb, int ky) {
-    const T* hs = s_in[hb];
-    const T* ws = s_w[wb];
+    const T* hs = halo_buf(hb);
+    const T* ws = wrow_buf(wb);
 #pragma unroll
     for (int kx = 0; kx < R; ++kx) {
 #pragma unroll
       for (int kk = 0; kk < Cf::CC / Op::KS; ++kk) {
         const int koff = kk * Op::KS + half * Op::KPL;
-        typename Op::frag x[4], w[2];
+        typename Op::frag x[TN], w[TM];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) x[t] = lds_frag16<T>(hs + (pix[t] + ky * Cf::HW + kx) * CS + koff);
+        for (int t = 0; t < TN; ++t) x[t] = lds_frag16<T>(hs + (pix[t] + ky * Cf::HW + kx) * CS + koff);
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-          w[mt] = lds_frag16<T>(ws + (kx * BM + wm * 64 + mt * 32 + l32) * CS + koff);
+        for (int mt = 0; mt < TM; ++mt)
+          w[mt] = lds_frag16<T>(ws + (kx * BM + wm * 32 * TM + mt * 32 + l32) * CS + koff);
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
+        for (int mt = 0; mt < TM; ++mt)
 #pragma unroll
-          for (int t = 0; t < 4; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
+          for (int t = 0; t < TN; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
       }
     }
   };
@@ -519,41 +528,90 @@ __global__ __launch_bounds__(2 * BM) void conv_s1_kernel(
     __syncthreads();
   }
 
-  // Epilogue: D[m][pixel]; register group q holds channels 8 q + 4 half + 0..3 of pixel l32.
+  // Epilogue: D[m][pixel]; register group q of MFMA tile mt holds channels 32 mt + 8 q + 4 half + 0..3
+  // of pixel l32.
   T* dst = out + plane * out_stride;
+  if constexpr (!Cf::F32 && TM == 2) {
+    // Stage each wave's 128 pixels x 64 channels (one 128-byte line per pixel) in LDS, 16-byte chunks
+    // XOR-swizzled by the pixel index, then write whole lines: 8 lanes per pixel, 16 bytes each.
+    typedef T vec8_t __attribute__((ext_vector_type(8)));
+    static_assert(Cf::WM * Cf::WN * 32 * TN * 64 <= 2 * HALO_E + 2 * W_E, "staging must fit in LDS");
+    T* stg = s_mem + wave * (32 * TN * 64);
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+    for (int mt = 0; mt < TM; ++mt)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = g * Mg + m0 + wm * 64 + mt * 32 + 8 * q + 4 * half;
-      const f32x4 bv = *(const f32x4*)(bias + m);
+      for (int q = 0; q < 4; ++q) {
+        const int j = 4 * mt + q;
+        const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int idx = wn * 128 + t * 32 + l32;
-        const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
-        if (oy < H && ox < W) {
+        for (int t = 0; t < TN; ++t) {
+          const int p = t * 32 + l32;
           out4_t r;
 #pragma unroll
           for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
-          *(out4_t*)(dst + ((int64_t)oy * W + ox) * M + m) = r;
+          *(out4_t*)(stg + p * 64 + ((j ^ (p & 7)) * 8) + 4 * half) = r;
         }
       }
+    __syncthreads();
+    const int j = lane & 7;
+#pragma unroll
+    for (int it = 0; it < (32 * TN) / 8; ++it) {
+      const int p = it * 8 + (lane >> 3);
+      const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ (p & 7)) * 8));
+      const int idx = wn * 32 * TN + p;
+      const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+      if (oy < H && ox < W)
+        *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
     }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = g * Mg + m0 + wm * 32 * TM + mt * 32 + 8 * q + 4 * half;
+        const f32x4 bv = *(const f32x4*)(bias + m);
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+          const int idx = wn * 32 * TN + t * 32 + l32;
+          const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+          if (oy < H && ox < W) {
+            out4_t r;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+            *(out4_t*)(dst + ((int64_t)oy * W + ox) * M + m) = r;
+          }
+        }
+      }
+  }
 }
 
-template <typename T, int R, int BM>
+template <typename T, int R, int BM, int TM, int OCC, int PAD>
 int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int H, int W, int C,
                 int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
-  using Cf = ConvCfg<T, R, BM>;
+  using Cf = ConvCfg<T, R, BM, TM, PAD>;
   const int Cg = C / G, Mg = M / G;
   const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
   const int mblocks = G * (Mg / BM);
   const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
   if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-  conv_s1_kernel<T, R, BM><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+  conv_s1_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
       in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   return (int)hipGetLastError();
 }
+
+// Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, LDS
+// row padding (elements, 16-bit types).  Chosen by timing each layer at the 96-plane batch shapes:
+// two waves per SIMD matter most; conv2's 25-tap weight rows need unpadded LDS rows to fit two
+// workgroups per CU; conv4's 192 channels per group run best as three 64-channel blocks.
+#ifndef DN_CONV2_CFG
+#define DN_CONV2_CFG 128, 2, 2, 0
+#endif
+#ifndef DN_CONV35_CFG
+#define DN_CONV35_CFG 128, 2, 2, 8
+#endif
+#ifndef DN_CONV4_CFG
+#define DN_CONV4_CFG 64, 2, 2, 0
+#endif
 
 template <typename T>
 int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
@@ -581,15 +639,15 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
   const int li = layer - 1;
   switch (layer) {
     case 2:
-      return run_conv_s1<T, 5, 128>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
-                                    out_stride, s);
+      return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+                                             in_stride, out_stride, s);
     case 3:
     case 5:
-      return run_conv_s1<T, 3, 128>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
-                                    out_stride, s);
+      return run_conv_s1<T, 3, DN_CONV35_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+                                              in_stride, out_stride, s);
     case 4:
-      return run_conv_s1<T, 3, 192>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li], in_stride,
-                                    out_stride, s);
+      return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+                                             in_stride, out_stride, s);
   }
   return (int)hipErrorInvalidValue;
 }
