@@ -368,7 +368,6 @@ struct ConvCfg {
   static constexpr int TN = 4;                     // 32-pixel MFMA tiles per wave (128 pixels)
   static constexpr int HH = TH + R - 1, HW = TW + R - 1;
   static constexpr bool F32 = std::is_same<T, float>::value;
-  static constexpr int CS = CC + (F32 ? 1 : PAD);  // LDS stride of a pixel / channel row (elements)
   static constexpr int WM = BM / (32 * TM), WN = (TH * TW) / (32 * TN);
   static constexpr int NT = 64 * WM * WN;
   static constexpr int VEC = 16 / sizeof(T);  // elements per 16-byte global load
@@ -376,6 +375,20 @@ struct ConvCfg {
   static constexpr int HALO_V = HH * HW * VPP, HALO_PER = (HALO_V + NT - 1) / NT;
   static constexpr int W_V = R * BM * VPP, W_PER = (W_V + NT - 1) / NT;
   static_assert(WM * 32 * TM == BM, "channel block must be whole wave tiles");
+  // LDS layout.  16-bit types: a pixel (or an output channel's weight row) is 32 bytes, two 16-byte
+  // slots.  The 32 lanes of a half-wave read 16 bytes each and must hit distinct slots modulo 512
+  // bytes: a halo row is padded by one slot, so the two tile rows a half-wave reads land on slots of
+  // opposite parity; the weight rows of channels 16..31 of a 32-channel group swap their two slots.
+  // fp32: a pixel or channel row is CC + 1 floats.
+  static constexpr int PS = F32 ? CC + 1 : CC;          // pixel stride (elements)
+  static constexpr int RS = F32 ? HW * PS : HW * PS + 8;  // halo row stride (elements)
+  static constexpr int HALO_E = HH * RS, W_E = R * BM * PS;
+  static constexpr int STAGE_E = F32 ? 0 : WM * WN * 32 * TN * 64;  // epilogue staging
+  static constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > STAGE_E ? (2 * HALO_E + 2 * W_E) : STAGE_E;
+  __device__ static inline int halo_off(int hy, int hx, int v) { return hy * RS + hx * PS + v * VEC; }
+  __device__ static inline int w_off(int kx, int m, int v) {
+    return (kx * BM + m) * PS + (F32 ? v * VEC : ((v ^ ((m >> 4) & 1)) * VEC));
+  }
 };
 
 constexpr int conv_threads(int BM, int TM) { return 64 * (BM / (32 * TM)) * 2; }
@@ -388,11 +401,11 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
   using Cf = ConvCfg<T, R, BM, TM, PAD>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
-  constexpr int VEC = Cf::VEC, VPP = Cf::VPP, CS = Cf::CS, NT = Cf::NT, TN = Cf::TN;
+  constexpr int VEC = Cf::VEC, VPP = Cf::VPP, NT = Cf::NT, TN = Cf::TN;
   typedef T vec_t __attribute__((ext_vector_type(VEC)));
   typedef T out4_t __attribute__((ext_vector_type(4)));
-  constexpr int HALO_E = Cf::HH * Cf::HW * CS, W_E = R * BM * CS;
-  __shared__ __align__(16) T s_mem[2 * HALO_E + 2 * W_E];
+  constexpr int HALO_E = Cf::HALO_E, W_E = Cf::W_E;
+  __shared__ __align__(16) T s_mem[Cf::LDS_E];
   auto halo_buf = [&](int b) { return s_mem + b * HALO_E; };
   auto wrow_buf = [&](int b) { return s_mem + 2 * HALO_E + b * W_E; };
 
@@ -417,11 +430,11 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave % Cf::WM, wn = wave / Cf::WM;
   const int half = lane >> 5, l32 = lane & 31;
-  int pix[TN];  // LDS pixel index (row * HW + col) of this lane's pixel in each pixel tile
+  int pix[TN];  // LDS element offset of this lane's pixel (tap 0, 0) in each pixel tile
 #pragma unroll
   for (int t = 0; t < TN; ++t) {
     const int idx = wn * 32 * TN + t * 32 + l32;
-    pix[t] = (idx / Cf::TW) * Cf::HW + idx % Cf::TW;
+    pix[t] = Cf::halo_off(idx / Cf::TW, idx % Cf::TW, 0);
   }
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -449,7 +462,8 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
     for (int i = 0; i < Cf::HALO_PER; ++i) {
       const int e = tid + i * NT;
       if (e < Cf::HALO_V) {
-        T* d = halo_buf(buf) + (e / VPP) * CS + (e % VPP) * VEC;
+        const int p = e / VPP;
+        T* d = halo_buf(buf) + Cf::halo_off(p / Cf::HW, p % Cf::HW, e % VPP);
         if constexpr (Cf::F32) {
 #pragma unroll
           for (int q = 0; q < VEC; ++q) d[q] = hreg[i][q];
@@ -479,7 +493,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
       if (e < Cf::W_V) {
         const int v = e % VPP, t = e / VPP;
         const int m = t % BM, kx = t / BM;
-        T* d = wrow_buf(buf) + (kx * BM + m) * CS + v * VEC;
+        T* d = wrow_buf(buf) + Cf::w_off(kx, m, v);
         if constexpr (Cf::F32) {
 #pragma unroll
           for (int q = 0; q < VEC; ++q) d[q] = wreg[i][q];
@@ -498,11 +512,18 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
       for (int kk = 0; kk < Cf::CC / Op::KS; ++kk) {
         const int koff = kk * Op::KS + half * Op::KPL;
         typename Op::frag x[TN], w[TM];
+        // k offset of this lane: element koff of the 16-channel chunk (16-bit: slot `half`)
 #pragma unroll
-        for (int t = 0; t < TN; ++t) x[t] = lds_frag16<T>(hs + (pix[t] + ky * Cf::HW + kx) * CS + koff);
+        for (int t = 0; t < TN; ++t)
+          x[t] = lds_frag16<T>(hs + pix[t] + ky * Cf::RS + kx * Cf::PS + koff);
 #pragma unroll
-        for (int mt = 0; mt < TM; ++mt)
-          w[mt] = lds_frag16<T>(ws + (kx * BM + wm * 32 * TM + mt * 32 + l32) * CS + koff);
+        for (int mt = 0; mt < TM; ++mt) {
+          const int m = wm * 32 * TM + mt * 32 + l32;
+          if constexpr (Cf::F32)
+            w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, m, 0) + koff);
+          else
+            w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, m, half));
+        }
 #pragma unroll
         for (int mt = 0; mt < TM; ++mt)
 #pragma unroll
@@ -535,7 +556,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
     // Stage each wave's 128 pixels x 64 channels (one 128-byte line per pixel) in LDS, 16-byte chunks
     // XOR-swizzled by the pixel index, then write whole lines: 8 lanes per pixel, 16 bytes each.
     typedef T vec8_t __attribute__((ext_vector_type(8)));
-    static_assert(Cf::WM * Cf::WN * 32 * TN * 64 <= 2 * HALO_E + 2 * W_E, "staging must fit in LDS");
+    static_assert(Cf::STAGE_E <= Cf::LDS_E, "staging must fit in LDS");
     T* stg = s_mem + wave * (32 * TN * 64);
 #pragma unroll
     for (int mt = 0; mt < TM; ++mt)
@@ -549,7 +570,8 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
           out4_t r;
 #pragma unroll
           for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
-          *(out4_t*)(stg + p * 64 + ((j ^ (p & 7)) * 8) + 4 * half) = r;
+          const int key = (p & 7) ^ ((p >> 3) & 3);
+          *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
         }
       }
     __syncthreads();
@@ -557,7 +579,8 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
 #pragma unroll
     for (int it = 0; it < (32 * TN) / 8; ++it) {
       const int p = it * 8 + (lane >> 3);
-      const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ (p & 7)) * 8));
+      const int key = (p & 7) ^ ((p >> 3) & 3);
+      const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
       const int idx = wn * 32 * TN + p;
       const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
       if (oy < H && ox < W)
@@ -599,10 +622,9 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
   return (int)hipGetLastError();
 }
 
-// Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, LDS
-// row padding (elements, 16-bit types).  Chosen by timing each layer at the 96-plane batch shapes:
-// two waves per SIMD matter most; conv2's 25-tap weight rows need unpadded LDS rows to fit two
-// workgroups per CU; conv4's 192 channels per group run best as three 64-channel blocks.
+// Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, and
+// a spare layout parameter.  Chosen by timing each layer at the 96-plane batch shapes: two waves per
+// SIMD matter most; conv4's 192 channels per group run best as three 64-channel blocks.
 #ifndef DN_CONV2_CFG
 #define DN_CONV2_CFG 128, 2, 2, 0
 #endif

@@ -32,21 +32,35 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
                y2 = boxes[4 * r + 3];
   const double bw = x2 - x1, bh = y2 - y1;
   const int img = box_img ? box_img[r] : 0;
-  int best = -1;
-  if (img >= 0 && img < a.n_img && isfinite(x1) && isfinite(y1) && isfinite(x2) && isfinite(y2) && bw > 0 && bh > 0) {
-    const double T2 = a.target * a.target;
-    double best_cost = 0;
-    for (int k = 0; k < a.n_scales; ++k) {
-      if (a.s[k].empty) continue;
+  const bool valid = img >= 0 && img < a.n_img && isfinite(x1) && isfinite(y1) && isfinite(x2) &&
+                     isfinite(y2) && bw > 0 && bh > 0;
+  // Scale choice: lane k of wave 0 evaluates scale k (k < n_scales <= 64), then the wave takes the
+  // minimum cost, ties to the smaller k, which is the first minimum in increasing k.
+  __shared__ int s_best;
+  if (tid < 64) {
+    double cost = INFINITY;
+    int k = tid;
+    if (valid && k < a.n_scales && !a.s[k].empty) {
+      const double T2 = a.target * a.target;
       const double area = (a.s[k].sy * bh) * (a.s[k].sx * bw);
       const double p = area / T2, q = T2 / area;
-      const double cost = p < q ? q : p;
-      if (best < 0 || cost < best_cost) {
-        best = k;
-        best_cost = cost;
+      cost = p < q ? q : p;
+    } else {
+      k = 1 << 30;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const double oc = __shfl_xor(cost, off);
+      const int ok = __shfl_xor(k, off);
+      if (oc < cost || (oc == cost && ok < k)) {
+        cost = oc;
+        k = ok;
       }
     }
+    if (tid == 0) s_best = k < a.n_scales ? k : -1;
   }
+  __syncthreads();
+  const int best = s_best;
   float* dst = out + (int64_t)r * C * SS;
   if (best < 0) {
     for (int e = tid; e < C * SS; e += blockDim.x) dst[e] = 0.f;
