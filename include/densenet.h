@@ -155,6 +155,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
  * b * planes_per_img + j), channels-last with 256 channels, offsets multiples of 16 bytes.  d_box_img: nullable [n] image index per box (NULL => image 0).
  * d_scale: [n] chosen scale, -1 for a box with a non-finite or non-positive side (its row is 0).
  * d_idx: nullable [n][S][S][2] int32 (i0, j0) conv5 cell of each sample's top-left neighbour.
+ * With n == 0 nothing is launched and d_boxes, d_out, d_scale may be NULL.
  * Index arithmetic is fp64 with + - * / only, so scales and indices are reproducible bit for bit. */
 int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
                             dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,

@@ -381,8 +381,9 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
                             const int32_t* d_box_img, int32_t n, float target, int32_t S,
                             float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream) {
   try {
-    if (!d_conv5 || !conv5_desc || !geom || !d_boxes || !d_out || !d_scale)
-      return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (!d_conv5 || !conv5_desc || !geom) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (n > 0 && (!d_boxes || !d_out || !d_scale))
+      return fail(DN_E_INVALID_ARG, "null box or output pointer");
     if (!valid_dtype(conv5_dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
     if (n_scales <= 0 || n_scales > DN_MAX_SCALES) return fail(DN_E_INVALID_ARG, "bad n_scales");
     if (planes_per_img <= 0 || planes_per_img > DN_MAX_PLANES_PER_IMAGE || n_maps < planes_per_img ||

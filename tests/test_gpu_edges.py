@@ -1,0 +1,166 @@
+"""GPU parity on edge cases of the path, through the C ABI, against the oracle: ragged image sizes on
+small stitched planes, the smallest plane that still has a conv5 cell, the pool-then-LRN order,
+a 2000 x 2000 plane (the paper's larger plane size), region windows with no boxes, 1 x 1 and 8 x 8
+bins and out-of-range image indices, and planes too small for conv5 rejected before any launch."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1404_1869_amd import synth
+from tests.parity import assert_layer_close, chw, round_to
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DTS = {"f32": 0, "f16": 1, "bf16": 2}
+W7 = synth.weights(7)
+
+
+@pytest.fixture(scope="module")
+def D():
+    from paper_1404_1869_amd import densenet
+    assert torch.cuda.is_available()
+    densenet.lib()
+    return densenet
+
+
+_packed = {}
+
+
+def packed(D, dt):
+    if dt not in _packed:
+        ws = [(torch.from_numpy(w).cuda(), torch.from_numpy(b).cuda()) for w, b in W7]
+        _packed[dt] = D.densenet_pack_weights(ws, DTS[dt])
+    return _packed[dt]
+
+
+def run(D, img, p, dt, net=None):
+    pyra = D.convnet_featpyramid(torch.from_numpy(img).cuda()[None], p, packed(D, dt), DTS[dt], net)
+    torch.cuda.synchronize()
+    return pyra
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16", "f32"])
+def test_ragged_image_small_stitched_planes(D, dt):
+    H, W = 97, 131
+    img = synth.image(77, H, W)
+    p = D.pyramid_params(4, 3, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=208, plane_w=240,
+                         mean=synth.IMAGENET_MEAN)
+    pyra = run(D, img, p, dt)
+    op = oracle.plan(H, W, 4, 3, 1.0, 0, 16, 208, 240)
+    planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    maps = pyra.conv.conv5_maps()
+    assert len(maps) == op.n_planes
+    for j, pl in enumerate(planes):
+        ref = oracle.net(pl.astype(np.float32), W7)
+        assert_layer_close(chw(maps[j].float().cpu().numpy()), ref, dt, f"ragged plane {j}")
+
+
+def test_smallest_plane_with_a_conv5_cell(D):
+    # a 1 x 1 image with 13 px of zero padding is a 27 x 27 plane: conv5 is 1 x 1
+    img = synth.image(5, 1, 1)
+    p = D.pyramid_params(1, 1, pad=13, pad_mode=D.DN_PAD_ZERO, mean=synth.IMAGENET_MEAN)
+    pyra = run(D, img, p, "f32")
+    op = oracle.plan(1, 1, 1, 1, 1.0, 0, 13, 0, 0)
+    pl = oracle.build_planes(img, op, 0, synth.IMAGENET_MEAN)[0]
+    assert pl.shape == (3, 27, 27)
+    ref = oracle.net(pl.astype(np.float32), W7)
+    got = pyra.conv.conv5_maps()[0]
+    assert tuple(got.shape) == (1, 1, 256)
+    assert_layer_close(chw(got.cpu().numpy()), ref, "f32", "27x27 plane")
+
+
+def test_plane_too_small_is_rejected_before_launch(D):
+    img = torch.from_numpy(synth.image(5, 1, 1)).cuda()[None]
+    p = D.pyramid_params(1, 1, pad=8, pad_mode=D.DN_PAD_ZERO)   # 17 x 17 plane: conv5 empty
+    planes, plan = D.densenet_build_pyramid(img, p, DTS["f16"])
+    with pytest.raises(D.DenseNetError) as e:
+        D.ConvFeatures(plan.planes, DTS["f16"], D.net_params())
+    assert e.value.status == D.DN_E_INVALID_ARG and "too small" in D.last_error()
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_pool_then_lrn_order_end_to_end(D, dt):
+    img = synth.image(101, 227, 227)
+    p = D.pyramid_params(2, 2, mean=synth.IMAGENET_MEAN)
+    pyra = run(D, img, p, dt, D.net_params(lrn_before_pool=False, pool5=True))
+    op = oracle.plan(227, 227, 2, 2)
+    planes = oracle.build_planes(img, op, 0, synth.IMAGENET_MEAN)
+    for j, pl in enumerate(planes):
+        c5, p5 = oracle.net(pl.astype(np.float32), W7, lrn_before_pool=False, pool5=True)
+        assert_layer_close(chw(pyra.conv.conv5_maps()[j].float().cpu().numpy()), c5, dt, f"conv5 {j}")
+        assert_layer_close(chw(pyra.conv.pool5_maps()[j].float().cpu().numpy()), p5, dt, f"pool5 {j}")
+
+
+def test_2000_plane_f16(D):
+    # one 1536 x 2000 image at scale 1 with ramp padding, stitched onto a 2000 x 2000 plane
+    H, W = 1536, 1900
+    img = synth.image(2000, H, W)
+    p = D.pyramid_params(1, 1, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=2000, plane_w=2000,
+                         mean=synth.IMAGENET_MEAN)
+    pyra = run(D, img, p, "f16")
+    op = oracle.plan(H, W, 1, 1, 1.0, 0, 16, 2000, 2000)
+    pl = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)[0]
+    ref = oracle.net(pl.astype(np.float32), W7)
+    got = pyra.conv.conv5_maps()[0]
+    assert tuple(got.shape) == (124, 124, 256)
+    assert_layer_close(chw(got.float().cpu().numpy()), ref, "f16", "2000 plane")
+
+
+def _shared_maps(p, seed):
+    rng = np.random.default_rng(seed)
+    return [rng.normal(0, 1, (256, oracle.conv5_side(h), oracle.conv5_side(w))).astype(np.float32)
+            for h, w in p.plane_sizes]
+
+
+def _descs(D, maps, n_img=1):
+    descs, off = [], 0
+    for _ in range(n_img):
+        for m in maps:
+            d = D.dn_plane_desc()
+            d.h, d.w, d.offset = m.shape[1], m.shape[2], off
+            off += m.size
+            descs.append(d)
+    return descs
+
+
+@pytest.mark.parametrize("S", [1, 8])
+def test_region_windows_bins_and_edges(D, S):
+    H, W = 480, 640
+    p = oracle.plan(H, W, 8, 4, 1.0, 0, 16, 800, 800)
+    plan = D.densenet_plan_pyramid(H, W, D.pyramid_params(8, 4, pad=16, pad_mode=D.DN_PAD_RAMP,
+                                                          plane_h=800, plane_w=800))
+    maps = _shared_maps(p, 3)
+    flat = np.concatenate([np.moveaxis(m, 0, -1).ravel() for m in maps] * 2)
+    c5 = torch.from_numpy(flat).cuda()
+    boxes = synth.boxes(11, 300, H, W)
+    box_img = np.zeros(300, np.int32)
+    box_img[::3] = 1
+    box_img[5] = 2          # out of range: scale -1, zero row
+    box_img[7] = -1
+    out, sc, ix = D.densenet_region_windows(c5, _descs(D, maps, 2), DTS["f32"], plan, 16, p.n_planes,
+                                            torch.from_numpy(boxes).cuda(),
+                                            torch.from_numpy(box_img).cuda(), target=227.0, S=S,
+                                            want_idx=True)
+    torch.cuda.synchronize()
+    # image 1's maps are a copy of image 0's: the oracle sees image 0 for all valid boxes
+    desc, scale, idx, _ = oracle.region_windows(maps, p, boxes, S=S)
+    sc = sc.cpu().numpy()
+    valid = (box_img >= 0) & (box_img < 2)
+    np.testing.assert_array_equal(sc[valid], scale[valid])
+    np.testing.assert_array_equal(ix.cpu().numpy()[valid], idx[valid])
+    np.testing.assert_allclose(out.cpu().numpy()[valid], desc[valid], rtol=2e-6, atol=2e-6)
+    assert (sc[~valid] == -1).all() and not out.cpu().numpy()[~valid].any()
+
+
+def test_region_windows_no_boxes(D):
+    p = oracle.plan(227, 227, 2, 2)
+    plan = D.densenet_plan_pyramid(227, 227, D.pyramid_params(2, 2))
+    maps = _shared_maps(p, 1)
+    c5 = torch.from_numpy(np.concatenate([np.moveaxis(m, 0, -1).ravel() for m in maps])).cuda()
+    out, sc, _ = D.densenet_region_windows(c5, _descs(D, maps), DTS["f32"], plan, 0, 2,
+                                           torch.zeros((0, 4), dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 9216) and sc.shape == (0,)
