@@ -608,6 +608,171 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
   }
 }
 
+// ------------------------------------------------------------------------------------------------
+// Stride-1 conv for 16-bit storage with direct global->LDS loads.  Same tiling, stages, LDS layout and
+// epilogue as conv_s1_kernel, but every stage buffer is filled by buffer_load_dwordx4 ... lds: one
+// wave instruction writes 64 consecutive 16-byte LDS slots, each lane choosing the global address of
+// its slot (padding slots and halo pixels outside the map use an offset past the buffer's end, which
+// the hardware returns as zeros).  No registers hold staged data and no LDS store instructions are
+// issued; a stage's loads are waited for (vmcnt) just before the barrier that publishes them.
+// ------------------------------------------------------------------------------------------------
+template <int BYTES>
+struct Pieces {  // 1 KB LDS pieces, rounded up to a whole number per wave
+  static constexpr int count(int slots, int waves) { return ((slots + 63) / 64 + waves - 1) / waves; }
+};
+
+__device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds_piece,
+                                           16, voff, 0, 0, 0);
+}
+
+template <typename T, int R, int BM, int TM, int OCC, int PAD>
+__global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_kernel(
+    const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
+    const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
+    int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
+  using Cf = ConvCfg<T, R, BM, TM, PAD>;
+  using Op = Mfma<T>;
+  static_assert(!Cf::F32 && TM == 2, "direct-load path is for 16-bit storage");
+  constexpr int pad = (R - 1) / 2;
+  constexpr int TN = Cf::TN, NW = Cf::WM * Cf::WN;
+  constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2;
+  constexpr int DH = Pieces<16>::count(HSLOTS, NW), DW = Pieces<16>::count(WSLOTS, NW);
+  constexpr int HALO_E = DH * NW * 512, W_E = DW * NW * 512;  // elements (2 bytes)
+  constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > Cf::STAGE_E ? (2 * HALO_E + 2 * W_E) : Cf::STAGE_E;
+  typedef T out4_t __attribute__((ext_vector_type(4)));
+  __shared__ __align__(1024) T s_mem[LDS_E];
+  auto halo_buf = [&](int b) { return s_mem + b * HALO_E; };
+  auto wrow_buf = [&](int b) { return s_mem + 2 * HALO_E + b * W_E; };
+
+  const int nb = gridDim.x, xcd = blockIdx.x % 8, per = nb / 8, rem = nb % 8;
+  int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int mb = bid % mblocks;
+  bid /= mblocks;
+  const int tx = bid % tiles_x;
+  bid /= tiles_x;
+  const int ty = bid % tiles_y;
+  const int plane = bid / tiles_y;
+  const int mpg = Mg / BM;
+  const int g = mb / mpg, m0 = (mb % mpg) * BM;
+  const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
+  const T* src = in + plane * in_stride + g * Cg;
+  const T* wg = wp + ((int64_t)g * Mg + m0) * R * R * Cg;
+  const __amdgpu_buffer_rsrc_t rsrc_in = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)src, 0, (int)(((int64_t)H * W * C - g * Cg) * sizeof(T)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)wg, 0, (int)((int64_t)BM * R * R * Cg * sizeof(T)), 0x00020000);
+  constexpr uint32_t OOB = 0x80000000u;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % Cf::WM, wn = wave / Cf::WM;
+  const int half = lane >> 5, l32 = lane & 31;
+  int pix[TN];
+#pragma unroll
+  for (int t = 0; t < TN; ++t) {
+    const int idx = wn * 32 * TN + t * 32 + l32;
+    pix[t] = Cf::halo_off(idx / Cf::TW, idx % Cf::TW, 0);
+  }
+  // Byte offsets (chunk 0, tap row 0) of this lane's slot in each of its wave's LDS pieces.
+  uint32_t hoff[DH], woff[DW];
+#pragma unroll
+  for (int i = 0; i < DH; ++i) {
+    const int q = (wave * DH + i) * 64 + lane;
+    const int row = q / (2 * Cf::HW + 1), r = q % (2 * Cf::HW + 1);
+    const int iy = oy0 - pad + row, ix = ox0 - pad + r / 2;
+    const bool ok = row < Cf::HH && r < 2 * Cf::HW && iy >= 0 && iy < H && ix >= 0 && ix < W;
+    hoff[i] = ok ? (uint32_t)((((int64_t)iy * W + ix) * C + (r & 1) * 8) * sizeof(T)) : OOB;
+  }
+#pragma unroll
+  for (int i = 0; i < DW; ++i) {
+    const int q = (wave * DW + i) * 64 + lane;
+    const int kx = q / (2 * BM), r = q % (2 * BM), m = r / 2;
+    const int v = (r & 1) ^ ((m >> 4) & 1);
+    woff[i] = q < WSLOTS ? (uint32_t)((((int64_t)m * R * R + kx) * Cg + v * 8) * sizeof(T)) : OOB;
+  }
+  auto load_halo = [&](int buf, int c0) {
+#pragma unroll
+    for (int i = 0; i < DH; ++i)
+      lds_direct16(rsrc_in, halo_buf(buf) + (wave * DH + i) * 512,
+                   hoff[i] == OOB ? OOB : hoff[i] + (uint32_t)(c0 * sizeof(T)));
+  };
+  auto load_w = [&](int buf, int c0, int ky) {
+    const uint32_t add = (uint32_t)((ky * R * Cg + c0) * sizeof(T));
+#pragma unroll
+    for (int i = 0; i < DW; ++i)
+      lds_direct16(rsrc_w, wrow_buf(buf) + (wave * DW + i) * 512, woff[i] == OOB ? OOB : woff[i] + add);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int t = 0; t < TN; ++t) acc[a][t] = f32x16{};
+
+  const int nchunks = Cg / Cf::CC, nst = nchunks * R;
+  load_halo(0, 0);
+  load_w(0, 0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int chunk = st / R, ky = st - chunk * R;
+    if (st + 1 < nst) load_w((st + 1) & 1, ((st + 1) / R) * Cf::CC, (st + 1) % R);
+    if (ky == 0 && chunk + 1 < nchunks) load_halo((chunk + 1) & 1, (chunk + 1) * Cf::CC);
+    const T* hs = halo_buf(chunk & 1);
+    const T* ws = wrow_buf(st & 1);
+#pragma unroll
+    for (int kx = 0; kx < R; ++kx) {
+      typename Op::frag x[TN], w[TM];
+#pragma unroll
+      for (int t = 0; t < TN; ++t)
+        x[t] = lds_frag16<T>(hs + pix[t] + ky * Cf::RS + kx * Cf::PS + half * 8);
+#pragma unroll
+      for (int mt = 0; mt < TM; ++mt)
+        w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, wm * 32 * TM + mt * 32 + l32, half));
+#pragma unroll
+      for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+        for (int t = 0; t < TN; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // Epilogue as in conv_s1_kernel: stage 128 pixels x 64 channels per wave, write whole lines.
+  typedef T vec8_t __attribute__((ext_vector_type(8)));
+  T* dst = out + plane * out_stride;
+  T* stg = s_mem + wave * (32 * TN * 64);
+#pragma unroll
+  for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = 4 * mt + q;
+      const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
+#pragma unroll
+      for (int t = 0; t < TN; ++t) {
+        const int p = t * 32 + l32;
+        out4_t r;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+        const int key = (p & 7) ^ ((p >> 3) & 3);
+        *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
+      }
+    }
+  __syncthreads();
+  const int j = lane & 7;
+#pragma unroll
+  for (int it = 0; it < (32 * TN) / 8; ++it) {
+    const int p = it * 8 + (lane >> 3);
+    const int key = (p & 7) ^ ((p >> 3) & 3);
+    const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
+    const int idx = wn * 32 * TN + p;
+    const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+    if (oy < H && ox < W)
+      *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
+  }
+}
+
 template <typename T, int R, int BM, int TM, int OCC, int PAD>
 int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int H, int W, int C,
                 int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
@@ -617,8 +782,15 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
   const int mblocks = G * (Mg / BM);
   const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
   if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-  conv_s1_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
-      in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+  if constexpr (Cf::F32 || TM != 2) {
+    conv_s1_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+        in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+  } else {
+    // buffer descriptors address one plane with 32-bit byte offsets
+    if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
+    conv_s1_direct_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+        in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+  }
   return (int)hipGetLastError();
 }
 
