@@ -639,7 +639,11 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
   constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2;
   constexpr int DH = Pieces<16>::count(HSLOTS, NW), DW = Pieces<16>::count(WSLOTS, NW);
   constexpr int HALO_E = DH * NW * 512, W_E = DW * NW * 512;  // elements (2 bytes)
-  constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > Cf::STAGE_E ? (2 * HALO_E + 2 * W_E) : Cf::STAGE_E;
+  // The epilogue stages 16 KB per wave; when that would set the LDS size, it runs in two rounds of
+  // half the waves each.
+  constexpr int ROUNDS = (Cf::STAGE_E > 2 * HALO_E + 2 * W_E && NW % 2 == 0) ? 2 : 1;
+  constexpr int STG_E = Cf::STAGE_E / ROUNDS;
+  constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > STG_E ? (2 * HALO_E + 2 * W_E) : STG_E;
   typedef T out4_t __attribute__((ext_vector_type(4)));
   __shared__ __align__(1024) T s_mem[LDS_E];
   auto halo_buf = [&](int b) { return s_mem + b * HALO_E; };
@@ -742,34 +746,45 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
   // Epilogue as in conv_s1_kernel: stage 128 pixels x 64 channels per wave, write whole lines.
   typedef T vec8_t __attribute__((ext_vector_type(8)));
   T* dst = out + plane * out_stride;
-  T* stg = s_mem + wave * (32 * TN * 64);
+  constexpr int WPR = NW / ROUNDS;  // waves staging per round
 #pragma unroll
-  for (int mt = 0; mt < TM; ++mt)
+  for (int round = 0; round < ROUNDS; ++round) {
+    if (round) __syncthreads();
+    const bool mine = wave / WPR == round;
+    T* stg = s_mem + (wave % WPR) * (32 * TN * 64);
+    if (mine) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = 4 * mt + q;
-      const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
+      for (int mt = 0; mt < TM; ++mt)
 #pragma unroll
-      for (int t = 0; t < TN; ++t) {
-        const int p = t * 32 + l32;
-        out4_t r;
+        for (int q = 0; q < 4; ++q) {
+          const int j = 4 * mt + q;
+          const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+          for (int t = 0; t < TN; ++t) {
+            const int p = t * 32 + l32;
+            out4_t r;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+            const int key = (p & 7) ^ ((p >> 3) & 3);
+            *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
+          }
+        }
+    }
+    __syncthreads();
+    if (mine) {
+      const int j = lane & 7;
+#pragma unroll
+      for (int it = 0; it < (32 * TN) / 8; ++it) {
+        const int p = it * 8 + (lane >> 3);
         const int key = (p & 7) ^ ((p >> 3) & 3);
-        *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
+        const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
+        const int idx = wn * 32 * TN + p;
+        const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+        if (oy < H && ox < W)
+          *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
       }
     }
-  __syncthreads();
-  const int j = lane & 7;
-#pragma unroll
-  for (int it = 0; it < (32 * TN) / 8; ++it) {
-    const int p = it * 8 + (lane >> 3);
-    const int key = (p & 7) ^ ((p >> 3) & 3);
-    const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
-    const int idx = wn * 32 * TN + p;
-    const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
-    if (oy < H && ox < W)
-      *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
   }
 }
 
@@ -801,7 +816,7 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
 #define DN_CONV2_CFG 128, 2, 2, 0
 #endif
 #ifndef DN_CONV35_CFG
-#define DN_CONV35_CFG 128, 2, 2, 8
+#define DN_CONV35_CFG 128, 2, 3, 8
 #endif
 #ifndef DN_CONV4_CFG
 #define DN_CONV4_CFG 64, 2, 2, 0
