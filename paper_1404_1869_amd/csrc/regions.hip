@@ -2,11 +2,12 @@
 // pyramid at the scale whose scaled area is closest to target^2, as S x S bilinear samples at the
 // bin centres of the box, all channels.
 //
-// One workgroup per box; each thread blends one 16-byte vector of channels of one bin at a time.  The scale choice and the sample positions are
-// computed in fp64 with + - * / only and FP contraction off, in the same order as the definition, so
-// the chosen scale and cell indices are reproducible bit for bit on any IEEE fp64 implementation.
-// Samples of one bin read 4 cells x C contiguous channels (coalesced); the descriptor row is staged
-// in LDS and written out with 16-byte stores.
+// One workgroup per box; each thread blends one 16-byte vector of channels of one bin at a time.
+// The scale choice and the sample positions are computed in fp64 with + - * / only and FP
+// contraction off, in the same order as the definition, so the chosen scale and cell indices are
+// reproducible bit for bit on any IEEE fp64 implementation.  Samples of one bin read 4 cells x C
+// contiguous channels (coalesced); the descriptor row is transposed through LDS into its
+// channel-major order and written with coalesced stores.
 #include "common.h"
 
 namespace dn {
@@ -22,7 +23,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
                                                              int32_t* __restrict__ scale_out,
                                                              int32_t* __restrict__ idx_out) {
 #pragma clang fp contract(off)
-  extern __shared__ __align__(16) float s_row[];  // C * S * S
+  extern __shared__ __align__(16) float s_row[];  // S * S rows of C + 4 floats
   __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
   __shared__ float s_ly[MAX_S], s_lx[MAX_S];
   const int r = blockIdx.x;
@@ -106,11 +107,16 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   const T* F = maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
   const int Wc = a.map_w[sc.plane];
   // Each thread blends VT consecutive channels (one 16-byte vector per neighbour cell); C / VT
-  // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.
+  // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.  The
+  // results are staged bin-major, one row of C + 4 floats per bin with the thread's 16-byte halves
+  // interleaved across the row (conflict-free writes), then read out in the output's channel-major
+  // order one float per thread: consecutive bins of a channel are 4 banks apart (row stride C + 4).
   constexpr int VT = 16 / sizeof(T);
   typedef T vec_t __attribute__((ext_vector_type(VT)));
   const int per_bin = C / VT, groups = blockDim.x / per_bin;
   const int lt = tid % per_bin, grp = tid / per_bin;
+  const int RSTR = C + 4;
+  constexpr int NQ = VT / 4;  // 16-byte float chunks per thread and bin
   if (grp < groups) {
     const int c0 = lt * VT;
     for (int bin = grp; bin < SS; bin += groups) {
@@ -122,18 +128,27 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       const vec_t a10 = *(const vec_t*)(F + ((int64_t)i1 * Wc + j0) * C + c0);
       const vec_t a11 = *(const vec_t*)(F + ((int64_t)i1 * Wc + j1) * C + c0);
 #pragma unroll
-      for (int q = 0; q < VT; ++q) {
-        const float v00 = to_f32(a00[q]), v01 = to_f32(a01[q]);
-        const float v10 = to_f32(a10[q]), v11 = to_f32(a11[q]);
-        const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
-        s_row[(c0 + q) * SS + bin] = top + ly * (bot - top);
+      for (int k = 0; k < NQ; ++k) {
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int q = 4 * k + e;
+          const float v00 = to_f32(a00[q]), v01 = to_f32(a01[q]);
+          const float v10 = to_f32(a10[q]), v11 = to_f32(a11[q]);
+          const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
+          o[e] = top + ly * (bot - top);
+        }
+        // chunk k of thread lt holds channels lt * VT + 4 k .. + 3
+        *(f32x4*)(s_row + bin * RSTR + (k * per_bin + lt) * 4) = o;
       }
     }
   }
   __syncthreads();
-  const int n4 = (C * SS) / 4;
-  for (int e = tid; e < n4; e += blockDim.x) ((f32x4*)dst)[e] = ((const f32x4*)s_row)[e];
-  for (int e = n4 * 4 + tid; e < C * SS; e += blockDim.x) dst[e] = s_row[e];
+  for (int e = tid; e < C * SS; e += blockDim.x) {
+    const int c = e / SS, bin = e - c * SS;
+    const int l = c / VT, q = c % VT;
+    dst[e] = s_row[bin * RSTR + ((q / 4) * per_bin + l) * 4 + (q % 4)];
+  }
   if (tid == 0) scale_out[r] = best;
   if (idx_out)
     for (int e = tid; e < SS; e += blockDim.x) {
@@ -149,7 +164,7 @@ int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, co
                           int32_t* d_idx, void* stream) {
   if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
   hipStream_t s = (hipStream_t)stream;
-  const size_t lds = sizeof(float) * (size_t)a.C * a.S * a.S;
+  const size_t lds = sizeof(float) * (size_t)(a.C + 4) * a.S * a.S;
   switch (dt) {
     case DN_F32:
       region_windows_kernel<float><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes, d_box_img,
