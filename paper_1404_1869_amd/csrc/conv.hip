@@ -7,10 +7,11 @@
 // chunk of 16 input channels and reuses it for every kernel tap, so each input element is read from
 // L2 once per output-channel block instead of once per tap.
 //
-//  conv1 (11x11, stride 4, 3 channels) reads channel-major planes.  Its k index runs over
-//  (channel, row ky in 0..11, column group of 4 in 0..2, column in group): each lane's 8 k values
-//  are two runs of 4 consecutive input pixels of one row, read as two 8-byte LDS loads; taps with
-//  ky = 11 or kx = 11 carry zero weights (144 k per channel instead of 121).
+//  conv1 (11x11, stride 4, 3 channels) reads channel-major planes.  Per input channel its 144 k
+//  values cover a 12 x 12 tap square (taps with ky = 11 or kx = 11 carry zero weights): k-step s
+//  (16 k) covers rows 4 (s / 3) .. + 3 and columns 4 (s % 3) .. + 3, and each lane's 8 k values are
+//  4 consecutive input pixels of one row and the 4 below them, read as two 8-byte LDS loads at
+//  offsets that do not depend on the lane.
 //  conv2..conv5 (stride 1, R x R, pad (R-1)/2, groups) read channels-last maps; k = (tap, channel),
 //  each lane's 8 k values are 8 consecutive channels of one pixel (one 16-byte LDS load).
 #include <algorithm>
@@ -23,7 +24,8 @@ namespace {
 
 // ------------------------------------------------------------------------------------------------
 // Packed weight layout
-//   conv1: [96][3][144] in dtype, k = (ky * 3 + kx / 4) * 4 + kx % 4 (ky, kx in 0..11, zero beyond 10)
+//   conv1: [96][3][144] in dtype, k = 16 s + 8 h + 4 j + e holds tap ky = 4 (s / 3) + 2 h + j,
+//          kx = 4 (s % 3) + e (zero where ky or kx is 11)
 //   conv2..5: [M][R*R][C/G] in dtype (tap-major, channels contiguous)
 //   biases: fp32 [M]
 // ------------------------------------------------------------------------------------------------
@@ -32,6 +34,10 @@ constexpr int L_C[5] = {3, 96, 256, 384, 384};
 constexpr int L_R[5] = {11, 5, 3, 3, 3};
 constexpr int L_G[5] = {1, 2, 1, 2, 2};
 constexpr int K1 = 144;  // conv1 packed k per input channel
+__host__ __device__ constexpr int conv1_ky(int k) {
+  return 4 * ((k >> 4) / 3) + 2 * ((k >> 3) & 1) + ((k >> 2) & 1);
+}
+__host__ __device__ constexpr int conv1_kx(int k) { return 4 * ((k >> 4) % 3) + (k & 3); }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -40,7 +46,7 @@ __global__ void pack_conv1_kernel(const float* __restrict__ w, T* __restrict__ o
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= 96 * 3 * K1) return;
   const int k = i % K1, mc = i / K1;  // mc = m * 3 + c
-  const int q = k >> 2, kx = (q % 3) * 4 + (k & 3), ky = q / 3;
+  const int ky = conv1_ky(k), kx = conv1_kx(k);
   float v = 0.f;
   if (ky < 11 && kx < 11) v = w[(mc * 11 + ky) * 11 + kx];
   out[i] = from_f32<T>(v);
@@ -80,10 +86,11 @@ __device__ inline float lds_frag16<float>(const float* p) {
 // ------------------------------------------------------------------------------------------------
 template <typename T>
 struct Conv1Cfg {
+  static_assert(std::is_same<T, float>::value, "16-bit storage uses the direct or persistent kernel");
   static constexpr int TH = 16, TW = 16;
-  static constexpr int HR = 72;                                       // halo rows / cols (4*15+12)
-  static constexpr int HS = std::is_same<T, float>::value ? 72 : 80;  // halo row stride
-  static constexpr int WS = K1 + (std::is_same<T, float>::value ? 1 : 8);
+  static constexpr int HR = 72;  // halo rows / cols (4*15+12)
+  static constexpr int HS = 72;  // halo row stride
+  static constexpr int WS = K1 + 1;
 };
 
 template <typename T>
@@ -139,33 +146,11 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
 #pragma unroll 3
     for (int ks = 0; ks < K1 / Op::KS; ++ks) {
       typename Op::frag a[2], b[3];
-      if constexpr (std::is_same<T, float>::value) {
-        const int k = ks * 2 + half;
-        const int q = k >> 2, ky = q / 3, kx = (q % 3) * 4 + (k & 3);
+      const int k = ks * 2 + half, ky = conv1_ky(k), kx = conv1_kx(k);
 #pragma unroll
-        for (int t = 0; t < 2; ++t) a[t] = s_in[(4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx];
+      for (int t = 0; t < 2; ++t) a[t] = s_in[(4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx];
 #pragma unroll
-        for (int mt = 0; mt < 3; ++mt) b[mt] = s_w[(mt * 32 + l32) * C::WS + k];
-      } else {
-        // two groups of 4 columns: q0 = 4 ks + 2 half and q0 + 1
-        const int q0 = 4 * ks + 2 * half;
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          typename Op::half_frag lo, hi;
-          {
-            const int ky = q0 / 3, kx = (q0 % 3) * 4;
-            lo = *(const typename Op::half_frag*)(s_in + (4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx);
-          }
-          {
-            const int q1 = q0 + 1, ky = q1 / 3, kx = (q1 % 3) * 4;
-            hi = *(const typename Op::half_frag*)(s_in + (4 * prow[t] + ky) * C::HS + 4 * pcol[t] + kx);
-          }
-          a[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        }
-#pragma unroll
-        for (int mt = 0; mt < 3; ++mt)
-          b[mt] = lds_frag16<T>(s_w + (mt * 32 + l32) * C::WS + ks * Op::KS + half * 8);
-      }
+      for (int mt = 0; mt < 3; ++mt) b[mt] = s_w[(mt * 32 + l32) * C::WS + k];
 #pragma unroll
       for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
@@ -290,15 +275,13 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     for (int c = 0; c < 3; ++c) {
 #pragma unroll
       for (int ks = 0; ks < K1 / 16; ++ks) {
-        // k-step ks of channel c: column groups q0 = 4 ks + 2 half and q0 + 1 (q = ky * 3 + kx / 4)
-        const int q0 = 4 * ks + 2 * half, q1 = q0 + 1;
-        const int o0 = (c * P::HR + q0 / 3) * P::HS + 4 * (q0 % 3);
-        const int o1 = (c * P::HR + q1 / 3) * P::HS + 4 * (q1 % 3);
+        // k-step ks of channel c: rows ky, ky + 1 (ky = 4 (ks / 3) + 2 half), columns 4 (ks % 3) + 0..3
+        const int o0 = (c * P::HR + 4 * (ks / 3) + 2 * half) * P::HS + 4 * (ks % 3);
         typename Op::frag x[2], w[3];
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
           const typename Op::half_frag lo = *(const typename Op::half_frag*)(hs + lpix[b] + o0);
-          const typename Op::half_frag hi = *(const typename Op::half_frag*)(hs + lpix[b] + o1);
+          const typename Op::half_frag hi = *(const typename Op::half_frag*)(hs + lpix[b] + o0 + P::HS);
           x[b] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         }
 #pragma unroll
@@ -621,6 +604,10 @@ struct Pieces {  // 1 KB LDS pieces, rounded up to a whole number per wave
   static constexpr int count(int slots, int waves) { return ((slots + 63) / 64 + waves - 1) / waves; }
 };
 
+// Wait until every vector-memory access of this wave has completed (vmcnt 0; other counters left
+// free), as an instruction the compiler's own wait bookkeeping sees.
+__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece, uint32_t voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds_piece,
                                            16, voff, 0, 0, 0);
@@ -717,7 +704,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
   const int nchunks = Cg / Cf::CC, nst = nchunks * R;
   load_halo(0, 0);
   load_w(0, 0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  wait_vmem();
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int chunk = st / R, ky = st - chunk * R;
@@ -739,7 +726,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
 #pragma unroll
         for (int t = 0; t < TN; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_vmem();
     __syncthreads();
   }
 
@@ -784,6 +771,184 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
         if (oy < H && ox < W)
           *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
       }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// conv1 for 16-bit storage with direct global->LDS loads (plane width a multiple of 8, 16-byte
+// aligned planes).  Output tiles of 16 x 16 pixels x 96 channels; a workgroup of 4 waves (96 channels
+// x 64 pixels each) walks tiles with the grid's stride, and two workgroups share a CU (78 KB of LDS
+// each).  A stage is one input channel of one tile: its 72 x 72 input halo (each row nine 16-byte
+// slots of plane data and one zero slot) and its 96 x 144 packed weights (18 slots per output
+// channel; for channels 16..31 of every 32-channel group the two slots of each 32-byte pair are
+// swapped, so that the 32 lanes of a half-wave reading one k-step's 16 bytes of 32 channels hit
+// distinct slots modulo 512 bytes).  Stages run back to back across tiles: the next stage (next
+// channel, or the first channel of the workgroup's next tile) loads while the current one computes,
+// with one vmcnt wait and one barrier per stage; within a stage, each wave reads k-step ks + 1's
+// fragments from LDS while k-step ks's MFMAs run.
+// ------------------------------------------------------------------------------------------------
+struct Conv1D {
+  static constexpr int TH = 16, TW = 16, HR = 72;
+  static constexpr int HSL = 10, HS = HSL * 8;  // halo row: slots, elements
+  static constexpr int WSL = K1 / 8;            // weight slots per output channel
+  static constexpr int NH = 12, NW = 27;        // 1 KB load pieces per stage: halo, weights
+  static constexpr int DH = (NH + 3) / 4, DW = (NW + 3) / 4;  // pieces per wave, at most
+  static constexpr int HALO_E = NH * 512, W_E = NW * 512, STAGE_E = HALO_E + W_E;
+};
+static_assert(Conv1D::NH * 64 >= Conv1D::HR * Conv1D::HSL, "halo pieces cover the halo");
+static_assert(Conv1D::NW * 64 >= 96 * Conv1D::WSL, "weight pieces cover the weights");
+
+template <typename T>
+__global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
+    const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
+    const float* __restrict__ bias, int H, int W, int Ho, int Wo, int64_t in_stride,
+    int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
+  using P = Conv1D;
+  using Op = Mfma<T>;
+  using frag = typename Op::frag;
+  using hfrag = typename Op::half_frag;
+  typedef T out4_t __attribute__((ext_vector_type(4)));
+  __shared__ __align__(1024) T s_mem[2 * P::STAGE_E];
+  auto halo_buf = [&](int b) { return s_mem + b * P::STAGE_E; };
+  auto w_buf = [&](int b) { return s_mem + b * P::STAGE_E + P::HALO_E; };
+
+  // XCD-aware rank: workgroups are dispatched round-robin over the 8 XCDs; rank r of XCD x is
+  // x * (workgroups per XCD) + i, and rank r takes tiles r, r + G, ..., so the tiles in flight on
+  // one XCD at a time are neighbours and share its L2.
+  const int G = gridDim.x, xcd = blockIdx.x % 8, per = G / 8, rem = G % 8;
+  const int rank = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int ntile = rank < ntiles ? (ntiles - rank + G - 1) / G : 0;
+  const __amdgpu_buffer_rsrc_t rsrc_w =
+      __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(96 * 3 * K1 * sizeof(T)), 0x00020000);
+  constexpr uint32_t OOB = 0x80000000u;
+  const uint32_t chan_bytes = (uint32_t)((int64_t)H * W * sizeof(T));
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  // This lane's slot in each of its wave's pieces (piece wave + 4 i): byte offsets for channel 0.
+  uint32_t hoff[P::DH], woff[P::DW];
+#pragma unroll
+  for (int i = 0; i < P::DW; ++i) {
+    const int q = (wave + 4 * i) * 64 + lane;
+    const int m = q / P::WSL, v = (q % P::WSL) ^ ((m >> 4) & 1);
+    woff[i] = m < 96 ? (uint32_t)((m * 3 * K1 + 8 * v) * sizeof(T)) : OOB;
+  }
+  __amdgpu_buffer_rsrc_t rsrc_in;
+  auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of tile t
+    const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
+    rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + plane * in_stride), 0,
+                                                (int)(3 * chan_bytes), 0x00020000);
+    const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
+#pragma unroll
+    for (int i = 0; i < P::DH; ++i) {
+      const int q = (wave + 4 * i) * 64 + lane;
+      const int row = q / P::HSL, r = q % P::HSL;
+      const int iy = iy0 + row, ix = ix0 + 8 * r;
+      const bool ok = row < P::HR && r < 9 && iy < H && ix < W;
+      hoff[i] = ok ? (uint32_t)(((int64_t)iy * W + ix) * sizeof(T)) : OOB;
+    }
+  };
+  auto load = [&](int buf, int c) {
+    const uint32_t ha = c * chan_bytes, wa = (uint32_t)(c * K1 * sizeof(T));
+#pragma unroll
+    for (int i = 0; i < P::DH; ++i)
+      if (wave + 4 * i < P::NH)
+        lds_direct16(rsrc_in, halo_buf(buf) + (wave + 4 * i) * 512,
+                     hoff[i] == OOB ? OOB : hoff[i] + ha);
+#pragma unroll
+    for (int i = 0; i < P::DW; ++i)
+      if (wave + 4 * i < P::NW)
+        lds_direct16(rsrc_w, w_buf(buf) + (wave + 4 * i) * 512, woff[i] == OOB ? OOB : woff[i] + wa);
+  };
+
+  // Lane bases: this lane's pixel (input row 4 prow + 2 half, column 4 pcol) per pixel tile, and its
+  // output channel's weight row at slot (half ^ swap); every k-step adds an offset common to all lanes.
+  int lpix[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int idx = wave * 64 + b * 32 + l32;
+    lpix[b] = (4 * (idx / P::TW) + 2 * half) * P::HS + 4 * (idx % P::TW);
+  }
+  const int lw = 8 * (P::WSL * l32 + (half ^ ((l32 >> 4) & 1)));
+  auto read = [&](const T* hs, const T* ws, int ks, frag* x, frag* w) {
+    // k-step ks: rows ky, ky + 1 (ky = 4 (ks / 3) + 2 half), columns 4 (ks % 3) + 0..3
+    const int o0 = 4 * (ks / 3) * P::HS + 4 * (ks % 3);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const hfrag lo = *(const hfrag*)(hs + lpix[b] + o0);
+      const hfrag hi = *(const hfrag*)(hs + lpix[b] + o0 + P::HS);
+      x[b] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+#pragma unroll
+    for (int mt = 0; mt < 3; ++mt) w[mt] = *(const frag*)(ws + lw + 8 * (P::WSL * 32 * mt + 2 * ks));
+  };
+
+  f32x16 acc[3][2];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+
+  if (ntile > 0) {
+    set_tile(rank);
+    load(0, 0);
+  }
+  wait_vmem();
+  __syncthreads();
+  for (int j = 0; j < ntile; ++j) {
+    const int t = rank + j * G;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      const int buf = (j + c) & 1;  // stage 3 j + c
+      if (c < 2) {
+        load(buf ^ 1, c + 1);
+      } else if (j + 1 < ntile) {
+        set_tile(t + G);
+        load(buf ^ 1, 0);
+      }
+      const T* hs = halo_buf(buf);
+      const T* ws = w_buf(buf);
+      frag xr[2][2], wr[2][3];
+      read(hs, ws, 0, xr[0], wr[0]);
+#pragma unroll
+      for (int ks = 0; ks < K1 / 16; ++ks) {
+        if (ks + 1 < K1 / 16) read(hs, ws, ks + 1, xr[(ks + 1) & 1], wr[(ks + 1) & 1]);
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[ks & 1][mt], xr[ks & 1][b], acc[mt][b]);
+      }
+      if (c == 2) {
+        // epilogue: bias + ReLU, 4 consecutive channels per store
+        const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
+        T* dst = out + plane * out_stride;
+#pragma unroll
+        for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int m = mt * 32 + 8 * q + 4 * half;
+            const f32x4 bv = *(const f32x4*)(bias + m);
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              const int idx = wave * 64 + b * 32 + l32;
+              const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
+              if (oy < Ho && ox < Wo) {
+                out4_t v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  v[e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
+                *(out4_t*)(dst + ((int64_t)oy * Wo + ox) * 96 + m) = v;
+              }
+            }
+          }
+#pragma unroll
+        for (int a = 0; a < 3; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+      }
+      wait_vmem();
+      __syncthreads();
     }
   }
 }
@@ -839,9 +1004,18 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
       conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
                                                       out_stride, tiles_x, tiles_y);
     } else {
-      const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
-      conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
-                                                     out_stride, tiles_x, tiles_y, (int)blocks);
+      // Direct loads take 16-byte slots of plane rows at 32-bit byte offsets within one plane.
+      const bool direct = W % 8 == 0 && in_stride % 8 == 0 && ((uintptr_t)in & 15) == 0 &&
+                          (int64_t)3 * H * W * (int64_t)sizeof(T) < 0x7fffffffLL;
+      if (direct) {
+        const int grid = (int)std::min<int64_t>(blocks, 2 * device_cu_count());
+        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+                                                   out_stride, tiles_x, tiles_y, (int)blocks);
+      } else {
+        const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
+        conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+                                                       out_stride, tiles_x, tiles_y, (int)blocks);
+      }
     }
     return (int)hipGetLastError();
   }

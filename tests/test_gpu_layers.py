@@ -42,7 +42,10 @@ def oracle_weights(dt):
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("shape", [(2, 227, 227), (1, 300, 263), (1, 83, 51)])
+# Widths that are not multiples of 8 take the register-staged kernel, the others the direct-load one
+# (16-bit types); 1200 x 1200 is a full stitched plane.
+@pytest.mark.parametrize("shape", [(2, 227, 227), (1, 300, 263), (1, 83, 51), (2, 232, 240),
+                                   (3, 48, 64), (1, 11, 16), (1, 1200, 1200)])
 def test_conv1(D, dt, shape):
     n, H, W = shape
     rng = np.random.default_rng(H * 7 + W)
