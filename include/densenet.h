@@ -119,7 +119,9 @@ int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_s
 /* Image(s) in -> centred, padded, stitched planes out (Sec. 3.1, 3.2), one fused kernel.
  * d_images: uint8 [n_img][3][H][W].  d_planes: n_img consecutive blocks of *image_elems elements of
  * `dtype`, image b's plane j at b * image_elems + planes[j].offset, or NULL for a size query.
- * geom/planes/n_planes/image_elems as densenet_plan_pyramid. */
+ * *bytes_needed (and so planes_bytes) also covers a trailing scratch region after the planes
+ * (8 * H * W * n_img bytes, 256-byte aligned) that the call uses while it runs; its contents
+ * afterwards are unspecified.  geom/planes/n_planes/image_elems as densenet_plan_pyramid. */
 int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                            const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
                            size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,

@@ -129,7 +129,9 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     if (n_img <= 0) return fail(DN_E_INVALID_ARG, "n_img must be positive");
     int st = densenet_plan_pyramid(H, W, p, geom, planes, max_planes, n_planes, image_elems);
     if (st != DN_OK) return st;
-    const size_t need = (size_t)n_img * (size_t)*image_elems * dtype_size(dtype);
+    const size_t planes_end = ((size_t)n_img * (size_t)*image_elems * dtype_size(dtype) + 255) &
+                              ~(size_t)255;
+    const size_t need = planes_end + (size_t)n_img * 8 * (size_t)H * (size_t)W;
     *bytes_needed = need;
     if (!d_planes) return DN_OK;
     if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
@@ -161,7 +163,8 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
       mw = std::max(mw, planes[j].w);
     }
     TraceScope trace("build_planes", stream);
-    return hip_status(launch_build_planes(d_images, n_img, a, pl, mh, mw, dtype, d_planes, stream),
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, mh, mw, dtype, d_planes,
+                                          (uint8_t*)d_planes + planes_end, stream),
                       "build_planes launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");

@@ -64,8 +64,10 @@ struct PyrPlanes {
   PyrPlane p[DN_MAX_PLANES_PER_IMAGE];
 };
 
+// d_pairs: scratch of 8 * H * W * n_img bytes for the pair image (see pyramid.hip).
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, void* stream);
+                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_pairs,
+                        void* stream);
 
 // Packed weight blob: offsets in bytes of each layer's weights and fp32 biases.
 struct PackedLayout {

@@ -2,11 +2,12 @@
 // centring (Sec. 3.2), the 16-px border (ramp to the mean, or the mean itself) and stitching onto
 // planes with a zero background (Sec. 3.1), fused into one pass that writes every plane pixel once.
 //
-// Each thread produces 4 consecutive pixels of a plane row and stores them as one vector per channel;
-// a wave covers 256 columns.  The owner scale is found among the scales of the workgroup's plane
-// (a uniform skip of the others).  The source image (a few MB) stays in L2 / MALL for the gathers.
-// The half-pixel source coordinate ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers;
-// only the blend is fp32.
+// A pre-pass rewrites each image as a pair image: 8 bytes per source pixel x holding the three
+// channels at columns x and min(x + 1, W - 1), so that one bilinear row tap, all channels, is a single
+// 8-byte load.  The builder then produces 4 consecutive plane pixels per thread and stores them as one
+// vector per channel; a wave covers 256 columns.  The pair images (8 bytes per image pixel) stay in
+// L2 / MALL for the gathers.  The half-pixel source coordinate ((2 y + 1) H - h) / (2 h) is formed
+// exactly in 32-bit integers; only the blend is fp32.
 #include "common.h"
 
 namespace dn {
@@ -41,101 +42,176 @@ __device__ inline float border_weight(int d, int pad, bool ramp) {
   return (float)(pad + 1 - d) / (float)(pad + 1);
 }
 
-// One thread per PX consecutive pixels of a plane row; a wave covers 64 * PX columns.  In stitched
-// planes every rectangle edge is a multiple of 16 px, and a per-scale plane is its scale's rectangle,
-// so an aligned group of PX pixels has a single owner (or none), found among the plane's own scales.
+// Workgroup tile: 16 plane rows x 64 * PX columns; each lane owns PX consecutive columns and the
+// four waves take the tile's rows in turn.  In stitched planes every rectangle edge is a multiple of
+// 16 px, and a per-scale plane is its scale's rectangle, so each 16 x 16 cell of a 16-row-aligned tile
+// has a single owner scale (or none).  Per tile the workgroup finds the owner of each of its 16 cells
+// and tabulates, per (cell, row), the two source rows, the row fraction and the row's border weight;
+// each lane computes its columns' source coordinates and border weights once and then only blends
+// per row.
+constexpr int TROWS = 16;                // rows per tile
+constexpr int TCELLS = 64 * PX / 16;     // 16-px cells per tile row
+
+// Pair image: pairs[b][y][x] = {R[x], R[x1], G[x], G[x1], B[x], B[x1], 0, 0}, x1 = min(x + 1, W - 1),
+// one thread per pixel.
+__global__ __launch_bounds__(256) void pair_image_kernel(const uint8_t* __restrict__ img, int H, int W,
+                                                         uint2* __restrict__ pairs) {
+  const int x = blockIdx.x * 256 + threadIdx.x, y = blockIdx.y, b = blockIdx.z;
+  if (x >= W) return;
+  const int64_t HW = (int64_t)H * W;
+  const uint8_t* row = img + (int64_t)b * 3 * HW + (int64_t)y * W;
+  const int x1 = min(x + 1, W - 1);
+  const uint32_t r0 = row[x], r1 = row[x1], g0 = row[HW + x], g1 = row[HW + x1];
+  const uint32_t b0 = row[2 * HW + x], b1 = row[2 * HW + x1];
+  pairs[(int64_t)b * HW + (int64_t)y * W + x] =
+      make_uint2(r0 | (r1 << 8) | (g0 << 16) | (g1 << 24), b0 | (b1 << 8));
+}
+
+struct RowEntry {
+  uint32_t r0, r1;  // source row offsets sy0 * W, sy1 * W (pixels)
+  float ly, wy;     // row fraction, row border weight (0: background)
+};
+
 template <typename T>
-__global__ __launch_bounds__(256) void build_planes_kernel(const uint8_t* __restrict__ img,
+__global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restrict__ pairs,
                                                            PyrArgs a, PyrPlanes pl,
                                                            T* __restrict__ out) {
   typedef T vec_t __attribute__((ext_vector_type(PX)));
+  static_assert(TCELLS * TROWS == 256, "one table entry per thread");
+  __shared__ int s_own[TCELLS];
+  __shared__ RowEntry s_row[TCELLS * TROWS];
   const int z = blockIdx.z;
   const int b = z / pl.n, j = z - b * pl.n;
   const int PH = pl.p[j].h, PW = pl.p[j].w;
-  const int x0 = (blockIdx.x * 64 + (threadIdx.x & 63)) * PX;
-  const int y = blockIdx.y * 4 + (threadIdx.x >> 6);
-  if (x0 >= PW || y >= PH) return;
-
-  float v[PX][3];
-#pragma unroll
-  for (int i = 0; i < PX; ++i) v[i][0] = v[i][1] = v[i][2] = 0.f;
-
-  int owner = -1;
+  const int tx0 = blockIdx.x * 64 * PX, ty0 = blockIdx.y * TROWS;
+  if (tx0 >= PW || ty0 >= PH) return;  // uniform per workgroup
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int f0 = a.plane_first[j], f1 = f0 + a.plane_count[j];
-  for (int e = f0; e < f1; ++e) {
-    const PyrScale& s = a.s[e];
-    if (y >= s.y && y < s.y + s.rh && x0 >= s.x && x0 < s.x + s.rw) {
-      owner = e;
-      break;
+
+  if (tid < TCELLS) {
+    const int cx = tx0 + 16 * tid;
+    int owner = -1;
+    for (int e = f0; e < f1 && cx < PW; ++e) {
+      const PyrScale& s = a.s[e];
+      if (ty0 >= s.y && ty0 < s.y + s.rh && cx >= s.x && cx < s.x + s.rw) {
+        owner = e;
+        break;
+      }
     }
+    s_own[tid] = owner;
+  }
+  __syncthreads();
+  {
+    const int cell = tid / TROWS, r = tid % TROWS, y = ty0 + r;
+    const int e = s_own[cell];
+    RowEntry re{0u, 0u, 0.f, 0.f};
+    if (e >= 0 && y < PH) {
+      const PyrScale& s = a.s[e];
+      const int vy = y - s.y - a.pad;
+      const int dy = max(0, max(-vy, vy - (s.h - 1)));
+      re.wy = border_weight(dy, a.pad, a.ramp);
+      int sy0, sy1;
+      src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, 1.0 / (2.0 * s.h), sy0, sy1, re.ly);
+      re.r0 = (uint32_t)sy0 * (uint32_t)a.W;
+      re.r1 = (uint32_t)sy1 * (uint32_t)a.W;
+    }
+    s_row[tid] = re;
+  }
+  __syncthreads();
+
+  // This lane's columns: owner, border weights, source columns and fractions.
+  const int x0 = tx0 + lane * PX, cell = lane * PX / 16;
+  const int owner = x0 < PW ? s_own[cell] : -1;
+  float wx[PX], lx[PX];
+  uint32_t sx0[PX];
+#pragma unroll
+  for (int i = 0; i < PX; ++i) {
+    wx[i] = 0.f;
+    lx[i] = 0.f;
+    sx0[i] = 0u;
   }
   if (owner >= 0) {
-    const PyrScale s = a.s[owner];
-    const int vy = y - s.y - a.pad;
-    const int dy = max(0, max(-vy, vy - (s.h - 1)));
-    const float wy = border_weight(dy, a.pad, a.ramp);
-    if (wy != 0.f) {
-      const uint8_t* I = img + (int64_t)b * 3 * a.H * a.W;
-      const int64_t HW = (int64_t)a.H * a.W;
-      int sy0, sy1;
-      float ly;
-      src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, 1.0 / (2.0 * s.h), sy0, sy1, ly);
-      const double inv2w = 1.0 / (2.0 * s.w);
-      const int r0 = sy0 * a.W, r1 = sy1 * a.W;
+    const PyrScale& s = a.s[owner];
+    const double inv2w = 1.0 / (2.0 * s.w);
+#pragma unroll
+    for (int i = 0; i < PX; ++i) {
+      const int ux = x0 + i - s.x - a.pad;
+      const int dx = max(0, max(-ux, ux - (s.w - 1)));
+      wx[i] = x0 + i < PW ? border_weight(dx, a.pad, a.ramp) : 0.f;
+      int c0, c1;  // c1 = min(c0 + 1, W - 1) is the pair image's second column
+      src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, inv2w, c0, c1, lx[i]);
+      sx0[i] = (uint32_t)c0;
+    }
+  }
+  const uint2* P = pairs + (int64_t)b * a.H * a.W;
+  T* o = out + (int64_t)b * pl.image_elems + pl.p[j].offset;
+  const int64_t plane = (int64_t)PH * PW;
+  const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
+
+  for (int r = wave; r < TROWS; r += 4) {
+    const int y = ty0 + r;
+    if (y >= PH) break;  // uniform per wave
+    const RowEntry re = s_row[cell * TROWS + r];
+    float v[PX][3];
+#pragma unroll
+    for (int i = 0; i < PX; ++i) v[i][0] = v[i][1] = v[i][2] = 0.f;
+    if (owner >= 0 && re.wy != 0.f) {
 #pragma unroll
       for (int i = 0; i < PX; ++i) {
-        const int ux = x0 + i - s.x - a.pad;
-        const int dx = max(0, max(-ux, ux - (s.w - 1)));
-        const float wgt = wy * border_weight(dx, a.pad, a.ramp);
-        if (wgt == 0.f || x0 + i >= PW) continue;
-        int sx0, sx1;
-        float lx;
-        src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, inv2w, sx0, sx1, lx);
+        const float wgt = re.wy * wx[i];
+        if (wgt == 0.f) continue;
+        const uint2 t0 = P[re.r0 + sx0[i]], t1 = P[re.r1 + sx0[i]];  // rows sy0, sy1
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-          const uint8_t* P = I + c * HW;
-          const float i00 = P[r0 + sx0], i01 = P[r0 + sx1];
-          const float i10 = P[r1 + sx0], i11 = P[r1 + sx1];
-          const float top = i00 + lx * (i01 - i00), bot = i10 + lx * (i11 - i10);
-          v[i][c] = (top + ly * (bot - top) - a.mean[c]) * wgt;
+          // channel c's pair: 16 bits at bit 16 c of the 8-byte word
+          const uint32_t w0 = c < 2 ? t0.x : t0.y, w1 = c < 2 ? t1.x : t1.y;
+          const int sh = c == 1 ? 16 : 0;
+          const float i00 = (float)((w0 >> sh) & 255u), i01 = (float)((w0 >> (sh + 8)) & 255u);
+          const float i10 = (float)((w1 >> sh) & 255u), i11 = (float)((w1 >> (sh + 8)) & 255u);
+          const float top = i00 + lx[i] * (i01 - i00), bot = i10 + lx[i] * (i11 - i10);
+          v[i][c] = (top + re.ly * (bot - top) - a.mean[c]) * wgt;
         }
       }
     }
-  }
-  T* o = out + (int64_t)b * pl.image_elems + pl.p[j].offset;
-  const int64_t plane = (int64_t)PH * PW, at = (int64_t)y * PW + x0;
-  if ((PW % PX) == 0) {  // whole, aligned vectors (uniform per plane)
+    if (x0 >= PW) continue;
+    const int64_t at = (int64_t)y * PW + x0;
+    if (vec_rows) {
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
-      vec_t r;
+      for (int c = 0; c < 3; ++c) {
+        vec_t rv;
 #pragma unroll
-      for (int i = 0; i < PX; ++i) r[i] = from_f32<T>(v[i][c]);
-      *(vec_t*)(o + c * plane + at) = r;
+        for (int i = 0; i < PX; ++i) rv[i] = from_f32<T>(v[i][c]);
+        *(vec_t*)(o + c * plane + at) = rv;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 3; ++c)
+#pragma unroll
+        for (int i = 0; i < PX; ++i)
+          if (x0 + i < PW) o[c * plane + at + i] = from_f32<T>(v[i][c]);
     }
-  } else {
-#pragma unroll
-    for (int c = 0; c < 3; ++c)
-#pragma unroll
-      for (int i = 0; i < PX; ++i)
-        if (x0 + i < PW) o[c * plane + at + i] = from_f32<T>(v[i][c]);
   }
 }
 
 }  // namespace
 
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, void* stream) {
-  dim3 grid((max_w + 64 * PX - 1) / (64 * PX), (max_h + 3) / 4, n_img * pl.n);
+                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_pairs,
+                        void* stream) {
   hipStream_t s = (hipStream_t)stream;
+  uint2* pairs = (uint2*)d_pairs;
+  pair_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pairs);
+  dim3 grid((max_w + 64 * PX - 1) / (64 * PX), (max_h + TROWS - 1) / TROWS, n_img * pl.n);
   switch (dt) {
     case DN_F32:
-      build_planes_kernel<float><<<grid, 256, 0, s>>>(d_img, a, pl, (float*)d_out);
+      build_planes_kernel<float><<<grid, 256, 0, s>>>(pairs, a, pl, (float*)d_out);
       break;
     case DN_F16:
-      build_planes_kernel<_Float16><<<grid, 256, 0, s>>>(d_img, a, pl, (_Float16*)d_out);
+      build_planes_kernel<_Float16><<<grid, 256, 0, s>>>(pairs, a, pl, (_Float16*)d_out);
       break;
     case DN_BF16:
-      build_planes_kernel<__bf16><<<grid, 256, 0, s>>>(d_img, a, pl, (__bf16*)d_out);
+      build_planes_kernel<__bf16><<<grid, 256, 0, s>>>(pairs, a, pl, (__bf16*)d_out);
       break;
   }
   return (int)hipGetLastError();

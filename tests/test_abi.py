@@ -52,13 +52,15 @@ def test_size_queries_without_device():
                                     ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
                                     ctypes.byref(e), None) == 0
     assert n.value == 6 and e.value == 6 * 3 * 1200 * 1200
-    assert need.value == 16 * e.value * 2
+    # the planes, then the pair-image scratch (8 bytes per image pixel) 256-byte aligned after them
+    full = (16 * e.value * 2 + 255) // 256 * 256 + 16 * 8 * 768 * 1024
+    assert need.value == full
     # short buffer: error, needed size still reported (no device work happens)
     fake = ctypes.c_void_p(256)
     assert L.densenet_build_pyramid(fake, 16, 768, 1024, ctypes.byref(p), D.DN_BF16, fake, 10,
                                     ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
                                     ctypes.byref(e), None) == D.DN_E_BUFFER_TOO_SMALL
-    assert need.value == 16 * e.value * 2
+    assert need.value == full
     assert L.densenet_build_pyramid(None, 1, 768, 1024, ctypes.byref(p), 9, None, 0,
                                     ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
                                     ctypes.byref(e), None) == D.DN_E_UNSUPPORTED

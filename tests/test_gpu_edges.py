@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_1404_1869_amd import synth
-from tests.parity import assert_layer_close, chw, round_to
+from tests.parity import assert_layer_close, chw, round_to, ulp
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -56,6 +56,28 @@ def test_ragged_image_small_stitched_planes(D, dt):
     for j, pl in enumerate(planes):
         ref = oracle.net(pl.astype(np.float32), W7)
         assert_layer_close(chw(maps[j].float().cpu().numpy()), ref, dt, f"ragged plane {j}")
+
+
+@pytest.mark.parametrize("W", [4000, 3999])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_planes_strongly_reduced_wide_image(D, W, dt):
+    """Scales 0.3 .. 0.106 of a 4000-px-wide image: at the two smaller ones a wave's 256 plane
+    columns need more source columns than the builder stages, so those taps are gathered from the
+    image directly; rows of 4000 px start on 4-byte boundaries, rows of 3999 px do not."""
+    H = 40
+    img = synth.image(91, H, W)
+    p = D.pyramid_params(4, 2, base_scale=0.3, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=64,
+                         plane_w=1248, mean=synth.IMAGENET_MEAN)
+    planes, plan = D.densenet_build_pyramid(torch.from_numpy(img).cuda()[None], p, DTS[dt])
+    op = oracle.plan(H, W, 4, 2, 0.3, 0, 16, 64, 1248)
+    ref = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    assert len(plan.planes) == op.n_planes
+    for j, d in enumerate(plan.planes):
+        got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        if dt == "f32":
+            assert np.max(np.abs(got - ref[j])) <= 1e-5 * 255, f"plane {j}"
+        else:
+            assert np.all(np.abs(got - ref[j]) <= 0.5 * ulp(ref[j], dt) + 1e-3), f"plane {j}"
 
 
 def test_smallest_plane_with_a_conv5_cell(D):
