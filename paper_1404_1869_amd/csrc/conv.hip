@@ -786,7 +786,8 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
 // distinct slots modulo 512 bytes).  Stages run back to back across tiles: the next stage (next
 // channel, or the first channel of the workgroup's next tile) loads while the current one computes,
 // with one vmcnt wait and one barrier per stage; within a stage, each wave reads k-step ks + 1's
-// fragments from LDS while k-step ks's MFMAs run.
+// fragments from LDS while k-step ks's MFMAs run.  A tile's outputs leave through LDS, as whole
+// pixel rows.
 // ------------------------------------------------------------------------------------------------
 struct Conv1D {
   static constexpr int TH = 16, TW = 16, HR = 72;
@@ -795,7 +796,9 @@ struct Conv1D {
   static constexpr int NH = 12, NW = 27;        // 1 KB load pieces per stage: halo, weights
   static constexpr int DH = (NH + 3) / 4, DW = (NW + 3) / 4;  // pieces per wave, at most
   static constexpr int HALO_E = NH * 512, W_E = NW * 512, STAGE_E = HALO_E + W_E;
+  static constexpr int SROW = 104;  // epilogue staging: elements per pixel row (96 + 8 padding)
 };
+static_assert(4 * 32 * Conv1D::SROW <= Conv1D::STAGE_E, "epilogue staging fits one stage buffer");
 static_assert(Conv1D::NH * 64 >= Conv1D::HR * Conv1D::HSL, "halo pieces cover the halo");
 static_assert(Conv1D::NW * 64 >= 96 * Conv1D::WSL, "weight pieces cover the weights");
 
@@ -809,9 +812,12 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   using frag = typename Op::frag;
   using hfrag = typename Op::half_frag;
   typedef T out4_t __attribute__((ext_vector_type(4)));
+  typedef T vec8_t __attribute__((ext_vector_type(8)));
   __shared__ __align__(1024) T s_mem[2 * P::STAGE_E];
+  __shared__ __align__(16) float s_bias[96];
   auto halo_buf = [&](int b) { return s_mem + b * P::STAGE_E; };
   auto w_buf = [&](int b) { return s_mem + b * P::STAGE_E + P::HALO_E; };
+  if (threadIdx.x < 96) s_bias[threadIdx.x] = bias[threadIdx.x];
 
   // XCD-aware rank: workgroups are dispatched round-robin over the 8 XCDs; rank r of XCD x is
   // x * (workgroups per XCD) + i, and rank r takes tiles r, r + G, ..., so the tiles in flight on
@@ -920,28 +926,36 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
           for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[ks & 1][mt], xr[ks & 1][b], acc[mt][b]);
       }
       if (c == 2) {
-        // epilogue: bias + ReLU, 4 consecutive channels per store
+        // Epilogue: bias + ReLU, staged per wave in the stage buffer just consumed (once every wave
+        // has finished reading it), 32 pixels at a time with rows padded to 104 channels; then whole
+        // 192-byte pixel rows are written with 16-byte stores.
+        __syncthreads();
         const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
         T* dst = out + plane * out_stride;
+        T* stg = halo_buf(buf) + wave * (32 * P::SROW);
 #pragma unroll
-        for (int mt = 0; mt < 3; ++mt)
+        for (int b = 0; b < 2; ++b) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int m = mt * 32 + 8 * q + 4 * half;
-            const f32x4 bv = *(const f32x4*)(bias + m);
+          for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-              const int idx = wave * 64 + b * 32 + l32;
-              const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
-              if (oy < Ho && ox < Wo) {
-                out4_t v;
+            for (int q = 0; q < 4; ++q) {
+              const int m = mt * 32 + 8 * q + 4 * half;
+              const f32x4 bv = *(const f32x4*)(s_bias + m);
+              out4_t v;
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  v[e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
-                *(out4_t*)(dst + ((int64_t)oy * Wo + ox) * 96 + m) = v;
-              }
+              for (int e = 0; e < 4; ++e)
+                v[e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
+              *(out4_t*)(stg + l32 * P::SROW + m) = v;
             }
+#pragma unroll
+          for (int it = 0; it < 6; ++it) {  // 32 pixels x 12 chunks of 8 channels
+            const int u = it * 64 + lane, p = u / 12, ch = u % 12;
+            const vec8_t v = *(const vec8_t*)(stg + p * P::SROW + 8 * ch);
+            const int idx = wave * 64 + b * 32 + p;
+            const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
+            if (oy < Ho && ox < Wo) *(vec8_t*)(dst + ((int64_t)oy * Wo + ox) * 96 + 8 * ch) = v;
           }
+        }
 #pragma unroll
         for (int a = 0; a < 3; ++a)
 #pragma unroll
