@@ -120,7 +120,7 @@ int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_s
  * d_images: uint8 [n_img][3][H][W].  d_planes: n_img consecutive blocks of *image_elems elements of
  * `dtype`, image b's plane j at b * image_elems + planes[j].offset, or NULL for a size query.
  * *bytes_needed (and so planes_bytes) also covers a trailing scratch region after the planes
- * (8 * H * W * n_img bytes, 256-byte aligned) that the call uses while it runs; its contents
+ * (4 * H * W * n_img bytes, 256-byte aligned) that the call uses while it runs; its contents
  * afterwards are unspecified.  geom/planes/n_planes/image_elems as densenet_plan_pyramid. */
 int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                            const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,

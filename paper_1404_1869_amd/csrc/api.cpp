@@ -131,7 +131,7 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     if (st != DN_OK) return st;
     const size_t planes_end = ((size_t)n_img * (size_t)*image_elems * dtype_size(dtype) + 255) &
                               ~(size_t)255;
-    const size_t need = planes_end + (size_t)n_img * 8 * (size_t)H * (size_t)W;
+    const size_t need = planes_end + (size_t)n_img * 4 * (size_t)H * (size_t)W;
     *bytes_needed = need;
     if (!d_planes) return DN_OK;
     if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");

@@ -64,9 +64,9 @@ struct PyrPlanes {
   PyrPlane p[DN_MAX_PLANES_PER_IMAGE];
 };
 
-// d_pairs: scratch of 8 * H * W * n_img bytes for the pair image (see pyramid.hip).
+// d_scratch: 4 * H * W * n_img bytes (4-byte aligned) for the pixel-interleaved image.
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_pairs,
+                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_scratch,
                         void* stream);
 
 // Packed weight blob: offsets in bytes of each layer's weights and fp32 biases.

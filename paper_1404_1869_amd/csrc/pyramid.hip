@@ -2,11 +2,11 @@
 // centring (Sec. 3.2), the 16-px border (ramp to the mean, or the mean itself) and stitching onto
 // planes with a zero background (Sec. 3.1), fused into one pass that writes every plane pixel once.
 //
-// A pre-pass rewrites each image as a pair image: 8 bytes per source pixel x holding the three
-// channels at columns x and min(x + 1, W - 1), so that one bilinear row tap, all channels, is a single
-// 8-byte load.  The builder then produces 4 consecutive plane pixels per thread and stores them as one
-// vector per channel; a wave covers 256 columns.  The pair images (8 bytes per image pixel) stay in
-// L2 / MALL for the gathers.  The half-pixel source coordinate ((2 y + 1) H - h) / (2 h) is formed
+// A pre-pass rewrites each image pixel-interleaved, 4 bytes per pixel (R, G, B, 0), so that one
+// bilinear tap of all three channels is a single 4-byte load, and one image (3 MB at 768 x 1024) fits
+// an XCD's L2.  The builder then produces 4 consecutive plane pixels per thread and stores them as
+// one vector per channel; a wave covers 256 columns.  Workgroups are ordered so that each XCD works
+// through a contiguous range of images and planes.  The half-pixel source coordinate ((2 y + 1) H - h) / (2 h) is formed
 // exactly in 32-bit integers; only the blend is fp32.
 #include "common.h"
 
@@ -52,19 +52,15 @@ __device__ inline float border_weight(int d, int pad, bool ramp) {
 constexpr int TROWS = 16;                // rows per tile
 constexpr int TCELLS = 64 * PX / 16;     // 16-px cells per tile row
 
-// Pair image: pairs[b][y][x] = {R[x], R[x1], G[x], G[x1], B[x], B[x1], 0, 0}, x1 = min(x + 1, W - 1),
-// one thread per pixel.
-__global__ __launch_bounds__(256) void pair_image_kernel(const uint8_t* __restrict__ img, int H, int W,
-                                                         uint2* __restrict__ pairs) {
+// Pixel image: pix[b][y][x] = R | G << 8 | B << 16, one thread per pixel.
+__global__ __launch_bounds__(256) void pixel_image_kernel(const uint8_t* __restrict__ img, int H, int W,
+                                                          uint32_t* __restrict__ pix) {
   const int x = blockIdx.x * 256 + threadIdx.x, y = blockIdx.y, b = blockIdx.z;
   if (x >= W) return;
   const int64_t HW = (int64_t)H * W;
   const uint8_t* row = img + (int64_t)b * 3 * HW + (int64_t)y * W;
-  const int x1 = min(x + 1, W - 1);
-  const uint32_t r0 = row[x], r1 = row[x1], g0 = row[HW + x], g1 = row[HW + x1];
-  const uint32_t b0 = row[2 * HW + x], b1 = row[2 * HW + x1];
-  pairs[(int64_t)b * HW + (int64_t)y * W + x] =
-      make_uint2(r0 | (r1 << 8) | (g0 << 16) | (g1 << 24), b0 | (b1 << 8));
+  const uint32_t r0 = row[x], g0 = row[HW + x], b0 = row[2 * HW + x];
+  pix[(int64_t)b * HW + (int64_t)y * W + x] = r0 | (g0 << 8) | (b0 << 16);
 }
 
 struct RowEntry {
@@ -73,17 +69,25 @@ struct RowEntry {
 };
 
 template <typename T>
-__global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restrict__ pairs,
+__global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __restrict__ pix,
                                                            PyrArgs a, PyrPlanes pl,
-                                                           T* __restrict__ out) {
+                                                           T* __restrict__ out, int tiles_x,
+                                                           int tiles_y) {
   typedef T vec_t __attribute__((ext_vector_type(PX)));
-  static_assert(TCELLS * TROWS == 256, "one table entry per thread");
+  static_assert(TCELLS <= 256, "one owner search per thread");
   __shared__ int s_own[TCELLS];
   __shared__ RowEntry s_row[TCELLS * TROWS];
-  const int z = blockIdx.z;
+  // XCD-aware order over a flat grid: XCD x takes a contiguous range of (image, plane, row tile,
+  // column tile) indices, so the tiles in flight on one XCD read the same image from its L2.
+  const int nbk = gridDim.x, xcd = blockIdx.x % 8, per = nbk / 8, rem = nbk % 8;
+  int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int gx = bid % tiles_x;
+  bid /= tiles_x;
+  const int gy = bid % tiles_y;
+  const int z = bid / tiles_y;
   const int b = z / pl.n, j = z - b * pl.n;
   const int PH = pl.p[j].h, PW = pl.p[j].w;
-  const int tx0 = blockIdx.x * 64 * PX, ty0 = blockIdx.y * TROWS;
+  const int tx0 = gx * 64 * PX, ty0 = gy * TROWS;
   if (tx0 >= PW || ty0 >= PH) return;  // uniform per workgroup
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -102,8 +106,8 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
     s_own[tid] = owner;
   }
   __syncthreads();
-  {
-    const int cell = tid / TROWS, r = tid % TROWS, y = ty0 + r;
+  for (int ent = tid; ent < TCELLS * TROWS; ent += 256) {
+    const int cell = ent / TROWS, r = ent % TROWS, y = ty0 + r;
     const int e = s_own[cell];
     RowEntry re{0u, 0u, 0.f, 0.f};
     if (e >= 0 && y < PH) {
@@ -116,7 +120,7 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
       re.r0 = (uint32_t)sy0 * (uint32_t)a.W;
       re.r1 = (uint32_t)sy1 * (uint32_t)a.W;
     }
-    s_row[tid] = re;
+    s_row[ent] = re;
   }
   __syncthreads();
 
@@ -124,12 +128,12 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
   const int x0 = tx0 + lane * PX, cell = lane * PX / 16;
   const int owner = x0 < PW ? s_own[cell] : -1;
   float wx[PX], lx[PX];
-  uint32_t sx0[PX];
+  uint32_t sx0[PX], sx1[PX];
 #pragma unroll
   for (int i = 0; i < PX; ++i) {
     wx[i] = 0.f;
     lx[i] = 0.f;
-    sx0[i] = 0u;
+    sx0[i] = sx1[i] = 0u;
   }
   if (owner >= 0) {
     const PyrScale& s = a.s[owner];
@@ -139,12 +143,13 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
       const int ux = x0 + i - s.x - a.pad;
       const int dx = max(0, max(-ux, ux - (s.w - 1)));
       wx[i] = x0 + i < PW ? border_weight(dx, a.pad, a.ramp) : 0.f;
-      int c0, c1;  // c1 = min(c0 + 1, W - 1) is the pair image's second column
+      int c0, c1;  // c1 = min(c0 + 1, W - 1)
       src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, inv2w, c0, c1, lx[i]);
       sx0[i] = (uint32_t)c0;
+      sx1[i] = (uint32_t)c1;
     }
   }
-  const uint2* P = pairs + (int64_t)b * a.H * a.W;
+  const uint32_t* P = pix + (int64_t)b * a.H * a.W;
   T* o = out + (int64_t)b * pl.image_elems + pl.p[j].offset;
   const int64_t plane = (int64_t)PH * PW;
   const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
@@ -161,14 +166,13 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
       for (int i = 0; i < PX; ++i) {
         const float wgt = re.wy * wx[i];
         if (wgt == 0.f) continue;
-        const uint2 t0 = P[re.r0 + sx0[i]], t1 = P[re.r1 + sx0[i]];  // rows sy0, sy1
+        const uint32_t q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
+        const uint32_t q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-          // channel c's pair: 16 bits at bit 16 c of the 8-byte word
-          const uint32_t w0 = c < 2 ? t0.x : t0.y, w1 = c < 2 ? t1.x : t1.y;
-          const int sh = c == 1 ? 16 : 0;
-          const float i00 = (float)((w0 >> sh) & 255u), i01 = (float)((w0 >> (sh + 8)) & 255u);
-          const float i10 = (float)((w1 >> sh) & 255u), i11 = (float)((w1 >> (sh + 8)) & 255u);
+          const int sh = 8 * c;
+          const float i00 = (float)((q00 >> sh) & 255u), i01 = (float)((q01 >> sh) & 255u);
+          const float i10 = (float)((q10 >> sh) & 255u), i11 = (float)((q11 >> sh) & 255u);
           const float top = i00 + lx[i] * (i01 - i00), bot = i10 + lx[i] * (i11 - i10);
           v[i][c] = (top + re.ly * (bot - top) - a.mean[c]) * wgt;
         }
@@ -197,21 +201,25 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint2* __restri
 }  // namespace
 
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_pairs,
+                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_scratch,
                         void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  uint2* pairs = (uint2*)d_pairs;
-  pair_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pairs);
-  dim3 grid((max_w + 64 * PX - 1) / (64 * PX), (max_h + TROWS - 1) / TROWS, n_img * pl.n);
+  uint32_t* pix = (uint32_t*)d_scratch;
+  pixel_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
+  const int tiles_x = (max_w + 64 * PX - 1) / (64 * PX), tiles_y = (max_h + TROWS - 1) / TROWS;
+  const int64_t nblk = (int64_t)tiles_x * tiles_y * n_img * pl.n;
+  if (nblk > 0x7fffffff) return (int)hipErrorInvalidValue;
+  const unsigned grid = (unsigned)nblk;
   switch (dt) {
     case DN_F32:
-      build_planes_kernel<float><<<grid, 256, 0, s>>>(pairs, a, pl, (float*)d_out);
+      build_planes_kernel<float><<<grid, 256, 0, s>>>(pix, a, pl, (float*)d_out, tiles_x, tiles_y);
       break;
     case DN_F16:
-      build_planes_kernel<_Float16><<<grid, 256, 0, s>>>(pairs, a, pl, (_Float16*)d_out);
+      build_planes_kernel<_Float16><<<grid, 256, 0, s>>>(pix, a, pl, (_Float16*)d_out, tiles_x,
+                                                         tiles_y);
       break;
     case DN_BF16:
-      build_planes_kernel<__bf16><<<grid, 256, 0, s>>>(pairs, a, pl, (__bf16*)d_out);
+      build_planes_kernel<__bf16><<<grid, 256, 0, s>>>(pix, a, pl, (__bf16*)d_out, tiles_x, tiles_y);
       break;
   }
   return (int)hipGetLastError();

@@ -52,8 +52,8 @@ def test_size_queries_without_device():
                                     ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
                                     ctypes.byref(e), None) == 0
     assert n.value == 6 and e.value == 6 * 3 * 1200 * 1200
-    # the planes, then the pair-image scratch (8 bytes per image pixel) 256-byte aligned after them
-    full = (16 * e.value * 2 + 255) // 256 * 256 + 16 * 8 * 768 * 1024
+    # the planes, then the builder's scratch (4 bytes per image pixel) 256-byte aligned after them
+    full = (16 * e.value * 2 + 255) // 256 * 256 + 16 * 4 * 768 * 1024
     assert need.value == full
     # short buffer: error, needed size still reported (no device work happens)
     fake = ctypes.c_void_p(256)
