@@ -23,7 +23,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
                                                              int32_t* __restrict__ scale_out,
                                                              int32_t* __restrict__ idx_out) {
 #pragma clang fp contract(off)
-  extern __shared__ __align__(16) float s_row[];  // S * S rows of C + 4 floats
+  extern __shared__ __align__(16) float s_row[];  // S * S rows of C + 2 floats
   __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
   __shared__ float s_ly[MAX_S], s_lx[MAX_S];
   const int r = blockIdx.x;
@@ -108,14 +108,15 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   const int Wc = a.map_w[sc.plane];
   // Each thread blends VT consecutive channels (one 16-byte vector per neighbour cell); C / VT
   // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.  The
-  // results are staged bin-major, one row of C + 4 floats per bin with the thread's 16-byte halves
-  // interleaved across the row (conflict-free writes), then read out in the output's channel-major
-  // order one float per thread: consecutive bins of a channel are 4 banks apart (row stride C + 4).
+  // results are staged bin-major, one row of C + 2 floats per bin in channel order (8-byte writes),
+  // then read out in the output's channel-major order: each thread gathers 4 consecutive bins of one
+  // channel and writes them with one 16-byte store.  With the row stride C + 2, the lanes of a read
+  // (up to 8 channels x bins 4 apart) fall on distinct banks.
   constexpr int VT = 16 / sizeof(T);
   typedef T vec_t __attribute__((ext_vector_type(VT)));
   const int per_bin = C / VT, groups = blockDim.x / per_bin;
   const int lt = tid % per_bin, grp = tid / per_bin;
-  const int RSTR = C + 4;
+  const int RSTR = C + 2;
   constexpr int NQ = VT / 4;  // 16-byte float chunks per thread and bin
   if (grp < groups) {
     const int c0 = lt * VT;
@@ -138,16 +139,27 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
           const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
           o[e] = top + ly * (bot - top);
         }
-        // chunk k of thread lt holds channels lt * VT + 4 k .. + 3
-        *(f32x4*)(s_row + bin * RSTR + (k * per_bin + lt) * 4) = o;
+        float* d = s_row + bin * RSTR + c0 + 4 * k;  // natural channel order, 8-byte aligned
+        *(float2*)d = make_float2(o[0], o[1]);
+        *(float2*)(d + 2) = make_float2(o[2], o[3]);
       }
     }
   }
   __syncthreads();
-  for (int e = tid; e < C * SS; e += blockDim.x) {
-    const int c = e / SS, bin = e - c * SS;
-    const int l = c / VT, q = c % VT;
-    dst[e] = s_row[bin * RSTR + ((q / 4) * per_bin + l) * 4 + (q % 4)];
+  if ((SS & 3) == 0 && ((uintptr_t)dst & 15) == 0) {
+    // four consecutive bins of one channel per thread, one 16-byte store
+    for (int e4 = tid; e4 < (C * SS) / 4; e4 += blockDim.x) {
+      const int e = 4 * e4, c = e / SS, bin = e - c * SS;
+      f32x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = s_row[(bin + i) * RSTR + c];
+      *(f32x4*)(dst + e) = o;
+    }
+  } else {
+    for (int e = tid; e < C * SS; e += blockDim.x) {
+      const int c = e / SS, bin = e - c * SS;
+      dst[e] = s_row[bin * RSTR + c];
+    }
   }
   if (tid == 0) scale_out[r] = best;
   if (idx_out)
@@ -164,7 +176,7 @@ int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, co
                           int32_t* d_idx, void* stream) {
   if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
   hipStream_t s = (hipStream_t)stream;
-  const size_t lds = sizeof(float) * (size_t)(a.C + 4) * a.S * a.S;
+  const size_t lds = sizeof(float) * (size_t)(a.C + 2) * a.S * a.S;
   switch (dt) {
     case DN_F32:
       region_windows_kernel<float><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes, d_box_img,
