@@ -620,17 +620,18 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
     int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
   using Cf = ConvCfg<T, R, BM, TM, PAD>;
   using Op = Mfma<T>;
-  static_assert(!Cf::F32 && TM == 2, "direct-load path is for 16-bit storage");
+  static_assert(!Cf::F32 && (TM == 2 || TM == 3), "direct-load path is for 16-bit storage");
   constexpr int pad = (R - 1) / 2;
   constexpr int TN = Cf::TN, NW = Cf::WM * Cf::WN;
   constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2;
   constexpr int DH = Pieces<16>::count(HSLOTS, NW), DW = Pieces<16>::count(WSLOTS, NW);
   constexpr int HALO_E = DH * NW * 512, W_E = DW * NW * 512;  // elements (2 bytes)
-  // The epilogue stages 16 KB per wave; when that would set the LDS size, it runs in two rounds of
-  // half the waves each.
-  constexpr int ROUNDS = (Cf::STAGE_E > 2 * HALO_E + 2 * W_E && NW % 2 == 0) ? 2 : 1;
-  constexpr int STG_E = Cf::STAGE_E / ROUNDS;
-  constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > STG_E ? (2 * HALO_E + 2 * W_E) : STG_E;
+  constexpr int PIPE_E = 2 * HALO_E + 2 * W_E;
+  // TM = 2: the epilogue stages 16 KB per wave; when that would set the LDS size, it runs in two
+  // rounds of half the waves each.  TM = 3 stages 32 pixels per wave at a time (below).
+  constexpr int ROUNDS = (TM == 2 && Cf::STAGE_E > PIPE_E && NW % 2 == 0) ? 2 : 1;
+  constexpr int STG_E = TM == 2 ? Cf::STAGE_E / ROUNDS : 0;
+  constexpr int LDS_E = PIPE_E > STG_E ? PIPE_E : STG_E;
   typedef T out4_t __attribute__((ext_vector_type(4)));
   __shared__ __align__(1024) T s_mem[LDS_E];
   auto halo_buf = [&](int b) { return s_mem + b * HALO_E; };
@@ -730,46 +731,79 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
     __syncthreads();
   }
 
-  // Epilogue as in conv_s1_kernel: stage 128 pixels x 64 channels per wave, write whole lines.
   typedef T vec8_t __attribute__((ext_vector_type(8)));
   T* dst = out + plane * out_stride;
-  constexpr int WPR = NW / ROUNDS;  // waves staging per round
+  if constexpr (TM == 2) {
+    // Epilogue as in conv_s1_kernel: stage 128 pixels x 64 channels per wave, write whole lines.
+    constexpr int WPR = NW / ROUNDS;  // waves staging per round
+  #pragma unroll
+    for (int round = 0; round < ROUNDS; ++round) {
+      if (round) __syncthreads();
+      const bool mine = wave / WPR == round;
+      T* stg = s_mem + (wave % WPR) * (32 * TN * 64);
+      if (mine) {
+  #pragma unroll
+        for (int mt = 0; mt < TM; ++mt)
+  #pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int j = 4 * mt + q;
+            const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
+  #pragma unroll
+            for (int t = 0; t < TN; ++t) {
+              const int p = t * 32 + l32;
+              out4_t r;
+  #pragma unroll
+              for (int e = 0; e < 4; ++e)
+                r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+              const int key = (p & 7) ^ ((p >> 3) & 3);
+              *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
+            }
+          }
+      }
+      __syncthreads();
+      if (mine) {
+        const int j = lane & 7;
+  #pragma unroll
+        for (int it = 0; it < (32 * TN) / 8; ++it) {
+          const int p = it * 8 + (lane >> 3);
+          const int key = (p & 7) ^ ((p >> 3) & 3);
+          const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
+          const int idx = wn * 32 * TN + p;
+          const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+          if (oy < H && ox < W)
+            *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
+        }
+      }
+    }
+  } else {
+    // TM = 3: each wave owns 96 channels (192 bytes) of each of its 128 pixels.  After the loop's
+    // last barrier no wave reads the stage buffers, so each wave stages one 32-pixel MFMA tile at a
+    // time in a private LDS region (rows of 96 channels + one 16-byte slot: conflict-free 8-byte
+    // writes), then writes each pixel's 192 bytes as 16-byte chunks.
+    constexpr int SROW = 32 * TM + 8, NCH = 4 * TM;
+    static_assert(NW * 32 * SROW <= LDS_E, "per-wave staging fits the stage buffers");
+    T* stg = s_mem + wave * (32 * SROW);
+    const int mw = g * Mg + m0 + wm * 32 * TM;  // this wave's first output channel
 #pragma unroll
-  for (int round = 0; round < ROUNDS; ++round) {
-    if (round) __syncthreads();
-    const bool mine = wave / WPR == round;
-    T* stg = s_mem + (wave % WPR) * (32 * TN * 64);
-    if (mine) {
+    for (int t = 0; t < TN; ++t) {
 #pragma unroll
       for (int mt = 0; mt < TM; ++mt)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int j = 4 * mt + q;
-          const f32x4 bv = *(const f32x4*)(bias + g * Mg + m0 + wm * 64 + 8 * j + 4 * half);
+          const int m = mt * 32 + 8 * q + 4 * half;
+          const f32x4 bv = *(const f32x4*)(bias + mw + m);
+          out4_t o;
 #pragma unroll
-          for (int t = 0; t < TN; ++t) {
-            const int p = t * 32 + l32;
-            out4_t r;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              r[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
-            const int key = (p & 7) ^ ((p >> 3) & 3);
-            *(out4_t*)(stg + p * 64 + ((j ^ key) * 8) + 4 * half) = r;
-          }
+          for (int e = 0; e < 4; ++e) o[e] = from_f32<T>(fmaxf(acc[mt][t][4 * q + e] + bv[e], 0.f));
+          *(out4_t*)(stg + l32 * SROW + m) = o;
         }
-    }
-    __syncthreads();
-    if (mine) {
-      const int j = lane & 7;
 #pragma unroll
-      for (int it = 0; it < (32 * TN) / 8; ++it) {
-        const int p = it * 8 + (lane >> 3);
-        const int key = (p & 7) ^ ((p >> 3) & 3);
-        const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
-        const int idx = wn * 32 * TN + p;
+      for (int it = 0; it < NCH / 2; ++it) {  // 32 pixels x NCH chunks over 64 lanes
+        const int u = it * 64 + lane, p = u / NCH, ch = u % NCH;
+        const vec8_t v = *(const vec8_t*)(stg + p * SROW + 8 * ch);
+        const int idx = wn * 32 * TN + t * 32 + p;
         const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
-        if (oy < H && ox < W)
-          *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
+        if (oy < H && ox < W) *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch) = v;
       }
     }
   }
@@ -973,10 +1007,11 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
   using Cf = ConvCfg<T, R, BM, TM, PAD>;
   const int Cg = C / G, Mg = M / G;
   const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
+  if (Mg % BM) return (int)hipErrorInvalidValue;  // whole channel blocks per group
   const int mblocks = G * (Mg / BM);
   const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
   if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-  if constexpr (Cf::F32 || TM != 2) {
+  if constexpr (Cf::F32 || (TM != 2 && TM != 3)) {
     conv_s1_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
         in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   } else {
@@ -990,15 +1025,19 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
 
 // Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, and
 // a spare layout parameter.  Chosen by timing each layer at the 96-plane batch shapes: two waves per
-// SIMD matter most; conv4's 192 channels per group run best as three 64-channel blocks.
+// SIMD matter most; conv3/conv5 run best at three waves per SIMD; conv4's 192 channels per group run
+// best as one block of 3 x 32 channels per wave (7 LDS fragment reads per 12 MFMAs instead of 6 per 8).
 #ifndef DN_CONV2_CFG
 #define DN_CONV2_CFG 128, 2, 2, 0
 #endif
-#ifndef DN_CONV35_CFG
-#define DN_CONV35_CFG 128, 2, 3, 8
+#ifndef DN_CONV3_CFG
+#define DN_CONV3_CFG 128, 2, 3, 8
+#endif
+#ifndef DN_CONV5_CFG
+#define DN_CONV5_CFG 128, 2, 3, 8
 #endif
 #ifndef DN_CONV4_CFG
-#define DN_CONV4_CFG 64, 2, 2, 0
+#define DN_CONV4_CFG 192, 3, 2, 0
 #endif
 
 template <typename T>
@@ -1039,9 +1078,11 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
       return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 3:
+      return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+                                             in_stride, out_stride, s);
     case 5:
-      return run_conv_s1<T, 3, DN_CONV35_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
-                                              in_stride, out_stride, s);
+      return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+                                             in_stride, out_stride, s);
     case 4:
       return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
