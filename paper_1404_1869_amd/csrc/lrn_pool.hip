@@ -127,26 +127,28 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
   }
 }
 
-// LRN then pool for C = CPT * TPP channels (96 = 96 x 1, 256 = 128 x 2): every thread owns one
-// input pixel's CPT consecutive channels.  It issues all of their 16-byte loads at once (plus one
-// neighbouring vector on each inner side when a pixel is split over two threads), computes the
-// channel-window sums from registers, and stores the LRN result to LDS; then the tile is pooled from
-// LDS as in the generic kernel.
-template <typename T, int CPT, int HN>
+// LRN then pool for C = CPT * TPP channels (96 = 96 x 1, 256 = 128 x 2) with the default window
+// n = 5: every thread owns one input pixel's CPT consecutive channels.  It issues all of their
+// 16-byte loads at once (plus one neighbouring vector on each inner side when a pixel is split over
+// two threads), forms the five-channel sums of squares from pair sums (four adds and one multiply per
+// element), and stores the LRN result to LDS.  Pixels of the tile outside the map are stored as
+// -inf, so every pooled output then takes the max over its full 3 x 3 window from LDS, unrolled, with
+// no clipping tests.  Channel count and tile shape are compile-time constants, so no index
+// arithmetic needs a division.
+template <typename T, int C, int CPT, int TPH, int TPW>
 __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict__ in,
                                                              T* __restrict__ out, int H, int W,
-                                                             int C, int Ho, int Wo, int TPH, int TPW,
-                                                             int tiles_x, int tiles_y,
-                                                             int64_t in_stride, int64_t out_stride,
-                                                             float alpha_n, float beta, float k) {
+                                                             int Ho, int Wo, int tiles_x,
+                                                             int tiles_y, int64_t in_stride,
+                                                             int64_t out_stride, float alpha_n,
+                                                             float beta, float k) {
   constexpr int N = Vec<T>::N;
-  constexpr int NV = CPT / N;
-  static_assert(CPT % N == 0 && HN <= N, "channel split must be whole vectors");
+  constexpr int NV = CPT / N, TPP = C / CPT, G = C / N, CS = C + N;
+  constexpr int IW = 2 * TPW + 1, NP = (2 * TPH + 1) * IW;
+  static_assert(CPT % N == 0 && C % CPT == 0 && N >= 2, "channel split must be whole vectors");
+  static_assert(NP * TPP <= 256, "one thread per (pixel, part)");
   typedef typename Vec<T>::type vec_t;
-  extern __shared__ __align__(16) unsigned char smem[];
-  T* s = (T*)smem;
-  const int CS = C + N;
-  const int TPP = C / CPT;
+  __shared__ __align__(16) T s[NP * CS];
 
   int bid = blockIdx.x;
   const int tx = bid % tiles_x;
@@ -155,61 +157,68 @@ __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict
   const int plane = bid / tiles_y;
   const int oy0 = ty * TPH, ox0 = tx * TPW;
   const int iy0 = 2 * oy0, ix0 = 2 * ox0;
-  const int IW = 2 * TPW + 1, NP = (2 * TPH + 1) * IW;
 
   const int p = threadIdx.x / TPP, part = threadIdx.x % TPP;
   if (p < NP) {
     const int y = iy0 + p / IW, x = ix0 + p % IW;
+    T* d = s + p * CS + part * CPT;
     if (y < H && x < W) {
       const T* px = in + plane * in_stride + ((int64_t)y * W + x) * C + part * CPT;
       vec_t v[NV], lv = vec_t{}, rv = vec_t{};
 #pragma unroll
       for (int i = 0; i < NV; ++i) v[i] = *(const vec_t*)(px + i * N);
-      if (part > 0) lv = *(const vec_t*)(px - N);
-      if (part + 1 < TPP) rv = *(const vec_t*)(px + CPT);
-      float sq[CPT + 2 * HN];
+      if (TPP > 1 && part > 0) lv = *(const vec_t*)(px - N);
+      if (TPP > 1 && part + 1 < TPP) rv = *(const vec_t*)(px + CPT);
+      // sq[2 + i] = a_i^2 for this thread's channels, two neighbours (or zeros) on each side
+      float sq[CPT + 4], pr[CPT + 3];
 #pragma unroll
-      for (int i = 0; i < HN; ++i) {
-        const float a = to_f32(lv[N - HN + i]), b = to_f32(rv[i]);
+      for (int i = 0; i < 2; ++i) {
+        const float a = to_f32(lv[N - 2 + i]), b = to_f32(rv[i]);
         sq[i] = a * a;
-        sq[HN + CPT + i] = b * b;
+        sq[CPT + 2 + i] = b * b;
       }
 #pragma unroll
       for (int i = 0; i < CPT; ++i) {
         const float a = to_f32(v[i / N][i % N]);
-        sq[HN + i] = a * a;
+        sq[2 + i] = a * a;
       }
-      T* d = s + p * CS + part * CPT;
+#pragma unroll
+      for (int i = 0; i < CPT + 3; ++i) pr[i] = sq[i] + sq[i + 1];
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         vec_t r;
 #pragma unroll
         for (int e = 0; e < N; ++e) {
-          const int c = i * N + e;
-          float sum = 0.f;
-#pragma unroll
-          for (int j = 0; j <= 2 * HN; ++j) sum += sq[c + j];
+          const int c = i * N + e;  // window sq[c .. c + 4]
+          const float sum = pr[c] + pr[c + 2] + sq[c + 4];
           r[e] = from_f32<T>(to_f32(v[i][e]) * lrn_scale(sum, alpha_n, beta, k));
         }
         *(vec_t*)(d + i * N) = r;
       }
+    } else {
+      vec_t f;
+#pragma unroll
+      for (int e = 0; e < N; ++e) f[e] = from_f32<T>(-INFINITY);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) *(vec_t*)(d + i * N) = f;
     }
   }
   __syncthreads();
 
-  const int G = C / N;
-  for (int e = threadIdx.x; e < TPH * TPW * G; e += blockDim.x) {
+  for (int e = threadIdx.x; e < TPH * TPW * G; e += 256) {
     const int g = e % G, q = e / G;
     const int qy = q / TPW, qx = q % TPW;
     const int oy = oy0 + qy, ox = ox0 + qx;
     if (oy >= Ho || ox >= Wo) continue;
-    const int y1 = min(2 * oy + 3, H) - iy0, x1 = min(2 * ox + 3, W) - ix0;
+    const T* b = s + ((2 * qy) * IW + 2 * qx) * CS + g * N;
     float m[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) m[i] = -INFINITY;
-    for (int hy = 2 * qy; hy < y1; ++hy)
-      for (int hx = 2 * qx; hx < x1; ++hx) {
-        const vec_t v = *(const vec_t*)(s + (hy * IW + hx) * CS + g * N);
+#pragma unroll
+    for (int wy = 0; wy < 3; ++wy)
+#pragma unroll
+      for (int wx = 0; wx < 3; ++wx) {
+        const vec_t v = *(const vec_t*)(b + (wy * IW + wx) * CS);
 #pragma unroll
         for (int i = 0; i < N; ++i) m[i] = fmaxf(m[i], to_f32(v[i]));
       }
@@ -287,28 +296,21 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
   constexpr int N = Vec<T>::N;
   if (C % N || hn > 4) return (int)hipErrorInvalidValue;
   // Per-pixel kernel for the two channel counts of the network with the default window (n = 5).
+  // Tiles: the largest whose input pixels fit one thread each (per part) and whose LDS tile stays
+  // within 64 KB.
   if (lrn && hn == 2 && (C == 96 || C == 256)) {
-    const int cpt = C == 96 ? 96 : 128, tpp = C / cpt;
-    int TPH = 0, TPW = 0;
-    const int cand[][2] = {{8, 7}, {4, 7}, {4, 6}, {2, 6}, {2, 5}, {2, 3}, {1, 3}, {1, 1}};
-    for (auto& c : cand) {
-      const int np = (2 * c[0] + 1) * (2 * c[1] + 1);
-      if (np * tpp <= 256 && (size_t)np * (C + N) * sizeof(T) <= 65536) {
-        TPH = c[0];
-        TPW = c[1];
-        break;
-      }
-    }
+    constexpr bool F32 = sizeof(T) == 4;
+    constexpr int TH96 = F32 ? 4 : 8, TW96 = 7, TH256 = F32 ? 2 : 4, TW256 = F32 ? 5 : 6;
+    const int TPH = C == 96 ? TH96 : TH256, TPW = C == 96 ? TW96 : TW256;
     const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
     if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-    const size_t lds = (size_t)(2 * TPH + 1) * (2 * TPW + 1) * (C + N) * sizeof(T);
     if (C == 96)
-      lrn_pool_pixel_kernel<T, 96, 2><<<(unsigned)blocks, 256, lds, s>>>(
-          in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+      lrn_pool_pixel_kernel<T, 96, 96, TH96, TW96><<<(unsigned)blocks, 256, 0, s>>>(
+          in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     else
-      lrn_pool_pixel_kernel<T, 128, 2><<<(unsigned)blocks, 256, lds, s>>>(
-          in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256><<<(unsigned)blocks, 256, 0, s>>>(
+          in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     return (int)hipGetLastError();
   }
   int TPH, TPW;
