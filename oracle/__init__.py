@@ -48,6 +48,8 @@ def lib():
         L.oracle_resize_center.restype = None
         L.oracle_build_planes.argtypes = [P, i32, i32, i32, P, P, i32, i32, P, i32, i32, i32, P]
         L.oracle_build_planes.restype = None
+        L.oracle_warp_regions.argtypes = [P, i32, i32, i32, P, P, i32, i32, P, P]
+        L.oracle_warp_regions.restype = None
         L.oracle_conv2d.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, i32, i32, i32, P]
         L.oracle_conv2d.restype = i32
         L.oracle_lrn.argtypes = [P, i32, i32, i32, i32, f64, f64, f64, P]
@@ -149,6 +151,24 @@ def build_planes(img: np.ndarray, pl: Plan, pad_mode: int, mean) -> list:
     lib().oracle_build_planes(_p(img), H, W, pl.gi.shape[0], _p(pl.gi), _p(pl.gd), pl.pad, pad_mode,
                               _p(m), pl.n_planes, PHm, PWm, _p(buf))
     return [np.ascontiguousarray(buf[i, :, :ph, :pw]) for i, (ph, pw) in enumerate(pl.plane_sizes)]
+
+
+def warp_regions(images: np.ndarray, boxes: np.ndarray, S=227, mean=(0.0, 0.0, 0.0), box_img=None):
+    """Crop-before windows (Sec. 3.4, Sec. 4): each box cut from its uint8 [3][H][W] image and warped
+    bilinearly to S x S with half-pixel centres, minus the mean pixel.  images: [3][H][W] or
+    [n_img][3][H][W]; boxes: [n][4] fp32 (x1, y1, x2, y2).  Returns fp32 [n][3][S][S]."""
+    images = np.ascontiguousarray(images, np.uint8)
+    if images.ndim == 3:
+        images = images[None]
+    n_img, _, H, W = images.shape
+    boxes = np.ascontiguousarray(boxes, np.float32).reshape(-1, 4)
+    n = boxes.shape[0]
+    bi = None if box_img is None else np.ascontiguousarray(box_img, np.int32)
+    m = np.ascontiguousarray(mean, np.float64)
+    out = np.zeros((n, 3, S, S), np.float32)
+    lib().oracle_warp_regions(_p(images), n_img, H, W, _p(boxes), None if bi is None else _p(bi), n, S,
+                              _p(m), _p(out))
+    return out
 
 
 # ----------------------------------------------------------------------------------------------

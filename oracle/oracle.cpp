@@ -231,6 +231,54 @@ void oracle_resize_center(const uint8_t* img, int H, int W, int h, int w, const 
 }
 
 // ------------------------------------------------------------------------------------------------
+// Crop-before baseline (Sec. 3.4, Sec. 4): every region is cut out of the image in pixel space and
+// warped on its own to the classifier's S x S input, then mean-centred, so that each window can be run
+// through the network in isolation.
+//   box (x1, y1, x2, y2) in pixel-edge coordinates of image b = box_img[r] (0 when box_img is null);
+//   output pixel (i, j) samples the image at
+//     sy = y1 + (i + 0.5) (y2 - y1) / S - 0.5,   sx = x1 + (j + 0.5) (x2 - x1) / S - 0.5,
+//   i.e. the box is stretched onto the S x S grid with half-pixel centres (no context margin), with
+//   the same bilinear rule as the pyramid's resize: coordinate clamped at 0 below, top-left neighbour
+//   clamped to the last row/column, the other neighbour one further (clamped).  Then the mean pixel
+//   of the channel is subtracted.  A box with a non-finite or non-positive side gives an all-zero
+//   window.  out[r][c][i][j], fp32 values of fp64 arithmetic.
+// ------------------------------------------------------------------------------------------------
+void oracle_warp_regions(const uint8_t* img, int n_img, int H, int W, const float* boxes,
+                         const int32_t* box_img, int n, int S, const double* mean, float* out) {
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int r = 0; r < n; ++r) {
+    float* o = out + (size_t)r * 3 * S * S;
+    std::fill(o, o + (size_t)3 * S * S, 0.f);
+    const double x1 = boxes[r * 4 + 0], y1 = boxes[r * 4 + 1], x2 = boxes[r * 4 + 2], y2 = boxes[r * 4 + 3];
+    if (!std::isfinite(x1) || !std::isfinite(y1) || !std::isfinite(x2) || !std::isfinite(y2)) continue;
+    if (!(x2 - x1 > 0) || !(y2 - y1 > 0)) continue;
+    const int b = box_img ? box_img[r] : 0;
+    if (b < 0 || b >= n_img) continue;
+    const double fy = (y2 - y1) / S, fx = (x2 - x1) / S;
+    for (int c = 0; c < 3; ++c) {
+      const uint8_t* I = img + ((size_t)b * 3 + c) * H * W;
+      for (int i = 0; i < S; ++i) {
+        double sy = y1 + (i + 0.5) * fy - 0.5;
+        if (sy < 0) sy = 0;
+        int y0 = (int)std::min(std::floor(sy), (double)(H - 1));
+        const int yb = std::min(y0 + 1, H - 1);
+        const double ly = sy - y0;
+        for (int j = 0; j < S; ++j) {
+          double sx = x1 + (j + 0.5) * fx - 0.5;
+          if (sx < 0) sx = 0;
+          int x0 = (int)std::min(std::floor(sx), (double)(W - 1));
+          const int xb = std::min(x0 + 1, W - 1);
+          const double lx = sx - x0;
+          const double top = (1 - lx) * I[(size_t)y0 * W + x0] + lx * I[(size_t)y0 * W + xb];
+          const double bot = (1 - lx) * I[(size_t)yb * W + x0] + lx * I[(size_t)yb * W + xb];
+          o[((size_t)c * S + i) * S + j] = (float)((1 - ly) * top + ly * bot - mean[c]);
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // Plane filling (Sec. 3.1 border and background, Sec. 3.2 background equals the mean pixel, hence 0
 // after centring).  For a plane pixel inside scale k's rectangle, with v, u its row/column relative to
 // the first real pixel and d the distance outside the image along each axis:
