@@ -165,6 +165,25 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
                             const int32_t* d_box_img, int32_t n, float target, int32_t S,
                             float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream);
 
+/* Crop-before windows: the per-window baseline the paper measures the dense pyramid against
+ * (Sec. 3.4: 2000 window proposals, each run through the network on its own) and the "crop before"
+ * pipeline of Sec. 4.  Each box (x1, y1, x2, y2) of original-image pixel-edge coordinates (fp32) is
+ * cut out of image d_box_img[i] (NULL => image 0) and warped to S x S by bilinear sampling with
+ * half-pixel centres, the box stretched onto the grid with no context margin: output pixel (i, j)
+ * samples sy = y1 + (i + 0.5)(y2 - y1)/S - 0.5, sx = x1 + (j + 0.5)(x2 - x1)/S - 0.5, each clamped
+ * to the image ([0, H-1], [0, W-1]: a box reaching outside repeats the edge pixel), top-left neighbour
+ * floor(s), the other one further (clamped); mean[c] (host, 3 floats) is then subtracted.  A box with a non-finite or non-positive side, or an
+ * image index outside [0, n_img), gives an all-zero window.
+ * d_images: uint8 [n_img][3][H][W].  d_out: [n][3][S][S] in `dtype` (n channel-major planes of S x S
+ * packed back to back, ready for densenet_conv_features with plane offsets i * 3 * S * S), or NULL
+ * for a size query into *bytes_needed.  S in 1 .. DN_MAX_WARP_SIDE.  With n == 0 nothing is launched.
+ * Coordinates are fp64 with + - * / only, so the taps are reproducible bit for bit. */
+#define DN_MAX_WARP_SIDE 1024
+int densenet_warp_regions(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                          const float* d_boxes, const int32_t* d_box_img, int32_t n, int32_t S,
+                          const float* mean, dn_dtype dtype, void* d_out, size_t out_bytes,
+                          size_t* bytes_needed, void* stream);
+
 /* Single layers of the conv stack, for callers composing their own schedule.  All on channels-last
  * maps of n planes of equal size, packed back to back.
  * densenet_conv_layer: layer 1..5 with bias and ReLU.  Layer 1 reads channel-major planes
@@ -186,7 +205,7 @@ int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw);
  * comma-separated list of names; NULL or "" = all) is bracketed by two hipEvents recorded on the
  * launch's own stream.  densenet_profile_stop() waits for the recorded events, writes per-name
  * totals (launches, summed elapsed ms) to out[max_entries] (*n_entries = number of names) and turns
- * tracing off.  Kernel names: build_planes, conv1..conv5, lrn_pool1, lrn_pool2, pool5,
+ * tracing off.  Kernel names: build_planes, conv1..conv5, lrn_pool1, lrn_pool2, pool5, warp_regions,
  * region_windows, pack_weights.  Events come from a pool owned by the library (no device memory). */
 typedef struct {
   char name[32];

@@ -238,9 +238,10 @@ void oracle_resize_center(const uint8_t* img, int H, int W, int h, int w, const 
 //   output pixel (i, j) samples the image at
 //     sy = y1 + (i + 0.5) (y2 - y1) / S - 0.5,   sx = x1 + (j + 0.5) (x2 - x1) / S - 0.5,
 //   i.e. the box is stretched onto the S x S grid with half-pixel centres (no context margin), with
-//   the same bilinear rule as the pyramid's resize: coordinate clamped at 0 below, top-left neighbour
-//   clamped to the last row/column, the other neighbour one further (clamped).  Then the mean pixel
-//   of the channel is subtracted.  A box with a non-finite or non-positive side gives an all-zero
+//   bilinear sampling with the coordinate clamped to [0, H - 1] (resp. [0, W - 1]): a box reaching
+//   outside the image repeats the edge pixel, with interpolation weights in [0, 1); the top-left
+//   neighbour is floor(s), the other one further (clamped).  Then the mean pixel of the channel is
+//   subtracted.  A box with a non-finite or non-positive side gives an all-zero
 //   window.  out[r][c][i][j], fp32 values of fp64 arithmetic.
 // ------------------------------------------------------------------------------------------------
 void oracle_warp_regions(const uint8_t* img, int n_img, int H, int W, const float* boxes,
@@ -259,14 +260,14 @@ void oracle_warp_regions(const uint8_t* img, int n_img, int H, int W, const floa
       const uint8_t* I = img + ((size_t)b * 3 + c) * H * W;
       for (int i = 0; i < S; ++i) {
         double sy = y1 + (i + 0.5) * fy - 0.5;
-        if (sy < 0) sy = 0;
-        int y0 = (int)std::min(std::floor(sy), (double)(H - 1));
+        sy = std::min(std::max(sy, 0.0), (double)(H - 1));
+        const int y0 = (int)std::floor(sy);
         const int yb = std::min(y0 + 1, H - 1);
         const double ly = sy - y0;
         for (int j = 0; j < S; ++j) {
           double sx = x1 + (j + 0.5) * fx - 0.5;
-          if (sx < 0) sx = 0;
-          int x0 = (int)std::min(std::floor(sx), (double)(W - 1));
+          sx = std::min(std::max(sx, 0.0), (double)(W - 1));
+          const int x0 = (int)std::floor(sx);
           const int xb = std::min(x0 + 1, W - 1);
           const double lx = sx - x0;
           const double top = (1 - lx) * I[(size_t)y0 * W + x0] + lx * I[(size_t)y0 * W + xb];

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdensenet.so")
-SOURCES = ("plan.cpp", "api.cpp", "trace.cpp", "pyramid.hip", "conv.hip", "lrn_pool.hip", "regions.hip")
+SOURCES = ("plan.cpp", "api.cpp", "trace.cpp", "pyramid.hip", "conv.hip", "lrn_pool.hip", "regions.hip", "windows.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-command-line-argument"]

@@ -378,6 +378,32 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
   }
 }
 
+int densenet_warp_regions(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                          const float* d_boxes, const int32_t* d_box_img, int32_t n, int32_t S,
+                          const float* mean, dn_dtype dtype, void* d_out, size_t out_bytes,
+                          size_t* bytes_needed, void* stream) {
+  try {
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
+    if (S <= 0 || S > DN_MAX_WARP_SIDE) return fail(DN_E_INVALID_ARG, "S must be in 1..DN_MAX_WARP_SIDE");
+    if (n_img <= 0 || H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "bad image batch size");
+    if (H > 32768 || W > 32768) return fail(DN_E_TOO_LARGE, "image sides are limited to 32768 px");
+    const size_t need = (size_t)n * 3 * (size_t)S * S * dtype_size(dtype);
+    if (bytes_needed) *bytes_needed = need;
+    if (!d_out) return DN_OK;
+    if (out_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "output buffer too small");
+    if (n == 0) return DN_OK;
+    if (!d_images || !d_boxes || !mean) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if ((int64_t)n * ((S + 15) / 16) > 0x7fffffffLL) return fail(DN_E_TOO_LARGE, "too many boxes");
+    return run_step("warp_regions", stream, [&] {
+      return launch_warp_regions(d_images, n_img, H, W, d_boxes, d_box_img, n, S, mean, dtype, d_out,
+                                 stream);
+    });
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
 int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
                             dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,
                             int32_t pad, int32_t planes_per_img, const float* d_boxes,

@@ -69,6 +69,11 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
                         int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_scratch,
                         void* stream);
 
+// Crop-before windows: n boxes warped to S x S channel-major planes (windows.hip).
+int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t W, const float* d_boxes,
+                        const int32_t* d_box_img, int32_t n, int32_t S, const float* mean, dn_dtype dt,
+                        void* d_out, void* stream);
+
 // Packed weight blob: offsets in bytes of each layer's weights and fp32 biases.
 struct PackedLayout {
   size_t w_off[5], b_off[5], total;

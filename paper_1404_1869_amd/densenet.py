@@ -21,12 +21,13 @@ DN_OK, DN_E_INVALID_ARG, DN_E_TOO_LARGE, DN_E_BUFFER_TOO_SMALL = 0, -1, -2, -3
 DN_E_UNSUPPORTED, DN_E_HIP, DN_E_INTERNAL = -4, -5, -6
 DN_F32, DN_F16, DN_BF16 = 0, 1, 2
 DN_PAD_ZERO, DN_PAD_RAMP = 0, 1
-DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE = 64, 64
+DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE, DN_MAX_WARP_SIDE = 64, 64, 1024
 DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
            "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
-           "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_profile_start",
+           "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_warp_regions",
+           "densenet_profile_start",
            "densenet_profile_stop", "densenet_last_error")
 
 
@@ -89,6 +90,8 @@ def lib():
             "densenet_lrn_pool": [P, i32, i32, i32, i32, i32, pn, P, P],
             "densenet_maxpool": [P, i32, i32, i32, i32, i32, P, P],
             "densenet_layer_sizes": [i32, i32, pi32],
+            "densenet_warp_regions": [P, i32, i32, i32, P, P, i32, i32, ctypes.POINTER(f32), i32, P, sz,
+                                      psz, P],
             "densenet_profile_start": [ctypes.c_char_p],
             "densenet_profile_stop": [ctypes.POINTER(dn_profile_entry), i32, pi32],
         }
@@ -287,6 +290,50 @@ def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad
                                         pad, planes_per_img, _ptr(boxes), _ptr(box_img), n, target, S,
                                         _ptr(out), _ptr(scale), _ptr(idx), _stream()))
     return out, scale, idx
+
+
+def densenet_warp_regions(images, boxes, dtype: int, S=227, mean=(0.0, 0.0, 0.0), box_img=None, out=None):
+    """Crop-before windows (Sec. 3.4 per-window baseline, Sec. 4): uint8 images [n_img][3][H][W], boxes
+    [n][4] fp32 -> [n][3][S][S] mean-centred windows in `dtype`."""
+    torch = _torch()
+    if images.dim() == 3:
+        images = images[None]
+    n_img, _, H, W = images.shape
+    n = boxes.shape[0]
+    if out is None:
+        out = torch.empty((n, 3, S, S), dtype=_tdtype(dtype), device=boxes.device)
+    m = (ctypes.c_float * 3)(*[float(v) for v in mean])
+    check(lib().densenet_warp_regions(_ptr(images), n_img, H, W, _ptr(boxes), _ptr(box_img), n, S, m, dtype,
+                                      _ptr(out), out.numel() * out.element_size(),
+                                      ctypes.byref(ctypes.c_size_t()), _stream()))
+    return out
+
+
+class PerWindow:
+    """The per-window baseline (Sec. 3.4): every box warped to S x S on its own, then the whole conv stack
+    with pool5 on each window as an independent plane (one launch per layer over all windows).  The
+    per-window descriptor is the window's pool5 map, [n][Hp][Wp][256] (6 x 6 x 256 at S = 227)."""
+
+    def __init__(self, n: int, dtype: int, S=227, device="cuda", net=None):
+        torch = _torch()
+        self.n, self.S, self.dtype = n, S, dtype
+        net = net or net_params(pool5=True)
+        net.pool5 = 1
+        desc = []
+        for i in range(n):
+            q = dn_plane_desc()
+            q.h, q.w, q.offset = S, S, i * 3 * S * S
+            desc.append(q)
+        self.windows = torch.empty((n, 3, S, S), dtype=_tdtype(dtype), device=device)
+        self.conv = ConvFeatures(desc, dtype, net, device=device)
+        hp = self.conv.p5d[0]
+        self.pool5_shape = (n, hp.h, hp.w, 256)
+
+    def __call__(self, images, boxes, packed, mean=(0.0, 0.0, 0.0), box_img=None):
+        densenet_warp_regions(images, boxes, self.dtype, self.S, mean, box_img, out=self.windows)
+        self.conv(self.windows, packed)
+        return self.conv.pool5[: self.pool5_shape[0] * self.pool5_shape[1] * self.pool5_shape[2] * 256].view(
+            self.pool5_shape)
 
 
 def densenet_conv_layer(layer: int, x, n: int, H: int, W: int, dtype: int, packed):

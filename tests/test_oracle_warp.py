@@ -59,7 +59,25 @@ def test_whole_image_upsampling_matches_torch_and_pyramid_resize():
     ref = F.interpolate(torch.from_numpy(I.astype(np.float64))[None], size=(S, S), mode="bilinear",
                         align_corners=False)[0].numpy() - np.array(MEAN)[:, None, None]
     np.testing.assert_allclose(out, ref, rtol=0, atol=1e-4)
-    np.testing.assert_array_equal(out, oracle.resize_center(I, S, S, MEAN).astype(np.float32))
+    np.testing.assert_allclose(out, oracle.resize_center(I, S, S, MEAN), rtol=0, atol=2e-5)  # fp32 rounding
+
+
+def test_box_outside_image_repeats_edge_pixels():
+    """Clamping the coordinate to the image: a box entirely right of / below the image gives the
+    bottom-right pixel everywhere; one straddling the left edge repeats the first column."""
+    I = img(7, 20, 30)
+    out = oracle.warp_regions(I, np.array([[40, 25, 70, 50], [-20, 0, 10, 20]], np.float32), S=10)
+    np.testing.assert_array_equal(out[0], np.broadcast_to(I[:, -1:, -1:], (3, 10, 10)).astype(np.float32))
+    # left box: output columns whose coordinate falls below 0 equal column 0 of the image rows
+    sx = -20 + (np.arange(10) + 0.5) * 3 - 0.5
+    cols = np.where(sx <= 0)[0]
+    sy = (np.arange(10) + 0.5) * 2 - 0.5
+    for i in range(10):
+        y = min(max(sy[i], 0), 19)
+        y0 = int(np.floor(y)); y1 = min(y0 + 1, 19); ly = y - y0
+        ref = (1 - ly) * I[:, y0, 0].astype(np.float64) + ly * I[:, y1, 0]
+        for j in cols:
+            np.testing.assert_allclose(out[1][:, i, j], ref, rtol=0, atol=1e-4)
 
 
 def test_degenerate_boxes_give_zero_windows_and_box_img_selects_image():
