@@ -4,6 +4,8 @@
 One step is one pass of the whole path over one batch of synthetic input already resident in HBM:
 fused pyramid build (resize, centring, padding, stitching) -> conv1..conv5 with ReLU, LRN and pooling
 on every stitched plane -> per-scale conv5 windows -> region windows for 2000 boxes per image.
+After the timed steps it also times the paper's per-window baseline (every box of one image warped to
+227 x 227 and run through the network on its own) and reports it beside the dense time per image.
 The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
 1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
 
@@ -43,6 +45,8 @@ def parse():
                     help="after the timed steps, run one plain device copy of this many MiB "
                          "(a known-size reference for hardware byte counters)")
     ap.add_argument("--kernels", action="store_true", help="also print the per-kernel breakdown")
+    ap.add_argument("--no-per-window", action="store_true",
+                    help="skip the per-window baseline (every box warped to 227 x 227 and run alone)")
     return ap.parse_args()
 
 
@@ -208,9 +212,48 @@ def main():
     if args.kernels:
         result["kernels_ms"] = {k: round(v[1] / v[0], 4) for k, v in breakdown.items()}
 
+    if not args.no_per_window:
+        result["per_window"] = per_window(D, w, dt, imgs[:1], boxes[:boxes_per_img], packed,
+                                          ms_per_step / n_img)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
     print(json.dumps(result), flush=True)
+
+
+def per_window(D, w, dt, img, boxes, packed, dense_ms_per_image):
+    """The per-window baseline the paper compares the dense pyramid with (Sec. 3.4): the 2000 boxes of
+    one image each warped to 227 x 227 and run through conv1..conv5 + pool5 on their own (one launch
+    per layer over all windows), timed after the main measurement; against the dense path's time per
+    image (pyramid, conv stack and 2000 region windows) from the timed steps."""
+    import torch
+
+    from paper_1404_1869_amd import workmodel
+
+    n = boxes.shape[0]
+    pw = D.PerWindow(n, dt, 227, device=boxes.device)
+    for _ in range(2):
+        pw(img, boxes, packed, w.mean)
+    torch.cuda.synchronize()
+    D.profile_start()
+    pw(img, boxes, packed, w.mean)
+    torch.cuda.synchronize()
+    kern = D.profile_stop()
+    reps = 5
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        pw(img, boxes, packed, w.mean)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    conv_ms = sum(kern[k][1] / kern[k][0] for k in CONV_NAMES if k in kern)
+    flops = n * sum(workmodel.conv_flops(227, 227))
+    return {"windows": n, "window": "227x227", "ms_per_image": round(ms, 4),
+            "dense_ms_per_image": round(dense_ms_per_image, 4),
+            "per_window_over_dense": round(ms / dense_ms_per_image, 2),
+            "conv_tflops": round(flops / (conv_ms / 1e3) / 1e12, 2),
+            "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()},
+            "paper_context": "Sec. 3.4, NVIDIA K20: 2000 windows ~10 s vs one 25-scale pyramid ~1 s"}
 
 
 def cpu_baseline(w, n_planes_sample):

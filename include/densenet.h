@@ -89,10 +89,16 @@ typedef struct {
   double s, sy, sx;
 } dn_scale_geom;
 
-/* One plane or map: h x w pixels at `offset` elements from the start of its buffer. */
+/* One plane or map: h x w pixels at `offset` elements from the start of its buffer.
+ * pitch: elements between consecutive rows of a channel-major input plane of densenet_conv_features
+ * (channels are h * pitch apart); 0 means w.  A pitch that is a multiple of 8 (16 bytes at 16-bit
+ * storage) lets conv1 load plane rows directly into LDS whatever the width; the columns between w and
+ * pitch are never read into a stored output.  Every other use ignores pitch and writes 0. */
 typedef struct {
   int32_t h, w;
   int64_t offset;
+  int32_t pitch;
+  int32_t reserved; /* 0 */
 } dn_plane_desc;
 
 /* Network options (Sec. 3: conv1..conv5 of the AlexNet topology, with ReLU, cross-channel LRN and
@@ -174,15 +180,17 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
  * to the image ([0, H-1], [0, W-1]: a box reaching outside repeats the edge pixel), top-left neighbour
  * floor(s), the other one further (clamped); mean[c] (host, 3 floats) is then subtracted.  A box with a non-finite or non-positive side, or an
  * image index outside [0, n_img), gives an all-zero window.
- * d_images: uint8 [n_img][3][H][W].  d_out: [n][3][S][S] in `dtype` (n channel-major planes of S x S
- * packed back to back, ready for densenet_conv_features with plane offsets i * 3 * S * S), or NULL
- * for a size query into *bytes_needed.  S in 1 .. DN_MAX_WARP_SIDE.  With n == 0 nothing is launched.
+ * d_images: uint8 [n_img][3][H][W].  d_out: [n][3][S][pitch] in `dtype` (n channel-major S x S planes
+ * with rows `pitch` elements apart, packed back to back, ready for densenet_conv_features with plane
+ * descriptors {S, S, i * 3 * S * pitch, pitch}), or NULL for a size query into *bytes_needed.
+ * pitch: 0 => S, else >= S; columns S .. pitch-1 are written as 0.  S in 1 .. DN_MAX_WARP_SIDE.
+ * With n == 0 nothing is launched.
  * Coordinates are fp64 with + - * / only, so the taps are reproducible bit for bit. */
 #define DN_MAX_WARP_SIDE 1024
 int densenet_warp_regions(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                           const float* d_boxes, const int32_t* d_box_img, int32_t n, int32_t S,
-                          const float* mean, dn_dtype dtype, void* d_out, size_t out_bytes,
-                          size_t* bytes_needed, void* stream);
+                          int32_t pitch, const float* mean, dn_dtype dtype, void* d_out,
+                          size_t out_bytes, size_t* bytes_needed, void* stream);
 
 /* Single layers of the conv stack, for callers composing their own schedule.  All on channels-last
  * maps of n planes of equal size, packed back to back.

@@ -46,19 +46,21 @@ static bool stack_shape(int32_t H, int32_t W, StackShape& s) {
   return s.h[6] > 0 && s.w[6] > 0;
 }
 
-// Planes grouped into runs of equal size and evenly spaced offsets (one launch per layer per run).
+// Planes grouped into runs of equal size and pitch and evenly spaced offsets (one launch per layer
+// per run).
 struct Run {
-  int32_t first, count, h, w;
+  int32_t first, count, h, w, pitch;
   int64_t stride;  // elements between consecutive planes (0 for a run of one)
 };
+static int32_t row_pitch(const dn_plane_desc& d) { return d.pitch ? d.pitch : d.w; }
 static std::vector<Run> make_runs(const dn_plane_desc* planes, int32_t n) {
   std::vector<Run> runs;
   for (int32_t i = 0; i < n;) {
-    Run r{i, 1, planes[i].h, planes[i].w, 0};
+    Run r{i, 1, planes[i].h, planes[i].w, row_pitch(planes[i]), 0};
     int32_t j = i + 1;
-    if (j < n && planes[j].h == r.h && planes[j].w == r.w) {
+    if (j < n && planes[j].h == r.h && planes[j].w == r.w && row_pitch(planes[j]) == r.pitch) {
       r.stride = planes[j].offset - planes[i].offset;
-      while (j < n && planes[j].h == r.h && planes[j].w == r.w &&
+      while (j < n && planes[j].h == r.h && planes[j].w == r.w && row_pitch(planes[j]) == r.pitch &&
              planes[j].offset - planes[j - 1].offset == r.stride && r.stride > 0)
         ++j;
       r.count = j - i;
@@ -208,7 +210,7 @@ int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, i
     const int64_t out_stride = (int64_t)Ms[layer - 1] * Ho * Wo;
     static const char* names[5] = {"conv1", "conv2", "conv3", "conv4", "conv5"};
     TraceScope trace(names[layer - 1], stream);
-    return hip_status(launch_conv(layer, d_in, n, H, W, in_stride, dtype, d_packed, d_out,
+    return hip_status(launch_conv(layer, d_in, n, H, W, in_stride, W, dtype, d_packed, d_out,
                                   out_stride, stream),
                       "conv launch");
   } catch (...) {
@@ -275,7 +277,8 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
     size_t ws_a = 0, ws_b = 0;
     for (int32_t i = 0; i < n_planes; ++i) {
       StackShape s;
-      if (planes[i].h <= 0 || planes[i].w <= 0 || planes[i].offset < 0)
+      if (planes[i].h <= 0 || planes[i].w <= 0 || planes[i].offset < 0 ||
+          (planes[i].pitch != 0 && planes[i].pitch < planes[i].w))
         return fail(DN_E_INVALID_ARG, "bad plane descriptor");
       if (!stack_shape(planes[i].h, planes[i].w, s)) {
         std::ostringstream os;
@@ -320,7 +323,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       stack_shape(r.h, r.w, s);
       const int n = r.count;
       const char* in = (const char*)d_planes + planes[r.first].offset * es;
-      const int64_t sp = r.count > 1 ? r.stride : 3LL * r.h * r.w;
+      const int64_t sp = r.count > 1 ? r.stride : 3LL * r.h * r.pitch;
       const int64_t H0 = r.h, W0 = r.w;
       const int64_t s1 = 96 * s.h[0] * s.w[0], p1 = 96 * s.h[1] * s.w[1];
       const int64_t s2 = 256 * s.h[2] * s.w[2], p2 = 256 * s.h[3] * s.w[3];
@@ -334,7 +337,8 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       const int ln = net->lrn_n;
       int st;
       if ((st = run_step("conv1", stream, [&] {
-             return launch_conv(1, in, n, (int)H0, (int)W0, sp, dtype, d_packed, A, s1, stream);
+             return launch_conv(1, in, n, (int)H0, (int)W0, sp, r.pitch, dtype, d_packed, A, s1,
+                                stream);
            })))
         return st;
       if ((st = run_step("lrn_pool1", stream, [&] {
@@ -343,7 +347,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
            })))
         return st;
       if ((st = run_step("conv2", stream, [&] {
-             return launch_conv(2, B, n, h1, w1, p1, dtype, d_packed, A, s2, stream);
+             return launch_conv(2, B, n, h1, w1, p1, 0, dtype, d_packed, A, s2, stream);
            })))
         return st;
       if ((st = run_step("lrn_pool2", stream, [&] {
@@ -352,15 +356,15 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
            })))
         return st;
       if ((st = run_step("conv3", stream, [&] {
-             return launch_conv(3, B, n, h3, w3, p2, dtype, d_packed, A, s3, stream);
+             return launch_conv(3, B, n, h3, w3, p2, 0, dtype, d_packed, A, s3, stream);
            })))
         return st;
       if ((st = run_step("conv4", stream, [&] {
-             return launch_conv(4, A, n, h4, w4, s3, dtype, d_packed, B, s4, stream);
+             return launch_conv(4, A, n, h4, w4, s3, 0, dtype, d_packed, B, s4, stream);
            })))
         return st;
       if ((st = run_step("conv5", stream, [&] {
-             return launch_conv(5, B, n, h4, w4, s4, dtype, d_packed, c5, s5, stream);
+             return launch_conv(5, B, n, h4, w4, s4, 0, dtype, d_packed, c5, s5, stream);
            })))
         return st;
       if (net->pool5) {
@@ -380,15 +384,17 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
 
 int densenet_warp_regions(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                           const float* d_boxes, const int32_t* d_box_img, int32_t n, int32_t S,
-                          const float* mean, dn_dtype dtype, void* d_out, size_t out_bytes,
-                          size_t* bytes_needed, void* stream) {
+                          int32_t pitch, const float* mean, dn_dtype dtype, void* d_out,
+                          size_t out_bytes, size_t* bytes_needed, void* stream) {
   try {
     if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
     if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
     if (S <= 0 || S > DN_MAX_WARP_SIDE) return fail(DN_E_INVALID_ARG, "S must be in 1..DN_MAX_WARP_SIDE");
     if (n_img <= 0 || H <= 0 || W <= 0) return fail(DN_E_INVALID_ARG, "bad image batch size");
     if (H > 32768 || W > 32768) return fail(DN_E_TOO_LARGE, "image sides are limited to 32768 px");
-    const size_t need = (size_t)n * 3 * (size_t)S * S * dtype_size(dtype);
+    if (pitch == 0) pitch = S;
+    if (pitch < S || pitch > 8 * DN_MAX_WARP_SIDE) return fail(DN_E_INVALID_ARG, "pitch must be 0 or >= S");
+    const size_t need = (size_t)n * 3 * (size_t)S * pitch * dtype_size(dtype);
     if (bytes_needed) *bytes_needed = need;
     if (!d_out) return DN_OK;
     if (out_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "output buffer too small");
@@ -396,8 +402,8 @@ int densenet_warp_regions(const uint8_t* d_images, int32_t n_img, int32_t H, int
     if (!d_images || !d_boxes || !mean) return fail(DN_E_INVALID_ARG, "null pointer argument");
     if ((int64_t)n * ((S + 15) / 16) > 0x7fffffffLL) return fail(DN_E_TOO_LARGE, "too many boxes");
     return run_step("warp_regions", stream, [&] {
-      return launch_warp_regions(d_images, n_img, H, W, d_boxes, d_box_img, n, S, mean, dtype, d_out,
-                                 stream);
+      return launch_warp_regions(d_images, n_img, H, W, d_boxes, d_box_img, n, S, pitch, mean, dtype,
+                                 d_out, stream);
     });
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");

@@ -71,8 +71,8 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
 
 // Crop-before windows: n boxes warped to S x S channel-major planes (windows.hip).
 int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t W, const float* d_boxes,
-                        const int32_t* d_box_img, int32_t n, int32_t S, const float* mean, dn_dtype dt,
-                        void* d_out, void* stream);
+                        const int32_t* d_box_img, int32_t n, int32_t S, int32_t pitch, const float* mean,
+                        dn_dtype dt, void* d_out, void* stream);
 
 // Packed weight blob: offsets in bytes of each layer's weights and fp32 biases.
 struct PackedLayout {
@@ -83,8 +83,10 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
                         void* stream);
 
 // One conv layer (1..5) with bias and ReLU over n equal planes spaced in_stride / out_stride elements.
+// in_pitch: row pitch (elements) of layer 1's channel-major input planes (>= W); ignored otherwise.
 int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride, void* stream);
+                int32_t in_pitch, dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride,
+                void* stream);
 
 // LRN + pool (order by lrn_first), or plain pool when lrn == false.  Channels-last maps.
 int launch_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in_stride,

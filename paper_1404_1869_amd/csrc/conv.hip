@@ -97,7 +97,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T* __restrict__ out,
                                                     const T* __restrict__ wp,
                                                     const float* __restrict__ bias, int H, int W,
-                                                    int Ho, int Wo, int64_t in_stride,
+                                                    int P, int Ho, int Wo, int64_t in_stride,
                                                     int64_t out_stride, int tiles_x, int tiles_y) {
   using C = Conv1Cfg<T>;
   using Op = Mfma<T>;
@@ -130,12 +130,12 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
 
   for (int c = 0; c < 3; ++c) {
     __syncthreads();
-    const T* sc = src + (int64_t)c * H * W;
+    const T* sc = src + (int64_t)c * H * P;
     for (int e = threadIdx.x; e < C::HR * C::HR; e += 256) {
       const int hy = e / C::HR, hx = e % C::HR;
       const int iy = iy0 + hy, ix = ix0 + hx;
       T v = from_f32<T>(0.f);
-      if (iy < H && ix < W) v = sc[(int64_t)iy * W + ix];
+      if (iy < H && ix < W) v = sc[(int64_t)iy * P + ix];
       s_in[hy * C::HS + hx] = v;
     }
     for (int e = threadIdx.x; e < 96 * K1; e += 256) {
@@ -196,7 +196,7 @@ struct Conv1P {
 template <typename T>
 __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int Ho, int Wo, int64_t in_stride,
+    const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
   using P = Conv1P<T>;
   using Op = Mfma<T>;
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     const int idx = wave * 64 + t * 32 + l32;
     lpix[t] = 4 * (idx / P::TW) * P::HS + 4 * (idx % P::TW);
   }
-  const bool vec_ok = (W % 8) == 0;
+  const bool vec_ok = (W % 8) == 0 && (pitch % 8) == 0;
   vec8 hreg[P::HPER];
   auto load_halo = [&](int t) {
     const int tx = t % tiles_x, r = t / tiles_x, ty = r % tiles_y, plane = r / tiles_y;
@@ -231,7 +231,7 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
         const int c = e / (P::HR * 9), rem = e % (P::HR * 9);
         const int iy = iy0 + rem / 9, ix = ix0 + 8 * (rem % 9);
         if (iy < H) {
-          const T* rowp = src + ((int64_t)c * H + iy) * W;
+          const T* rowp = src + ((int64_t)c * H + iy) * pitch;
           if (vec_ok && ix + 8 <= W) {
             val = *(const vec8*)(rowp + ix);
           } else {
@@ -839,7 +839,7 @@ static_assert(Conv1D::NW * 64 >= 96 * Conv1D::WSL, "weight pieces cover the weig
 template <typename T>
 __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int Ho, int Wo, int64_t in_stride,
+    const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
   using P = Conv1D;
   using Op = Mfma<T>;
@@ -862,7 +862,7 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   const __amdgpu_buffer_rsrc_t rsrc_w =
       __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(96 * 3 * K1 * sizeof(T)), 0x00020000);
   constexpr uint32_t OOB = 0x80000000u;
-  const uint32_t chan_bytes = (uint32_t)((int64_t)H * W * sizeof(T));
+  const uint32_t chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -886,7 +886,7 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
       const int row = q / P::HSL, r = q % P::HSL;
       const int iy = iy0 + row, ix = ix0 + 8 * r;
       const bool ok = row < P::HR && r < 9 && iy < H && ix < W;
-      hoff[i] = ok ? (uint32_t)(((int64_t)iy * W + ix) * sizeof(T)) : OOB;
+      hoff[i] = ok ? (uint32_t)(((int64_t)iy * pitch + ix) * sizeof(T)) : OOB;
     }
   };
   auto load = [&](int buf, int c) {
@@ -1042,7 +1042,7 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
 
 template <typename T>
 int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                  const void* d_packed, void* d_out, int64_t out_stride, const PackedLayout& L,
+                  int32_t P, const void* d_packed, void* d_out, int64_t out_stride, const PackedLayout& L,
                   hipStream_t s) {
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
@@ -1054,19 +1054,19 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
     if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
     if constexpr (std::is_same<T, float>::value) {
-      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
                                                       out_stride, tiles_x, tiles_y);
     } else {
       // Direct loads take 16-byte slots of plane rows at 32-bit byte offsets within one plane.
-      const bool direct = W % 8 == 0 && in_stride % 8 == 0 && ((uintptr_t)in & 15) == 0 &&
-                          (int64_t)3 * H * W * (int64_t)sizeof(T) < 0x7fffffffLL;
+      const bool direct = P % 8 == 0 && in_stride % 8 == 0 && ((uintptr_t)in & 15) == 0 &&
+                          (int64_t)3 * H * P * (int64_t)sizeof(T) < 0x7fffffffLL;
       if (direct) {
         const int grid = (int)std::min<int64_t>(blocks, 2 * device_cu_count());
-        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
                                                    out_stride, tiles_x, tiles_y, (int)blocks);
       } else {
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
-        conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, Ho, Wo, in_stride,
+        conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
                                                        out_stride, tiles_x, tiles_y, (int)blocks);
       }
     }
@@ -1139,17 +1139,19 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
 }
 
 int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride, void* stream) {
+                int32_t in_pitch, dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride,
+                void* stream) {
   const PackedLayout L = packed_layout(dt);
   hipStream_t s = (hipStream_t)stream;
+  const int32_t P = layer == 1 && in_pitch > 0 ? in_pitch : W;
   switch (dt) {
     case DN_F32:
-      return conv_dispatch<float>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L, s);
+      return conv_dispatch<float>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride, L, s);
     case DN_F16:
-      return conv_dispatch<_Float16>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L,
-                                     s);
+      return conv_dispatch<_Float16>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride,
+                                     L, s);
     case DN_BF16:
-      return conv_dispatch<__bf16>(layer, d_in, n, H, W, in_stride, d_packed, d_out, out_stride, L, s);
+      return conv_dispatch<__bf16>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride, L, s);
   }
   return (int)hipErrorInvalidValue;
 }

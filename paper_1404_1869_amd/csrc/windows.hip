@@ -13,7 +13,8 @@
 // bit; the blend is fp32.  A workgroup owns RB output rows of one box: it tabulates the S columns'
 // taps and fractions and its rows' taps in LDS once, then each thread produces one pixel per row
 // (three channels, 12 byte gathers that hit L2) and stores it channel by channel, coalesced along the
-// row.
+// row.  Rows are `pitch` elements apart; the columns from S to pitch - 1 are written as zeros (a
+// pitch that is a multiple of 8 lets conv1 load the rows straight into LDS).
 #include <cmath>
 
 #include "common.h"
@@ -44,8 +45,8 @@ template <typename T>
 __global__ __launch_bounds__(256) void warp_regions_kernel(const uint8_t* __restrict__ img, int n_img,
                                                            int H, int W, const float* __restrict__ boxes,
                                                            const int32_t* __restrict__ box_img, int S,
-                                                           int row_blocks, float m0, float m1, float m2,
-                                                           T* __restrict__ out) {
+                                                           int pitch, int row_blocks, float m0, float m1,
+                                                           float m2, T* __restrict__ out) {
   __shared__ Tap s_col[DN_MAX_WARP_SIDE];
   __shared__ Tap s_row[RB];
   const int r = blockIdx.x / row_blocks, i_first = (blockIdx.x % row_blocks) * RB;
@@ -54,13 +55,13 @@ __global__ __launch_bounds__(256) void warp_regions_kernel(const uint8_t* __rest
   const int b = box_img ? box_img[r] : 0;
   const bool ok = isfinite(x1) && isfinite(y1) && isfinite(x2) && isfinite(y2) && x2 - x1 > 0 &&
                   y2 - y1 > 0 && b >= 0 && b < n_img;
-  const int64_t SS = (int64_t)S * S;
+  const int64_t SS = (int64_t)S * pitch;
   T* o = out + (int64_t)r * 3 * SS;
   if (!ok) {
     for (int i = 0; i < rows; ++i)
-      for (int j = threadIdx.x; j < S; j += 256)
+      for (int j = threadIdx.x; j < pitch; j += 256)
 #pragma unroll
-        for (int c = 0; c < 3; ++c) o[c * SS + (int64_t)(i_first + i) * S + j] = from_f32<T>(0.f);
+        for (int c = 0; c < 3; ++c) o[c * SS + (int64_t)(i_first + i) * pitch + j] = from_f32<T>(0.f);
     return;
   }
   const double fx = (x2 - x1) / S, fy = (y2 - y1) / S;
@@ -74,7 +75,13 @@ __global__ __launch_bounds__(256) void warp_regions_kernel(const uint8_t* __rest
     const Tap ty = s_row[i];
     const uint8_t* r0 = I + (int64_t)ty.i0 * W;
     const uint8_t* r1 = I + (int64_t)ty.i1 * W;
-    for (int j = threadIdx.x; j < S; j += 256) {
+    T* orow = o + (int64_t)(i_first + i) * pitch;
+    for (int j = threadIdx.x; j < pitch; j += 256) {
+      if (j >= S) {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) orow[c * SS + j] = from_f32<T>(0.f);
+        continue;
+      }
       const Tap tx = s_col[j];
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
@@ -82,8 +89,7 @@ __global__ __launch_bounds__(256) void warp_regions_kernel(const uint8_t* __rest
         const float cq = r1[c * HW + tx.i0], d = r1[c * HW + tx.i1];
         const float top = (1.f - tx.frac) * a + tx.frac * bq;
         const float bot = (1.f - tx.frac) * cq + tx.frac * d;
-        o[c * SS + (int64_t)(i_first + i) * S + j] =
-            from_f32<T>((1.f - ty.frac) * top + ty.frac * bot - mean[c]);
+        orow[c * SS + j] = from_f32<T>((1.f - ty.frac) * top + ty.frac * bot - mean[c]);
       }
     }
   }
@@ -92,13 +98,14 @@ __global__ __launch_bounds__(256) void warp_regions_kernel(const uint8_t* __rest
 }  // namespace
 
 int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t W, const float* d_boxes,
-                        const int32_t* d_box_img, int32_t n, int32_t S, const float* mean, dn_dtype dt,
-                        void* d_out, void* stream) {
+                        const int32_t* d_box_img, int32_t n, int32_t S, int32_t pitch, const float* mean,
+                        dn_dtype dt, void* d_out, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const int row_blocks = (S + RB - 1) / RB;
   const int64_t blocks = (int64_t)n * row_blocks;
   if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-#define DN_WARP_ARGS d_img, n_img, H, W, d_boxes, d_box_img, S, row_blocks, mean[0], mean[1], mean[2]
+#define DN_WARP_ARGS \
+  d_img, n_img, H, W, d_boxes, d_box_img, S, pitch, row_blocks, mean[0], mean[1], mean[2]
   switch (dt) {
     case DN_F32:
       warp_regions_kernel<float><<<(unsigned)blocks, 256, 0, s>>>(DN_WARP_ARGS, (float*)d_out);

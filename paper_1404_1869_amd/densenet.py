@@ -45,7 +45,8 @@ class dn_scale_geom(ctypes.Structure):
 
 
 class dn_plane_desc(ctypes.Structure):
-    _fields_ = [("h", ctypes.c_int32), ("w", ctypes.c_int32), ("offset", ctypes.c_int64)]
+    _fields_ = [("h", ctypes.c_int32), ("w", ctypes.c_int32), ("offset", ctypes.c_int64),
+                ("pitch", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class dn_net_params(ctypes.Structure):
@@ -90,8 +91,8 @@ def lib():
             "densenet_lrn_pool": [P, i32, i32, i32, i32, i32, pn, P, P],
             "densenet_maxpool": [P, i32, i32, i32, i32, i32, P, P],
             "densenet_layer_sizes": [i32, i32, pi32],
-            "densenet_warp_regions": [P, i32, i32, i32, P, P, i32, i32, ctypes.POINTER(f32), i32, P, sz,
-                                      psz, P],
+            "densenet_warp_regions": [P, i32, i32, i32, P, P, i32, i32, i32, ctypes.POINTER(f32), i32, P,
+                                      sz, psz, P],
             "densenet_profile_start": [ctypes.c_char_p],
             "densenet_profile_stop": [ctypes.POINTER(dn_profile_entry), i32, pi32],
         }
@@ -292,19 +293,21 @@ def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad
     return out, scale, idx
 
 
-def densenet_warp_regions(images, boxes, dtype: int, S=227, mean=(0.0, 0.0, 0.0), box_img=None, out=None):
+def densenet_warp_regions(images, boxes, dtype: int, S=227, mean=(0.0, 0.0, 0.0), box_img=None, out=None,
+                          pitch=0):
     """Crop-before windows (Sec. 3.4 per-window baseline, Sec. 4): uint8 images [n_img][3][H][W], boxes
-    [n][4] fp32 -> [n][3][S][S] mean-centred windows in `dtype`."""
+    [n][4] fp32 -> [n][3][S][pitch or S] mean-centred windows in `dtype` (columns past S are 0)."""
     torch = _torch()
     if images.dim() == 3:
         images = images[None]
     n_img, _, H, W = images.shape
     n = boxes.shape[0]
+    P = pitch or S
     if out is None:
-        out = torch.empty((n, 3, S, S), dtype=_tdtype(dtype), device=boxes.device)
+        out = torch.empty((n, 3, S, P), dtype=_tdtype(dtype), device=boxes.device)
     m = (ctypes.c_float * 3)(*[float(v) for v in mean])
-    check(lib().densenet_warp_regions(_ptr(images), n_img, H, W, _ptr(boxes), _ptr(box_img), n, S, m, dtype,
-                                      _ptr(out), out.numel() * out.element_size(),
+    check(lib().densenet_warp_regions(_ptr(images), n_img, H, W, _ptr(boxes), _ptr(box_img), n, S, pitch, m,
+                                      dtype, _ptr(out), out.numel() * out.element_size(),
                                       ctypes.byref(ctypes.c_size_t()), _stream()))
     return out
 
@@ -312,25 +315,29 @@ def densenet_warp_regions(images, boxes, dtype: int, S=227, mean=(0.0, 0.0, 0.0)
 class PerWindow:
     """The per-window baseline (Sec. 3.4): every box warped to S x S on its own, then the whole conv stack
     with pool5 on each window as an independent plane (one launch per layer over all windows).  The
-    per-window descriptor is the window's pool5 map, [n][Hp][Wp][256] (6 x 6 x 256 at S = 227)."""
+    per-window descriptor is the window's pool5 map, [n][Hp][Wp][256] (6 x 6 x 256 at S = 227).
+    Window rows are padded to a multiple of 8 elements (zeros past S) so that conv1 loads them straight
+    into LDS; the padding never reaches a stored output."""
 
     def __init__(self, n: int, dtype: int, S=227, device="cuda", net=None):
         torch = _torch()
         self.n, self.S, self.dtype = n, S, dtype
+        self.pitch = (S + 7) // 8 * 8
         net = net or net_params(pool5=True)
         net.pool5 = 1
         desc = []
         for i in range(n):
             q = dn_plane_desc()
-            q.h, q.w, q.offset = S, S, i * 3 * S * S
+            q.h, q.w, q.offset, q.pitch = S, S, i * 3 * S * self.pitch, self.pitch
             desc.append(q)
-        self.windows = torch.empty((n, 3, S, S), dtype=_tdtype(dtype), device=device)
+        self.windows = torch.empty((n, 3, S, self.pitch), dtype=_tdtype(dtype), device=device)
         self.conv = ConvFeatures(desc, dtype, net, device=device)
         hp = self.conv.p5d[0]
         self.pool5_shape = (n, hp.h, hp.w, 256)
 
     def __call__(self, images, boxes, packed, mean=(0.0, 0.0, 0.0), box_img=None):
-        densenet_warp_regions(images, boxes, self.dtype, self.S, mean, box_img, out=self.windows)
+        densenet_warp_regions(images, boxes, self.dtype, self.S, mean, box_img, out=self.windows,
+                              pitch=self.pitch)
         self.conv(self.windows, packed)
         return self.conv.pool5[: self.pool5_shape[0] * self.pool5_shape[1] * self.pool5_shape[2] * 256].view(
             self.pool5_shape)

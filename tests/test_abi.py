@@ -113,20 +113,25 @@ def test_warp_regions_size_query_and_validation():
     L = D.lib()
     need = ctypes.c_size_t()
     m = (ctypes.c_float * 3)(1.0, 2.0, 3.0)
-    assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 2000, 227, m, D.DN_BF16, None, 0,
+    assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 2000, 227, 0, m, D.DN_BF16, None, 0,
                                    ctypes.byref(need), None) == D.DN_OK
     assert need.value == 2000 * 3 * 227 * 227 * 2
     fake = ctypes.c_void_p(256)
-    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 2000, 227, m, D.DN_BF16, fake, 10,
+    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 2000, 227, 0, m, D.DN_BF16, fake, 10,
                                    ctypes.byref(need), None) == D.DN_E_BUFFER_TOO_SMALL
-    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, 0, m, D.DN_F32, fake, 1 << 30,
+    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, 0, 0, m, D.DN_F32, fake, 1 << 30,
                                    None, None) == D.DN_E_INVALID_ARG
-    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, D.DN_MAX_WARP_SIDE + 1, m,
+    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, D.DN_MAX_WARP_SIDE + 1, 0, m,
                                    D.DN_F32, fake, 1 << 40, None, None) == D.DN_E_INVALID_ARG
-    assert L.densenet_warp_regions(fake, 0, 768, 1024, fake, None, 1, 227, m, D.DN_F32, fake, 1 << 30,
+    assert L.densenet_warp_regions(fake, 0, 768, 1024, fake, None, 1, 227, 0, m, D.DN_F32, fake, 1 << 30,
                                    None, None) == D.DN_E_INVALID_ARG
-    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, 227, m, 7, fake, 1 << 30, None,
+    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 1, 227, 0, m, 7, fake, 1 << 30, None,
                                    None) == D.DN_E_UNSUPPORTED
+    assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 10, 227, 232, m, D.DN_BF16, None, 0,
+                                   ctypes.byref(need), None) == D.DN_OK
+    assert need.value == 10 * 3 * 227 * 232 * 2
+    assert L.densenet_warp_regions(fake, 1, 768, 1024, fake, None, 10, 227, 200, m, D.DN_BF16, fake,
+                                   1 << 30, None, None) == D.DN_E_INVALID_ARG
     # n == 0 launches nothing and accepts null buffers
-    assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 0, 227, None, D.DN_F32, fake, 0,
+    assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 0, 227, 0, None, D.DN_F32, fake, 0,
                                    None, None) == D.DN_OK

@@ -117,3 +117,31 @@ def test_per_window_2000_boxes_sampled(D):
     for i in (0, 999, 1234, 1999):
         ref = oracle_pool5(IMGS, boxes, bimg, i)
         assert_layer_close(np.moveaxis(got[i], -1, 0), ref, "bf16", f"per-window pool5 box {i}")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_warp_regions_row_pitch(D, dt):
+    boxes = np.concatenate([synth.boxes(106, 40, WL.H, WL.W), special_boxes(WL.H, WL.W)])
+    x, b = torch.from_numpy(IMGS).cuda(), torch.from_numpy(boxes).cuda()
+    got = D.densenet_warp_regions(x, b, DTS[dt], 227, MEAN, pitch=232)
+    assert tuple(got.shape) == (len(boxes), 3, 227, 232)
+    check_windows(got[..., :227], oracle.warp_regions(IMGS, boxes, 227, MEAN), dt)
+    assert not got[..., 227:].any()
+
+
+def test_conv_features_row_pitch_matches_packed_rows(D):
+    """The same windows as pitch-232 planes (conv1 loads rows straight into LDS) and as packed 227-wide
+    planes (register-staged conv1) give the same pool5 descriptors."""
+    boxes = synth.boxes(107, 24, WL.H, WL.W)
+    x, b = torch.from_numpy(IMGS).cuda(), torch.from_numpy(boxes).cuda()
+    pk = packed(D, "bf16")
+    a = D.PerWindow(len(boxes), DTS["bf16"])(x, b, pk, MEAN).float()
+    win = D.densenet_warp_regions(x, b, DTS["bf16"], 227, MEAN)
+    desc = []
+    for i in range(len(boxes)):
+        q = D.dn_plane_desc()
+        q.h, q.w, q.offset = 227, 227, i * 3 * 227 * 227
+        desc.append(q)
+    cf = D.densenet_conv_features(win, desc, DTS["bf16"], pk, D.net_params(pool5=True))
+    c = torch.stack([m.float() for m in cf.pool5_maps()])
+    torch.testing.assert_close(a, c, rtol=0, atol=0)
