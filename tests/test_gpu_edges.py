@@ -186,3 +186,32 @@ def test_region_windows_no_boxes(D):
                                            torch.zeros((0, 4), dtype=torch.float32, device="cuda"))
     torch.cuda.synchronize()
     assert out.shape == (0, 9216) and sc.shape == (0,)
+
+
+@pytest.mark.parametrize("spo,base,plane,dt", [(5, 2.0, 2000, "bf16"), (3, 1.0, 1200, "f16")])
+def test_scale_and_plane_variants_end_to_end(D, spo, base, plane, dt):
+    """Sec. 3.1's other pyramid recipes: a maximum scale of 2 (upsampling) with 5 scales per octave on
+    2000 x 2000 planes, and 3 scales per octave on 1200 x 1200 planes; planes, conv5 of the fullest
+    plane, and region windows of the whole pyramid against the oracle."""
+    H, W, K = 240, 320, 2 * spo
+    img = synth.image(300 + spo, H, W)
+    p = D.pyramid_params(K, spo, base_scale=base, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=plane,
+                         plane_w=plane, mean=synth.IMAGENET_MEAN)
+    pyra = run(D, img, p, dt)
+    op = oracle.plan(H, W, K, spo, base, 0, 16, plane, plane)
+    assert len(pyra.plan.planes) == op.n_planes
+    ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    for j, d in enumerate(pyra.plan.planes):
+        got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        assert np.all(np.abs(got - ref_planes[j]) <= 0.5 * ulp(ref_planes[j], dt) + 1e-3), f"plane {j}"
+    maps = pyra.conv.conv5_maps()
+    c5 = {}
+    for j in range(op.n_planes):
+        c5[j] = oracle.net(ref_planes[j].astype(np.float32), W7)
+        assert_layer_close(chw(maps[j].float().cpu().numpy()), c5[j], dt, f"conv5 plane {j}")
+    boxes = synth.boxes(12, 200, H, W, smin=16, smax=240)
+    desc, scale, _ = D.densenet_region_windows(pyra.conv.conv5, list(pyra.conv.c5d), DTS[dt], pyra.plan,
+                                               16, op.n_planes, torch.from_numpy(boxes).cuda())
+    rd, rs, _, _ = oracle.region_windows([c5[j] for j in range(op.n_planes)], op, boxes)
+    np.testing.assert_array_equal(scale.cpu().numpy(), rs)
+    assert_layer_close(desc.cpu().numpy(), rd, dt, "region windows")
