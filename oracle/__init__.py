@@ -42,7 +42,7 @@ def lib():
         L = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         i32, f64 = ctypes.c_int, ctypes.c_double
-        L.oracle_plan.argtypes = [i32, i32, i32, i32, f64, i32, i32, i32, i32, P, P]
+        L.oracle_plan.argtypes = [i32, i32, i32, i32, f64, i32, i32, i32, i32, i32, P, P, P]
         L.oracle_plan.restype = i32
         L.oracle_resize_center.argtypes = [P, i32, i32, i32, i32, P, P]
         L.oracle_resize_center.restype = None
@@ -59,7 +59,7 @@ def lib():
         L.oracle_net.argtypes = [P, i32, i32, P, P, f64, f64, f64, i32, i32, P, P]
         L.oracle_net.restype = i32
         L.oracle_region_windows.argtypes = [P, P, P, P, i32, i32, P, P, i32, P, P, i32, f64, i32,
-                                            P, P, P, P]
+                                            i32, P, P, P, P]
         L.oracle_region_windows.restype = i32
         for name in ("oracle_conv5_side", "oracle_pool_side"):
             getattr(L, name).argtypes = [i32]
@@ -81,7 +81,7 @@ def _p(a: np.ndarray):
 # Geometry
 # ----------------------------------------------------------------------------------------------
 GI_FIELDS = ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0", "r1", "c0", "c1", "plane_h",
-             "plane_w")
+             "plane_w", "aspect")
 
 
 @dataclass
@@ -91,23 +91,28 @@ class Plan:
     n_planes: int
     pad: int
     plane_sizes: list       # [(PH, PW)] per plane
+    n_aspects: int = 0
 
     def field(self, name):
         return self.gi[:, GI_FIELDS.index(name)]
 
 
-def plan(H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, plane_w=0) -> Plan:
-    """Scales, sizes, rectangles, stitching and conv5 windows (Sec. 3.1)."""
-    gi = np.zeros((K, 16), np.int32)
-    gd = np.zeros((K, 3), np.float64)
+def plan(H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, plane_w=0,
+         aspects=None) -> Plan:
+    """Scales, sizes, rectangles, stitching and conv5 windows (Sec. 3.1); with `aspects`, one pyramid
+    per aspect ratio, all stitched together (Sec. 3.3), entries aspect-major."""
+    asp = np.ascontiguousarray(aspects if aspects is not None else [], np.float64)
+    E = K * max(1, len(asp))
+    gi = np.zeros((E, 16), np.int32)
+    gd = np.zeros((E, 3), np.float64)
     n = lib().oracle_plan(H, W, K, spo, float(base_scale), base_longest_side, pad, plane_h, plane_w,
-                          _p(gi), _p(gd))
+                          len(asp), _p(asp) if len(asp) else None, _p(gi), _p(gd))
     if n < 0:
         raise ValueError(f"oracle_plan failed with {n}")
     sizes = [None] * n
-    for k in range(K):
+    for k in range(E):
         sizes[gi[k, 3]] = (int(gi[k, 12]), int(gi[k, 13]))
-    return Plan(gi, gd, n, pad, sizes)
+    return Plan(gi, gd, n, pad, sizes, len(asp))
 
 
 def threads() -> int:
@@ -250,8 +255,8 @@ def region_windows(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None
     lam = np.zeros((n, S, S, 2), np.float64)
     rc = lib().oracle_region_windows(_p(flat), _p(offs), _p(Hcs), _p(Wcs), pl.n_planes,
                                      pl.gi.shape[0], _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
-                                     _p(bi) if bi is not None else None, n, float(T), S, _p(desc),
-                                     _p(scale), _p(idx), _p(lam))
+                                     _p(bi) if bi is not None else None, n, float(T), S,
+                                     pl.n_aspects, _p(desc), _p(scale), _p(idx), _p(lam))
     if rc:
         raise ValueError("oracle_region_windows: bad arguments")
     return desc, scale, idx, lam

@@ -54,7 +54,11 @@ int oracle_threads(void) {
 // -1 bad argument, -2 a rectangle larger than the stitching plane.
 //
 // Readings: s_k = base * 2^(-k/spo) for k = 0..K-1 (Sec. 3.1 scales per octave), base = base_scale or
-// longest_side / max(H, W); sizes round half up, minimum 1.  Per-scale mode (plane_h == 0): each
+// longest_side / max(H, W); sizes round half up, minimum 1.
+// Aspect-ratio pyramids (Sec. 3.3): with n_aspects > 0 ratios r_a, the image warped to each ratio gets
+// a whole pyramid: entry e = a K + k has h = floor(H (s_k / sqrt(r_a)) + 0.5), w = floor(W (s_k
+// sqrt(r_a)) + 0.5) (the warp keeps the image's area), and every entry is one item of the stitching
+// below; gi[e*16 + 0] = e, gi[e*16 + 14] = a.  n_aspects = 0 is the single pyramid of ratio 1.  Per-scale mode (plane_h == 0): each
 // scale padded by p on every side is its own plane.  Stitched mode: rectangle sides rounded up to a
 // multiple of 16 (the conv5 stride, so every scale keeps the same cell grid as when run alone); items
 // taken largest first (rh desc, rw desc, k asc); on each existing plane, in creation order, the
@@ -98,8 +102,13 @@ static int64_t conv5_side(int64_t n) {
 int oracle_conv5_side(int n) { return (int)conv5_side(n); }
 
 int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longest_side, int pad,
-                int plane_h, int plane_w, int32_t* gi, double* gd) {
-  if (H <= 0 || W <= 0 || K <= 0 || spo <= 0 || pad < 0) return -1;
+                int plane_h, int plane_w, int n_aspects, const double* aspects, int32_t* gi,
+                double* gd) {
+  if (H <= 0 || W <= 0 || K <= 0 || spo <= 0 || pad < 0 || n_aspects < 0) return -1;
+  for (int a = 0; a < n_aspects; ++a)
+    if (!(aspects[a] > 0.0) || !std::isfinite(aspects[a])) return -1;
+  const int A = n_aspects > 0 ? n_aspects : 1, NS = K;
+  K = A * NS;  // items: one per (aspect, scale)
   if ((plane_h == 0) != (plane_w == 0)) return -1;
   double base = base_scale;
   if (base_longest_side > 0) base = (double)base_longest_side / (double)std::max(H, W);
@@ -108,10 +117,12 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
   struct Item { int k, h, w, rh, rw, plane, y, x; };
   std::vector<Item> it(K);
   for (int k = 0; k < K; ++k) {
-    double s = base * std::pow(2.0, -(double)k / (double)spo);
+    const int a = k / NS;
+    double s = base * std::pow(2.0, -(double)(k % NS) / (double)spo);
     gd[k * 3 + 0] = s;
-    int h = (int)std::floor((double)H * s + 0.5);
-    int w = (int)std::floor((double)W * s + 0.5);
+    const double q = n_aspects > 0 ? std::sqrt(aspects[a]) : 1.0;
+    int h = (int)std::floor((double)H * (s / q) + 0.5);
+    int w = (int)std::floor((double)W * (s * q) + 0.5);
     if (h < 1) h = 1;
     if (w < 1) w = 1;
     gd[k * 3 + 1] = (double)h / (double)H;
@@ -190,7 +201,7 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
     int32_t* o = gi + k * 16;
     o[0] = k; o[1] = r.h; o[2] = r.w; o[3] = r.plane; o[4] = r.y; o[5] = r.x; o[6] = r.rh; o[7] = r.rw;
     o[8] = (int32_t)r0; o[9] = (int32_t)r1; o[10] = (int32_t)c0; o[11] = (int32_t)c1;
-    o[12] = PH; o[13] = PW; o[14] = 0; o[15] = 0;
+    o[12] = PH; o[13] = PW; o[14] = k / NS; o[15] = 0;
   }
   return n_planes;
 }
@@ -470,7 +481,9 @@ int oracle_net(const float* plane, int PH, int PW, const float* const* w, const 
 //   box (x1, y1, x2, y2) in original-image pixel-edge coordinates; bw = x2 - x1, bh = y2 - y1; a box
 //   with a non-finite or non-positive side gets scale -1 and a zero row.
 //   a_k = (sy_k bh)(sx_k bw); cost_k = max(a_k / T^2, T^2 / a_k); k* = argmin, ties to the smaller k,
-//   scales with an empty cell window are skipped.
+//   scales with an empty cell window are skipped.  With aspect-ratio pyramids (n_aspects > 1) the
+//   cost is multiplied by max(rho_k, 1 / rho_k), rho_k = (sx_k bw) / (sy_k bh) the aspect of the box on
+//   entry k, so the box is read where it is closest to a T x T square.
 //   X = x * sx + x_k + p (plane coordinates of the scale's real pixels); bin centre
 //   U = X1 + f_b (X2 - X1), f_b = (b + 0.5)/S; conv5 coordinate g = (U - 17.5) * 0.0625 (cell i is
 //   centred at 16 i + 17.5), clamped to [c0, c1]; j0 = floor(g), j1 = min(j0 + 1, c1), lambda = g - j0.
@@ -483,7 +496,8 @@ int oracle_net(const float* plane, int PH, int PW, const float* const* w, const 
 int oracle_region_windows(const float* conv5, const int64_t* plane_off, const int32_t* Hcs,
                           const int32_t* Wcs, int planes_per_img, int K, const int32_t* gi,
                           const double* gd, int pad, const float* boxes, const int32_t* box_img, int n,
-                          double T, int S, float* desc, int32_t* scale, int32_t* idx, double* lam) {
+                          double T, int S, int n_aspects, float* desc, int32_t* scale, int32_t* idx,
+                          double* lam) {
   if (S <= 0 || !(T > 0)) return -1;
   const int C = 256;
 #pragma omp parallel for schedule(dynamic, 16)
@@ -504,7 +518,11 @@ int oracle_region_windows(const float* conv5, const int64_t* plane_off, const in
       const int32_t* g = gi + k * 16;
       if (g[9] < g[8] || g[11] < g[10]) continue;
       const double a = (gd[k * 3 + 1] * bh) * (gd[k * 3 + 2] * bw);
-      const double cost = std::max(a / T2, T2 / a);
+      double cost = std::max(a / T2, T2 / a);
+      if (n_aspects > 1) {
+        const double rho = (gd[k * 3 + 2] * bw) / (gd[k * 3 + 1] * bh);
+        cost = cost * std::max(rho, 1.0 / rho);
+      }
       if (best < 0 || cost < best_cost) { best = k; best_cost = cost; }
     }
     if (best < 0) continue;
