@@ -49,8 +49,9 @@ typedef enum {
 typedef enum { DN_F32 = 0, DN_F16 = 1, DN_BF16 = 2 } dn_dtype;
 typedef enum { DN_PAD_ZERO = 0, DN_PAD_RAMP = 1 } dn_pad_mode;
 
-#define DN_MAX_SCALES 64
+#define DN_MAX_SCALES 64 /* pyramid entries (scales x aspect ratios) */
 #define DN_MAX_PLANES_PER_IMAGE 64
+#define DN_MAX_ASPECTS 8
 
 /* Pyramid recipe (Sec. 3.1, 3.2).
  *  scales: s_k = base * 2^(-k / steps_per_octave), k = 0 .. n_scales-1, where base = base_scale, or
@@ -63,7 +64,12 @@ typedef enum { DN_PAD_ZERO = 0, DN_PAD_RAMP = 1 } dn_pad_mode;
  *          rounded up to multiples of 16 px, are stitched onto planes of this size by Bottom-Left
  *          Fill (largest first; first plane, then topmost, then leftmost candidate corner).
  *  mean:   the mean pixel subtracted from input channels 0, 1, 2 (the background of every plane
- *          is the mean pixel, i.e. 0 after centring). */
+ *          is the mean pixel, i.e. 0 after centring).
+ *  n_aspects, aspects: aspect-ratio pyramids (Sec. 3.3).  0 => one pyramid of the image.  Otherwise
+ *          the image warped to each ratio r = aspects[a] > 0 gets a whole pyramid, keeping its area:
+ *          entry e = a * n_scales + k has sides floor(H (s_k / sqrt(r)) + 0.5) x floor(W (s_k sqrt(r))
+ *          + 0.5) (minimum 1), and all n_aspects * n_scales entries (at most DN_MAX_SCALES) are
+ *          stitched together; geometry arrays then hold one dn_scale_geom per entry. */
 typedef struct {
   int32_t n_scales;
   int32_t steps_per_octave;
@@ -73,9 +79,13 @@ typedef struct {
   int32_t pad_mode;
   int32_t plane_h, plane_w;
   float mean[3];
+  int32_t n_aspects;
+  double aspects[DN_MAX_ASPECTS];
 } dn_pyramid_params;
 
-/* Geometry of scale k, identical for every image of a batch (Sec. 3.1 unpacking).
+/* Geometry of pyramid entry k (a scale of one aspect ratio), identical for every image of a batch
+ * (Sec. 3.1 unpacking).  k: entry index (aspect * n_scales + scale); aspect: index into aspects (0
+ * for a single pyramid); s: the scale factor s_k of the entry's scale.
  *  (h, w): scaled image size; sy = h/H, sx = w/W are the effective factors.
  *  plane:  index of the scale's plane within one image's planes.
  *  (y, x, rh, rw): padded rectangle on that plane; the real pixels start at (y+pad, x+pad).
@@ -86,6 +96,7 @@ typedef struct {
   int32_t k, h, w, plane;
   int32_t y, x, rh, rw;
   int32_t r0, r1, c0, c1;
+  int32_t aspect, reserved;
   double s, sy, sx;
 } dn_scale_geom;
 
@@ -159,6 +170,9 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
  * ratio (ties to the smaller k; scales with an empty window skipped) is chosen, and S x S bilinear
  * samples at the bin centres of the box are read from that scale's conv5 window (coordinates clamped
  * to the window), all 256 channels: d_out[n][256 * S * S] fp32, flattened (channel, row, column).
+ * geom/n_scales: all pyramid entries; when they span several aspect ratios (geom[k].aspect > 0 for
+ * some k, Sec. 3.3) the cost of entry k is multiplied by max(rho, 1/rho), rho = (sx bw)/(sy bh) the
+ * box's aspect on that entry, so each box is read where it is closest to a target x target square.
  * conv5_desc: [n_img * planes_per_img] maps from densenet_conv_features (image b's plane j at index
  * b * planes_per_img + j), channels-last with 256 channels, offsets multiples of 16 bytes.  d_box_img: nullable [n] image index per box (NULL => image 0).
  * d_scale: [n] chosen scale, -1 for a box with a non-finite or non-positive side (its row is 0).

@@ -30,6 +30,7 @@ class Workload:
     n_boxes: int = 0
     box_seed: int = 0
     mean: tuple = field(default=IMAGENET_MEAN)
+    aspects: tuple = ()     # aspect-ratio pyramids (empty: one pyramid)
 
     @property
     def n_img(self) -> int:

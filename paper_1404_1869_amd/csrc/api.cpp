@@ -139,8 +139,9 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
     if (!d_images) return fail(DN_E_INVALID_ARG, "d_images is NULL");
     if ((int64_t)n_img * *n_planes > 65535) return fail(DN_E_TOO_LARGE, "too many planes in one call");
+    const int K = p->n_scales * (p->n_aspects > 0 ? p->n_aspects : 1);  // pyramid entries
     PyrArgs a{};
-    a.n_scales = p->n_scales;
+    a.n_scales = K;
     a.H = H;
     a.W = W;
     a.pad = p->pad;
@@ -149,7 +150,7 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     int e = 0;
     for (int j = 0; j < *n_planes; ++j) {
       a.plane_first[j] = (uint8_t)e;
-      for (int k = 0; k < p->n_scales; ++k)
+      for (int k = 0; k < K; ++k)
         if (geom[k].plane == j)
           a.s[e++] = PyrScale{geom[k].plane, geom[k].y, geom[k].x, geom[k].rh, geom[k].rw, geom[k].h,
                               geom[k].w};
@@ -430,6 +431,8 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
     if (n == 0) return DN_OK;
     RegArgs a{};
     a.n_scales = n_scales;
+    a.n_aspects = 1;
+    for (int k = 0; k < n_scales; ++k) a.n_aspects = std::max(a.n_aspects, geom[k].aspect + 1);
     a.pad = pad;
     a.planes_per_img = planes_per_img;
     a.S = S;

@@ -100,6 +100,7 @@ struct RegScale {
 };
 struct RegArgs {
   int32_t n_scales, pad, planes_per_img, S, C, n_img;
+  int32_t n_aspects;  // > 1: several aspect-ratio pyramids, the scale cost includes the box aspect
   double target;
   RegScale s[DN_MAX_SCALES];
   int64_t map_off[DN_MAX_PLANES_PER_IMAGE];  // offset of plane j's map within an image's maps

@@ -92,16 +92,31 @@ int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan) {
   const double base = p.base_longest_side > 0 ? (double)p.base_longest_side / (double)std::max(H, W)
                                                : p.base_scale;
   if (!(base > 0.0) || !std::isfinite(base)) return fail(DN_E_INVALID_ARG, "base scale must be > 0");
+  if (p.n_aspects < 0 || p.n_aspects > DN_MAX_ASPECTS)
+    return fail(DN_E_INVALID_ARG, "n_aspects must be in 0..DN_MAX_ASPECTS");
+  for (int a = 0; a < p.n_aspects; ++a)
+    if (!(p.aspects[a] > 0.0) || !std::isfinite(p.aspects[a]))
+      return fail(DN_E_INVALID_ARG, "aspect ratios must be positive and finite");
+  const int NA = p.n_aspects > 0 ? p.n_aspects : 1, NS = p.n_scales;
+  if (NA * NS > DN_MAX_SCALES) {
+    std::ostringstream os;
+    os << "n_aspects * n_scales must be at most " << DN_MAX_SCALES;
+    return fail(DN_E_INVALID_ARG, os.str());
+  }
 
-  const int K = p.n_scales;
+  // Entries: one per (aspect ratio, scale), aspect-major (Sec. 3.3: a whole pyramid per ratio).
+  const int K = NA * NS;
   const bool stitched = p.plane_h > 0;
   plan.scales.assign(K, dn_scale_geom{});
   plan.planes.clear();
   for (int k = 0; k < K; ++k) {
     dn_scale_geom& g = plan.scales[k];
     g.k = k;
-    g.s = base * std::pow(2.0, -(double)k / (double)p.steps_per_octave);
-    const double fh = std::floor((double)H * g.s + 0.5), fw = std::floor((double)W * g.s + 0.5);
+    g.aspect = k / NS;
+    g.s = base * std::pow(2.0, -(double)(k % NS) / (double)p.steps_per_octave);
+    // Area-keeping warp to ratio r: height over sqrt(r), width times sqrt(r) (r = 1: the plain scale).
+    const double q = p.n_aspects > 0 ? std::sqrt(p.aspects[g.aspect]) : 1.0;
+    const double fh = std::floor((double)H * (g.s / q) + 0.5), fw = std::floor((double)W * (g.s * q) + 0.5);
     if (!(fh <= 65535.0) || !(fw <= 65535.0))
       return fail(DN_E_TOO_LARGE, "scaled image sides are limited to 65535 px");
     g.h = std::max(1, (int)fh);

@@ -1,6 +1,8 @@
 // Region windows ("crop after", Sec. 4): a box of the original image is read out of the conv5
 // pyramid at the scale whose scaled area is closest to target^2, as S x S bilinear samples at the
-// bin centres of the box, all channels.
+// bin centres of the box, all channels.  With several aspect-ratio pyramids (Sec. 3.3) the cost of an
+// entry is multiplied by max(rho, 1 / rho), rho the aspect of the box on that entry, so the box is
+// read where it is closest to a target x target square.
 //
 // One workgroup per box; each thread blends one 16-byte vector of channels of one bin at a time.
 // The scale choice and the sample positions are computed in fp64 with + - * / only and FP
@@ -46,6 +48,10 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       const double area = (a.s[k].sy * bh) * (a.s[k].sx * bw);
       const double p = area / T2, q = T2 / area;
       cost = p < q ? q : p;
+      if (a.n_aspects > 1) {
+        const double rho = (a.s[k].sx * bw) / (a.s[k].sy * bh), irho = 1.0 / rho;
+        cost = cost * (rho < irho ? irho : rho);
+      }
     } else {
       k = 1 << 30;
     }

@@ -21,7 +21,7 @@ DN_OK, DN_E_INVALID_ARG, DN_E_TOO_LARGE, DN_E_BUFFER_TOO_SMALL = 0, -1, -2, -3
 DN_E_UNSUPPORTED, DN_E_HIP, DN_E_INTERNAL = -4, -5, -6
 DN_F32, DN_F16, DN_BF16 = 0, 1, 2
 DN_PAD_ZERO, DN_PAD_RAMP = 0, 1
-DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE, DN_MAX_WARP_SIDE = 64, 64, 1024
+DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE, DN_MAX_WARP_SIDE, DN_MAX_ASPECTS = 64, 64, 1024, 8
 DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
@@ -35,12 +35,13 @@ class dn_pyramid_params(ctypes.Structure):
     _fields_ = [("n_scales", ctypes.c_int32), ("steps_per_octave", ctypes.c_int32),
                 ("base_scale", ctypes.c_double), ("base_longest_side", ctypes.c_int32),
                 ("pad", ctypes.c_int32), ("pad_mode", ctypes.c_int32), ("plane_h", ctypes.c_int32),
-                ("plane_w", ctypes.c_int32), ("mean", ctypes.c_float * 3)]
+                ("plane_w", ctypes.c_int32), ("mean", ctypes.c_float * 3), ("n_aspects", ctypes.c_int32),
+                ("aspects", ctypes.c_double * DN_MAX_ASPECTS)]
 
 
 class dn_scale_geom(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
-                                              "r1", "c0", "c1")] + \
+                                              "r1", "c0", "c1", "aspect", "reserved")] + \
                [(n, ctypes.c_double) for n in ("s", "sy", "sx")]
 
 
@@ -141,19 +142,27 @@ def _tdtype(dt: int):
 
 
 def pyramid_params(n_scales, steps_per_octave, base_scale=1.0, base_longest_side=0, pad=0,
-                   pad_mode=DN_PAD_ZERO, plane_h=0, plane_w=0, mean=(0.0, 0.0, 0.0)):
+                   pad_mode=DN_PAD_ZERO, plane_h=0, plane_w=0, mean=(0.0, 0.0, 0.0), aspects=()):
     p = dn_pyramid_params()
     p.n_scales, p.steps_per_octave, p.base_scale = n_scales, steps_per_octave, base_scale
     p.base_longest_side, p.pad, p.pad_mode = base_longest_side, pad, pad_mode
     p.plane_h, p.plane_w = plane_h, plane_w
     p.mean = (ctypes.c_float * 3)(*mean)
+    p.n_aspects = len(aspects)
+    for i, r in enumerate(aspects):
+        p.aspects[i] = float(r)
     return p
+
+
+def n_entries(p: dn_pyramid_params) -> int:
+    """Pyramid entries (scales x aspect ratios) of a recipe: the length of its geometry arrays."""
+    return p.n_scales * max(1, p.n_aspects)
 
 
 def params_for(w):
     """dn_pyramid_params of a configs.Workload."""
     return pyramid_params(w.n_scales, w.steps_per_octave, w.base_scale, w.base_longest_side, w.pad,
-                          w.pad_mode, w.plane_h, w.plane_w, w.mean)
+                          w.pad_mode, w.plane_h, w.plane_w, w.mean, w.aspects)
 
 
 def net_params(alpha=1e-4, beta=0.75, k=1.0, n=5, lrn_before_pool=True, pool5=False):
@@ -173,16 +182,17 @@ class PlanResult:
     image_elems: int
 
     def geom_array(self) -> np.ndarray:
-        """[K][12] int32: k, h, w, plane, y, x, rh, rw, r0, r1, c0, c1."""
+        """[K][13] int32: k, h, w, plane, y, x, rh, rw, r0, r1, c0, c1, aspect."""
         return np.array([[getattr(g, f) for f in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
-                                                   "r1", "c0", "c1")] for g in self.geom], np.int32)
+                                                   "r1", "c0", "c1", "aspect")] for g in self.geom],
+                        np.int32)
 
     def scale_array(self) -> np.ndarray:
         return np.array([[g.s, g.sy, g.sx] for g in self.geom], np.float64)
 
 
 def densenet_plan_pyramid(H: int, W: int, p: dn_pyramid_params) -> PlanResult:
-    geom = (dn_scale_geom * p.n_scales)()
+    geom = (dn_scale_geom * n_entries(p))()
     planes = (dn_plane_desc * DN_MAX_PLANES_PER_IMAGE)()
     n = ctypes.c_int32()
     e = ctypes.c_int64()
@@ -197,7 +207,7 @@ def densenet_build_pyramid(images, p: dn_pyramid_params, dtype: int, out=None):
     if images.dim() == 3:
         images = images[None]
     n_img, _, H, W = images.shape
-    geom = (dn_scale_geom * p.n_scales)()
+    geom = (dn_scale_geom * n_entries(p))()
     planes = (dn_plane_desc * DN_MAX_PLANES_PER_IMAGE)()
     n = ctypes.c_int32()
     e = ctypes.c_int64()

@@ -215,3 +215,39 @@ def test_scale_and_plane_variants_end_to_end(D, spo, base, plane, dt):
     rd, rs, _, _ = oracle.region_windows([c5[j] for j in range(op.n_planes)], op, boxes)
     np.testing.assert_array_equal(scale.cpu().numpy(), rs)
     assert_layer_close(desc.cpu().numpy(), rd, dt, "region windows")
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_aspect_ratio_pyramids_end_to_end(D, dt):
+    """Sec. 3.3: one area-keeping warped pyramid per aspect ratio (1/2, 1, 2), all stitched onto shared
+    1200 x 1200 planes; planes, conv5 of every plane, and region windows (entry choice bit for bit,
+    including boxes whose aspect picks the warped pyramids) against the oracle."""
+    H, W, K, r = 480, 640, 6, (0.5, 1.0, 2.0)
+    img = synth.image(333, H, W)
+    p = D.pyramid_params(K, 4, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=1200, plane_w=1200,
+                         mean=synth.IMAGENET_MEAN, aspects=r)
+    pyra = run(D, img, p, dt)
+    op = oracle.plan(H, W, K, 4, 1.0, 0, 16, 1200, 1200, aspects=list(r))
+    assert len(pyra.plan.geom) == K * len(r) and len(pyra.plan.planes) == op.n_planes
+    ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    for j, d in enumerate(pyra.plan.planes):
+        got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        if dt == "f32":
+            assert np.max(np.abs(got - ref_planes[j])) <= 1e-5 * 255, f"plane {j}"
+        else:
+            assert np.all(np.abs(got - ref_planes[j]) <= 0.5 * ulp(ref_planes[j], dt) + 1e-3), f"plane {j}"
+    maps = pyra.conv.conv5_maps()
+    c5 = []
+    for j in range(op.n_planes):
+        c5.append(oracle.net(ref_planes[j].astype(np.float32), W7))
+        assert_layer_close(chw(maps[j].float().cpu().numpy()), c5[j], dt, f"conv5 plane {j}")
+    boxes = np.concatenate([synth.boxes(14, 300, H, W), np.array(
+        [[20, 100, 620, 400], [250, 10, 400, 470], [100, 100, 350, 350]], np.float32)])
+    desc, scale, _ = D.densenet_region_windows(pyra.conv.conv5, list(pyra.conv.c5d), DTS[dt], pyra.plan,
+                                               16, op.n_planes, torch.from_numpy(boxes).cuda())
+    rd, rs, _, _ = oracle.region_windows(c5, op, boxes)
+    sc = scale.cpu().numpy()
+    np.testing.assert_array_equal(sc, rs)
+    np.testing.assert_array_equal(op.field("aspect")[sc[-3:]], [0, 2, 1])
+    assert len(set(op.field("aspect")[sc])) == 3
+    assert_layer_close(desc.cpu().numpy(), rd, dt, "region windows")

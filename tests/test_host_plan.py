@@ -14,6 +14,10 @@ CASES = list(C.ALL) + [
     C.Workload("tiny", 1, 1, (1,), 1, 1, pad=16),
     C.Workload("wide", 64, 1000, (1,), 9, 3, pad=8, plane_h=600, plane_w=1200),
     C.Workload("many_small", 120, 160, (1,), 40, 10, pad=16, pad_mode=1, plane_h=480, plane_w=480),
+    C.Workload("aspects3", 480, 640, (1,), 12, 4, pad=16, pad_mode=1, plane_h=1200, plane_w=1200,
+               aspects=(0.5, 1.0, 2.0)),
+    C.Workload("aspects_per_scale_planes", 97, 131, (1,), 5, 2, pad=16, aspects=(1 / 3, 3.0)),
+    C.Workload("aspect_single", 300, 200, (1,), 6, 3, pad=8, plane_h=800, plane_w=800, aspects=(1.7,)),
 ]
 
 
@@ -21,9 +25,9 @@ CASES = list(C.ALL) + [
 def test_plan_bit_exact_vs_oracle(w):
     lib = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w))
     ref = oracle.plan(w.H, w.W, w.n_scales, w.steps_per_octave, w.base_scale, w.base_longest_side,
-                      w.pad, w.plane_h, w.plane_w)
+                      w.pad, w.plane_h, w.plane_w, aspects=list(w.aspects) or None)
     assert len(lib.planes) == ref.n_planes
-    np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, :12])
+    np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, [*range(12), 14]])
     np.testing.assert_array_equal(lib.scale_array(), ref.gd)   # bitwise equal fp64
     assert [(p.h, p.w) for p in lib.planes] == ref.plane_sizes
     off = np.cumsum([0] + [3 * h * w for h, w in ref.plane_sizes])
