@@ -61,6 +61,9 @@ def lib():
         L.oracle_region_windows.argtypes = [P, P, P, P, i32, i32, P, P, i32, P, P, i32, f64, i32,
                                             i32, P, P, P, P]
         L.oracle_region_windows.restype = i32
+        L.oracle_region_pool.argtypes = [P, P, P, P, i32, i32, P, P, i32, P, P, i32, f64, i32, i32,
+                                         P, P, P]
+        L.oracle_region_pool.restype = i32
         for name in ("oracle_conv5_side", "oracle_pool_side"):
             getattr(L, name).argtypes = [i32]
             getattr(L, name).restype = i32
@@ -260,3 +263,26 @@ def region_windows(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None
     if rc:
         raise ValueError("oracle_region_windows: bad arguments")
     return desc, scale, idx, lam
+
+
+def region_pool(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None, T=227.0, S=6):
+    """Max-pooled region bins: the box read at the same entry as region_windows, each of its S x S bins
+    the per-channel max over the conv5 cells centred inside it.  Returns desc [n][256*S*S], scale [n],
+    idx [n][S][S][4] (i_first, i_last, j_first, j_last)."""
+    flat = np.concatenate([np.ascontiguousarray(c, np.float32).ravel() for c in conv5_planes])
+    offs = np.cumsum([0] + [c.size for c in conv5_planes[:-1]]).astype(np.int64)
+    Hcs = np.array([c.shape[1] for c in conv5_planes], np.int32)
+    Wcs = np.array([c.shape[2] for c in conv5_planes], np.int32)
+    boxes = np.ascontiguousarray(boxes, np.float32)
+    n = boxes.shape[0]
+    bi = None if box_img is None else np.ascontiguousarray(box_img, np.int32)
+    desc = np.zeros((n, 256 * S * S), np.float32)
+    scale = np.zeros(n, np.int32)
+    idx = np.zeros((n, S, S, 4), np.int32)
+    rc = lib().oracle_region_pool(_p(flat), _p(offs), _p(Hcs), _p(Wcs), pl.n_planes, pl.gi.shape[0],
+                                  _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
+                                  _p(bi) if bi is not None else None, n, float(T), S, pl.n_aspects,
+                                  _p(desc), _p(scale), _p(idx))
+    if rc:
+        raise ValueError("oracle_region_pool: bad arguments")
+    return desc, scale, idx

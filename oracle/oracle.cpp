@@ -563,4 +563,94 @@ int oracle_region_windows(const float* conv5, const int64_t* plane_off, const in
   return 0;
 }
 
+// ------------------------------------------------------------------------------------------------
+// Max-pooled region bins (descriptor post-processing after the region windows, the pool5-style
+// alternative to bilinear samples): the box is read at the same entry as above (same cost, same
+// ties), and its S x S bins take, per channel, the maximum over the conv5 cells whose receptive-field
+// centre (16 i + 17.5 in plane coordinates) lies inside the bin.
+//   Bin a spans plane rows [Y1 + a (Y2 - Y1) / S, Y1 + (a + 1)(Y2 - Y1) / S); its cells are
+//   i in [ceil((lo - 17.5) / 16), ceil((hi - 17.5) / 16) - 1], clipped to the entry's window [r0, r1];
+//   a bin left with no cell takes the one cell nearest its centre: clamp(floor(g + 0.5), r0, r1) with
+//   g = (centre - 17.5) / 16.  Columns likewise.  Everything is fp64 with + - * / only.
+// idx (nullable) [n][S][S][4] = (i_first, i_last, j_first, j_last) of each bin.  Same layouts as
+// oracle_region_windows otherwise.
+// ------------------------------------------------------------------------------------------------
+static void pool_bin_range(double lo, double hi, int cmin, int cmax, int& first, int& last) {
+  // cells with lo <= 16 i + 17.5 < hi
+  int f = (int)std::ceil((lo - 17.5) / 16.0);
+  int l = (int)std::ceil((hi - 17.5) / 16.0) - 1;
+  f = std::max(f, cmin);
+  l = std::min(l, cmax);
+  if (l < f) {
+    const double g = ((lo + hi) * 0.5 - 17.5) / 16.0;
+    int c = (int)std::floor(g + 0.5);
+    c = std::min(std::max(c, cmin), cmax);
+    f = l = c;
+  }
+  first = f;
+  last = l;
+}
+
+int oracle_region_pool(const float* conv5, const int64_t* plane_off, const int32_t* Hcs,
+                       const int32_t* Wcs, int planes_per_img, int K, const int32_t* gi,
+                       const double* gd, int pad, const float* boxes, const int32_t* box_img, int n,
+                       double T, int S, int n_aspects, float* desc, int32_t* scale, int32_t* idx) {
+  if (S <= 0 || !(T > 0)) return -1;
+  const int C = 256;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int r = 0; r < n; ++r) {
+    float* d = desc + (size_t)r * C * S * S;
+    std::fill(d, d + (size_t)C * S * S, 0.f);
+    scale[r] = -1;
+    if (idx) std::fill(idx + (size_t)r * S * S * 4, idx + (size_t)(r + 1) * S * S * 4, 0);
+    const double x1 = boxes[r * 4 + 0], y1 = boxes[r * 4 + 1], x2 = boxes[r * 4 + 2], y2 = boxes[r * 4 + 3];
+    const double bw = x2 - x1, bh = y2 - y1;
+    if (!std::isfinite(x1) || !std::isfinite(y1) || !std::isfinite(x2) || !std::isfinite(y2)) continue;
+    if (!(bw > 0) || !(bh > 0)) continue;
+    const double T2 = T * T;
+    int best = -1;
+    double best_cost = 0;
+    for (int k = 0; k < K; ++k) {
+      const int32_t* g = gi + k * 16;
+      if (g[9] < g[8] || g[11] < g[10]) continue;
+      const double a = (gd[k * 3 + 1] * bh) * (gd[k * 3 + 2] * bw);
+      double cost = std::max(a / T2, T2 / a);
+      if (n_aspects > 1) {
+        const double rho = (gd[k * 3 + 2] * bw) / (gd[k * 3 + 1] * bh);
+        cost = cost * std::max(rho, 1.0 / rho);
+      }
+      if (best < 0 || cost < best_cost) { best = k; best_cost = cost; }
+    }
+    if (best < 0) continue;
+    const int32_t* g = gi + best * 16;
+    const double sy = gd[best * 3 + 1], sx = gd[best * 3 + 2];
+    const int pl = (box_img ? box_img[r] : 0) * planes_per_img + g[3];
+    const int Hc = Hcs[pl], Wc = Wcs[pl];
+    const float* F = conv5 + plane_off[pl];
+    const double X1 = x1 * sx + g[5] + pad, X2 = x2 * sx + g[5] + pad;
+    const double Y1 = y1 * sy + g[4] + pad, Y2 = y2 * sy + g[4] + pad;
+    scale[r] = best;
+    for (int a = 0; a < S; ++a) {
+      int i0, i1;
+      pool_bin_range(Y1 + a * (Y2 - Y1) / S, Y1 + (a + 1) * (Y2 - Y1) / S, g[8], g[9], i0, i1);
+      for (int b = 0; b < S; ++b) {
+        int j0, j1;
+        pool_bin_range(X1 + b * (X2 - X1) / S, X1 + (b + 1) * (X2 - X1) / S, g[10], g[11], j0, j1);
+        if (idx) {
+          int32_t* q = idx + ((size_t)r * S * S + a * S + b) * 4;
+          q[0] = i0; q[1] = i1; q[2] = j0; q[3] = j1;
+        }
+        for (int c = 0; c < C; ++c) {
+          const float* Fc = F + (size_t)c * Hc * Wc;
+          float m = Fc[(size_t)i0 * Wc + j0];
+          for (int i = i0; i <= i1; ++i)
+            for (int j = j0; j <= j1; ++j) m = std::max(m, Fc[(size_t)i * Wc + j]);
+          d[(size_t)c * S * S + a * S + b] = m;
+        }
+      }
+    }
+  }
+  return 0;
+}
+
 }  // extern "C"
