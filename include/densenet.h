@@ -185,6 +185,20 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
                             const int32_t* d_box_img, int32_t n, float target, int32_t S,
                             float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream);
 
+/* Max-pooled region bins: descriptor post-processing after the region windows, the pool5-style
+ * read-out of a box.  Same arguments, entry choice (scale and aspect) and output layout as
+ * densenet_region_windows, but bin (a, b) of the box takes, per channel, the maximum over the conv5
+ * cells whose receptive-field centre (16 i + 17.5) lies inside the bin (rows [Y1 + a (Y2-Y1)/S,
+ * Y1 + (a+1)(Y2-Y1)/S) in plane coordinates, columns likewise), clipped to the entry's window; a bin
+ * holding no cell centre takes the cell nearest its centre.  d_idx: nullable [n][S][S][4] int32
+ * (first row, last row, first column, last column) of each bin's cells.  Values are exact maxima of
+ * the stored conv5 values; ranges are fp64 with + - * / only, reproducible bit for bit. */
+int densenet_region_pool(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                         dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,
+                         int32_t pad, int32_t planes_per_img, const float* d_boxes,
+                         const int32_t* d_box_img, int32_t n, float target, int32_t S, float* d_out,
+                         int32_t* d_scale, int32_t* d_idx, void* stream);
+
 /* Crop-before windows: the per-window baseline the paper measures the dense pyramid against
  * (Sec. 3.4: 2000 window proposals, each run through the network on its own) and the "crop before"
  * pipeline of Sec. 4.  Each box (x1, y1, x2, y2) of original-image pixel-edge coordinates (fp32) is
@@ -228,7 +242,7 @@ int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw);
  * launch's own stream.  densenet_profile_stop() waits for the recorded events, writes per-name
  * totals (launches, summed elapsed ms) to out[max_entries] (*n_entries = number of names) and turns
  * tracing off.  Kernel names: build_planes, conv1..conv5, lrn_pool1, lrn_pool2, pool5, warp_regions,
- * region_windows, pack_weights.  Events come from a pool owned by the library (no device memory). */
+ * region_windows, region_pool, pack_weights.  Events come from a pool owned by the library (no device memory). */
 typedef struct {
   char name[32];
   int32_t launches;

@@ -76,6 +76,74 @@ static std::vector<Run> make_runs(const dn_plane_desc* planes, int32_t n) {
 
 using namespace dn;
 
+static int region_call(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                       dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales, int32_t pad,
+                       int32_t planes_per_img, const float* d_boxes, const int32_t* d_box_img,
+                       int32_t n, float target, int32_t S, float* d_out, int32_t* d_scale,
+                       int32_t* d_idx, bool pool, void* stream) {
+  try {
+    if (!d_conv5 || !conv5_desc || !geom) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (n > 0 && (!d_boxes || !d_out || !d_scale))
+      return fail(DN_E_INVALID_ARG, "null box or output pointer");
+    if (!valid_dtype(conv5_dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_scales <= 0 || n_scales > DN_MAX_SCALES) return fail(DN_E_INVALID_ARG, "bad n_scales");
+    if (planes_per_img <= 0 || planes_per_img > DN_MAX_PLANES_PER_IMAGE || n_maps < planes_per_img ||
+        n_maps % planes_per_img)
+      return fail(DN_E_INVALID_ARG, "n_maps must be a positive multiple of planes_per_img");
+    if (S <= 0 || S > 8) return fail(DN_E_UNSUPPORTED, "S must be in 1..8");
+    if (!(target > 0)) return fail(DN_E_INVALID_ARG, "target must be positive");
+    if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
+    if (n == 0) return DN_OK;
+    RegArgs a{};
+    a.n_scales = n_scales;
+    a.n_aspects = 1;
+    for (int k = 0; k < n_scales; ++k) a.n_aspects = std::max(a.n_aspects, geom[k].aspect + 1);
+    a.pad = pad;
+    a.planes_per_img = planes_per_img;
+    a.S = S;
+    a.C = 256;
+    a.target = (double)target;
+    const int64_t vec = 16 / (int64_t)dtype_size(conv5_dtype);
+    for (int32_t i = 0; i < n_maps; ++i)
+      if (conv5_desc[i].offset < 0 || conv5_desc[i].offset % vec)
+        return fail(DN_E_INVALID_ARG, "conv5 map offsets must be multiples of 16 bytes");
+    for (int32_t j = 0; j < planes_per_img; ++j) {
+      a.map_off[j] = conv5_desc[j].offset - conv5_desc[0].offset;
+      a.map_w[j] = conv5_desc[j].w;
+    }
+    const int n_img = n_maps / planes_per_img;
+    a.n_img = n_img;
+    a.image_stride = 0;
+    if (n_img > 1) {
+      a.image_stride = conv5_desc[planes_per_img].offset - conv5_desc[0].offset;
+      for (int b = 1; b < n_img; ++b)
+        for (int j = 0; j < planes_per_img; ++j) {
+          const dn_plane_desc& d = conv5_desc[b * planes_per_img + j];
+          if (d.offset - conv5_desc[0].offset != b * a.image_stride + a.map_off[j] ||
+              d.w != conv5_desc[j].w || d.h != conv5_desc[j].h)
+            return fail(DN_E_INVALID_ARG, "images' conv5 maps must be laid out identically");
+        }
+    }
+    for (int k = 0; k < n_scales; ++k) {
+      const dn_scale_geom& g = geom[k];
+      if (g.plane < 0 || g.plane >= planes_per_img) return fail(DN_E_INVALID_ARG, "bad geom plane");
+      const dn_plane_desc& d = conv5_desc[g.plane];
+      const bool empty = g.r1 < g.r0 || g.c1 < g.c0;
+      if (!empty && (g.r0 < 0 || g.c0 < 0 || g.r1 >= d.h || g.c1 >= d.w))
+        return fail(DN_E_INVALID_ARG, "scale window outside its conv5 map");
+      a.s[k] = RegScale{g.plane, g.y, g.x, g.r0, g.r1, g.c0, g.c1, empty ? 1 : 0, g.sy, g.sx};
+    }
+    const char* base = (const char*)d_conv5 + conv5_desc[0].offset * dtype_size(conv5_dtype);
+    TraceScope trace(pool ? "region_pool" : "region_windows", stream);
+    return hip_status(launch_region_windows(base, conv5_dtype, a, d_boxes, d_box_img, n, d_out,
+                                            d_scale, d_idx, pool, stream),
+                      pool ? "region_pool launch" : "region_windows launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+
 extern "C" {
 
 const char* densenet_last_error(void) { return g_error.c_str(); }
@@ -416,66 +484,17 @@ int densenet_region_windows(const void* d_conv5, const dn_plane_desc* conv5_desc
                             int32_t pad, int32_t planes_per_img, const float* d_boxes,
                             const int32_t* d_box_img, int32_t n, float target, int32_t S,
                             float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream) {
-  try {
-    if (!d_conv5 || !conv5_desc || !geom) return fail(DN_E_INVALID_ARG, "null pointer argument");
-    if (n > 0 && (!d_boxes || !d_out || !d_scale))
-      return fail(DN_E_INVALID_ARG, "null box or output pointer");
-    if (!valid_dtype(conv5_dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
-    if (n_scales <= 0 || n_scales > DN_MAX_SCALES) return fail(DN_E_INVALID_ARG, "bad n_scales");
-    if (planes_per_img <= 0 || planes_per_img > DN_MAX_PLANES_PER_IMAGE || n_maps < planes_per_img ||
-        n_maps % planes_per_img)
-      return fail(DN_E_INVALID_ARG, "n_maps must be a positive multiple of planes_per_img");
-    if (S <= 0 || S > 8) return fail(DN_E_UNSUPPORTED, "S must be in 1..8");
-    if (!(target > 0)) return fail(DN_E_INVALID_ARG, "target must be positive");
-    if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
-    if (n == 0) return DN_OK;
-    RegArgs a{};
-    a.n_scales = n_scales;
-    a.n_aspects = 1;
-    for (int k = 0; k < n_scales; ++k) a.n_aspects = std::max(a.n_aspects, geom[k].aspect + 1);
-    a.pad = pad;
-    a.planes_per_img = planes_per_img;
-    a.S = S;
-    a.C = 256;
-    a.target = (double)target;
-    const int64_t vec = 16 / (int64_t)dtype_size(conv5_dtype);
-    for (int32_t i = 0; i < n_maps; ++i)
-      if (conv5_desc[i].offset < 0 || conv5_desc[i].offset % vec)
-        return fail(DN_E_INVALID_ARG, "conv5 map offsets must be multiples of 16 bytes");
-    for (int32_t j = 0; j < planes_per_img; ++j) {
-      a.map_off[j] = conv5_desc[j].offset - conv5_desc[0].offset;
-      a.map_w[j] = conv5_desc[j].w;
-    }
-    const int n_img = n_maps / planes_per_img;
-    a.n_img = n_img;
-    a.image_stride = 0;
-    if (n_img > 1) {
-      a.image_stride = conv5_desc[planes_per_img].offset - conv5_desc[0].offset;
-      for (int b = 1; b < n_img; ++b)
-        for (int j = 0; j < planes_per_img; ++j) {
-          const dn_plane_desc& d = conv5_desc[b * planes_per_img + j];
-          if (d.offset - conv5_desc[0].offset != b * a.image_stride + a.map_off[j] ||
-              d.w != conv5_desc[j].w || d.h != conv5_desc[j].h)
-            return fail(DN_E_INVALID_ARG, "images' conv5 maps must be laid out identically");
-        }
-    }
-    for (int k = 0; k < n_scales; ++k) {
-      const dn_scale_geom& g = geom[k];
-      if (g.plane < 0 || g.plane >= planes_per_img) return fail(DN_E_INVALID_ARG, "bad geom plane");
-      const dn_plane_desc& d = conv5_desc[g.plane];
-      const bool empty = g.r1 < g.r0 || g.c1 < g.c0;
-      if (!empty && (g.r0 < 0 || g.c0 < 0 || g.r1 >= d.h || g.c1 >= d.w))
-        return fail(DN_E_INVALID_ARG, "scale window outside its conv5 map");
-      a.s[k] = RegScale{g.plane, g.y, g.x, g.r0, g.r1, g.c0, g.c1, empty ? 1 : 0, g.sy, g.sx};
-    }
-    const char* base = (const char*)d_conv5 + conv5_desc[0].offset * dtype_size(conv5_dtype);
-    TraceScope trace("region_windows", stream);
-    return hip_status(launch_region_windows(base, conv5_dtype, a, d_boxes, d_box_img, n, d_out,
-                                            d_scale, d_idx, stream),
-                      "region_windows launch");
-  } catch (...) {
-    return fail(DN_E_INTERNAL, "unexpected exception");
-  }
+  return region_call(d_conv5, conv5_desc, n_maps, conv5_dtype, geom, n_scales, pad, planes_per_img,
+                     d_boxes, d_box_img, n, target, S, d_out, d_scale, d_idx, false, stream);
+}
+
+int densenet_region_pool(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                         dn_dtype conv5_dtype, const dn_scale_geom* geom, int32_t n_scales,
+                         int32_t pad, int32_t planes_per_img, const float* d_boxes,
+                         const int32_t* d_box_img, int32_t n, float target, int32_t S, float* d_out,
+                         int32_t* d_scale, int32_t* d_idx, void* stream) {
+  return region_call(d_conv5, conv5_desc, n_maps, conv5_dtype, geom, n_scales, pad, planes_per_img,
+                     d_boxes, d_box_img, n, target, S, d_out, d_scale, d_idx, true, stream);
 }
 
 }  // extern "C"

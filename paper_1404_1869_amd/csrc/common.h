@@ -107,9 +107,11 @@ struct RegArgs {
   int32_t map_w[DN_MAX_PLANES_PER_IMAGE];
   int64_t image_stride;                       // elements between images' maps
 };
+// pool = false: bilinear samples at bin centres (d_idx [n][S][S][2]); true: per-bin max over the cells
+// centred inside each bin (d_idx [n][S][S][4]).
 int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
                           const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
-                          int32_t* d_idx, void* stream);
+                          int32_t* d_idx, bool pool, void* stream);
 
 inline size_t dtype_size(dn_dtype dt) { return dt == DN_F32 ? 4 : 2; }
 

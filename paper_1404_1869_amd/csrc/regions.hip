@@ -17,7 +17,27 @@ namespace {
 
 constexpr int MAX_S = 8;
 
-template <typename T>
+// Max-pooled bins: the cells of a bin spanning [lo, hi) in plane coordinates are those whose
+// receptive-field centre 16 i + 17.5 lies inside it, clipped to [cmin, cmax]; a bin left with no cell
+// takes the cell nearest its centre.
+__device__ inline void pool_bin_range(double lo, double hi, int cmin, int cmax, int& first, int& last) {
+#pragma clang fp contract(off)
+  int f = (int)ceil((lo - 17.5) / 16.0);
+  int l = (int)ceil((hi - 17.5) / 16.0) - 1;
+  f = f < cmin ? cmin : f;
+  l = l > cmax ? cmax : l;
+  if (l < f) {
+    const double g = ((lo + hi) * 0.5 - 17.5) / 16.0;
+    int c = (int)floor(g + 0.5);
+    c = c < cmin ? cmin : (c > cmax ? cmax : c);
+    f = l = c;
+  }
+  first = f;
+  last = l;
+}
+
+// POOL = false: bilinear samples at the bin centres; POOL = true: per-channel max over each bin's cells.
+template <typename T, bool POOL>
 __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict__ maps, RegArgs a,
                                                              const float* __restrict__ boxes,
                                                              const int32_t* __restrict__ box_img,
@@ -69,15 +89,32 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   __syncthreads();
   const int best = s_best;
   float* dst = out + (int64_t)r * C * SS;
+  constexpr int IDXW = POOL ? 4 : 2;  // idx_out entries per bin
   if (best < 0) {
     for (int e = tid; e < C * SS; e += blockDim.x) dst[e] = 0.f;
     if (tid == 0) scale_out[r] = -1;
     if (idx_out)
-      for (int e = tid; e < 2 * SS; e += blockDim.x) idx_out[(int64_t)r * 2 * SS + e] = 0;
+      for (int e = tid; e < IDXW * SS; e += blockDim.x) idx_out[(int64_t)r * IDXW * SS + e] = 0;
     return;
   }
   const RegScale sc = a.s[best];
-  if (tid < 2 * S) {
+  if (POOL && tid < 2 * S) {
+    const bool row = tid < S;
+    const int t = row ? tid : tid - S;
+    const double lo = row ? y1 * sc.sy + (double)sc.y + (double)a.pad : x1 * sc.sx + (double)sc.x + (double)a.pad;
+    const double hi = row ? y2 * sc.sy + (double)sc.y + (double)a.pad : x2 * sc.sx + (double)sc.x + (double)a.pad;
+    int first, last;
+    pool_bin_range(lo + ((double)t * (hi - lo)) / (double)S, lo + ((double)(t + 1) * (hi - lo)) / (double)S,
+                   row ? sc.r0 : sc.c0, row ? sc.r1 : sc.c1, first, last);
+    if (row) {
+      s_i0[t] = first;
+      s_i1[t] = last;
+    } else {
+      s_j0[t] = first;
+      s_j1[t] = last;
+    }
+  }
+  if (!POOL && tid < 2 * S) {
     // tid < S: row sample a = tid; S <= tid < 2S: column sample b = tid - S
     const bool row = tid < S;
     const int t = row ? tid : tid - S;
@@ -129,6 +166,25 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
     for (int bin = grp; bin < SS; bin += groups) {
       const int u = bin / S, v = bin - u * S;
       const int i0 = s_i0[u], i1 = s_i1[u], j0 = s_j0[v], j1 = s_j1[v];
+      if constexpr (POOL) {
+        float m[VT];
+        const vec_t f = *(const vec_t*)(F + ((int64_t)i0 * Wc + j0) * C + c0);
+#pragma unroll
+        for (int q = 0; q < VT; ++q) m[q] = to_f32(f[q]);
+        for (int i = i0; i <= i1; ++i)
+          for (int j = j0; j <= j1; ++j) {
+            const vec_t x = *(const vec_t*)(F + ((int64_t)i * Wc + j) * C + c0);
+#pragma unroll
+            for (int q = 0; q < VT; ++q) m[q] = fmaxf(m[q], to_f32(x[q]));
+          }
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+          float* d = s_row + bin * RSTR + c0 + 4 * k;
+          *(float2*)d = make_float2(m[4 * k], m[4 * k + 1]);
+          *(float2*)(d + 2) = make_float2(m[4 * k + 2], m[4 * k + 3]);
+        }
+        continue;
+      }
       const float ly = s_ly[u], lx = s_lx[v];
       const vec_t a00 = *(const vec_t*)(F + ((int64_t)i0 * Wc + j0) * C + c0);
       const vec_t a01 = *(const vec_t*)(F + ((int64_t)i0 * Wc + j1) * C + c0);
@@ -170,34 +226,50 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   if (tid == 0) scale_out[r] = best;
   if (idx_out)
     for (int e = tid; e < SS; e += blockDim.x) {
-      idx_out[((int64_t)r * SS + e) * 2 + 0] = s_i0[e / S];
-      idx_out[((int64_t)r * SS + e) * 2 + 1] = s_j0[e % S];
+      int32_t* q = idx_out + ((int64_t)r * SS + e) * IDXW;
+      if constexpr (POOL) {
+        q[0] = s_i0[e / S];
+        q[1] = s_i1[e / S];
+        q[2] = s_j0[e % S];
+        q[3] = s_j1[e % S];
+      } else {
+        q[0] = s_i0[e / S];
+        q[1] = s_j0[e % S];
+      }
     }
+}
+
+template <bool POOL>
+int launch(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
+           const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale, int32_t* d_idx,
+           hipStream_t s) {
+  if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
+  const size_t lds = sizeof(float) * (size_t)(a.C + 2) * a.S * a.S;
+  switch (dt) {
+    case DN_F32:
+      region_windows_kernel<float, POOL><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes,
+                                                             d_box_img, d_out, d_scale, d_idx);
+      break;
+    case DN_F16:
+      region_windows_kernel<_Float16, POOL><<<n, 256, lds, s>>>((const _Float16*)d_conv5, a, d_boxes,
+                                                                d_box_img, d_out, d_scale, d_idx);
+      break;
+    case DN_BF16:
+      region_windows_kernel<__bf16, POOL><<<n, 256, lds, s>>>((const __bf16*)d_conv5, a, d_boxes,
+                                                              d_box_img, d_out, d_scale, d_idx);
+      break;
+  }
+  return (int)hipGetLastError();
 }
 
 }  // namespace
 
 int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
                           const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
-                          int32_t* d_idx, void* stream) {
-  if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
+                          int32_t* d_idx, bool pool, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  const size_t lds = sizeof(float) * (size_t)(a.C + 2) * a.S * a.S;
-  switch (dt) {
-    case DN_F32:
-      region_windows_kernel<float><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes, d_box_img,
-                                                       d_out, d_scale, d_idx);
-      break;
-    case DN_F16:
-      region_windows_kernel<_Float16><<<n, 256, lds, s>>>((const _Float16*)d_conv5, a, d_boxes,
-                                                          d_box_img, d_out, d_scale, d_idx);
-      break;
-    case DN_BF16:
-      region_windows_kernel<__bf16><<<n, 256, lds, s>>>((const __bf16*)d_conv5, a, d_boxes,
-                                                        d_box_img, d_out, d_scale, d_idx);
-      break;
-  }
-  return (int)hipGetLastError();
+  return pool ? launch<true>(d_conv5, dt, a, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s)
+              : launch<false>(d_conv5, dt, a, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s);
 }
 
 }  // namespace dn

@@ -27,6 +27,7 @@ DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
            "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
            "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_warp_regions",
+           "densenet_region_pool",
            "densenet_profile_start",
            "densenet_profile_stop", "densenet_last_error")
 
@@ -88,6 +89,8 @@ def lib():
                                        pd, P],
             "densenet_region_windows": [P, pd, i32, i32, pg, i32, i32, i32, P, P, i32, f32, i32, P, P,
                                         P, P],
+            "densenet_region_pool": [P, pd, i32, i32, pg, i32, i32, i32, P, P, i32, f32, i32, P, P, P,
+                                     P],
             "densenet_conv_layer": [i32, P, i32, i32, i32, i32, P, P, P],
             "densenet_lrn_pool": [P, i32, i32, i32, i32, i32, pn, P, P],
             "densenet_maxpool": [P, i32, i32, i32, i32, i32, P, P],
@@ -285,22 +288,36 @@ def densenet_conv_features(planes_tensor, planes_desc, dtype: int, packed, net: 
     return cf
 
 
-def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad: int, planes_per_img,
-                            boxes, box_img=None, target=227.0, S=6, want_idx=False, out=None,
-                            scale=None):
+def _regions(fn, conv5, conv5_desc, dtype, plan, pad, planes_per_img, boxes, box_img, target, S, want_idx,
+             out, scale, idx_width):
     torch = _torch()
     n = boxes.shape[0]
     if out is None:
         out = torch.empty((n, 256 * S * S), dtype=torch.float32, device=boxes.device)
     if scale is None:
         scale = torch.empty(n, dtype=torch.int32, device=boxes.device)
-    idx = torch.empty((n, S, S, 2), dtype=torch.int32, device=boxes.device) if want_idx else None
+    idx = torch.empty((n, S, S, idx_width), dtype=torch.int32, device=boxes.device) if want_idx else None
     geom = (dn_scale_geom * len(plan.geom))(*plan.geom)
     cd = (dn_plane_desc * len(conv5_desc))(*conv5_desc)
-    check(lib().densenet_region_windows(_ptr(conv5), cd, len(conv5_desc), dtype, geom, len(plan.geom),
-                                        pad, planes_per_img, _ptr(boxes), _ptr(box_img), n, target, S,
-                                        _ptr(out), _ptr(scale), _ptr(idx), _stream()))
+    check(fn(_ptr(conv5), cd, len(conv5_desc), dtype, geom, len(plan.geom), pad, planes_per_img,
+             _ptr(boxes), _ptr(box_img), n, target, S, _ptr(out), _ptr(scale), _ptr(idx), _stream()))
     return out, scale, idx
+
+
+def densenet_region_windows(conv5, conv5_desc, dtype: int, plan: PlanResult, pad: int, planes_per_img,
+                            boxes, box_img=None, target=227.0, S=6, want_idx=False, out=None,
+                            scale=None):
+    """Region windows (Sec. 4, crop after): bilinear samples at the S x S bin centres of each box."""
+    return _regions(lib().densenet_region_windows, conv5, conv5_desc, dtype, plan, pad, planes_per_img,
+                    boxes, box_img, target, S, want_idx, out, scale, 2)
+
+
+def densenet_region_pool(conv5, conv5_desc, dtype: int, plan: PlanResult, pad: int, planes_per_img,
+                         boxes, box_img=None, target=227.0, S=6, want_idx=False, out=None, scale=None):
+    """Max-pooled region bins: per-channel max over the conv5 cells centred inside each of the S x S
+    bins of each box (idx: first/last row, first/last column of each bin)."""
+    return _regions(lib().densenet_region_pool, conv5, conv5_desc, dtype, plan, pad, planes_per_img,
+                    boxes, box_img, target, S, want_idx, out, scale, 4)
 
 
 def densenet_warp_regions(images, boxes, dtype: int, S=227, mean=(0.0, 0.0, 0.0), box_img=None, out=None,

@@ -107,6 +107,15 @@ def test_layer_sizes_and_layer_validation():
     assert L.densenet_conv_layer(2, None, 1, 10, 50, D.DN_F16, fake, fake, None) == D.DN_E_INVALID_ARG
     assert L.densenet_region_windows(fake, None, 1, D.DN_F16, None, 1, 16, 1, fake, None, 1, 227.0,
                                      6, fake, fake, None, None) == D.DN_E_INVALID_ARG
+    assert L.densenet_region_pool(fake, None, 1, D.DN_F16, None, 1, 16, 1, fake, None, 1, 227.0,
+                                  6, fake, fake, None, None) == D.DN_E_INVALID_ARG
+    pd = (D.dn_plane_desc * 1)()
+    pd[0].h, pd[0].w = 13, 13
+    g = (D.dn_scale_geom * 1)()
+    assert L.densenet_region_pool(fake, pd, 1, D.DN_F16, g, 1, 16, 1, fake, None, 1, 227.0,
+                                  9, fake, fake, None, None) == D.DN_E_UNSUPPORTED   # S > 8
+    assert L.densenet_region_pool(fake, pd, 1, D.DN_F16, g, 1, 16, 1, None, None, 0, 227.0,
+                                  6, None, None, None, None) == D.DN_OK               # no boxes
 
 
 def test_warp_regions_size_query_and_validation():

@@ -251,3 +251,34 @@ def test_aspect_ratio_pyramids_end_to_end(D, dt):
     np.testing.assert_array_equal(op.field("aspect")[sc[-3:]], [0, 2, 1])
     assert len(set(op.field("aspect")[sc])) == 3
     assert_layer_close(desc.cpu().numpy(), rd, dt, "region windows")
+
+
+@pytest.mark.parametrize("dt,S", [("f32", 6), ("bf16", 6), ("f16", 1), ("bf16", 8)])
+def test_region_pool_bit_exact(D, dt, S):
+    """Max-pooled region bins on shared conv5 maps (two images, stored in the path's dtype): chosen
+    entries, bin cell ranges and every descriptor value bit for bit against the oracle, including
+    degenerate boxes and image indices out of range (scale -1, zero row)."""
+    H, W = 480, 640
+    p = oracle.plan(H, W, 8, 4, 1.0, 0, 16, 800, 800)
+    plan = D.densenet_plan_pyramid(H, W, D.pyramid_params(8, 4, pad=16, pad_mode=D.DN_PAD_RAMP,
+                                                          plane_h=800, plane_w=800))
+    maps = [round_to(m, dt) for m in _shared_maps(p, 9)]
+    flat = np.concatenate([np.moveaxis(m, 0, -1).ravel() for m in maps] * 2)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
+    c5 = torch.from_numpy(flat).to("cuda", tdt)
+    boxes = np.concatenate([synth.boxes(31, 400, H, W, smin=8, smax=480),
+                            np.array([[5, 5, 5, 40], [10, 10, 12.5, 11], [np.nan, 0, 4, 4]], np.float32)])
+    box_img = (np.arange(len(boxes)) % 2).astype(np.int32)
+    box_img[3] = 2
+    out, sc, ix = D.densenet_region_pool(c5, _descs(D, maps, 2), DTS[dt], plan, 16, p.n_planes,
+                                         torch.from_numpy(boxes).cuda(), torch.from_numpy(box_img).cuda(),
+                                         S=S, want_idx=True)
+    torch.cuda.synchronize()
+    desc, scale, idx = oracle.region_pool(maps, p, boxes, S=S)
+    sc, ix, out = sc.cpu().numpy(), ix.cpu().numpy(), out.cpu().numpy()
+    valid = box_img < 2
+    np.testing.assert_array_equal(sc[valid], scale[valid])
+    np.testing.assert_array_equal(ix[valid], idx[valid])
+    np.testing.assert_array_equal(out[valid], desc[valid])
+    assert (sc[~valid] == -1).all() and not out[~valid].any()
+    assert (sc[-3] == scale[-3]) and (sc[-1] == -1)
