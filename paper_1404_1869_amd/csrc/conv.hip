@@ -345,9 +345,13 @@ int device_cu_count() {
 // next chunk's halo) is already in flight into registers; it is written to the other buffers after
 // the stage's MFMAs, and one barrier per stage publishes it.
 // ------------------------------------------------------------------------------------------------
-template <typename T, int R, int BM, int TM, int PAD>
+template <typename T, int R, int BM, int TM, int TS>
 struct ConvCfg {
-  static constexpr int TH = 16, TW = 16, CC = 16;
+  // Tile of TH x TW output pixels, TS = 100 TH + TW (TW 16 or 32, TH TW a multiple of 256) for 16-bit
+  // storage; fp32 uses 16 x 16.
+  static constexpr bool F32_ = std::is_same<T, float>::value;
+  static constexpr int TH = F32_ ? 16 : TS / 100, TW = F32_ ? 16 : TS % 100, CC = 16;
+  static_assert((TW == 16 || TW == 32) && TH % 2 == 0 && (TH * TW) % 256 == 0, "tile shape");
   static constexpr int TN = 4;                     // 32-pixel MFMA tiles per wave (128 pixels)
   static constexpr int HH = TH + R - 1, HW = TW + R - 1;
   static constexpr bool F32 = std::is_same<T, float>::value;
@@ -369,19 +373,27 @@ struct ConvCfg {
   static constexpr int STAGE_E = F32 ? 0 : WM * WN * 32 * TN * 64;  // epilogue staging
   static constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > STAGE_E ? (2 * HALO_E + 2 * W_E) : STAGE_E;
   __device__ static inline int halo_off(int hy, int hx, int v) { return hy * RS + hx * PS + v * VEC; }
+  // Tile pixel of index idx: each 32-pixel MFMA tile is 2 rows x 16 columns (the two rows a half-wave
+  // reads then fall on LDS slots of opposite parity); with 32-column tiles, MFMA tiles 2 p and 2 p + 1
+  // are the left and right halves of row pair p.
+  __device__ static inline int pix_row(int idx) { return 2 * ((idx >> 5) / (TW / 16)) + ((idx >> 4) & 1); }
+  __device__ static inline int pix_col(int idx) { return 16 * ((idx >> 5) % (TW / 16)) + (idx & 15); }
   __device__ static inline int w_off(int kx, int m, int v) {
     return (kx * BM + m) * PS + (F32 ? v * VEC : ((v ^ ((m >> 4) & 1)) * VEC));
   }
 };
 
-constexpr int conv_threads(int BM, int TM) { return 64 * (BM / (32 * TM)) * 2; }
+template <typename T, int BM, int TM, int TS>
+constexpr int conv_threads() {
+  return 64 * (BM / (32 * TM)) * (std::is_same<T, float>::value ? 256 : (TS / 100) * (TS % 100)) / 128;
+}
 
-template <typename T, int R, int BM, int TM, int OCC, int PAD>
-__global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
+template <typename T, int R, int BM, int TM, int OCC, int TS>
+__global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
-  using Cf = ConvCfg<T, R, BM, TM, PAD>;
+  using Cf = ConvCfg<T, R, BM, TM, TS>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
   constexpr int VEC = Cf::VEC, VPP = Cf::VPP, NT = Cf::NT, TN = Cf::TN;
@@ -417,7 +429,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
 #pragma unroll
   for (int t = 0; t < TN; ++t) {
     const int idx = wn * 32 * TN + t * 32 + l32;
-    pix[t] = Cf::halo_off(idx / Cf::TW, idx % Cf::TW, 0);
+    pix[t] = Cf::halo_off(Cf::pix_row(idx), Cf::pix_col(idx), 0);
   }
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -565,7 +577,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
       const int key = (p & 7) ^ ((p >> 3) & 3);
       const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
       const int idx = wn * 32 * TN + p;
-      const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+      const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
       if (oy < H && ox < W)
         *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
     }
@@ -579,7 +591,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_kernel(
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
           const int idx = wn * 32 * TN + t * 32 + l32;
-          const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+          const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
           if (oy < H && ox < W) {
             out4_t r;
 #pragma unroll
@@ -613,12 +625,12 @@ __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece
                                            16, voff, 0, 0, 0);
 }
 
-template <typename T, int R, int BM, int TM, int OCC, int PAD>
-__global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_kernel(
+template <typename T, int R, int BM, int TM, int OCC, int TS>
+__global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_direct_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
-  using Cf = ConvCfg<T, R, BM, TM, PAD>;
+  using Cf = ConvCfg<T, R, BM, TM, TS>;
   using Op = Mfma<T>;
   static_assert(!Cf::F32 && (TM == 2 || TM == 3), "direct-load path is for 16-bit storage");
   constexpr int pad = (R - 1) / 2;
@@ -664,7 +676,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
 #pragma unroll
   for (int t = 0; t < TN; ++t) {
     const int idx = wn * 32 * TN + t * 32 + l32;
-    pix[t] = Cf::halo_off(idx / Cf::TW, idx % Cf::TW, 0);
+    pix[t] = Cf::halo_off(Cf::pix_row(idx), Cf::pix_col(idx), 0);
   }
   // Byte offsets (chunk 0, tap row 0) of this lane's slot in each of its wave's LDS pieces.
   uint32_t hoff[DH], woff[DW];
@@ -769,7 +781,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
           const int key = (p & 7) ^ ((p >> 3) & 3);
           const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
           const int idx = wn * 32 * TN + p;
-          const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+          const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
           if (oy < H && ox < W)
             *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
         }
@@ -802,7 +814,7 @@ __global__ __launch_bounds__((conv_threads(BM, TM)), OCC) void conv_s1_direct_ke
         const int u = it * 64 + lane, p = u / NCH, ch = u % NCH;
         const vec8_t v = *(const vec8_t*)(stg + p * SROW + 8 * ch);
         const int idx = wn * 32 * TN + t * 32 + p;
-        const int oy = oy0 + idx / Cf::TW, ox = ox0 + idx % Cf::TW;
+        const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
         if (oy < H && ox < W) *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch) = v;
       }
     }
@@ -1001,10 +1013,10 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   }
 }
 
-template <typename T, int R, int BM, int TM, int OCC, int PAD>
+template <typename T, int R, int BM, int TM, int OCC, int TS>
 int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int H, int W, int C,
                 int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
-  using Cf = ConvCfg<T, R, BM, TM, PAD>;
+  using Cf = ConvCfg<T, R, BM, TM, TS>;
   const int Cg = C / G, Mg = M / G;
   const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
   if (Mg % BM) return (int)hipErrorInvalidValue;  // whole channel blocks per group
@@ -1012,32 +1024,35 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
   const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
   if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
   if constexpr (Cf::F32 || (TM != 2 && TM != 3)) {
-    conv_s1_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+    conv_s1_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(
         in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   } else {
     // buffer descriptors address one plane with 32-bit byte offsets
     if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
-    conv_s1_direct_kernel<T, R, BM, TM, OCC, PAD><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(
         in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   }
   return (int)hipGetLastError();
 }
 
 // Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, and
-// a spare layout parameter.  Chosen by timing each layer at the 96-plane batch shapes: two waves per
+// the tile shape (100 rows + columns).  Chosen by timing each layer at the 96-plane batch shapes: two waves per
 // SIMD matter most; conv3/conv5 run best at three waves per SIMD; conv4's 192 channels per group run
-// best as one block of 3 x 32 channels per wave (7 LDS fragment reads per 12 MFMAs instead of 6 per 8).
+// best as one block of 3 x 32 channels per wave (7 LDS fragment reads per 12 MFMAs instead of 6 per 8);
+// 16 x 32 and 8 x 32 tiles (eight waves sharing each stage's weight row; less edge waste on 149-wide
+// maps) were 2-3 % slower for conv2 on pipeline activations, and waste 20 % more MFMA work on the
+// 74-wide maps of conv3..conv5.
 #ifndef DN_CONV2_CFG
-#define DN_CONV2_CFG 128, 2, 2, 0
+#define DN_CONV2_CFG 128, 2, 2, 1616
 #endif
 #ifndef DN_CONV3_CFG
-#define DN_CONV3_CFG 128, 2, 3, 8
+#define DN_CONV3_CFG 128, 2, 3, 1616
 #endif
 #ifndef DN_CONV5_CFG
-#define DN_CONV5_CFG 128, 2, 3, 8
+#define DN_CONV5_CFG 128, 2, 3, 1616
 #endif
 #ifndef DN_CONV4_CFG
-#define DN_CONV4_CFG 192, 3, 2, 0
+#define DN_CONV4_CFG 192, 3, 2, 1616
 #endif
 
 template <typename T>
