@@ -134,9 +134,15 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
 // element), and stores the LRN result to LDS.  Pixels of the tile outside the map are stored as
 // -inf, so every pooled output then takes the max over its full 3 x 3 window from LDS, unrolled, with
 // no clipping tests.  Channel count and tile shape are compile-time constants, so no index
-// arithmetic needs a division.
-template <typename T, int C, int CPT, int TPH, int TPW>
-__global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict__ in,
+// arithmetic needs a division.  With 16-bit storage, a tile whose LRN values are all >= +0 (the usual
+// case after ReLU) takes its maxima on the raw 16-bit patterns, two per instruction (for such values,
+// and the -inf fill, signed-integer order is the float order); any other tile takes them in fp32.
+// The tile's sign is read from the inputs' sign bits (LRN keeps the sign; -0 counts as negative) or,
+// with OUT_SIGN, from the LRN values themselves (-0 is stored as +0): the same decision up to -0, and
+// the faster schedule of the two as measured for each channel count.
+template <typename T, int C, int CPT, int TPH, int TPW, int WPE, bool OUT_SIGN>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void lrn_pool_pixel_kernel(
+                                                             const T* __restrict__ in,
                                                              T* __restrict__ out, int H, int W,
                                                              int Ho, int Wo, int tiles_x,
                                                              int tiles_y, int64_t in_stride,
@@ -159,6 +165,7 @@ __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict
   const int iy0 = 2 * oy0, ix0 = 2 * ox0;
 
   const int p = threadIdx.x / TPP, part = threadIdx.x % TPP;
+  bool neg = false;
   if (p < NP) {
     const int y = iy0 + p / IW, x = ix0 + p % IW;
     T* d = s + p * CS + part * CPT;
@@ -169,6 +176,17 @@ __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict
       for (int i = 0; i < NV; ++i) v[i] = *(const vec_t*)(px + i * N);
       if (TPP > 1 && part > 0) lv = *(const vec_t*)(px - N);
       if (TPP > 1 && part + 1 < TPP) rv = *(const vec_t*)(px + CPT);
+      if constexpr (sizeof(T) == 2 && !OUT_SIGN) {
+        typedef uint32_t uvec_t __attribute__((ext_vector_type(N / 2)));
+        uint32_t bits = 0;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+          const uvec_t u = __builtin_bit_cast(uvec_t, v[i]);
+#pragma unroll
+          for (int j = 0; j < N / 2; ++j) bits |= u[j];
+        }
+        neg = (bits & 0x80008000u) != 0;
+      }
       // sq[2 + i] = a_i^2 for this thread's channels, two neighbours (or zeros) on each side
       float sq[CPT + 4], pr[CPT + 3];
 #pragma unroll
@@ -190,8 +208,12 @@ __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict
 #pragma unroll
         for (int e = 0; e < N; ++e) {
           const int c = i * N + e;  // window sq[c .. c + 4]
-          const float sum = pr[c] + pr[c + 2] + sq[c + 4];
-          r[e] = from_f32<T>(to_f32(v[i][e]) * lrn_scale(sum, alpha_n, beta, k));
+          float o = to_f32(v[i][e]) * lrn_scale(pr[c] + pr[c + 2] + sq[c + 4], alpha_n, beta, k);
+          if constexpr (OUT_SIGN && sizeof(T) == 2) {
+            o = o + 0.0f;  // -0 -> +0
+            neg |= o < 0.f;
+          }
+          r[e] = from_f32<T>(o);
         }
         *(vec_t*)(d + i * N) = r;
       }
@@ -203,8 +225,28 @@ __global__ __launch_bounds__(256) void lrn_pool_pixel_kernel(const T* __restrict
       for (int i = 0; i < NV; ++i) *(vec_t*)(d + i * N) = f;
     }
   }
-  __syncthreads();
+  const bool any_neg = __syncthreads_or(neg);
 
+  if constexpr (sizeof(T) == 2) {
+    if (!any_neg) {
+      typedef short svec_t __attribute__((ext_vector_type(N)));
+      for (int e = threadIdx.x; e < TPH * TPW * G; e += 256) {
+        const int g = e % G, q = e / G;
+        const int qy = q / TPW, qx = q % TPW;
+        const int oy = oy0 + qy, ox = ox0 + qx;
+        if (oy >= Ho || ox >= Wo) continue;
+        const T* b = s + ((2 * qy) * IW + 2 * qx) * CS + g * N;
+        svec_t m = *(const svec_t*)b;
+#pragma unroll
+        for (int wy = 0; wy < 3; ++wy)
+#pragma unroll
+          for (int wx = 0; wx < 3; ++wx)
+            if (wy || wx) m = __builtin_elementwise_max(m, *(const svec_t*)(b + (wy * IW + wx) * CS));
+        *(svec_t*)(out + plane * out_stride + ((int64_t)oy * Wo + ox) * C + g * N) = m;
+      }
+      return;
+    }
+  }
   for (int e = threadIdx.x; e < TPH * TPW * G; e += 256) {
     const int g = e % G, q = e / G;
     const int qy = q / TPW, qx = q % TPW;
@@ -305,11 +347,13 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
     const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
     if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    // Waves per SIMD the LDS tile allows (3 and 2 workgroups of 4 waves per CU): the compiler may use
+    // the registers that occupancy leaves free for more independent work in flight.
     if (C == 96)
-      lrn_pool_pixel_kernel<T, 96, 96, TH96, TW96><<<(unsigned)blocks, 256, 0, s>>>(
+      lrn_pool_pixel_kernel<T, 96, 96, TH96, TW96, 3, false><<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     else
-      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256><<<(unsigned)blocks, 256, 0, s>>>(
+      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256, 2, true><<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     return (int)hipGetLastError();
   }

@@ -97,6 +97,25 @@ def test_lrn_pool(D, dt, C, shape, lrn_first):
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("C", [96, 256])
+def test_lrn_pool_signed_and_zero_inputs(D, dt, C):
+    """Inputs of both signs (tiles holding negative LRN values pool in fp32), all-zero and negative-zero
+    regions (tiles of values >= +0 pool on the raw 16-bit patterns)."""
+    n, H, W = 1, 41, 38
+    rng = np.random.default_rng(C + 3)
+    x = rng.normal(0, 30, (n, H, W, C))
+    x[:, :20] = np.abs(x[:, :20])      # upper rows non-negative
+    x[:, :6, :9] = 0.0                 # zeros
+    x[:, 6:10, :9] = -0.0              # negative zeros
+    x = round_to(x, dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_lrn_pool(xg, DTS[dt], D.net_params()).float().cpu().numpy()
+    ref = oracle.maxpool(oracle.lrn(chw(x[0])))
+    assert_layer_close(chw(out[0]), ref, dt, f"signed lrn_pool {C}")
+    assert np.array_equal(chw(out[0])[:, :2, :4], ref[:, :2, :4])   # pooled zeros are exact
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_maxpool_exact(D, dt):
     rng = np.random.default_rng(5)
     x = round_to(rng.normal(0, 1, (3, 13, 14, 256)), dt)
