@@ -161,7 +161,48 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   const int lt = tid % per_bin, grp = tid / per_bin;
   const int RSTR = C + 2;
   constexpr int NQ = VT / 4;  // 16-byte float chunks per thread and bin
-  if (grp < groups) {
+  constexpr int MAXIT = 5;  // bins per thread whose loads are all issued before any blend
+  if (!POOL && grp < groups && SS <= MAXIT * groups) {
+    // Bilinear bins, up to MAXIT per thread (S <= 6 with 16-bit maps): all 4 MAXIT cell vectors are
+    // in flight at once, then blended.
+    const int c0 = lt * VT;
+    vec_t a[MAXIT][4];
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it) {
+      const int bin = grp + it * groups;
+      if (bin < SS) {
+        const int u = bin / S, v = bin - u * S;
+        const int i0 = s_i0[u], i1 = s_i1[u], j0 = s_j0[v], j1 = s_j1[v];
+        a[it][0] = *(const vec_t*)(F + ((int64_t)i0 * Wc + j0) * C + c0);
+        a[it][1] = *(const vec_t*)(F + ((int64_t)i0 * Wc + j1) * C + c0);
+        a[it][2] = *(const vec_t*)(F + ((int64_t)i1 * Wc + j0) * C + c0);
+        a[it][3] = *(const vec_t*)(F + ((int64_t)i1 * Wc + j1) * C + c0);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it) {
+      const int bin = grp + it * groups;
+      if (bin < SS) {
+        const int u = bin / S, v = bin - u * S;
+        const float ly = s_ly[u], lx = s_lx[v];
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+          f32x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int q = 4 * k + e;
+            const float v00 = to_f32(a[it][0][q]), v01 = to_f32(a[it][1][q]);
+            const float v10 = to_f32(a[it][2][q]), v11 = to_f32(a[it][3][q]);
+            const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
+            o[e] = top + ly * (bot - top);
+          }
+          float* d = s_row + bin * RSTR + c0 + 4 * k;
+          *(float2*)d = make_float2(o[0], o[1]);
+          *(float2*)(d + 2) = make_float2(o[2], o[3]);
+        }
+      }
+    }
+  } else if (grp < groups) {
     const int c0 = lt * VT;
     for (int bin = grp; bin < SS; bin += groups) {
       const int u = bin / S, v = bin - u * S;
