@@ -154,7 +154,12 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   const int64_t plane = (int64_t)PH * PW;
   const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
 
-  for (int r = wave; r < TROWS; r += 4) {
+  // Rows wave, wave + 4, ... of the tile, unrolled so that the taps of several rows are in flight.
+  // Every lane reads its four taps per pixel (a pixel outside the scale's border reads valid pixels
+  // and gets weight 0), so the loads carry no per-pixel branch.
+#pragma unroll
+  for (int rr = 0; rr < TROWS / 4; ++rr) {
+    const int r = wave + 4 * rr;
     const int y = ty0 + r;
     if (y >= PH) break;  // uniform per wave
     const RowEntry re = s_row[cell * TROWS + r];
@@ -165,7 +170,6 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
 #pragma unroll
       for (int i = 0; i < PX; ++i) {
         const float wgt = re.wy * wx[i];
-        if (wgt == 0.f) continue;
         const uint32_t q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
         const uint32_t q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
 #pragma unroll
