@@ -44,6 +44,8 @@ def lib():
         i32, f64 = ctypes.c_int, ctypes.c_double
         L.oracle_plan.argtypes = [i32, i32, i32, i32, f64, i32, i32, i32, i32, i32, P, P, P]
         L.oracle_plan.restype = i32
+        L.oracle_plan_batch.argtypes = [i32] + L.oracle_plan.argtypes
+        L.oracle_plan_batch.restype = i32
         L.oracle_resize_center.argtypes = [P, i32, i32, i32, i32, P, P]
         L.oracle_resize_center.restype = None
         L.oracle_build_planes.argtypes = [P, i32, i32, i32, P, P, i32, i32, P, i32, i32, i32, P]
@@ -84,7 +86,7 @@ def _p(a: np.ndarray):
 # Geometry
 # ----------------------------------------------------------------------------------------------
 GI_FIELDS = ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0", "r1", "c0", "c1", "plane_h",
-             "plane_w", "aspect")
+             "plane_w", "aspect", "image")
 
 
 @dataclass
@@ -95,6 +97,13 @@ class Plan:
     pad: int
     plane_sizes: list       # [(PH, PW)] per plane
     n_aspects: int = 0
+    n_img: int = 1          # images whose entries the rows hold (cross-image packing: n_img > 1)
+    packed: bool = False    # rows are n_img blocks of entries stitched over the batch
+
+    @property
+    def entries(self) -> int:
+        """Pyramid entries per image."""
+        return self.gi.shape[0] // self.n_img
 
     def field(self, name):
         return self.gi[:, GI_FIELDS.index(name)]
@@ -116,6 +125,22 @@ def plan(H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, pl
     for k in range(E):
         sizes[gi[k, 3]] = (int(gi[k, 12]), int(gi[k, 13]))
     return Plan(gi, gd, n, pad, sizes, len(asp))
+
+
+def plan_batch(n_img, H, W, K, spo, base_scale=1.0, base_longest_side=0, pad=0, plane_h=0, plane_w=0,
+               aspects=None) -> Plan:
+    """Cross-image packing: the rectangles of all n_img images (each H x W) stitched as one set of items
+    (Sec. 3.1 stitching over a batch).  Row b * E + e is entry e of image b; plane indices count over the
+    batch."""
+    asp = np.ascontiguousarray(aspects if aspects is not None else [], np.float64)
+    E = K * max(1, len(asp))
+    gi = np.zeros((n_img * E, 16), np.int32)
+    gd = np.zeros((n_img * E, 3), np.float64)
+    n = lib().oracle_plan_batch(n_img, H, W, K, spo, float(base_scale), base_longest_side, pad, plane_h,
+                                plane_w, len(asp), _p(asp) if len(asp) else None, _p(gi), _p(gd))
+    if n < 0:
+        raise ValueError(f"oracle_plan_batch failed with {n}")
+    return Plan(gi, gd, n, pad, [(plane_h, plane_w)] * n, len(asp), n_img, True)
 
 
 def threads() -> int:
@@ -149,9 +174,14 @@ def resize_center(img: np.ndarray, h: int, w: int, mean) -> np.ndarray:
 
 
 def build_planes(img: np.ndarray, pl: Plan, pad_mode: int, mean) -> list:
-    """Stitched, centred, padded planes of one image, as a list of fp64 [3][PH][PW] arrays."""
+    """Stitched, centred, padded planes of one image ([3][H][W]), or of a cross-image packed batch
+    ([n_img][3][H][W] with a plan_batch plan), as a list of fp64 [3][PH][PW] arrays."""
     img = np.ascontiguousarray(img, np.uint8)
-    _, H, W = img.shape
+    if img.ndim == 3:
+        img = img[None]
+    if img.shape[0] < pl.n_img:
+        raise ValueError("fewer images than the plan holds")
+    _, _, H, W = img.shape
     PHm = max(s[0] for s in pl.plane_sizes)
     PWm = max(s[1] for s in pl.plane_sizes)
     m = np.ascontiguousarray(mean, np.float64)
@@ -244,7 +274,8 @@ def net(plane: np.ndarray, weights, lrn_params=(1e-4, 0.75, 1.0, 5), lrn_before_
 # Region windows
 # ----------------------------------------------------------------------------------------------
 def region_windows(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None, T=227.0, S=6):
-    """conv5_planes: list over (image, plane) of fp32 [256][Hc][Wc]; returns desc, scale, idx, lam."""
+    """conv5_planes: list over (image, plane) of fp32 [256][Hc][Wc] (over the batch's planes for a
+    plan_batch plan); returns desc, scale, idx, lam."""
     flat = np.concatenate([np.ascontiguousarray(c, np.float32).ravel() for c in conv5_planes])
     offs = np.cumsum([0] + [c.size for c in conv5_planes[:-1]]).astype(np.int64)
     Hcs = np.array([c.shape[1] for c in conv5_planes], np.int32)
@@ -256,8 +287,8 @@ def region_windows(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None
     scale = np.zeros(n, np.int32)
     idx = np.zeros((n, S, S, 2), np.int32)
     lam = np.zeros((n, S, S, 2), np.float64)
-    rc = lib().oracle_region_windows(_p(flat), _p(offs), _p(Hcs), _p(Wcs), pl.n_planes,
-                                     pl.gi.shape[0], _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
+    rc = lib().oracle_region_windows(_p(flat), _p(offs), _p(Hcs), _p(Wcs), 0 if pl.packed else pl.n_planes,
+                                     pl.entries, _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
                                      _p(bi) if bi is not None else None, n, float(T), S,
                                      pl.n_aspects, _p(desc), _p(scale), _p(idx), _p(lam))
     if rc:
@@ -279,7 +310,8 @@ def region_pool(conv5_planes: list, pl: Plan, boxes: np.ndarray, box_img=None, T
     desc = np.zeros((n, 256 * S * S), np.float32)
     scale = np.zeros(n, np.int32)
     idx = np.zeros((n, S, S, 4), np.int32)
-    rc = lib().oracle_region_pool(_p(flat), _p(offs), _p(Hcs), _p(Wcs), pl.n_planes, pl.gi.shape[0],
+    rc = lib().oracle_region_pool(_p(flat), _p(offs), _p(Hcs), _p(Wcs), 0 if pl.packed else pl.n_planes,
+                                  pl.entries,
                                   _p(pl.gi), _p(pl.gd), pl.pad, _p(boxes),
                                   _p(bi) if bi is not None else None, n, float(T), S, pl.n_aspects,
                                   _p(desc), _p(scale), _p(idx))

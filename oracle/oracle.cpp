@@ -53,6 +53,14 @@ int oracle_threads(void) {
 // scale (empty when r1 < r0 or c1 < c0).  Returns the number of planes, or a negative error:
 // -1 bad argument, -2 a rectangle larger than the stitching plane.
 //
+// Cross-image packing (oracle_plan_batch): the rectangles of all n_img images of a batch (same size
+// H x W, so the same entries) are stitched as one set of items, so that small scales of several images
+// share planes instead of leaving each image a half-empty last plane.  Item (b, e) is row b E + e of
+// gi/gd (E entries per image), with gi[.. + 0] = e and gi[.. + 15] = b; its plane index counts over the
+// whole batch.  The order is the one above with ties going to the smaller item index b E + e; a plane
+// whose free area is smaller than the item's rectangle is skipped (it could not hold it anyway).
+// oracle_plan is the case n_img = 1.
+//
 // Readings: s_k = base * 2^(-k/spo) for k = 0..K-1 (Sec. 3.1 scales per octave), base = base_scale or
 // longest_side / max(H, W); sizes round half up, minimum 1.
 // Aspect-ratio pyramids (Sec. 3.3): with n_aspects > 0 ratios r_a, the image warped to each ratio gets
@@ -101,10 +109,11 @@ static int64_t conv5_side(int64_t n) {
 
 int oracle_conv5_side(int n) { return (int)conv5_side(n); }
 
-int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longest_side, int pad,
-                int plane_h, int plane_w, int n_aspects, const double* aspects, int32_t* gi,
-                double* gd) {
-  if (H <= 0 || W <= 0 || K <= 0 || spo <= 0 || pad < 0 || n_aspects < 0) return -1;
+int oracle_plan_batch(int n_img, int H, int W, int K, int spo, double base_scale,
+                      int base_longest_side, int pad, int plane_h, int plane_w, int n_aspects,
+                      const double* aspects, int32_t* gi, double* gd) {
+  if (n_img <= 0 || H <= 0 || W <= 0 || K <= 0 || spo <= 0 || pad < 0 || n_aspects < 0) return -1;
+  if (n_img > 1 && plane_h == 0) return -1;  // cross-image packing needs stitching planes
   for (int a = 0; a < n_aspects; ++a)
     if (!(aspects[a] > 0.0) || !std::isfinite(aspects[a])) return -1;
   const int A = n_aspects > 0 ? n_aspects : 1, NS = K;
@@ -115,9 +124,11 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
   if (!(base > 0.0)) return -1;
 
   struct Item { int k, h, w, rh, rw, plane, y, x; };
+  const int E = K;    // entries per image
+  K = n_img * E;      // items of the whole batch: item b E + e is entry e of image b
   std::vector<Item> it(K);
   for (int k = 0; k < K; ++k) {
-    const int a = k / NS;
+    const int a = (k % E) / NS;
     double s = base * std::pow(2.0, -(double)(k % NS) / (double)spo);
     gd[k * 3 + 0] = s;
     const double q = n_aspects > 0 ? std::sqrt(aspects[a]) : 1.0;
@@ -127,7 +138,7 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
     if (w < 1) w = 1;
     gd[k * 3 + 1] = (double)h / (double)H;
     gd[k * 3 + 2] = (double)w / (double)W;
-    it[k].k = k; it[k].h = h; it[k].w = w;
+    it[k].k = k % E; it[k].h = h; it[k].w = w;
     if (plane_h == 0) {
       it[k].rh = h + 2 * pad;
       it[k].rw = w + 2 * pad;
@@ -156,10 +167,12 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
       return a < b;
     });
     std::vector<std::vector<int>> on_plane;  // item indices placed on each plane
+    std::vector<int64_t> free_area;          // plane area not covered by rectangles
     for (int idx : order) {
       Item& r = it[idx];
       bool placed = false;
       for (int p = 0; p < n_planes && !placed; ++p) {
+        if (free_area[p] < (int64_t)r.rh * r.rw) continue;
         std::vector<int> ys{0}, xs{0};
         for (int j : on_plane[p]) { ys.push_back(it[j].y + it[j].rh); xs.push_back(it[j].x + it[j].rw); }
         std::sort(ys.begin(), ys.end());
@@ -173,12 +186,19 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
               const Item& q = it[j];
               if (y < q.y + q.rh && q.y < y + r.rh && x < q.x + q.rw && q.x < x + r.rw) { overlap = true; break; }
             }
-            if (!overlap) { r.plane = p; r.y = y; r.x = x; on_plane[p].push_back(idx); placed = true; break; }
+            if (!overlap) {
+              r.plane = p; r.y = y; r.x = x;
+              on_plane[p].push_back(idx);
+              free_area[p] -= (int64_t)r.rh * r.rw;
+              placed = true;
+              break;
+            }
           }
         }
       }
       if (!placed) {
         on_plane.push_back({idx});
+        free_area.push_back((int64_t)plane_h * plane_w - (int64_t)r.rh * r.rw);
         r.plane = n_planes; r.y = 0; r.x = 0;
         ph.push_back(plane_h); pw.push_back(plane_w);
         ++n_planes;
@@ -199,11 +219,18 @@ int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longes
     r0 = std::max<int64_t>(r0, 0); c0 = std::max<int64_t>(c0, 0);
     r1 = std::min<int64_t>(r1, Hc - 1); c1 = std::min<int64_t>(c1, Wc - 1);
     int32_t* o = gi + k * 16;
-    o[0] = k; o[1] = r.h; o[2] = r.w; o[3] = r.plane; o[4] = r.y; o[5] = r.x; o[6] = r.rh; o[7] = r.rw;
+    o[0] = r.k; o[1] = r.h; o[2] = r.w; o[3] = r.plane; o[4] = r.y; o[5] = r.x; o[6] = r.rh; o[7] = r.rw;
     o[8] = (int32_t)r0; o[9] = (int32_t)r1; o[10] = (int32_t)c0; o[11] = (int32_t)c1;
-    o[12] = PH; o[13] = PW; o[14] = k / NS; o[15] = 0;
+    o[12] = PH; o[13] = PW; o[14] = r.k / NS; o[15] = k / E;
   }
   return n_planes;
+}
+
+int oracle_plan(int H, int W, int K, int spo, double base_scale, int base_longest_side, int pad,
+                int plane_h, int plane_w, int n_aspects, const double* aspects, int32_t* gi,
+                double* gd) {
+  return oracle_plan_batch(1, H, W, K, spo, base_scale, base_longest_side, pad, plane_h, plane_w,
+                           n_aspects, aspects, gi, gd);
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -299,7 +326,8 @@ void oracle_warp_regions(const uint8_t* img, int n_img, int H, int W, const floa
 //   ZERO (pad_mode 0): w(d) = [d == 0].
 // Pixels covered by no rectangle are 0.  planes: [n_planes][3][PH][PW] fp64, every plane of size
 // (PH_max, PW_max) with the plane's own (plane_h, plane_w) region used; the caller passes the sizes.
-// gi/gd as produced by oracle_plan.
+// gi/gd as produced by oracle_plan or oracle_plan_batch (K rows); row k samples image gi[k*16 + 15]
+// of img ([n_img][3][H][W] uint8).
 // ------------------------------------------------------------------------------------------------
 void oracle_build_planes(const uint8_t* img, int H, int W, int K, const int32_t* gi, const double* gd,
                          int pad, int pad_mode, const double* mean, int n_planes, int PHmax, int PWmax,
@@ -310,7 +338,7 @@ void oracle_build_planes(const uint8_t* img, int H, int W, int K, const int32_t*
     const int32_t* g = gi + k * 16;
     int h = g[1], w = g[2], pl = g[3], y0 = g[4], x0 = g[5], rh = g[6], rw = g[7];
     std::vector<double> C((size_t)3 * h * w);
-    oracle_resize_center(img, H, W, h, w, mean, C.data());
+    oracle_resize_center(img + (size_t)g[15] * 3 * H * W, H, W, h, w, mean, C.data());
     auto weight = [&](int d) -> double {
       if (d == 0) return 1.0;
       if (pad_mode == 0) return 0.0;
@@ -489,7 +517,10 @@ int oracle_net(const float* plane, int PH, int PW, const float* const* w, const 
 //   centred at 16 i + 17.5), clamped to [c0, c1]; j0 = floor(g), j1 = min(j0 + 1, c1), lambda = g - j0.
 //   Rows likewise.  The value is the bilinear blend of the four cells, fp64.
 // conv5 planes: [n_img * planes_per_img][256][Hc][Wc] fp32, each plane (Hc, Wc) = (Hcs[p], Wcs[p])
-// stored at plane_off[p] (elements).  desc [n][256 * S * S] flattened (channel, row, col);
+// stored at plane_off[p] (elements); the box's image b reads plane b * planes_per_img + plane_k.
+// planes_per_img = 0 is a cross-image packed batch (oracle_plan_batch): gi/gd hold K rows per image,
+// image b's entries are rows b K .. b K + K - 1, and their plane indices count over the batch.
+// desc [n][256 * S * S] flattened (channel, row, col);
 // scale [n]; idx (nullable) [n][S][S][2] = (i0, j0) plane cell of the top-left sample;
 // lam (nullable) [n][S][S][2] = (lambda_y, lambda_x).
 // ------------------------------------------------------------------------------------------------
@@ -511,24 +542,27 @@ int oracle_region_windows(const float* conv5, const int64_t* plane_off, const in
     const double bw = x2 - x1, bh = y2 - y1;
     if (!std::isfinite(x1) || !std::isfinite(y1) || !std::isfinite(x2) || !std::isfinite(y2)) continue;
     if (!(bw > 0) || !(bh > 0)) continue;
+    const int img = box_img ? box_img[r] : 0;
+    const int32_t* gi_b = planes_per_img ? gi : gi + (size_t)img * K * 16;
+    const double* gd_b = planes_per_img ? gd : gd + (size_t)img * K * 3;
     const double T2 = T * T;
     int best = -1;
     double best_cost = 0;
     for (int k = 0; k < K; ++k) {
-      const int32_t* g = gi + k * 16;
+      const int32_t* g = gi_b + k * 16;
       if (g[9] < g[8] || g[11] < g[10]) continue;
-      const double a = (gd[k * 3 + 1] * bh) * (gd[k * 3 + 2] * bw);
+      const double a = (gd_b[k * 3 + 1] * bh) * (gd_b[k * 3 + 2] * bw);
       double cost = std::max(a / T2, T2 / a);
       if (n_aspects > 1) {
-        const double rho = (gd[k * 3 + 2] * bw) / (gd[k * 3 + 1] * bh);
+        const double rho = (gd_b[k * 3 + 2] * bw) / (gd_b[k * 3 + 1] * bh);
         cost = cost * std::max(rho, 1.0 / rho);
       }
       if (best < 0 || cost < best_cost) { best = k; best_cost = cost; }
     }
     if (best < 0) continue;
-    const int32_t* g = gi + best * 16;
-    const double sy = gd[best * 3 + 1], sx = gd[best * 3 + 2];
-    const int pl = (box_img ? box_img[r] : 0) * planes_per_img + g[3];
+    const int32_t* g = gi_b + best * 16;
+    const double sy = gd_b[best * 3 + 1], sx = gd_b[best * 3 + 2];
+    const int pl = img * planes_per_img + g[3];
     const int Hc = Hcs[pl], Wc = Wcs[pl];
     (void)Hc;
     const float* F = conv5 + plane_off[pl];
@@ -572,8 +606,8 @@ int oracle_region_windows(const float* conv5, const int64_t* plane_off, const in
 //   i in [ceil((lo - 17.5) / 16), ceil((hi - 17.5) / 16) - 1], clipped to the entry's window [r0, r1];
 //   a bin left with no cell takes the one cell nearest its centre: clamp(floor(g + 0.5), r0, r1) with
 //   g = (centre - 17.5) / 16.  Columns likewise.  Everything is fp64 with + - * / only.
-// idx (nullable) [n][S][S][4] = (i_first, i_last, j_first, j_last) of each bin.  Same layouts as
-// oracle_region_windows otherwise.
+// idx (nullable) [n][S][S][4] = (i_first, i_last, j_first, j_last) of each bin.  Same layouts (and the
+// same cross-image packed mode, planes_per_img = 0) as oracle_region_windows otherwise.
 // ------------------------------------------------------------------------------------------------
 static void pool_bin_range(double lo, double hi, int cmin, int cmax, int& first, int& last) {
   // cells with lo <= 16 i + 17.5 < hi
@@ -607,24 +641,27 @@ int oracle_region_pool(const float* conv5, const int64_t* plane_off, const int32
     const double bw = x2 - x1, bh = y2 - y1;
     if (!std::isfinite(x1) || !std::isfinite(y1) || !std::isfinite(x2) || !std::isfinite(y2)) continue;
     if (!(bw > 0) || !(bh > 0)) continue;
+    const int img = box_img ? box_img[r] : 0;
+    const int32_t* gi_b = planes_per_img ? gi : gi + (size_t)img * K * 16;
+    const double* gd_b = planes_per_img ? gd : gd + (size_t)img * K * 3;
     const double T2 = T * T;
     int best = -1;
     double best_cost = 0;
     for (int k = 0; k < K; ++k) {
-      const int32_t* g = gi + k * 16;
+      const int32_t* g = gi_b + k * 16;
       if (g[9] < g[8] || g[11] < g[10]) continue;
-      const double a = (gd[k * 3 + 1] * bh) * (gd[k * 3 + 2] * bw);
+      const double a = (gd_b[k * 3 + 1] * bh) * (gd_b[k * 3 + 2] * bw);
       double cost = std::max(a / T2, T2 / a);
       if (n_aspects > 1) {
-        const double rho = (gd[k * 3 + 2] * bw) / (gd[k * 3 + 1] * bh);
+        const double rho = (gd_b[k * 3 + 2] * bw) / (gd_b[k * 3 + 1] * bh);
         cost = cost * std::max(rho, 1.0 / rho);
       }
       if (best < 0 || cost < best_cost) { best = k; best_cost = cost; }
     }
     if (best < 0) continue;
-    const int32_t* g = gi + best * 16;
-    const double sy = gd[best * 3 + 1], sx = gd[best * 3 + 2];
-    const int pl = (box_img ? box_img[r] : 0) * planes_per_img + g[3];
+    const int32_t* g = gi_b + best * 16;
+    const double sy = gd_b[best * 3 + 1], sx = gd_b[best * 3 + 2];
+    const int pl = img * planes_per_img + g[3];
     const int Hc = Hcs[pl], Wc = Wcs[pl];
     const float* F = conv5 + plane_off[pl];
     const double X1 = x1 * sx + g[5] + pad, X2 = x2 * sx + g[5] + pad;
