@@ -85,9 +85,11 @@ typedef struct {
 
 /* Geometry of pyramid entry k (a scale of one aspect ratio), identical for every image of a batch
  * (Sec. 3.1 unpacking).  k: entry index (aspect * n_scales + scale); aspect: index into aspects (0
- * for a single pyramid); s: the scale factor s_k of the entry's scale.
+ * for a single pyramid); s: the scale factor s_k of the entry's scale.  image: the image the entry
+ * belongs to in a cross-image packed batch (densenet_plan_batch), else 0.
  *  (h, w): scaled image size; sy = h/H, sx = w/W are the effective factors.
- *  plane:  index of the scale's plane within one image's planes.
+ *  plane:  index of the scale's plane within one image's planes (within the whole batch's planes for
+ *          a cross-image packed batch).
  *  (y, x, rh, rw): padded rectangle on that plane; the real pixels start at (y+pad, x+pad).
  *  [r0, r1] x [c0, c1]: conv5 cells of that plane whose receptive-field centre (16 i + 17.5 in
  *          continuous plane coordinates) lies on a real pixel of the scale; the scale's feature map
@@ -96,7 +98,7 @@ typedef struct {
   int32_t k, h, w, plane;
   int32_t y, x, rh, rw;
   int32_t r0, r1, c0, c1;
-  int32_t aspect, reserved;
+  int32_t aspect, image;
   double s, sy, sx;
 } dn_scale_geom;
 
@@ -144,6 +146,36 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
                            size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
                            dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
                            int64_t* image_elems, void* stream);
+
+/* Cross-image packing: Bottom-Left Fill stitching (Sec. 3.1) applied to a whole batch, so that the
+ * small scales of several images share planes instead of each image leaving a half-empty last plane
+ * (16 images of 768 x 1024, 25 scales at 2^-0.1 on 1200 x 1200 planes: 88 planes instead of 96).
+ * Geometry only (host, no device work).  The E = n_scales * max(1, n_aspects) entries of each of the
+ * n_img images (all H x W) are n_img * E items, stitched as densenet_plan_pyramid stitches one
+ * image's entries, ties going to the smaller item index b * E + e.  p->plane_h and plane_w must be
+ * positive.  geom: [n_img * E] out, entry e of image b at b * E + e, with .image = b, .k = e and .plane
+ * counting over the batch.  planes: [max_planes] out, plane j of plane_h x plane_w at offset
+ * j * 3 * plane_h * plane_w elements; *total_elems = elements of all planes.  Returns DN_E_TOO_LARGE
+ * when more than max_planes planes are needed (*n_planes still receives the count) or n_img * E
+ * exceeds DN_MAX_BATCH_ITEMS. */
+#define DN_MAX_BATCH_ITEMS 65536
+int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_params* p,
+                        dn_scale_geom* geom, dn_plane_desc* planes, int32_t max_planes,
+                        int32_t* n_planes, int64_t* total_elems);
+
+/* Planes of a cross-image packed batch: the fused resize + centre + pad + stitch of
+ * densenet_build_pyramid, with every rectangle sampled from its own image.
+ * geom: the host array of n_img * E entries that densenet_plan_batch wrote for (n_img, H, W, *p), and
+ * d_geom: a device copy of it (the kernel reads the placements there; upload it once per plan).
+ * The host array is validated; an entry of d_geom that is not a placement inside a plane of this
+ * batch is ignored by the kernel (its pixels stay background), so a stale copy gives wrong planes but
+ * no out-of-bounds access.  d_planes: [n_planes][3][plane_h][plane_w] in `dtype`, followed by the
+ * builder's scratch (4 * H * W * n_img bytes, 256-byte aligned; contents afterwards unspecified), or
+ * NULL for a size query into *bytes_needed. */
+int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                         const dn_pyramid_params* p, dn_dtype dtype, const dn_scale_geom* geom,
+                         const dn_scale_geom* d_geom, int32_t n_planes, void* d_planes,
+                         size_t planes_bytes, size_t* bytes_needed, void* stream);
 
 /* Repack conv1..conv5 weights for the kernels.  d_w[l]: device fp32 OIHW weights of layer l
  * (96x3x11x11, 256x48x5x5, 384x256x3x3, 384x192x3x3, 256x192x3x3); d_b[l]: device fp32 biases.
@@ -199,6 +231,21 @@ int densenet_region_pool(const void* d_conv5, const dn_plane_desc* conv5_desc, i
                          const int32_t* d_box_img, int32_t n, float target, int32_t S, float* d_out,
                          int32_t* d_scale, int32_t* d_idx, void* stream);
 
+/* Region windows (pooled = 0, as densenet_region_windows) or max-pooled bins (pooled = 1, as
+ * densenet_region_pool) over the conv5 maps of a cross-image packed batch: a box of image b chooses
+ * among entries b * n_entries .. b * n_entries + n_entries - 1 of geom and is read from the map of
+ * that entry's (batch-wide) plane.  geom: the host array densenet_plan_batch wrote (n_img * n_entries
+ * entries, validated here); d_geom: its device copy (read by the kernel; entries that fall outside
+ * the maps are skipped as empty).  conv5_desc: [n_maps] maps of one size, evenly spaced, as
+ * densenet_conv_features writes them for the batch's planes.  Outputs and d_idx as the per-image
+ * calls. */
+int densenet_region_windows_batch(const void* d_conv5, const dn_plane_desc* conv5_desc,
+                                  int32_t n_maps, dn_dtype conv5_dtype, const dn_scale_geom* geom,
+                                  const dn_scale_geom* d_geom, int32_t n_img, int32_t n_entries,
+                                  int32_t pad, int32_t pooled, const float* d_boxes,
+                                  const int32_t* d_box_img, int32_t n, float target, int32_t S,
+                                  float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream);
+
 /* Crop-before windows: the per-window baseline the paper measures the dense pyramid against
  * (Sec. 3.4: 2000 window proposals, each run through the network on its own) and the "crop before"
  * pipeline of Sec. 4.  Each box (x1, y1, x2, y2) of original-image pixel-edge coordinates (fp32) is
@@ -242,7 +289,8 @@ int densenet_layer_sizes(int32_t H, int32_t W, int32_t* hw);
  * launch's own stream.  densenet_profile_stop() waits for the recorded events, writes per-name
  * totals (launches, summed elapsed ms) to out[max_entries] (*n_entries = number of names) and turns
  * tracing off.  Kernel names: build_planes, conv1..conv5, lrn_pool1, lrn_pool2, pool5, warp_regions,
- * region_windows, region_pool, pack_weights.  Events come from a pool owned by the library (no device memory). */
+ * region_windows, region_pool, pack_weights (a cross-image packed batch traces as build_planes,
+ * region_windows, region_pool).  Events come from a pool owned by the library (no device memory). */
 typedef struct {
   char name[32];
   int32_t launches;

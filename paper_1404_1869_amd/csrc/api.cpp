@@ -135,7 +135,7 @@ static int region_call(const void* d_conv5, const dn_plane_desc* conv5_desc, int
     }
     const char* base = (const char*)d_conv5 + conv5_desc[0].offset * dtype_size(conv5_dtype);
     TraceScope trace(pool ? "region_pool" : "region_windows", stream);
-    return hip_status(launch_region_windows(base, conv5_dtype, a, d_boxes, d_box_img, n, d_out,
+    return hip_status(launch_region_windows(base, conv5_dtype, a, nullptr, d_boxes, d_box_img, n, d_out,
                                             d_scale, d_idx, pool, stream),
                       pool ? "region_pool launch" : "region_windows launch");
   } catch (...) {
@@ -143,6 +143,79 @@ static int region_call(const void* d_conv5, const dn_plane_desc* conv5_desc, int
   }
 }
 
+
+// Validates a cross-image packed plan's host geometry against the batch and the stitching planes.
+static int check_batch_geom(const dn_scale_geom* geom, int32_t n_img, int32_t E, int32_t n_planes,
+                            int32_t PH, int32_t PW) {
+  for (int32_t b = 0; b < n_img; ++b)
+    for (int32_t e = 0; e < E; ++e) {
+      const dn_scale_geom& g = geom[(int64_t)b * E + e];
+      if (g.image != b || g.k != e) return fail(DN_E_INVALID_ARG, "geom is not a batch plan's entry array");
+      if (g.plane < 0 || g.plane >= n_planes) return fail(DN_E_INVALID_ARG, "geom plane out of range");
+      if (g.h < 1 || g.w < 1 || g.h > 65535 || g.w > 65535 || g.rh < 16 || g.rw < 16 ||
+          ((g.y | g.x | g.rh | g.rw) & 15) || g.y < 0 || g.x < 0 || g.y > PH - g.rh || g.x > PW - g.rw)
+        return fail(DN_E_INVALID_ARG, "geom rectangle is not a placement on the batch's planes");
+    }
+  return DN_OK;
+}
+
+static int region_batch_call(const void* d_conv5, const dn_plane_desc* conv5_desc, int32_t n_maps,
+                             dn_dtype conv5_dtype, const dn_scale_geom* geom, const dn_scale_geom* d_geom,
+                             int32_t n_img, int32_t E, int32_t pad, bool pool, const float* d_boxes,
+                             const int32_t* d_box_img, int32_t n, float target, int32_t S, float* d_out,
+                             int32_t* d_scale, int32_t* d_idx, void* stream) {
+  try {
+    if (!d_conv5 || !conv5_desc || !geom || !d_geom) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (n > 0 && (!d_boxes || !d_out || !d_scale))
+      return fail(DN_E_INVALID_ARG, "null box or output pointer");
+    if (!valid_dtype(conv5_dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_img <= 0 || E <= 0 || E > DN_MAX_SCALES || (int64_t)n_img * E > DN_MAX_BATCH_ITEMS)
+      return fail(DN_E_INVALID_ARG, "bad n_img or n_entries");
+    if (n_maps <= 0) return fail(DN_E_INVALID_ARG, "n_maps must be positive");
+    if (S <= 0 || S > 8) return fail(DN_E_UNSUPPORTED, "S must be in 1..8");
+    if (!(target > 0)) return fail(DN_E_INVALID_ARG, "target must be positive");
+    if (n < 0) return fail(DN_E_INVALID_ARG, "n must be >= 0");
+    const dn_plane_desc& d0 = conv5_desc[0];
+    const int64_t vec = 16 / (int64_t)dtype_size(conv5_dtype);
+    const int64_t stride = n_maps > 1 ? conv5_desc[1].offset - d0.offset : 0;
+    if (d0.h <= 0 || d0.w <= 0 || (n_maps > 1 && stride < (int64_t)d0.h * d0.w * 256))
+      return fail(DN_E_INVALID_ARG, "conv5 maps must be non-empty and not overlap");
+    for (int32_t j = 0; j < n_maps; ++j) {
+      const dn_plane_desc& d = conv5_desc[j];
+      if (d.h != d0.h || d.w != d0.w || d.offset != d0.offset + j * stride || d.offset < 0 || d.offset % vec)
+        return fail(DN_E_INVALID_ARG,
+                    "conv5 maps of a packed batch must be of one size, evenly spaced, 16-byte aligned");
+    }
+    RegArgs a{};
+    a.n_scales = E;
+    a.n_aspects = 1;
+    a.pad = pad;
+    a.planes_per_img = 0;
+    a.S = S;
+    a.C = 256;
+    a.n_img = n_img;
+    a.target = (double)target;
+    for (int32_t b = 0; b < n_img; ++b)
+      for (int32_t e = 0; e < E; ++e) {
+        const dn_scale_geom& g = geom[(int64_t)b * E + e];
+        if (g.image != b || g.k != e) return fail(DN_E_INVALID_ARG, "geom is not a batch plan's entry array");
+        if (g.plane < 0 || g.plane >= n_maps) return fail(DN_E_INVALID_ARG, "bad geom plane");
+        const bool empty = g.r1 < g.r0 || g.c1 < g.c0;
+        if (!empty && (g.r0 < 0 || g.c0 < 0 || g.r1 >= d0.h || g.c1 >= d0.w))
+          return fail(DN_E_INVALID_ARG, "scale window outside its conv5 map");
+        a.n_aspects = std::max(a.n_aspects, g.aspect + 1);
+      }
+    if (n == 0) return DN_OK;
+    RegBatch bt{d_geom, stride, n_maps, d0.h, d0.w};
+    const char* base = (const char*)d_conv5 + d0.offset * dtype_size(conv5_dtype);
+    TraceScope trace(pool ? "region_pool" : "region_windows", stream);
+    return hip_status(launch_region_windows(base, conv5_dtype, a, &bt, d_boxes, d_box_img, n, d_out,
+                                            d_scale, d_idx, pool, stream),
+                      pool ? "region_pool launch" : "region_windows launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
 
 extern "C" {
 
@@ -234,8 +307,79 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
       mw = std::max(mw, planes[j].w);
     }
     TraceScope trace("build_planes", stream);
-    return hip_status(launch_build_planes(d_images, n_img, a, pl, mh, mw, dtype, d_planes,
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, nullptr, mh, mw, dtype, d_planes,
                                           (uint8_t*)d_planes + planes_end, stream),
+                      "build_planes launch");
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_params* p,
+                        dn_scale_geom* geom, dn_plane_desc* planes, int32_t max_planes,
+                        int32_t* n_planes, int64_t* total_elems) {
+  try {
+    if (!p || !geom || !planes || !n_planes || !total_elems)
+      return fail(DN_E_INVALID_ARG, "null pointer argument");
+    std::vector<dn_scale_geom> items;
+    int np = 0;
+    const int st = make_plan_batch(n_img, H, W, *p, items, np);
+    if (st != DN_OK) return st;
+    *n_planes = np;
+    if (np > max_planes) return fail(DN_E_TOO_LARGE, "more planes than max_planes");
+    std::copy(items.begin(), items.end(), geom);
+    const int64_t pe = 3LL * p->plane_h * p->plane_w;
+    for (int32_t j = 0; j < np; ++j) {
+      planes[j] = dn_plane_desc{};
+      planes[j].h = p->plane_h;
+      planes[j].w = p->plane_w;
+      planes[j].offset = j * pe;
+    }
+    *total_elems = np * pe;
+    return DN_OK;
+  } catch (...) {
+    return fail(DN_E_INTERNAL, "unexpected exception");
+  }
+}
+
+int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                         const dn_pyramid_params* p, dn_dtype dtype, const dn_scale_geom* geom,
+                         const dn_scale_geom* d_geom, int32_t n_planes, void* d_planes,
+                         size_t planes_bytes, size_t* bytes_needed, void* stream) {
+  try {
+    if (!bytes_needed || !p) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
+    if (n_img <= 0 || H <= 0 || W <= 0 || H > 32768 || W > 32768)
+      return fail(DN_E_INVALID_ARG, "bad batch or image size");
+    if (p->plane_h <= 0 || p->plane_w <= 0)
+      return fail(DN_E_INVALID_ARG, "cross-image packing needs stitching planes (plane_h, plane_w > 0)");
+    if (p->pad < 0 || p->pad > 1024 || (p->pad_mode != DN_PAD_ZERO && p->pad_mode != DN_PAD_RAMP))
+      return fail(DN_E_INVALID_ARG, "bad pad or pad_mode");
+    const int64_t E = (int64_t)p->n_scales * std::max(1, p->n_aspects);
+    if (p->n_scales <= 0 || E > DN_MAX_SCALES || n_img * E > DN_MAX_BATCH_ITEMS)
+      return fail(DN_E_INVALID_ARG, "bad n_scales, n_aspects or batch size");
+    if (n_planes <= 0) return fail(DN_E_INVALID_ARG, "n_planes must be positive");
+    const int64_t pe = 3LL * p->plane_h * p->plane_w;
+    const size_t planes_end = ((size_t)n_planes * (size_t)pe * dtype_size(dtype) + 255) & ~(size_t)255;
+    const size_t need = planes_end + (size_t)n_img * 4 * (size_t)H * (size_t)W;
+    *bytes_needed = need;
+    if (!d_planes) return DN_OK;
+    if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
+    if (!d_images || !geom || !d_geom) return fail(DN_E_INVALID_ARG, "null pointer argument");
+    const int st = check_batch_geom(geom, n_img, (int32_t)E, n_planes, p->plane_h, p->plane_w);
+    if (st != DN_OK) return st;
+    PyrArgs a{};
+    a.n_scales = 0;
+    a.H = H;
+    a.W = W;
+    a.pad = p->pad;
+    a.ramp = p->pad_mode == DN_PAD_RAMP;
+    for (int c = 0; c < 3; ++c) a.mean[c] = p->mean[c];
+    PyrPlanes pl{};
+    BatchGeom bg{d_geom, (int32_t)(n_img * E), n_img, n_planes, p->plane_h, p->plane_w};
+    TraceScope trace("build_planes", stream);
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, &bg, p->plane_h, p->plane_w, dtype,
+                                          d_planes, (uint8_t*)d_planes + planes_end, stream),
                       "build_planes launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
@@ -495,6 +639,17 @@ int densenet_region_pool(const void* d_conv5, const dn_plane_desc* conv5_desc, i
                          int32_t* d_scale, int32_t* d_idx, void* stream) {
   return region_call(d_conv5, conv5_desc, n_maps, conv5_dtype, geom, n_scales, pad, planes_per_img,
                      d_boxes, d_box_img, n, target, S, d_out, d_scale, d_idx, true, stream);
+}
+
+int densenet_region_windows_batch(const void* d_conv5, const dn_plane_desc* conv5_desc,
+                                  int32_t n_maps, dn_dtype conv5_dtype, const dn_scale_geom* geom,
+                                  const dn_scale_geom* d_geom, int32_t n_img, int32_t n_entries,
+                                  int32_t pad, int32_t pooled, const float* d_boxes,
+                                  const int32_t* d_box_img, int32_t n, float target, int32_t S,
+                                  float* d_out, int32_t* d_scale, int32_t* d_idx, void* stream) {
+  if (pooled != 0 && pooled != 1) return fail(DN_E_INVALID_ARG, "pooled must be 0 or 1");
+  return region_batch_call(d_conv5, conv5_desc, n_maps, conv5_dtype, geom, d_geom, n_img, n_entries, pad,
+                           pooled == 1, d_boxes, d_box_img, n, target, S, d_out, d_scale, d_idx, stream);
 }
 
 }  // extern "C"

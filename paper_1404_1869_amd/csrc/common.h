@@ -39,6 +39,11 @@ void stack_sides(int64_t n, int64_t out[8]);
 // set).
 int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan);
 
+// Cross-image packing: the entries of n_img images stitched as one set of items (item b * E + e is
+// entry e of image b, .image = b, batch-wide plane indices).  Returns DN_OK or an error status.
+int make_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_params& p,
+                    std::vector<dn_scale_geom>& items, int& n_planes);
+
 // ---------------------------------------------------------------------------------------------
 // Launchers (device code in the .hip files).  Every launcher enqueues on `stream` and returns
 // hipGetLastError() as an int (0 = success).
@@ -64,10 +69,19 @@ struct PyrPlanes {
   PyrPlane p[DN_MAX_PLANES_PER_IMAGE];
 };
 
-// d_scratch: 4 * H * W * n_img bytes (4-byte aligned) for the pixel-interleaved image.
+// A cross-image packed batch: placements read from a device copy of the plan (n_items entries),
+// planes all PH x PW, plane j at j * 3 * PH * PW elements.
+struct BatchGeom {
+  const dn_scale_geom* geom;
+  int32_t n_items, n_img, n_planes, PH, PW;
+};
+
+// d_scratch: 4 * H * W * n_img bytes (4-byte aligned) for the pixel-interleaved image.  batch: NULL for
+// per-image planes (a.s / pl), else the packed batch's placements (a.s and pl unused but H, W, pad,
+// ramp, mean).
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_scratch,
-                        void* stream);
+                        const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
+                        uint8_t* d_scratch, void* stream);
 
 // Crop-before windows: n boxes warped to S x S channel-major planes (windows.hip).
 int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t W, const float* d_boxes,
@@ -107,11 +121,18 @@ struct RegArgs {
   int32_t map_w[DN_MAX_PLANES_PER_IMAGE];
   int64_t image_stride;                       // elements between images' maps
 };
+// Conv5 maps of a cross-image packed batch: entry e of image b at geom[b * a.n_scales + e] (device),
+// map j at j * map_stride elements, every map map_h x map_w.
+struct RegBatch {
+  const dn_scale_geom* geom;
+  int64_t map_stride;
+  int32_t n_maps, map_h, map_w;
+};
 // pool = false: bilinear samples at bin centres (d_idx [n][S][S][2]); true: per-bin max over the cells
-// centred inside each bin (d_idx [n][S][S][4]).
-int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
-                          const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
-                          int32_t* d_idx, bool pool, void* stream);
+// centred inside each bin (d_idx [n][S][S][4]).  batch: NULL for per-image maps (a.s, a.map_*).
+int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const RegBatch* batch,
+                          const float* d_boxes, const int32_t* d_box_img, int32_t n, float* d_out,
+                          int32_t* d_scale, int32_t* d_idx, bool pool, void* stream);
 
 inline size_t dtype_size(dn_dtype dt) { return dt == DN_F32 ? 4 : 2; }
 

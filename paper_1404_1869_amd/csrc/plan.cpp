@@ -39,9 +39,10 @@ namespace {
 
 struct Grid {  // occupancy of one plane in 16 x 16 px cells
   int gh, gw;
+  int64_t free_cells;
   std::vector<uint8_t> used;
   std::vector<int> tops, lefts;  // candidate corner coordinates in cells
-  Grid(int h, int w) : gh(h), gw(w), used((size_t)h * w, 0), tops{0}, lefts{0} {}
+  Grid(int h, int w) : gh(h), gw(w), free_cells((int64_t)h * w), used((size_t)h * w, 0), tops{0}, lefts{0} {}
   bool free_at(int cy, int cx, int nh, int nw) const {
     if (cy + nh > gh || cx + nw > gw) return false;
     for (int r = cy; r < cy + nh; ++r) {
@@ -53,11 +54,13 @@ struct Grid {  // occupancy of one plane in 16 x 16 px cells
   }
   void occupy(int cy, int cx, int nh, int nw) {
     for (int r = cy; r < cy + nh; ++r) std::memset(used.data() + (size_t)r * gw + cx, 1, nw);
+    free_cells -= (int64_t)nh * nw;
     tops.insert(std::upper_bound(tops.begin(), tops.end(), cy + nh), cy + nh);
     lefts.insert(std::upper_bound(lefts.begin(), lefts.end(), cx + nw), cx + nw);
   }
   // First corner in (top, left) order where an nh x nw block fits, or false.
   bool place(int nh, int nw, int& cy, int& cx) const {
+    if (free_cells < (int64_t)nh * nw) return false;
     for (size_t i = 0; i < tops.size(); ++i) {
       if (i && tops[i] == tops[i - 1]) continue;
       for (size_t j = 0; j < lefts.size(); ++j) {
@@ -72,6 +75,59 @@ struct Grid {  // occupancy of one plane in 16 x 16 px cells
     return false;
   }
 };
+
+// Bottom-Left Fill of rectangles (sides multiples of 16 px) onto planes of PH x PW: items largest
+// first (height, then width, then index), each on the first plane, in creation order, with a fitting
+// candidate corner, topmost then leftmost; else on a new plane.  Writes plane, y, x of every item.
+int stitch(std::vector<dn_scale_geom>& items, int32_t PH, int32_t PW, int max_planes, int& n_planes) {
+  const int N = (int)items.size();
+  std::vector<int> order(N);
+  for (int i = 0; i < N; ++i) order[i] = i;
+  std::sort(order.begin(), order.end(), [&](int a, int b) {
+    const dn_scale_geom &A = items[a], &B = items[b];
+    if (A.rh != B.rh) return A.rh > B.rh;
+    if (A.rw != B.rw) return A.rw > B.rw;
+    return a < b;
+  });
+  std::vector<Grid> grids;
+  for (int i : order) {
+    dn_scale_geom& g = items[i];
+    const int nh = g.rh / 16, nw = g.rw / 16;
+    int cy = 0, cx = 0;
+    size_t pi = 0;
+    for (; pi < grids.size(); ++pi)
+      if (grids[pi].place(nh, nw, cy, cx)) break;
+    if (pi == grids.size()) {
+      if ((int)grids.size() >= max_planes) {
+        std::ostringstream os;
+        os << "more than " << max_planes << " planes";
+        return fail(DN_E_TOO_LARGE, os.str());
+      }
+      grids.emplace_back(PH / 16, PW / 16);
+      cy = cx = 0;
+    }
+    grids[pi].occupy(cy, cx, nh, nw);
+    g.plane = (int32_t)pi;
+    g.y = cy * 16;
+    g.x = cx * 16;
+  }
+  n_planes = (int)grids.size();
+  return DN_OK;
+}
+
+// conv5 window of an entry on a PH x PW plane: cell i is centred at 16 i + 17.5; keep the cells
+// centred on rows [y+p, y+p+h) (columns likewise), clipped to the plane's conv5 map.
+void set_window(dn_scale_geom& g, int32_t PH, int32_t PW, int32_t pad) {
+  int64_t sh[8], sw[8];
+  stack_sides(PH, sh);
+  stack_sides(PW, sw);
+  const int64_t top = g.y + pad, left = g.x + pad;
+  // first i with 32 i + 35 >= 2 top; last i with 32 i + 35 <= 2 (top + h) - 1
+  g.r0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * top - 35, 32));
+  g.r1 = (int32_t)std::min<int64_t>(sh[6] - 1, div_floor(2 * (top + g.h) - 36, 32));
+  g.c0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * left - 35, 32));
+  g.c1 = (int32_t)std::min<int64_t>(sw[6] - 1, div_floor(2 * (left + g.w) - 36, 32));
+}
 
 }  // namespace
 
@@ -145,53 +201,44 @@ int make_plan(int32_t H, int32_t W, const dn_pyramid_params& p, Plan& plan) {
       plan.planes.push_back({g.rh, g.rw});
     }
   } else {
-    // Largest rectangles first: by height, then width, then scale index.
-    std::vector<int> order(K);
-    for (int k = 0; k < K; ++k) order[k] = k;
-    std::sort(order.begin(), order.end(), [&](int a, int b) {
-      const dn_scale_geom &A = plan.scales[a], &B = plan.scales[b];
-      if (A.rh != B.rh) return A.rh > B.rh;
-      if (A.rw != B.rw) return A.rw > B.rw;
-      return a < b;
-    });
-    std::vector<Grid> grids;
-    for (int k : order) {
-      dn_scale_geom& g = plan.scales[k];
-      const int nh = g.rh / 16, nw = g.rw / 16;
-      int cy = 0, cx = 0;
-      size_t pi = 0;
-      for (; pi < grids.size(); ++pi)
-        if (grids[pi].place(nh, nw, cy, cx)) break;
-      if (pi == grids.size()) {
-        if ((int)grids.size() >= DN_MAX_PLANES_PER_IMAGE)
-          return fail(DN_E_TOO_LARGE, "more planes than DN_MAX_PLANES_PER_IMAGE");
-        grids.emplace_back(p.plane_h / 16, p.plane_w / 16);
-        cy = cx = 0;
-      }
-      grids[pi].occupy(cy, cx, nh, nw);
-      g.plane = (int32_t)pi;
-      g.y = cy * 16;
-      g.x = cx * 16;
-    }
-    plan.planes.assign(grids.size(), PlaneSize{p.plane_h, p.plane_w});
+    int n_planes = 0;
+    const int st = stitch(plan.scales, p.plane_h, p.plane_w, DN_MAX_PLANES_PER_IMAGE, n_planes);
+    if (st != DN_OK) return st;
+    plan.planes.assign(n_planes, PlaneSize{p.plane_h, p.plane_w});
   }
   if ((int)plan.planes.size() > DN_MAX_PLANES_PER_IMAGE)
     return fail(DN_E_TOO_LARGE, "more planes than DN_MAX_PLANES_PER_IMAGE");
-
-  // conv5 windows: cell i is centred at 16 i + 17.5; keep cells centred on rows [y+p, y+p+h).
-  for (int k = 0; k < K; ++k) {
-    dn_scale_geom& g = plan.scales[k];
+  for (dn_scale_geom& g : plan.scales) {
     const PlaneSize ps = plan.planes[g.plane];
-    int64_t sh[8], sw[8];
-    stack_sides(ps.h, sh);
-    stack_sides(ps.w, sw);
-    const int64_t top = g.y + p.pad, left = g.x + p.pad;
-    // first i with 32 i + 35 >= 2 top; last i with 32 i + 35 <= 2 (top + h) - 1
-    g.r0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * top - 35, 32));
-    g.r1 = (int32_t)std::min<int64_t>(sh[6] - 1, div_floor(2 * (top + g.h) - 36, 32));
-    g.c0 = (int32_t)std::max<int64_t>(0, div_ceil(2 * left - 35, 32));
-    g.c1 = (int32_t)std::min<int64_t>(sw[6] - 1, div_floor(2 * (left + g.w) - 36, 32));
+    set_window(g, ps.h, ps.w, p.pad);
   }
+  return DN_OK;
+}
+
+int make_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_params& p,
+                    std::vector<dn_scale_geom>& items, int& n_planes) {
+  if (n_img <= 0) return fail(DN_E_INVALID_ARG, "n_img must be positive");
+  if (p.plane_h <= 0 || p.plane_w <= 0)
+    return fail(DN_E_INVALID_ARG, "cross-image packing needs stitching planes (plane_h, plane_w > 0)");
+  Plan one;  // the entries' sizes and rectangles; its own placement is replaced below
+  const int st = make_plan(H, W, p, one);
+  if (st != DN_OK) return st;
+  const int64_t E = (int64_t)one.scales.size();
+  if ((int64_t)n_img * E > DN_MAX_BATCH_ITEMS) {
+    std::ostringstream os;
+    os << "n_img * entries must be at most " << DN_MAX_BATCH_ITEMS;
+    return fail(DN_E_TOO_LARGE, os.str());
+  }
+  items.assign((size_t)(n_img * E), dn_scale_geom{});
+  for (int32_t b = 0; b < n_img; ++b)
+    for (int64_t e = 0; e < E; ++e) {
+      dn_scale_geom& g = items[(size_t)(b * E + e)];
+      g = one.scales[(size_t)e];
+      g.image = b;
+    }
+  const int st2 = stitch(items, p.plane_h, p.plane_w, (int)items.size(), n_planes);
+  if (st2 != DN_OK) return st2;
+  for (dn_scale_geom& g : items) set_window(g, p.plane_h, p.plane_w, p.pad);
   return DN_OK;
 }
 

@@ -68,14 +68,26 @@ struct RowEntry {
   float ly, wy;     // row fraction, row border weight (0: background)
 };
 
-template <typename T>
+// Whether a placement read from a device copy of a packed plan is a rectangle of 16-px cells inside a
+// PH x PW plane of image < n_img with a real size; other entries are ignored (background).
+__device__ inline bool valid_item(const dn_scale_geom& g, const BatchGeom& bg) {
+  return g.image >= 0 && g.image < bg.n_img && g.h >= 1 && g.w >= 1 && g.h <= 65535 &&
+         g.w <= 65535 && g.rh >= 16 && g.rw >= 16 && ((g.y | g.x | g.rh | g.rw) & 15) == 0 &&
+         g.y >= 0 && g.x >= 0 && g.y <= bg.PH - g.rh && g.x <= bg.PW - g.rw;
+}
+
+// BATCH = false: planes of each image (a.s, pl), blocks z = image * pl.n + plane.  BATCH = true: the
+// planes of a cross-image packed batch (bg), blocks z = plane, each cell sampling its owner's image.
+template <typename T, bool BATCH>
 __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __restrict__ pix,
-                                                           PyrArgs a, PyrPlanes pl,
+                                                           PyrArgs a, PyrPlanes pl, BatchGeom bg,
                                                            T* __restrict__ out, int tiles_x,
                                                            int tiles_y) {
   typedef T vec_t __attribute__((ext_vector_type(PX)));
   static_assert(TCELLS <= 256, "one owner search per thread");
   __shared__ int s_own[TCELLS];
+  __shared__ PyrScale s_sc[TCELLS];  // owner's rectangle, per cell
+  __shared__ int s_img[TCELLS];      // owner's image, per cell
   __shared__ RowEntry s_row[TCELLS * TROWS];
   // XCD-aware order over a flat grid: XCD x takes a contiguous range of (image, plane, row tile,
   // column tile) indices, so the tiles in flight on one XCD read the same image from its L2.
@@ -85,33 +97,60 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   bid /= tiles_x;
   const int gy = bid % tiles_y;
   const int z = bid / tiles_y;
-  const int b = z / pl.n, j = z - b * pl.n;
-  const int PH = pl.p[j].h, PW = pl.p[j].w;
+  const int b = BATCH ? 0 : z / pl.n, j = BATCH ? z : z - b * pl.n;
+  const int PH = BATCH ? bg.PH : pl.p[j].h, PW = BATCH ? bg.PW : pl.p[j].w;
   const int tx0 = gx * 64 * PX, ty0 = gy * TROWS;
   if (tx0 >= PW || ty0 >= PH) return;  // uniform per workgroup
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
-  const int f0 = a.plane_first[j], f1 = f0 + a.plane_count[j];
 
-  if (tid < TCELLS) {
-    const int cx = tx0 + 16 * tid;
-    int owner = -1;
-    for (int e = f0; e < f1 && cx < PW; ++e) {
-      const PyrScale& s = a.s[e];
-      if (ty0 >= s.y && ty0 < s.y + s.rh && cx >= s.x && cx < s.x + s.rw) {
-        owner = e;
-        break;
+  if constexpr (BATCH) {
+    // Rectangles never overlap and their edges are multiples of 16, so each cell of this 16-row band
+    // has at most one owner among the items on plane j.
+    if (tid < TCELLS) s_own[tid] = -1;
+    __syncthreads();
+    for (int e = tid; e < bg.n_items; e += 256) {
+      const dn_scale_geom& g = bg.geom[e];
+      if (g.plane != j || !valid_item(g, bg) || ty0 < g.y || ty0 >= g.y + g.rh) continue;
+      const int c_lo = max(0, (g.x - tx0) / 16), c_hi = min(TCELLS, (g.x + g.rw - tx0) / 16);
+      for (int c = c_lo; c < c_hi; ++c) s_own[c] = e;
+    }
+    __syncthreads();
+    if (tid < TCELLS) {
+      const int e = s_own[tid];
+      if (e >= 0 && tx0 + 16 * tid < PW) {
+        const dn_scale_geom& g = bg.geom[e];
+        s_sc[tid] = PyrScale{g.plane, g.y, g.x, g.rh, g.rw, g.h, g.w};
+        s_img[tid] = g.image;
+      } else {
+        s_own[tid] = -1;
       }
     }
-    s_own[tid] = owner;
+  } else {
+    const int f0 = a.plane_first[j], f1 = f0 + a.plane_count[j];
+    if (tid < TCELLS) {
+      const int cx = tx0 + 16 * tid;
+      int owner = -1;
+      for (int e = f0; e < f1 && cx < PW; ++e) {
+        const PyrScale& s = a.s[e];
+        if (ty0 >= s.y && ty0 < s.y + s.rh && cx >= s.x && cx < s.x + s.rw) {
+          owner = e;
+          break;
+        }
+      }
+      s_own[tid] = owner;
+      if (owner >= 0) {
+        s_sc[tid] = a.s[owner];
+        s_img[tid] = b;
+      }
+    }
   }
   __syncthreads();
   for (int ent = tid; ent < TCELLS * TROWS; ent += 256) {
     const int cell = ent / TROWS, r = ent % TROWS, y = ty0 + r;
-    const int e = s_own[cell];
     RowEntry re{0u, 0u, 0.f, 0.f};
-    if (e >= 0 && y < PH) {
-      const PyrScale& s = a.s[e];
+    if (s_own[cell] >= 0 && y < PH) {
+      const PyrScale& s = s_sc[cell];
       const int vy = y - s.y - a.pad;
       const int dy = max(0, max(-vy, vy - (s.h - 1)));
       re.wy = border_weight(dy, a.pad, a.ramp);
@@ -136,7 +175,7 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     sx0[i] = sx1[i] = 0u;
   }
   if (owner >= 0) {
-    const PyrScale& s = a.s[owner];
+    const PyrScale& s = s_sc[cell];
     const double inv2w = 1.0 / (2.0 * s.w);
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
@@ -149,8 +188,8 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       sx1[i] = (uint32_t)c1;
     }
   }
-  const uint32_t* P = pix + (int64_t)b * a.H * a.W;
-  T* o = out + (int64_t)b * pl.image_elems + pl.p[j].offset;
+  const uint32_t* P = pix + (int64_t)(owner >= 0 ? s_img[cell] : 0) * a.H * a.W;
+  T* o = out + (BATCH ? (int64_t)j * 3 * PH * PW : (int64_t)b * pl.image_elems + pl.p[j].offset);
   const int64_t plane = (int64_t)PH * PW;
   const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
 
@@ -205,26 +244,27 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
 }  // namespace
 
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out, uint8_t* d_scratch,
-                        void* stream) {
+                        const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
+                        uint8_t* d_scratch, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   uint32_t* pix = (uint32_t*)d_scratch;
   pixel_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
   const int tiles_x = (max_w + 64 * PX - 1) / (64 * PX), tiles_y = (max_h + TROWS - 1) / TROWS;
-  const int64_t nblk = (int64_t)tiles_x * tiles_y * n_img * pl.n;
+  const int64_t nblk = (int64_t)tiles_x * tiles_y * (batch ? batch->n_planes : n_img * pl.n);
   if (nblk > 0x7fffffff) return (int)hipErrorInvalidValue;
   const unsigned grid = (unsigned)nblk;
+  const BatchGeom bg = batch ? *batch : BatchGeom{};
+  auto go = [&](auto tag) {
+    using T = decltype(tag);
+    if (batch)
+      build_planes_kernel<T, true><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+    else
+      build_planes_kernel<T, false><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+  };
   switch (dt) {
-    case DN_F32:
-      build_planes_kernel<float><<<grid, 256, 0, s>>>(pix, a, pl, (float*)d_out, tiles_x, tiles_y);
-      break;
-    case DN_F16:
-      build_planes_kernel<_Float16><<<grid, 256, 0, s>>>(pix, a, pl, (_Float16*)d_out, tiles_x,
-                                                         tiles_y);
-      break;
-    case DN_BF16:
-      build_planes_kernel<__bf16><<<grid, 256, 0, s>>>(pix, a, pl, (__bf16*)d_out, tiles_x, tiles_y);
-      break;
+    case DN_F32: go(float{}); break;
+    case DN_F16: go(_Float16{}); break;
+    case DN_BF16: go(__bf16{}); break;
   }
   return (int)hipGetLastError();
 }

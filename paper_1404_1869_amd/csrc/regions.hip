@@ -36,9 +36,27 @@ __device__ inline void pool_bin_range(double lo, double hi, int cmin, int cmax, 
   last = l;
 }
 
+// Entry k of image img: from the kernel arguments (per-image maps), or from the device copy of a
+// cross-image packed plan, where an entry whose window does not lie inside a map is taken as empty.
+template <bool BATCH>
+__device__ inline RegScale entry(const RegArgs& a, const RegBatch& bt, int img, int k) {
+  if constexpr (!BATCH) {
+    return a.s[k];
+  } else {
+    const dn_scale_geom& g = bt.geom[(int64_t)img * a.n_scales + k];
+    RegScale r{g.plane, g.y, g.x, g.r0, g.r1, g.c0, g.c1, 0, g.sy, g.sx};
+    const bool inside = g.plane >= 0 && g.plane < bt.n_maps && g.r0 >= 0 && g.c0 >= 0 &&
+                        g.r1 < bt.map_h && g.c1 < bt.map_w;
+    r.empty = (!inside || g.r1 < g.r0 || g.c1 < g.c0) ? 1 : 0;
+    return r;
+  }
+}
+
 // POOL = false: bilinear samples at the bin centres; POOL = true: per-channel max over each bin's cells.
-template <typename T, bool POOL>
+// BATCH = true: the maps of a cross-image packed batch (bt), else per-image maps (a).
+template <typename T, bool POOL, bool BATCH>
 __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict__ maps, RegArgs a,
+                                                             RegBatch bt,
                                                              const float* __restrict__ boxes,
                                                              const int32_t* __restrict__ box_img,
                                                              float* __restrict__ out,
@@ -63,13 +81,14 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   if (tid < 64) {
     double cost = INFINITY;
     int k = tid;
-    if (valid && k < a.n_scales && !a.s[k].empty) {
+    const RegScale ek = valid && k < a.n_scales ? entry<BATCH>(a, bt, img, k) : RegScale{};
+    if (valid && k < a.n_scales && !ek.empty) {
       const double T2 = a.target * a.target;
-      const double area = (a.s[k].sy * bh) * (a.s[k].sx * bw);
+      const double area = (ek.sy * bh) * (ek.sx * bw);
       const double p = area / T2, q = T2 / area;
       cost = p < q ? q : p;
       if (a.n_aspects > 1) {
-        const double rho = (a.s[k].sx * bw) / (a.s[k].sy * bh), irho = 1.0 / rho;
+        const double rho = (ek.sx * bw) / (ek.sy * bh), irho = 1.0 / rho;
         cost = cost * (rho < irho ? irho : rho);
       }
     } else {
@@ -97,7 +116,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       for (int e = tid; e < IDXW * SS; e += blockDim.x) idx_out[(int64_t)r * IDXW * SS + e] = 0;
     return;
   }
-  const RegScale sc = a.s[best];
+  const RegScale sc = entry<BATCH>(a, bt, img, best);
   if (POOL && tid < 2 * S) {
     const bool row = tid < S;
     const int t = row ? tid : tid - S;
@@ -147,8 +166,9 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
     }
   }
   __syncthreads();
-  const T* F = maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
-  const int Wc = a.map_w[sc.plane];
+  const T* F = BATCH ? maps + (int64_t)sc.plane * bt.map_stride
+                     : maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
+  const int Wc = BATCH ? bt.map_w : a.map_w[sc.plane];
   // Each thread blends VT consecutive channels (one 16-byte vector per neighbour cell); C / VT
   // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.  The
   // results are staged bin-major, one row of C + 2 floats per bin in channel order (8-byte writes),
@@ -280,37 +300,37 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
     }
 }
 
-template <bool POOL>
-int launch(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
+template <bool POOL, bool BATCH>
+int launch(const void* d_conv5, dn_dtype dt, const RegArgs& a, const RegBatch& bt, const float* d_boxes,
            const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale, int32_t* d_idx,
            hipStream_t s) {
   if (a.S > MAX_S || a.S <= 0) return (int)hipErrorInvalidValue;
   const size_t lds = sizeof(float) * (size_t)(a.C + 2) * a.S * a.S;
-  switch (dt) {
-    case DN_F32:
-      region_windows_kernel<float, POOL><<<n, 256, lds, s>>>((const float*)d_conv5, a, d_boxes,
-                                                             d_box_img, d_out, d_scale, d_idx);
-      break;
-    case DN_F16:
-      region_windows_kernel<_Float16, POOL><<<n, 256, lds, s>>>((const _Float16*)d_conv5, a, d_boxes,
-                                                                d_box_img, d_out, d_scale, d_idx);
-      break;
-    case DN_BF16:
-      region_windows_kernel<__bf16, POOL><<<n, 256, lds, s>>>((const __bf16*)d_conv5, a, d_boxes,
+  auto go = [&](auto tag) {
+    using T = decltype(tag);
+    region_windows_kernel<T, POOL, BATCH><<<n, 256, lds, s>>>((const T*)d_conv5, a, bt, d_boxes,
                                                               d_box_img, d_out, d_scale, d_idx);
-      break;
+  };
+  switch (dt) {
+    case DN_F32: go(float{}); break;
+    case DN_F16: go(_Float16{}); break;
+    case DN_BF16: go(__bf16{}); break;
   }
   return (int)hipGetLastError();
 }
 
 }  // namespace
 
-int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const float* d_boxes,
-                          const int32_t* d_box_img, int32_t n, float* d_out, int32_t* d_scale,
-                          int32_t* d_idx, bool pool, void* stream) {
+int launch_region_windows(const void* d_conv5, dn_dtype dt, const RegArgs& a, const RegBatch* batch,
+                          const float* d_boxes, const int32_t* d_box_img, int32_t n, float* d_out,
+                          int32_t* d_scale, int32_t* d_idx, bool pool, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  return pool ? launch<true>(d_conv5, dt, a, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s)
-              : launch<false>(d_conv5, dt, a, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s);
+  const RegBatch bt = batch ? *batch : RegBatch{};
+  if (batch)
+    return pool ? launch<true, true>(d_conv5, dt, a, bt, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s)
+                : launch<false, true>(d_conv5, dt, a, bt, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s);
+  return pool ? launch<true, false>(d_conv5, dt, a, bt, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s)
+              : launch<false, false>(d_conv5, dt, a, bt, d_boxes, d_box_img, n, d_out, d_scale, d_idx, s);
 }
 
 }  // namespace dn

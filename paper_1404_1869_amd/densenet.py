@@ -22,13 +22,14 @@ DN_E_UNSUPPORTED, DN_E_HIP, DN_E_INTERNAL = -4, -5, -6
 DN_F32, DN_F16, DN_BF16 = 0, 1, 2
 DN_PAD_ZERO, DN_PAD_RAMP = 0, 1
 DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE, DN_MAX_WARP_SIDE, DN_MAX_ASPECTS = 64, 64, 1024, 8
+DN_MAX_BATCH_ITEMS = 65536
 DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
            "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
            "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_warp_regions",
-           "densenet_region_pool",
-           "densenet_profile_start",
+           "densenet_region_pool", "densenet_plan_batch", "densenet_build_batch",
+           "densenet_region_windows_batch", "densenet_profile_start",
            "densenet_profile_stop", "densenet_last_error")
 
 
@@ -42,7 +43,7 @@ class dn_pyramid_params(ctypes.Structure):
 
 class dn_scale_geom(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
-                                              "r1", "c0", "c1", "aspect", "reserved")] + \
+                                              "r1", "c0", "c1", "aspect", "image")] + \
                [(n, ctypes.c_double) for n in ("s", "sy", "sx")]
 
 
@@ -97,6 +98,10 @@ def lib():
             "densenet_layer_sizes": [i32, i32, pi32],
             "densenet_warp_regions": [P, i32, i32, i32, P, P, i32, i32, i32, ctypes.POINTER(f32), i32, P,
                                       sz, psz, P],
+            "densenet_plan_batch": [i32, i32, i32, pp, pg, pd, i32, pi32, pi64],
+            "densenet_build_batch": [P, i32, i32, i32, pp, i32, pg, P, i32, P, sz, psz, P],
+            "densenet_region_windows_batch": [P, pd, i32, i32, pg, P, i32, i32, i32, i32, P, P, i32, f32,
+                                              i32, P, P, P, P],
             "densenet_profile_start": [ctypes.c_char_p],
             "densenet_profile_stop": [ctypes.POINTER(dn_profile_entry), i32, pi32],
         }
@@ -227,6 +232,80 @@ def densenet_build_pyramid(images, p: dn_pyramid_params, dtype: int, out=None):
                                    DN_MAX_PLANES_PER_IMAGE, ctypes.byref(n), ctypes.byref(e),
                                    _stream()))
     return out, PlanResult(list(geom), list(planes[:n.value]), e.value)
+
+
+class BatchPlan:
+    """Cross-image packing (Sec. 3.1 stitching over a whole batch): the plan of n_img images of H x W,
+    its host geometry (entry e of image b at b * E + e) and a device copy of it for the kernels,
+    uploaded once."""
+
+    def __init__(self, n_img: int, H: int, W: int, p: dn_pyramid_params, device="cuda"):
+        """device=None plans on the host only (no device copy)."""
+        self.n_img, self.H, self.W, self.params = n_img, H, W, p
+        self.E = n_entries(p)
+        self.geom = (dn_scale_geom * (n_img * self.E))()
+        n, e = ctypes.c_int32(), ctypes.c_int64()
+        cap = n_img * self.E
+        planes = (dn_plane_desc * cap)()
+        check(lib().densenet_plan_batch(n_img, H, W, ctypes.byref(p), self.geom, planes, cap,
+                                        ctypes.byref(n), ctypes.byref(e)))
+        self.planes = list(planes[:n.value])
+        self.total_elems = e.value
+        self.d_geom = None
+        if device is not None:
+            raw = np.frombuffer(bytes(self.geom), np.uint8).copy()
+            self.d_geom = _torch().from_numpy(raw).to(device)
+
+    @property
+    def n_planes(self) -> int:
+        return len(self.planes)
+
+    def entry(self, b: int, e: int) -> dn_scale_geom:
+        return self.geom[b * self.E + e]
+
+    def geom_array(self) -> np.ndarray:
+        """[n_img * E][14] int32: k, h, w, plane, y, x, rh, rw, r0, r1, c0, c1, aspect, image."""
+        return np.array([[getattr(g, f) for f in ("k", "h", "w", "plane", "y", "x", "rh", "rw", "r0",
+                                                   "r1", "c0", "c1", "aspect", "image")]
+                         for g in self.geom], np.int32)
+
+
+def densenet_build_batch(images, plan: BatchPlan, dtype: int, out=None):
+    """images: uint8 device tensor [n_img][3][H][W] -> the packed batch's planes (flat tensor; plane j
+    at j * 3 * plane_h * plane_w, followed by the builder's scratch)."""
+    torch = _torch()
+    n_img, _, H, W = images.shape
+    assert (n_img, H, W) == (plan.n_img, plan.H, plan.W), "images do not match the plan"
+    need = ctypes.c_size_t()
+    L = lib()
+    check(L.densenet_build_batch(None, n_img, H, W, ctypes.byref(plan.params), dtype, plan.geom, None,
+                                 plan.n_planes, None, 0, ctypes.byref(need), None))
+    es = 4 if dtype == DN_F32 else 2
+    if out is None:
+        out = torch.empty(need.value // es, dtype=_tdtype(dtype), device=images.device)
+    check(L.densenet_build_batch(_ptr(images), n_img, H, W, ctypes.byref(plan.params), dtype, plan.geom,
+                                 _ptr(plan.d_geom), plan.n_planes, _ptr(out),
+                                 out.numel() * out.element_size(), ctypes.byref(need), _stream()))
+    return out
+
+
+def densenet_region_windows_batch(conv5, conv5_desc, dtype: int, plan: BatchPlan, boxes, box_img=None,
+                                  target=227.0, S=6, pooled=False, want_idx=False, out=None, scale=None):
+    """Region windows (pooled=False) or max-pooled bins (pooled=True) over a cross-image packed batch."""
+    torch = _torch()
+    n = boxes.shape[0]
+    if out is None:
+        out = torch.empty((n, 256 * S * S), dtype=torch.float32, device=boxes.device)
+    if scale is None:
+        scale = torch.empty(n, dtype=torch.int32, device=boxes.device)
+    idx = torch.empty((n, S, S, 4 if pooled else 2), dtype=torch.int32, device=boxes.device) if want_idx \
+        else None
+    cd = (dn_plane_desc * len(conv5_desc))(*conv5_desc)
+    check(lib().densenet_region_windows_batch(_ptr(conv5), cd, len(conv5_desc), dtype, plan.geom,
+                                              _ptr(plan.d_geom), plan.n_img, plan.E, plan.params.pad,
+                                              int(pooled), _ptr(boxes), _ptr(box_img), n, target, S,
+                                              _ptr(out), _ptr(scale), _ptr(idx), _stream()))
+    return out, scale, idx
 
 
 def densenet_pack_weights(weights, dtype: int):
@@ -455,3 +534,17 @@ def convnet_featpyramid(images, p: dn_pyramid_params, packed, dtype: int, net=No
         for g in plan.geom:
             feat.append(maps[b * npl + g.plane][g.r0:g.r1 + 1, g.c0:g.c1 + 1])
     return Pyramid(feat, np.array([g.s for g in plan.geom]), plan, planes, cf, n_img)
+
+
+def convnet_featpyramid_batch(images, p: dn_pyramid_params, packed, dtype: int, net=None,
+                              plan: BatchPlan | None = None) -> Pyramid:
+    """A batch of images stitched together (cross-image packing) -> per-(image, scale) conv5 maps
+    (views, image-major) + the batch plan."""
+    net = net or net_params()
+    n_img, _, H, W = images.shape
+    plan = plan or BatchPlan(n_img, H, W, p, device=images.device)
+    planes = densenet_build_batch(images, plan, dtype)
+    cf = densenet_conv_features(planes, plan.planes, dtype, packed, net)
+    maps = cf.conv5_maps()
+    feat = [maps[g.plane][g.r0:g.r1 + 1, g.c0:g.c1 + 1] for g in plan.geom]
+    return Pyramid(feat, np.array([plan.geom[e].s for e in range(plan.E)]), plan, planes, cf, n_img)

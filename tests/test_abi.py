@@ -144,3 +144,59 @@ def test_warp_regions_size_query_and_validation():
     # n == 0 launches nothing and accepts null buffers
     assert L.densenet_warp_regions(None, 1, 768, 1024, None, None, 0, 227, 0, None, D.DN_F32, fake, 0,
                                    None, None) == D.DN_OK
+
+
+def test_batch_entry_points_validation():
+    L = D.lib()
+    p = D.pyramid_params(25, 10, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=1200, plane_w=1200)
+    E, n_img = 25, 16
+    geom = (D.dn_scale_geom * (n_img * E))()
+    planes = (D.dn_plane_desc * 200)()
+    n, e = ctypes.c_int32(), ctypes.c_int64()
+    assert L.densenet_plan_batch(n_img, 768, 1024, ctypes.byref(p), geom, planes, 200, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_OK
+    assert n.value == 88 and e.value == 88 * 3 * 1200 * 1200
+    assert L.densenet_plan_batch(n_img, 768, 1024, ctypes.byref(p), geom, planes, 50, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_E_TOO_LARGE and n.value == 88
+    q = D.pyramid_params(25, 10, pad=16)                       # no stitching planes
+    assert L.densenet_plan_batch(2, 768, 1024, ctypes.byref(q), geom, planes, 200, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_E_INVALID_ARG
+    assert L.densenet_plan_batch(0, 768, 1024, ctypes.byref(p), geom, planes, 200, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_E_INVALID_ARG
+    big = D.pyramid_params(64, 10, pad=16, plane_h=4000, plane_w=4000)
+    assert L.densenet_plan_batch(1025, 100, 100, ctypes.byref(big), geom, planes, 200, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_E_TOO_LARGE   # 1025 * 64 > DN_MAX_BATCH_ITEMS
+    assert L.densenet_plan_batch(2, 100, 100, ctypes.byref(big), None, planes, 200, ctypes.byref(n),
+                                 ctypes.byref(e)) == D.DN_E_INVALID_ARG            # null geom
+    # build: size query (no device work), then host validation of the geometry before any launch
+    need = ctypes.c_size_t()
+    assert L.densenet_build_batch(None, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, None, 88,
+                                  None, 0, ctypes.byref(need), None) == D.DN_OK
+    assert need.value == (88 * 3 * 1200 * 1200 * 2 + 255) // 256 * 256 + n_img * 4 * 768 * 1024
+    fake = ctypes.c_void_p(256)
+    assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 88, fake,
+                                  10, ctypes.byref(need), None) == D.DN_E_BUFFER_TOO_SMALL
+    assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 87, fake,
+                                  1 << 40, ctypes.byref(need), None) == D.DN_E_INVALID_ARG  # plane 87
+    geom[3].x = 8                                               # not on the 16-px grid
+    assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 88, fake,
+                                  1 << 40, ctypes.byref(need), None) == D.DN_E_INVALID_ARG
+    geom[3].x = 0
+    geom[5].image = 3                                           # rows out of order
+    assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 88, fake,
+                                  1 << 40, ctypes.byref(need), None) == D.DN_E_INVALID_ARG
+    geom[5].image = 0
+    # region reads: maps must be one size and evenly spaced; windows inside them
+    cd = (D.dn_plane_desc * 88)()
+    for j in range(88):
+        cd[j].h, cd[j].w, cd[j].offset = 74, 74, j * 74 * 74 * 256
+    args = lambda cdesc, nm, pooled: (fake, cdesc, nm, D.DN_BF16, geom, fake, n_img, E, 16, pooled, fake,
+                                      None, 0, 227.0, 6, fake, fake, None, None)
+    assert L.densenet_region_windows_batch(*args(cd, 88, 0)) == D.DN_OK            # n = 0: nothing runs
+    assert L.densenet_region_windows_batch(*args(cd, 88, 2)) == D.DN_E_INVALID_ARG
+    assert L.densenet_region_windows_batch(*args(cd, 87, 1)) == D.DN_E_INVALID_ARG  # plane 87 missing
+    cd[7].offset += 256
+    assert L.densenet_region_windows_batch(*args(cd, 88, 0)) == D.DN_E_INVALID_ARG
+    cd[7].offset -= 256
+    cd[0].h = cd[1].h = 20
+    assert L.densenet_region_windows_batch(*args(cd, 88, 0)) == D.DN_E_INVALID_ARG

@@ -40,3 +40,37 @@ def test_plan_is_deterministic():
     a = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w)).geom_array()
     b = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w)).geom_array()
     np.testing.assert_array_equal(a, b)
+
+
+BATCH_CASES = [
+    (16, C.XGA_25SCALE_B16),
+    (5, C.Workload("vga_batch", 480, 640, (1,), 8, 4, pad=16, pad_mode=1, plane_h=1200, plane_w=1200)),
+    (7, C.Workload("small_batch", 300, 200, (1,), 6, 3, pad=16, pad_mode=1, plane_h=400, plane_w=400)),
+    (4, C.Workload("aspect_batch", 240, 320, (1,), 6, 3, pad=16, pad_mode=1, plane_h=800, plane_w=800,
+                   aspects=(0.5, 2.0))),
+    (3, C.Workload("wide_batch", 64, 1000, (1,), 9, 3, pad=8, plane_h=600, plane_w=1200)),
+    (1, C.XGA_25SCALE),
+]
+
+
+@pytest.mark.parametrize("n_img,w", BATCH_CASES, ids=lambda v: getattr(v, "name", str(v)))
+def test_batch_plan_bit_exact_vs_oracle(n_img, w):
+    lib = D.BatchPlan(n_img, w.H, w.W, D.params_for(w), device=None)
+    ref = oracle.plan_batch(n_img, w.H, w.W, w.n_scales, w.steps_per_octave, w.base_scale,
+                            w.base_longest_side, w.pad, w.plane_h, w.plane_w,
+                            aspects=list(w.aspects) or None)
+    assert lib.n_planes == ref.n_planes
+    np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, [*range(12), 14, 15]])
+    np.testing.assert_array_equal(np.array([[g.s, g.sy, g.sx] for g in lib.geom]), ref.gd)
+    pe = 3 * w.plane_h * w.plane_w
+    assert [(p.h, p.w, p.offset) for p in lib.planes] == [(w.plane_h, w.plane_w, j * pe)
+                                                          for j in range(ref.n_planes)]
+    assert lib.total_elems == ref.n_planes * pe
+
+
+def test_batch_of_one_is_the_image_plan():
+    w = C.XGA_25SCALE
+    a = D.densenet_plan_pyramid(w.H, w.W, D.params_for(w))
+    b = D.BatchPlan(1, w.H, w.W, D.params_for(w), device=None)
+    np.testing.assert_array_equal(a.geom_array(), b.geom_array()[:, :13])
+    assert b.n_planes == len(a.planes)
