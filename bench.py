@@ -5,7 +5,9 @@ One step is one pass of the whole path over one batch of synthetic input already
 fused pyramid build (resize, centring, padding, stitching) -> conv1..conv5 with ReLU, LRN and pooling
 on every stitched plane -> per-scale conv5 windows -> region windows for 2000 boxes per image.
 After the timed steps it also times the paper's per-window baseline (every box of one image warped to
-227 x 227 and run through the network on its own) and reports it beside the dense time per image.
+227 x 227 and run through the network on its own) and reports it beside the dense time per image, and
+the same batch with cross-image packing (the scales of all 16 images stitched together: 88 planes
+instead of 96), reported beside the headline, which keeps each image's own planes.
 The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
 1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
 
@@ -47,6 +49,8 @@ def parse():
     ap.add_argument("--kernels", action="store_true", help="also print the per-kernel breakdown")
     ap.add_argument("--no-per-window", action="store_true",
                     help="skip the per-window baseline (every box warped to 227 x 227 and run alone)")
+    ap.add_argument("--no-packed", action="store_true",
+                    help="skip the cross-image packed variant (the batch's scales stitched together)")
     return ap.parse_args()
 
 
@@ -215,6 +219,9 @@ def main():
     if not args.no_per_window:
         result["per_window"] = per_window(D, w, dt, imgs[:1], boxes[:boxes_per_img], packed,
                                           ms_per_step / n_img)
+    if not args.no_packed and n_img > 1:
+        result["cross_image_packing"] = cross_image(D, w, dt, imgs, boxes, box_img, packed, args.steps,
+                                                    args.warmup, ms_per_step)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
     print(json.dumps(result), flush=True)
@@ -254,6 +261,45 @@ def per_window(D, w, dt, img, boxes, packed, dense_ms_per_image):
             "conv_tflops": round(flops / (conv_ms / 1e3) / 1e12, 2),
             "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()},
             "paper_context": "Sec. 3.4, NVIDIA K20: 2000 windows ~10 s vs one 25-scale pyramid ~1 s"}
+
+
+def cross_image(D, w, dt, imgs, boxes, box_img, packed, steps, warmup, per_image_ms):
+    """The same step on the same batch with cross-image packing: the rectangles of all images
+    stitched together (fewer, fuller planes), the conv stack over the packed planes and the region
+    windows read through the packed layout; timed over the same number of steps."""
+    import time
+
+    import torch
+
+    n_img = imgs.shape[0]
+    plan = D.BatchPlan(n_img, w.H, w.W, D.params_for(w), device=imgs.device)
+    planes = D.densenet_build_batch(imgs, plan, dt)
+    cf = D.ConvFeatures(plan.planes, dt, D.net_params(pool5=False), device=imgs.device)
+    c5d = list(cf.c5d)
+    out = torch.empty((boxes.shape[0], 256 * 36), dtype=torch.float32, device=imgs.device)
+    scale = torch.empty(boxes.shape[0], dtype=torch.int32, device=imgs.device)
+
+    def step():
+        D.densenet_build_batch(imgs, plan, dt, out=planes)
+        cf(planes, packed)
+        D.densenet_region_windows_batch(cf.conv5, c5d, dt, plan, boxes, box_img, out=out, scale=scale)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    D.profile_start()
+    step()
+    torch.cuda.synchronize()
+    kern = D.profile_stop()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = 1e3 * (time.perf_counter() - t0) / steps
+    return {"planes": plan.n_planes, "ms_per_step": round(ms, 4),
+            "pyramids_per_s": round(n_img / (ms / 1e3), 2),
+            "speedup_vs_per_image_planes": round(per_image_ms / ms, 4),
+            "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()}}
 
 
 def cpu_baseline(w, n_planes_sample):

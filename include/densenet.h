@@ -170,8 +170,10 @@ int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_pa
  * The host array is validated; an entry of d_geom that is not a placement inside a plane of this
  * batch is ignored by the kernel (its pixels stay background), so a stale copy gives wrong planes but
  * no out-of-bounds access.  d_planes: [n_planes][3][plane_h][plane_w] in `dtype`, followed by the
- * builder's scratch (4 * H * W * n_img bytes, 256-byte aligned; contents afterwards unspecified), or
- * NULL for a size query into *bytes_needed. */
+ * builder's scratch (the pixel image, 4 * H * W * n_img bytes, then per-plane item lists,
+ * 4 * (n_planes + 1 + n_img * E) bytes, each part 256-byte aligned; contents afterwards unspecified),
+ * or NULL for a size query into *bytes_needed.  n_img * H * W must be below 2^32 and n_planes at most
+ * 16384 (DN_E_TOO_LARGE). */
 int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                          const dn_pyramid_params* p, dn_dtype dtype, const dn_scale_geom* geom,
                          const dn_scale_geom* d_geom, int32_t n_planes, void* d_planes,

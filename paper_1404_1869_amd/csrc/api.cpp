@@ -359,9 +359,16 @@ int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int3
     if (p->n_scales <= 0 || E > DN_MAX_SCALES || n_img * E > DN_MAX_BATCH_ITEMS)
       return fail(DN_E_INVALID_ARG, "bad n_scales, n_aspects or batch size");
     if (n_planes <= 0) return fail(DN_E_INVALID_ARG, "n_planes must be positive");
+    if (n_planes > MAX_INDEX_PLANES) {
+      std::ostringstream os;
+      os << "a packed batch is limited to " << MAX_INDEX_PLANES << " planes";
+      return fail(DN_E_TOO_LARGE, os.str());
+    }
+    if ((int64_t)n_img * H * W > 0xffffffffLL)
+      return fail(DN_E_TOO_LARGE, "a packed batch is limited to 2^32 - 1 image pixels");
     const int64_t pe = 3LL * p->plane_h * p->plane_w;
     const size_t planes_end = ((size_t)n_planes * (size_t)pe * dtype_size(dtype) + 255) & ~(size_t)255;
-    const size_t need = planes_end + (size_t)n_img * 4 * (size_t)H * (size_t)W;
+    const size_t need = planes_end + builder_scratch_bytes(n_img, H, W, n_planes, (int32_t)(n_img * E));
     *bytes_needed = need;
     if (!d_planes) return DN_OK;
     if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
@@ -376,7 +383,7 @@ int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int3
     a.ramp = p->pad_mode == DN_PAD_RAMP;
     for (int c = 0; c < 3; ++c) a.mean[c] = p->mean[c];
     PyrPlanes pl{};
-    BatchGeom bg{d_geom, (int32_t)(n_img * E), n_img, n_planes, p->plane_h, p->plane_w};
+    BatchGeom bg{d_geom, (int32_t)(n_img * E), n_img, n_planes, p->plane_h, p->plane_w, nullptr, nullptr};
     TraceScope trace("build_planes", stream);
     return hip_status(launch_build_planes(d_images, n_img, a, pl, &bg, p->plane_h, p->plane_w, dtype,
                                           d_planes, (uint8_t*)d_planes + planes_end, stream),
@@ -479,6 +486,11 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       return fail(DN_E_INVALID_ARG, "null pointer argument");
     if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
     if (n_planes <= 0) return fail(DN_E_INVALID_ARG, "n_planes must be positive");
+    if (n_planes > MAX_INDEX_PLANES) {
+      std::ostringstream os;
+      os << "a packed batch is limited to " << MAX_INDEX_PLANES << " planes";
+      return fail(DN_E_TOO_LARGE, os.str());
+    }
     if (net->lrn_n <= 0 || net->lrn_n % 2 == 0 || net->lrn_n > 9)
       return fail(DN_E_INVALID_ARG, "lrn_n must be odd and at most 9");
     if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");

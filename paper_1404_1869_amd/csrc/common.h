@@ -70,15 +70,28 @@ struct PyrPlanes {
 };
 
 // A cross-image packed batch: placements read from a device copy of the plan (n_items entries),
-// planes all PH x PW, plane j at j * 3 * PH * PW elements.
+// planes all PH x PW, plane j at j * 3 * PH * PW elements.  first/list: per-plane item lists the
+// launcher builds in the scratch (set by the launcher).
 struct BatchGeom {
   const dn_scale_geom* geom;
   int32_t n_items, n_img, n_planes, PH, PW;
+  const int32_t* first;
+  const int32_t* list;
 };
+constexpr int32_t MAX_INDEX_PLANES = 16384;  // planes of one packed batch (per-plane lists in LDS)
 
-// d_scratch: 4 * H * W * n_img bytes (4-byte aligned) for the pixel-interleaved image.  batch: NULL for
-// per-image planes (a.s / pl), else the packed batch's placements (a.s and pl unused but H, W, pad,
-// ramp, mean).
+// Builder scratch: the pixel-interleaved image (4 * H * W * n_img bytes), then for a packed batch the
+// per-plane item lists (4 * (n_planes + 1 + n_items) bytes), each part 256-byte aligned.
+inline size_t index_offset(int32_t n_img, int32_t H, int32_t W) {
+  return ((size_t)n_img * 4 * (size_t)H * (size_t)W + 255) & ~(size_t)255;
+}
+inline size_t builder_scratch_bytes(int32_t n_img, int32_t H, int32_t W, int32_t n_planes, int32_t n_items) {
+  return index_offset(n_img, H, W) + 4 * ((size_t)n_planes + 1 + (size_t)n_items);
+}
+
+// d_scratch: builder_scratch_bytes (256-byte aligned; n_planes = n_items = 0 without a batch).  batch:
+// NULL for per-image planes (a.s / pl), else the packed batch's placements (a.s and pl unused but H,
+// W, pad, ramp, mean).
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
                         const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
                         uint8_t* d_scratch, void* stream);

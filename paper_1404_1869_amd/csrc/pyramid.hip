@@ -64,9 +64,57 @@ __global__ __launch_bounds__(256) void pixel_image_kernel(const uint8_t* __restr
 }
 
 struct RowEntry {
-  uint32_t r0, r1;  // source row offsets sy0 * W, sy1 * W (pixels)
+  uint32_t r0, r1;  // source row offsets sy0 * W, sy1 * W (pixels; plus image * H * W in a packed batch)
   float ly, wy;     // row fraction, row border weight (0: background)
 };
+
+// Per-plane item lists of a packed plan, so that a builder workgroup scans only its plane's items:
+// items of plane j are list[first[j]] .. list[first[j + 1] - 1] (their order within a plane is
+// unspecified; rectangles do not overlap, so the builder's result does not depend on it).  One
+// workgroup: per-plane counts in LDS, an exclusive scan, then a scatter.  Items whose plane is out of
+// range are left out.
+constexpr int IDX_THREADS = 1024;
+__global__ __launch_bounds__(IDX_THREADS) void index_items_kernel(const dn_scale_geom* __restrict__ geom,
+                                                                  int n_items, int n_planes,
+                                                                  int32_t* __restrict__ first,
+                                                                  int32_t* __restrict__ list) {
+  extern __shared__ int s_cnt[];          // n_planes counts, then cursors
+  __shared__ int s_part[IDX_THREADS];     // per-thread chunk sums, scanned
+  const int tid = threadIdx.x;
+  for (int j = tid; j < n_planes; j += IDX_THREADS) s_cnt[j] = 0;
+  __syncthreads();
+  for (int e = tid; e < n_items; e += IDX_THREADS) {
+    const int pl = geom[e].plane;
+    if (pl >= 0 && pl < n_planes) atomicAdd(&s_cnt[pl], 1);
+  }
+  __syncthreads();
+  // exclusive scan: thread t owns planes [t C, (t + 1) C)
+  const int C = (n_planes + IDX_THREADS - 1) / IDX_THREADS, j0 = min(tid * C, n_planes),
+            j1 = min(j0 + C, n_planes);
+  int sum = 0;
+  for (int j = j0; j < j1; ++j) sum += s_cnt[j];
+  s_part[tid] = sum;
+  __syncthreads();
+  for (int off = 1; off < IDX_THREADS; off <<= 1) {  // inclusive Hillis-Steele scan of the chunk sums
+    const int v = tid >= off ? s_part[tid - off] : 0;
+    __syncthreads();
+    s_part[tid] += v;
+    __syncthreads();
+  }
+  int run = s_part[tid] - sum;
+  for (int j = j0; j < j1; ++j) {
+    const int c = s_cnt[j];
+    first[j] = run;
+    s_cnt[j] = run;  // cursor
+    run += c;
+  }
+  if (tid == IDX_THREADS - 1) first[n_planes] = s_part[tid];
+  __syncthreads();
+  for (int e = tid; e < n_items; e += IDX_THREADS) {
+    const int pl = geom[e].plane;
+    if (pl >= 0 && pl < n_planes) list[atomicAdd(&s_cnt[pl], 1)] = e;
+  }
+}
 
 // Whether a placement read from a device copy of a packed plan is a rectangle of 16-px cells inside a
 // PH x PW plane of image < n_img with a real size; other entries are ignored (background).
@@ -109,7 +157,8 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     // has at most one owner among the items on plane j.
     if (tid < TCELLS) s_own[tid] = -1;
     __syncthreads();
-    for (int e = tid; e < bg.n_items; e += 256) {
+    for (int i = bg.first[j] + tid; i < bg.first[j + 1]; i += 256) {
+      const int e = bg.list[i];
       const dn_scale_geom& g = bg.geom[e];
       if (g.plane != j || !valid_item(g, bg) || ty0 < g.y || ty0 >= g.y + g.rh) continue;
       const int c_lo = max(0, (g.x - tx0) / 16), c_hi = min(TCELLS, (g.x + g.rw - tx0) / 16);
@@ -156,8 +205,11 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       re.wy = border_weight(dy, a.pad, a.ramp);
       int sy0, sy1;
       src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, 1.0 / (2.0 * s.h), sy0, sy1, re.ly);
-      re.r0 = (uint32_t)sy0 * (uint32_t)a.W;
-      re.r1 = (uint32_t)sy1 * (uint32_t)a.W;
+      // a packed batch reads the owner's image: its offset is folded into the row offsets, so the
+      // pixel loads keep one base address for the whole workgroup
+      const uint32_t img_off = BATCH ? (uint32_t)s_img[cell] * (uint32_t)a.H * (uint32_t)a.W : 0u;
+      re.r0 = img_off + (uint32_t)sy0 * (uint32_t)a.W;
+      re.r1 = img_off + (uint32_t)sy1 * (uint32_t)a.W;
     }
     s_row[ent] = re;
   }
@@ -188,7 +240,7 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       sx1[i] = (uint32_t)c1;
     }
   }
-  const uint32_t* P = pix + (int64_t)(owner >= 0 ? s_img[cell] : 0) * a.H * a.W;
+  const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
   T* o = out + (BATCH ? (int64_t)j * 3 * PH * PW : (int64_t)b * pl.image_elems + pl.p[j].offset);
   const int64_t plane = (int64_t)PH * PW;
   const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
@@ -253,7 +305,17 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
   const int64_t nblk = (int64_t)tiles_x * tiles_y * (batch ? batch->n_planes : n_img * pl.n);
   if (nblk > 0x7fffffff) return (int)hipErrorInvalidValue;
   const unsigned grid = (unsigned)nblk;
-  const BatchGeom bg = batch ? *batch : BatchGeom{};
+  BatchGeom bg = batch ? *batch : BatchGeom{};
+  if (batch) {
+    // per-plane item lists in the scratch after the pixel image
+    if (bg.n_planes > MAX_INDEX_PLANES) return (int)hipErrorInvalidValue;
+    int32_t* first = (int32_t*)(d_scratch + index_offset(n_img, a.H, a.W));
+    int32_t* list = first + bg.n_planes + 1;
+    index_items_kernel<<<1, IDX_THREADS, sizeof(int) * bg.n_planes, s>>>(bg.geom, bg.n_items, bg.n_planes,
+                                                                        first, list);
+    bg.first = first;
+    bg.list = list;
+  }
   auto go = [&](auto tag) {
     using T = decltype(tag);
     if (batch)

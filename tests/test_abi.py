@@ -172,7 +172,8 @@ def test_batch_entry_points_validation():
     need = ctypes.c_size_t()
     assert L.densenet_build_batch(None, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, None, 88,
                                   None, 0, ctypes.byref(need), None) == D.DN_OK
-    assert need.value == (88 * 3 * 1200 * 1200 * 2 + 255) // 256 * 256 + n_img * 4 * 768 * 1024
+    assert need.value == (88 * 3 * 1200 * 1200 * 2 + 255) // 256 * 256 + n_img * 4 * 768 * 1024 + \
+        4 * (88 + 1 + n_img * E)
     fake = ctypes.c_void_p(256)
     assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 88, fake,
                                   10, ctypes.byref(need), None) == D.DN_E_BUFFER_TOO_SMALL
