@@ -672,10 +672,13 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave % Cf::WM, wn = wave / Cf::WM;
   const int half = lane >> 5, l32 = lane & 31;
+  // MFMA pixel tile t of wave wn is the tile's (t WN + wn)-th 32-pixel tile: the waves along pixels
+  // take the tiles in turn, so a partly filled bottom band splits its rows over them.
+  auto gtile = [&](int t) { return t * Cf::WN + wn; };
   int pix[TN];
 #pragma unroll
   for (int t = 0; t < TN; ++t) {
-    const int idx = wn * 32 * TN + t * 32 + l32;
+    const int idx = gtile(t) * 32 + l32;
     pix[t] = Cf::halo_off(Cf::pix_row(idx), Cf::pix_col(idx), 0);
   }
   // Byte offsets (chunk 0, tap row 0) of this lane's slot in each of its wave's LDS pieces.
@@ -715,32 +718,53 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     for (int t = 0; t < TN; ++t) acc[a][t] = f32x16{};
 
   const int nchunks = Cg / Cf::CC, nst = nchunks * R;
-  load_halo(0, 0);
-  load_w(0, 0, 0);
-  wait_vmem();
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int chunk = st / R, ky = st - chunk * R;
-    if (st + 1 < nst) load_w((st + 1) & 1, ((st + 1) / R) * Cf::CC, (st + 1) % R);
-    if (ky == 0 && chunk + 1 < nchunks) load_halo((chunk + 1) & 1, (chunk + 1) * Cf::CC);
-    const T* hs = halo_buf(chunk & 1);
-    const T* ws = wrow_buf(st & 1);
+  // MFMA pixel tiles of this wave that hold a pixel of the map: a prefix of its TN tiles, since the
+  // tiles are in row order.  Below the map's last row (the bottom band of tiles) the wave runs a
+  // stage loop that skips the empty tiles' reads and MFMAs; every wave still issues its share of the
+  // loads and reaches the same barriers.
+  int tnv = 0;
 #pragma unroll
-    for (int kx = 0; kx < R; ++kx) {
-      typename Op::frag x[TN], w[TM];
-#pragma unroll
-      for (int t = 0; t < TN; ++t)
-        x[t] = lds_frag16<T>(hs + pix[t] + ky * Cf::RS + kx * Cf::PS + half * 8);
-#pragma unroll
-      for (int mt = 0; mt < TM; ++mt)
-        w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, wm * 32 * TM + mt * 32 + l32, half));
-#pragma unroll
-      for (int mt = 0; mt < TM; ++mt)
-#pragma unroll
-        for (int t = 0; t < TN; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
-    }
+  for (int t = 0; t < TN; ++t) tnv += oy0 + Cf::pix_row(gtile(t) * 32) < H ? 1 : 0;
+  tnv = __builtin_amdgcn_readfirstlane(tnv);
+  auto stage_loop = [&](auto tnv_c) {
+    constexpr int TNV = decltype(tnv_c)::value;
+    load_halo(0, 0);
+    load_w(0, 0, 0);
     wait_vmem();
     __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+      const int chunk = st / R, ky = st - chunk * R;
+      if (st + 1 < nst) load_w((st + 1) & 1, ((st + 1) / R) * Cf::CC, (st + 1) % R);
+      if (ky == 0 && chunk + 1 < nchunks) load_halo((chunk + 1) & 1, (chunk + 1) * Cf::CC);
+      const T* hs = halo_buf(chunk & 1);
+      const T* ws = wrow_buf(st & 1);
+      if constexpr (TNV > 0) {
+#pragma unroll
+        for (int kx = 0; kx < R; ++kx) {
+          typename Op::frag x[TNV], w[TM];
+#pragma unroll
+          for (int t = 0; t < TNV; ++t)
+            x[t] = lds_frag16<T>(hs + pix[t] + ky * Cf::RS + kx * Cf::PS + half * 8);
+#pragma unroll
+          for (int mt = 0; mt < TM; ++mt)
+            w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, wm * 32 * TM + mt * 32 + l32, half));
+#pragma unroll
+          for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+            for (int t = 0; t < TNV; ++t) acc[mt][t] = Op::mma(w[mt], x[t], acc[mt][t]);
+        }
+      }
+      wait_vmem();
+      __syncthreads();
+    }
+  };
+  static_assert(TN == 4, "stage loop variants cover 0..4 tiles");
+  switch (tnv) {
+    case 4: stage_loop(std::integral_constant<int, 4>{}); break;
+    case 3: stage_loop(std::integral_constant<int, 3>{}); break;
+    case 2: stage_loop(std::integral_constant<int, 2>{}); break;
+    case 1: stage_loop(std::integral_constant<int, 1>{}); break;
+    default: stage_loop(std::integral_constant<int, 0>{}); break;
   }
 
   typedef T vec8_t __attribute__((ext_vector_type(8)));
@@ -780,7 +804,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
           const int p = it * 8 + (lane >> 3);
           const int key = (p & 7) ^ ((p >> 3) & 3);
           const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
-          const int idx = wn * 32 * TN + p;
+          const int idx = gtile(p >> 5) * 32 + (p & 31);
           const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
           if (oy < H && ox < W)
             *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
@@ -813,7 +837,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
       for (int it = 0; it < NCH / 2; ++it) {  // 32 pixels x NCH chunks over 64 lanes
         const int u = it * 64 + lane, p = u / NCH, ch = u % NCH;
         const vec8_t v = *(const vec8_t*)(stg + p * SROW + 8 * ch);
-        const int idx = wn * 32 * TN + t * 32 + p;
+        const int idx = gtile(t) * 32 + p;
         const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
         if (oy < H && ox < W) *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch) = v;
       }
