@@ -4,16 +4,25 @@
 //
 // A pre-pass rewrites each image pixel-interleaved, 4 bytes per pixel (R, G, B, 0), so that one
 // bilinear tap of all three channels is a single 4-byte load, and one image (3 MB at 768 x 1024) fits
-// an XCD's L2.  The builder then produces 4 consecutive plane pixels per thread and stores them as
-// one vector per channel; a wave covers 256 columns.  Workgroups are ordered so that each XCD works
-// through a contiguous range of images and planes.  The half-pixel source coordinate ((2 y + 1) H - h) / (2 h) is formed
-// exactly in 32-bit integers; only the blend is fp32.
+// an XCD's L2.  The builder then produces 4 plane pixels per thread, 64 columns apart, so that each
+// of a wave's gathers reads the taps of 64 consecutive pixels and each store writes 64 consecutive
+// pixels of a channel; a wave covers 256 columns.  Workgroups are ordered so that each XCD works
+// through a contiguous range of images and planes.  The half-pixel source coordinate
+// ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers; only the blend is fp32.
 #include "common.h"
 
 namespace dn {
 namespace {
 
-constexpr int PX = 4;  // consecutive plane pixels per thread
+#ifndef DN_BUILD_PX
+#define DN_BUILD_PX 4
+#endif
+#ifndef DN_BUILD_ROWS
+#define DN_BUILD_ROWS 16
+#endif
+constexpr int PX = DN_BUILD_PX;  // plane pixels per thread
+
+
 
 // floor(n / d) and the remainder for n, d < 2^32 with d > 0: a double-precision reciprocal estimate,
 // corrected to the exact quotient with integer arithmetic.
@@ -49,10 +58,12 @@ __device__ inline float border_weight(int d, int pad, bool ramp) {
 // and tabulates, per (cell, row), the two source rows, the row fraction and the row's border weight;
 // each lane computes its columns' source coordinates and border weights once and then only blends
 // per row.
-constexpr int TROWS = 16;                // rows per tile
+constexpr int TROWS = DN_BUILD_ROWS;     // rows per tile
+static_assert(16 % TROWS == 0 && TROWS % 4 == 0, "a tile's rows lie in one row of 16-px cells");
 constexpr int TCELLS = 64 * PX / 16;     // 16-px cells per tile row
 
-// Pixel image: pix[b][y][x] = R | G << 8 | B << 16, one thread per pixel.
+// Pixel image: pix[b][y][x] = R | G << 8 | B << 16, one thread per pixel (any width), or per 4 pixels
+// (width a multiple of 4: three 4-byte channel loads, one 16-byte store).
 __global__ __launch_bounds__(256) void pixel_image_kernel(const uint8_t* __restrict__ img, int H, int W,
                                                           uint32_t* __restrict__ pix) {
   const int x = blockIdx.x * 256 + threadIdx.x, y = blockIdx.y, b = blockIdx.z;
@@ -61,6 +72,22 @@ __global__ __launch_bounds__(256) void pixel_image_kernel(const uint8_t* __restr
   const uint8_t* row = img + (int64_t)b * 3 * HW + (int64_t)y * W;
   const uint32_t r0 = row[x], g0 = row[HW + x], b0 = row[2 * HW + x];
   pix[(int64_t)b * HW + (int64_t)y * W + x] = r0 | (g0 << 8) | (b0 << 16);
+}
+
+__global__ __launch_bounds__(256) void pixel_image4_kernel(const uint8_t* __restrict__ img, int H, int W,
+                                                           uint32_t* __restrict__ pix) {
+  const int x = 4 * (blockIdx.x * 256 + threadIdx.x), y = blockIdx.y, b = blockIdx.z;
+  if (x >= W) return;
+  const int64_t HW = (int64_t)H * W;
+  const uint8_t* row = img + (int64_t)b * 3 * HW + (int64_t)y * W + x;
+  const uint32_t r = *(const uint32_t*)row, g = *(const uint32_t*)(row + HW),
+                 bl = *(const uint32_t*)(row + 2 * HW);
+  uint4 o;
+  o.x = (r & 0xffu) | ((g & 0xffu) << 8) | ((bl & 0xffu) << 16);
+  o.y = ((r >> 8) & 0xffu) | (g & 0xff00u) | ((bl & 0xff00u) << 8);
+  o.z = ((r >> 16) & 0xffu) | ((g >> 8) & 0xff00u) | (bl & 0xff0000u);
+  o.w = (r >> 24) | ((g >> 16) & 0xff00u) | ((bl >> 8) & 0xff0000u);
+  *(uint4*)(pix + (int64_t)b * HW + (int64_t)y * W + x) = o;
 }
 
 struct RowEntry {
@@ -131,7 +158,6 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
                                                            PyrArgs a, PyrPlanes pl, BatchGeom bg,
                                                            T* __restrict__ out, int tiles_x,
                                                            int tiles_y) {
-  typedef T vec_t __attribute__((ext_vector_type(PX)));
   static_assert(TCELLS <= 256, "one owner search per thread");
   __shared__ int s_own[TCELLS];
   __shared__ PyrScale s_sc[TCELLS];  // owner's rectangle, per cell
@@ -215,27 +241,28 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   }
   __syncthreads();
 
-  // This lane's columns: owner, border weights, source columns and fractions.
-  const int x0 = tx0 + lane * PX, cell = lane * PX / 16;
-  const int owner = x0 < PW ? s_own[cell] : -1;
+  // This lane's columns x_i = tx0 + lane + 64 i: each gather instruction of a wave then reads the
+  // taps of 64 consecutive plane pixels (few cache lines), and each store writes 64 consecutive
+  // pixels of one channel.  Per column: its cell, border weight, source columns and fraction.
+  int cl[PX];
+  bool inside[PX];
   float wx[PX], lx[PX];
   uint32_t sx0[PX], sx1[PX];
 #pragma unroll
   for (int i = 0; i < PX; ++i) {
+    const int xl = lane + 64 * i, x = tx0 + xl;
+    cl[i] = xl >> 4;
+    inside[i] = x < PW;
     wx[i] = 0.f;
     lx[i] = 0.f;
     sx0[i] = sx1[i] = 0u;
-  }
-  if (owner >= 0) {
-    const PyrScale& s = s_sc[cell];
-    const double inv2w = 1.0 / (2.0 * s.w);
-#pragma unroll
-    for (int i = 0; i < PX; ++i) {
-      const int ux = x0 + i - s.x - a.pad;
+    if (inside[i] && s_own[cl[i]] >= 0) {
+      const PyrScale& s = s_sc[cl[i]];
+      const int ux = x - s.x - a.pad;
       const int dx = max(0, max(-ux, ux - (s.w - 1)));
-      wx[i] = x0 + i < PW ? border_weight(dx, a.pad, a.ramp) : 0.f;
+      wx[i] = border_weight(dx, a.pad, a.ramp);
       int c0, c1;  // c1 = min(c0 + 1, W - 1)
-      src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, inv2w, c0, c1, lx[i]);
+      src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, 1.0 / (2.0 * s.w), c0, c1, lx[i]);
       sx0[i] = (uint32_t)c0;
       sx1[i] = (uint32_t)c1;
     }
@@ -243,54 +270,39 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
   T* o = out + (BATCH ? (int64_t)j * 3 * PH * PW : (int64_t)b * pl.image_elems + pl.p[j].offset);
   const int64_t plane = (int64_t)PH * PW;
-  const bool vec_rows = (PW % PX) == 0;  // whole, aligned vectors (uniform per plane)
 
   // Rows wave, wave + 4, ... of the tile, unrolled so that the taps of several rows are in flight.
-  // Every lane reads its four taps per pixel (a pixel outside the scale's border reads valid pixels
-  // and gets weight 0), so the loads carry no per-pixel branch.
+  // Every pixel reads its four taps (background pixels and pixels outside a scale's border read valid
+  // pixels, with weight 0), so the loads carry no per-pixel branch.
 #pragma unroll
   for (int rr = 0; rr < TROWS / 4; ++rr) {
     const int r = wave + 4 * rr;
     const int y = ty0 + r;
     if (y >= PH) break;  // uniform per wave
-    const RowEntry re = s_row[cell * TROWS + r];
     float v[PX][3];
 #pragma unroll
-    for (int i = 0; i < PX; ++i) v[i][0] = v[i][1] = v[i][2] = 0.f;
-    if (owner >= 0 && re.wy != 0.f) {
-#pragma unroll
-      for (int i = 0; i < PX; ++i) {
-        const float wgt = re.wy * wx[i];
-        const uint32_t q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
-        const uint32_t q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
-#pragma unroll
-        for (int c = 0; c < 3; ++c) {
-          const int sh = 8 * c;
-          const float i00 = (float)((q00 >> sh) & 255u), i01 = (float)((q01 >> sh) & 255u);
-          const float i10 = (float)((q10 >> sh) & 255u), i11 = (float)((q11 >> sh) & 255u);
-          const float top = i00 + lx[i] * (i01 - i00), bot = i10 + lx[i] * (i11 - i10);
-          v[i][c] = (top + re.ly * (bot - top) - a.mean[c]) * wgt;
-        }
-      }
-    }
-    if (x0 >= PW) continue;
-    const int64_t at = (int64_t)y * PW + x0;
-    if (vec_rows) {
+    for (int i = 0; i < PX; ++i) {
+      const RowEntry re = s_row[cl[i] * TROWS + r];
+      const float wgt = re.wy * wx[i];
+      const uint32_t q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
+      const uint32_t q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
-        vec_t rv;
-#pragma unroll
-        for (int i = 0; i < PX; ++i) rv[i] = from_f32<T>(v[i][c]);
-        *(vec_t*)(o + c * plane + at) = rv;
+        const int sh = 8 * c;
+        const float i00 = (float)((q00 >> sh) & 255u), i01 = (float)((q01 >> sh) & 255u);
+        const float i10 = (float)((q10 >> sh) & 255u), i11 = (float)((q11 >> sh) & 255u);
+        const float top = i00 + lx[i] * (i01 - i00), bot = i10 + lx[i] * (i11 - i10);
+        v[i][c] = (top + re.ly * (bot - top) - a.mean[c]) * wgt;
       }
-    } else {
-#pragma unroll
-      for (int c = 0; c < 3; ++c)
-#pragma unroll
-        for (int i = 0; i < PX; ++i)
-          if (x0 + i < PW) o[c * plane + at + i] = from_f32<T>(v[i][c]);
     }
+    T* orow = o + (int64_t)y * PW + tx0 + lane;
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+#pragma unroll
+      for (int i = 0; i < PX; ++i)
+        if (inside[i]) orow[c * plane + 64 * i] = from_f32<T>(v[i][c]);
   }
+
 }
 
 }  // namespace
@@ -300,7 +312,10 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
                         uint8_t* d_scratch, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   uint32_t* pix = (uint32_t*)d_scratch;
-  pixel_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
+  if (a.W % 4 == 0)
+    pixel_image4_kernel<<<dim3((a.W / 4 + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
+  else
+    pixel_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
   const int tiles_x = (max_w + 64 * PX - 1) / (64 * PX), tiles_y = (max_h + TROWS - 1) / TROWS;
   const int64_t nblk = (int64_t)tiles_x * tiles_y * (batch ? batch->n_planes : n_img * pl.n);
   if (nblk > 0x7fffffff) return (int)hipErrorInvalidValue;
