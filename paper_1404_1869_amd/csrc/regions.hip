@@ -9,7 +9,8 @@
 // contraction off, in the same order as the definition, so the chosen scale and cell indices are
 // reproducible bit for bit on any IEEE fp64 implementation.  Samples of one bin read 4 cells x C
 // contiguous channels (coalesced); the descriptor row is transposed through LDS into its
-// channel-major order and written with coalesced stores.
+// channel-major order and written with coalesced non-temporal stores (the rows are not read back by
+// this path, so they need not displace the conv5 maps from the caches).
 #include "common.h"
 
 namespace dn {
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       f32x4 o;
 #pragma unroll
       for (int i = 0; i < 4; ++i) o[i] = s_row[(bin + i) * RSTR + c];
-      *(f32x4*)(dst + e) = o;
+      __builtin_nontemporal_store(o, (f32x4*)(dst + e));  // written once, not read back here
     }
   } else {
     for (int e = tid; e < C * SS; e += blockDim.x) {
