@@ -619,10 +619,17 @@ struct Pieces {  // 1 KB LDS pieces, rounded up to a whole number per wave
 // Wait until every vector-memory access of this wave has completed (vmcnt 0; other counters left
 // free), as an instruction the compiler's own wait bookkeeping sees.
 __device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Wait until at most N (< 16) vector-memory accesses of this wave are outstanding.
+template <int N>
+__device__ inline void wait_vmem_but() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
-__device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece, uint32_t voff) {
+__device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece, uint32_t voff,
+                                    uint32_t soff = 0) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds_piece,
-                                           16, voff, 0, 0, 0);
+                                           16, voff, soff, 0, 0);
 }
 
 template <typename T, int R, int BM, int TM, int OCC, int TS>
@@ -859,6 +866,8 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
 // fragments from LDS while k-step ks's MFMAs run.  A tile's outputs leave through LDS, as whole
 // pixel rows.
 // ------------------------------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 struct Conv1D {
   static constexpr int TH = 16, TW = 16, HR = 72;
   static constexpr int HSL = 10, HS = HSL * 8;  // halo row: slots, elements
@@ -868,6 +877,7 @@ struct Conv1D {
   static constexpr int HALO_E = NH * 512, W_E = NW * 512, STAGE_E = HALO_E + W_E;
   static constexpr int SROW = 104;  // epilogue staging: elements per pixel row (96 + 8 padding)
 };
+constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's epilogue
 static_assert(4 * 32 * Conv1D::SROW <= Conv1D::STAGE_E, "epilogue staging fits one stage buffer");
 static_assert(Conv1D::NH * 64 >= Conv1D::HR * Conv1D::HSL, "halo pieces cover the halo");
 static_assert(Conv1D::NW * 64 >= 96 * Conv1D::WSL, "weight pieces cover the weights");
@@ -883,8 +893,10 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   using hfrag = typename Op::half_frag;
   typedef T out4_t __attribute__((ext_vector_type(4)));
   typedef T vec8_t __attribute__((ext_vector_type(8)));
-  __shared__ __align__(1024) T s_mem[2 * P::STAGE_E];
-  __shared__ __align__(16) float s_bias[96];
+  // One LDS object: the stage buffers, then the biases.  (A second __shared__ array made the
+  // compiler wait for every in-flight direct load before each LDS read, serializing the stages.)
+  __shared__ __align__(1024) T s_mem[2 * P::STAGE_E + 2 * 96];
+  float* s_bias = (float*)(s_mem + 2 * P::STAGE_E);
   auto halo_buf = [&](int b) { return s_mem + b * P::STAGE_E; };
   auto w_buf = [&](int b) { return s_mem + b * P::STAGE_E + P::HALO_E; };
   if (threadIdx.x < 96) s_bias[threadIdx.x] = bias[threadIdx.x];
@@ -926,16 +938,15 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
     }
   };
   auto load = [&](int buf, int c) {
+    // The channel offset goes in the scalar offset, so the per-lane offsets stay in the same
+    // registers for the whole tile (a lane past the plane keeps an offset the hardware drops).
     const uint32_t ha = c * chan_bytes, wa = (uint32_t)(c * K1 * sizeof(T));
 #pragma unroll
     for (int i = 0; i < P::DH; ++i)
-      if (wave + 4 * i < P::NH)
-        lds_direct16(rsrc_in, halo_buf(buf) + (wave + 4 * i) * 512,
-                     hoff[i] == OOB ? OOB : hoff[i] + ha);
+      if (wave + 4 * i < P::NH) lds_direct16(rsrc_in, halo_buf(buf) + (wave + 4 * i) * 512, hoff[i], ha);
 #pragma unroll
     for (int i = 0; i < P::DW; ++i)
-      if (wave + 4 * i < P::NW)
-        lds_direct16(rsrc_w, w_buf(buf) + (wave + 4 * i) * 512, woff[i] == OOB ? OOB : woff[i] + wa);
+      if (wave + 4 * i < P::NW) lds_direct16(rsrc_w, w_buf(buf) + (wave + 4 * i) * 512, woff[i], wa);
   };
 
   // Lane bases: this lane's pixel (input row 4 prow + 2 half, column 4 pcol) per pixel tile, and its
@@ -998,10 +1009,15 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
       if (c == 2) {
         // Epilogue: bias + ReLU, staged per wave in the stage buffer just consumed (once every wave
         // has finished reading it), 32 pixels at a time with rows padded to 104 channels; then whole
-        // 192-byte pixel rows are written with 16-byte stores.
+        // 192-byte pixel rows are written with 16-byte buffer stores.  Every lane issues all of
+        // them (a pixel outside the map stores at an offset past the plane, which the hardware
+        // drops), so the wave has exactly EPI_STORES stores in flight after the next stage's loads,
+        // and the stage-end wait below lets them drain while the next tile computes.
         __syncthreads();
         const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
         T* dst = out + plane * out_stride;
+        const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)dst, 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)), 0x00020000);
         T* stg = halo_buf(buf) + wave * (32 * P::SROW);
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
@@ -1023,15 +1039,22 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
             const vec8_t v = *(const vec8_t*)(stg + p * P::SROW + 8 * ch);
             const int idx = wave * 64 + b * 32 + p;
             const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
-            if (oy < Ho && ox < Wo) *(vec8_t*)(dst + ((int64_t)oy * Wo + ox) * 96 + 8 * ch) = v;
+            const uint32_t off = oy < Ho && ox < Wo
+                                     ? (uint32_t)((((int64_t)oy * Wo + ox) * 96 + 8 * ch) * sizeof(T))
+                                     : OOB;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rsrc_out, off, 0, 0);
           }
         }
 #pragma unroll
         for (int a = 0; a < 3; ++a)
 #pragma unroll
           for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+        // Vector-memory operations retire in issue order: once no more than the epilogue's stores
+        // are outstanding, the next stage's loads (issued before them) have landed in LDS.
+        wait_vmem_but<EPI_STORES>();
+      } else {
+        wait_vmem();
       }
-      wait_vmem();
       __syncthreads();
     }
   }
@@ -1098,7 +1121,8 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
     } else {
       // Direct loads take 16-byte slots of plane rows at 32-bit byte offsets within one plane.
       const bool direct = P % 8 == 0 && in_stride % 8 == 0 && ((uintptr_t)in & 15) == 0 &&
-                          (int64_t)3 * H * P * (int64_t)sizeof(T) < 0x7fffffffLL;
+                          (int64_t)3 * H * P * (int64_t)sizeof(T) < 0x7fffffffLL &&
+                          (int64_t)Ho * Wo * 96 * (int64_t)sizeof(T) < 0x7fffffffLL;
       if (direct) {
         const int grid = (int)std::min<int64_t>(blocks, 2 * device_cu_count());
         conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
