@@ -27,6 +27,35 @@ __device__ inline float lrn_scale(float s, float alpha_n, float beta, float k) {
 }
 
 constexpr int VECB = 16;  // bytes per channel vector
+
+#ifndef DN_LRN96_CPT
+#define DN_LRN96_CPT 96
+#endif
+#ifndef DN_LRN96_TH
+#define DN_LRN96_TH 8
+#endif
+#ifndef DN_LRN96_TW
+#define DN_LRN96_TW 7
+#endif
+#ifndef DN_LRN96_WPE
+#define DN_LRN96_WPE 3
+#endif
+// Per-pixel kernel configurations for 16-bit storage (channels per thread, output tile rows and
+// columns, waves per SIMD), chosen by timing each layer on the 96-plane batch: C = 96 keeps a whole
+// pixel per thread; C = 256 splits a pixel over 4 threads, so a thread needs half the registers
+// and 4 waves per SIMD fit (lrn_pool2 0.40 -> 0.35 ms against 2 threads per pixel).
+#ifndef DN_LRN256_CPT
+#define DN_LRN256_CPT 64
+#endif
+#ifndef DN_LRN256_TH
+#define DN_LRN256_TH 3
+#endif
+#ifndef DN_LRN256_TW
+#define DN_LRN256_TW 4
+#endif
+#ifndef DN_LRN256_WPE
+#define DN_LRN256_WPE 4
+#endif
 constexpr int MAX_HALF = 8;
 
 template <typename T>
@@ -127,10 +156,10 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
   }
 }
 
-// LRN then pool for C = CPT * TPP channels (96 = 96 x 1, 256 = 128 x 2) with the default window
-// n = 5: every thread owns one input pixel's CPT consecutive channels.  It issues all of their
+// LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 64 x 4 at 16-bit storage, 128 x 2 at
+// fp32) with the default window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
 // 16-byte loads at once (plus one neighbouring vector on each inner side when a pixel is split over
-// two threads), forms the five-channel sums of squares from pair sums (four adds and one multiply per
+// several threads), forms the five-channel sums of squares from pair sums (four adds and one multiply per
 // element), and stores the LRN result to LDS.  Pixels of the tile outside the map are stored as
 // -inf, so every pooled output then takes the max over its full 3 x 3 window from LDS, unrolled, with
 // no clipping tests.  Channel count and tile shape are compile-time constants, so no index
@@ -342,7 +371,8 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
   // within 64 KB.
   if (lrn && hn == 2 && (C == 96 || C == 256)) {
     constexpr bool F32 = sizeof(T) == 4;
-    constexpr int TH96 = F32 ? 4 : 8, TW96 = 7, TH256 = F32 ? 2 : 4, TW256 = F32 ? 5 : 6;
+    constexpr int TH96 = F32 ? 4 : DN_LRN96_TH, TW96 = F32 ? 7 : DN_LRN96_TW, TH256 = F32 ? 2 : DN_LRN256_TH,
+                  TW256 = F32 ? 5 : DN_LRN256_TW;
     const int TPH = C == 96 ? TH96 : TH256, TPW = C == 96 ? TW96 : TW256;
     const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
@@ -350,10 +380,12 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
     // Waves per SIMD the LDS tile allows (3 and 2 workgroups of 4 waves per CU): the compiler may use
     // the registers that occupancy leaves free for more independent work in flight.
     if (C == 96)
-      lrn_pool_pixel_kernel<T, 96, 96, TH96, TW96, 3, false><<<(unsigned)blocks, 256, 0, s>>>(
+      lrn_pool_pixel_kernel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE, false>
+          <<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     else
-      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256, 2, true><<<(unsigned)blocks, 256, 0, s>>>(
+      lrn_pool_pixel_kernel<T, 256, F32 ? 128 : DN_LRN256_CPT, TH256, TW256, F32 ? 2 : DN_LRN256_WPE, true>
+          <<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     return (int)hipGetLastError();
   }
