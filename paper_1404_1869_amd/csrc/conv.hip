@@ -27,6 +27,11 @@ namespace {
 //   conv1: [96][3][144] in dtype, k = 16 s + 8 h + 4 j + e holds tap ky = 4 (s / 3) + 2 h + j,
 //          kx = 4 (s % 3) + e (zero where ky or kx is 11)
 //   conv2..5: [M][R*R][C/G] in dtype (tap-major, channels contiguous)
+//   conv2..5, 16-bit types, stage-major copy for conv_s1_direct_kernel: per channel block (group g,
+//          block of BM output channels) and stage (chunk of 16 input channels, kernel row ky), one
+//          contiguous block of R * BM * 2 16-byte pieces, piece (kx BM + m) 2 + p holding input
+//          channels 8 (p ^ ((m >> 4) & 1)) .. + 7 of the chunk at tap (ky, kx) of channel m: exactly
+//          the order of the LDS weight-row buffer, so each direct load reads 1 KB of contiguous memory
 //   biases: fp32 [M]
 // ------------------------------------------------------------------------------------------------
 constexpr int L_M[5] = {96, 256, 384, 384, 256};
@@ -61,6 +66,28 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, T* __restrict__ ou
   const int t = (int)((i / Cg) % RR);
   const int m = (int)(i / ((int64_t)Cg * RR));
   out[i] = from_f32<T>(w[((int64_t)m * Cg + c) * RR + t]);
+}
+
+template <typename T>
+__global__ void pack_stage_kernel(const float* __restrict__ w, T* __restrict__ out, int Mg, int Cg,
+                                  int R, int BM, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int e = (int)(i % 8), p = (int)((i / 8) % 2), m = (int)((i / 16) % BM);
+  int64_t r = i / (16 * (int64_t)BM);
+  const int kx = (int)(r % R);
+  r /= R;
+  const int ky = (int)(r % R);
+  r /= R;
+  const int nchunks = Cg / 16;
+  const int chunk = (int)(r % nchunks);
+  const int64_t blk = r / nchunks;  // channel block: group * (Mg / BM) + block within the group
+  const int mpg = Mg / BM;
+  const int g = (int)(blk / mpg), mb = (int)(blk % mpg);
+  const int v = p ^ ((m >> 4) & 1);
+  const int64_t oc = (int64_t)g * Mg + (int64_t)mb * BM + m;
+  const int c = chunk * 16 + v * 8 + e;
+  out[i] = from_f32<T>(w[((oc * Cg + c) * R + ky) * R + kx]);
 }
 
 __global__ void copy_f32_kernel(const float* __restrict__ a, float* __restrict__ b, int n) {
@@ -668,11 +695,12 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   const int g = mb / mpg, m0 = (mb % mpg) * BM;
   const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
   const T* src = in + plane * in_stride + g * Cg;
-  const T* wg = wp + ((int64_t)g * Mg + m0) * R * R * Cg;
+  // This channel block's stage-major weights: one contiguous block of WSLOTS 16-byte pieces per stage.
+  const T* wg = wp + (int64_t)mb * (Cg / Cf::CC) * R * (WSLOTS * 8);
   const __amdgpu_buffer_rsrc_t rsrc_in = __builtin_amdgcn_make_buffer_rsrc(
       (void*)src, 0, (int)(((int64_t)H * W * C - g * Cg) * sizeof(T)), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)wg, 0, (int)((int64_t)BM * R * R * Cg * sizeof(T)), 0x00020000);
+      (void*)wg, 0, (int)((int64_t)(Cg / Cf::CC) * R * WSLOTS * 16), 0x00020000);
   constexpr uint32_t OOB = 0x80000000u;
 
   const int tid = threadIdx.x;
@@ -700,10 +728,8 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   }
 #pragma unroll
   for (int i = 0; i < DW; ++i) {
-    const int q = (wave * DW + i) * 64 + lane;
-    const int kx = q / (2 * BM), r = q % (2 * BM), m = r / 2;
-    const int v = (r & 1) ^ ((m >> 4) & 1);
-    woff[i] = q < WSLOTS ? (uint32_t)((((int64_t)m * R * R + kx) * Cg + v * 8) * sizeof(T)) : OOB;
+    const int q = (wave * DW + i) * 64 + lane;  // piece q of a stage block lands in LDS slot q
+    woff[i] = q < WSLOTS ? (uint32_t)(q * 16) : OOB;
   }
   auto load_halo = [&](int buf, int c0) {
 #pragma unroll
@@ -711,8 +737,8 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
       lds_direct16(rsrc_in, halo_buf(buf) + (wave * DH + i) * 512,
                    hoff[i] == OOB ? OOB : hoff[i] + (uint32_t)(c0 * sizeof(T)));
   };
-  auto load_w = [&](int buf, int c0, int ky) {
-    const uint32_t add = (uint32_t)((ky * R * Cg + c0) * sizeof(T));
+  auto load_w = [&](int buf, int c0, int ky) {  // stage (chunk c0 / 16, kernel row ky)
+    const uint32_t add = (uint32_t)(((c0 / Cf::CC) * R + ky) * WSLOTS * 16);
 #pragma unroll
     for (int i = 0; i < DW; ++i)
       lds_direct16(rsrc_w, wrow_buf(buf) + (wave * DW + i) * 512, woff[i] == OOB ? OOB : woff[i] + add);
@@ -741,10 +767,13 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     __syncthreads();
     for (int st = 0; st < nst; ++st) {
       const int chunk = st / R, ky = st - chunk * R;
-      if (st + 1 < nst) load_w((st + 1) & 1, ((st + 1) / R) * Cf::CC, (st + 1) % R);
-      if (ky == 0 && chunk + 1 < nchunks) load_halo((chunk + 1) & 1, (chunk + 1) * Cf::CC);
+      const bool next_w = st + 1 < nst, next_h = ky == 0 && chunk + 1 < nchunks;
+      const int wbuf = (st + 1) & 1, wc0 = ((st + 1) / R) * Cf::CC, wky = (st + 1) % R;
+      const int hbuf = (chunk + 1) & 1, hc0 = (chunk + 1) * Cf::CC;
       const T* hs = halo_buf(chunk & 1);
       const T* ws = wrow_buf(st & 1);
+      if (next_w) load_w(wbuf, wc0, wky);
+      if (next_h) load_halo(hbuf, hc0);
       if constexpr (TNV > 0) {
 #pragma unroll
         for (int kx = 0; kx < R; ++kx) {
@@ -1061,8 +1090,8 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
 }
 
 template <typename T, int R, int BM, int TM, int OCC, int TS>
-int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int H, int W, int C,
-                int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
+int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, int n, int H,
+                int W, int C, int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
   using Cf = ConvCfg<T, R, BM, TM, TS>;
   const int Cg = C / G, Mg = M / G;
   const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
@@ -1076,8 +1105,9 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
   } else {
     // buffer descriptors address one plane with 32-bit byte offsets
     if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
+    if (wstage == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
     conv_s1_direct_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(
-        in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+        in, out, wstage, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   }
   return (int)hipGetLastError();
 }
@@ -1102,6 +1132,14 @@ int run_conv_s1(const T* in, T* out, const T* wp, const float* bias, int n, int 
 #define DN_CONV4_CFG 192, 3, 2, 1616
 #endif
 
+template <int BM_, int TM_, int OCC_, int TS_>
+struct CfgBM {
+  static constexpr int BM = BM_;
+};
+// Channel block of the direct-load kernel per layer (the stage-major weight copy is cut in these).
+constexpr int L_BM[5] = {0, CfgBM<DN_CONV2_CFG>::BM, CfgBM<DN_CONV3_CFG>::BM, CfgBM<DN_CONV4_CFG>::BM,
+                         CfgBM<DN_CONV5_CFG>::BM};
+
 template <typename T>
 int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
                   int32_t P, const void* d_packed, void* d_out, int64_t out_stride, const PackedLayout& L,
@@ -1109,6 +1147,8 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
   const T* wp = (const T*)((const char*)d_packed + L.w_off[layer - 1]);
+  // conv2..5 with 16-bit storage stream the stage-major copy
+  const T* ws = layer > 1 && L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
   const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
   if (layer == 1) {
     const int Ho = (H - 11) / 4 + 1, Wo = (W - 11) / 4 + 1;
@@ -1138,16 +1178,16 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
   const int li = layer - 1;
   switch (layer) {
     case 2:
-      return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+      return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 3:
-      return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+      return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 5:
-      return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+      return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 4:
-      return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, bias, n, H, W, L_C[li], L_G[li], L_M[li],
+      return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
   }
   return (int)hipErrorInvalidValue;
@@ -1168,6 +1208,12 @@ PackedLayout packed_layout(dn_dtype dt) {
   for (int l = 0; l < 5; ++l) {
     L.b_off[l] = off;
     off = align256(off + (size_t)L_M[l] * 4);
+  }
+  for (int l = 0; l < 5; ++l) {
+    L.s_off[l] = 0;
+    if (l == 0 || dt == DN_F32) continue;
+    L.s_off[l] = off;
+    off = align256(off + (size_t)L_M[l] * (L_C[l] / L_G[l]) * L_R[l] * L_R[l] * es);
   }
   L.total = off;
   return L;
@@ -1197,6 +1243,16 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
         pack_conv_kernel<__bf16><<<nb, 256, 0, s>>>(d_w[l], (__bf16*)dst, L_M[l], Cg, RR);
     }
     copy_f32_kernel<<<(L_M[l] + 255) / 256, 256, 0, s>>>(d_b[l], (float*)(base + L.b_off[l]), L_M[l]);
+    if (L.s_off[l]) {
+      const int Cg = L_C[l] / L_G[l], Mg = L_M[l] / L_G[l];
+      const int64_t n = (int64_t)L_M[l] * Cg * L_R[l] * L_R[l];
+      const unsigned nb = (unsigned)((n + 255) / 256);
+      void* sd = base + L.s_off[l];
+      if (dt == DN_F16)
+        pack_stage_kernel<_Float16><<<nb, 256, 0, s>>>(d_w[l], (_Float16*)sd, Mg, Cg, L_R[l], L_BM[l], n);
+      if (dt == DN_BF16)
+        pack_stage_kernel<__bf16><<<nb, 256, 0, s>>>(d_w[l], (__bf16*)sd, Mg, Cg, L_R[l], L_BM[l], n);
+    }
   }
   return (int)hipGetLastError();
 }
