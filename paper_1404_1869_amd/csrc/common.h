@@ -101,9 +101,9 @@ int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t 
                         const int32_t* d_box_img, int32_t n, int32_t S, int32_t pitch, const float* mean,
                         dn_dtype dt, void* d_out, void* stream);
 
-// Packed weight blob: offsets in bytes of each layer's weights and fp32 biases, and (16-bit types,
-// layers 2..5) of a second, stage-major copy of the weights that the direct-load conv kernel streams
-// as contiguous blocks (0 when absent).
+// Packed weight blob: offsets in bytes of each layer's weights and fp32 biases, and (16-bit types)
+// of a second, stage-major copy of the weights that the direct-load conv kernels stream as
+// contiguous blocks (0 when absent).
 struct PackedLayout {
   size_t w_off[5], b_off[5], s_off[5], total;
 };

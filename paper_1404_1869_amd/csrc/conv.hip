@@ -68,6 +68,18 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, T* __restrict__ ou
   out[i] = from_f32<T>(w[((int64_t)m * Cg + c) * RR + t]);
 }
 
+// conv1, 16-bit types: per input channel c a contiguous block of 96 x 18 16-byte pieces in the order
+// of conv1_direct_kernel's LDS weight buffer: piece 18 m + p holds k = 8 (p ^ ((m >> 4) & 1)) .. + 7
+// of channel m.  Read from the plain packed weights.
+template <typename T>
+__global__ void pack_conv1_stage_kernel(const T* __restrict__ plain, T* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 96 * 3 * K1) return;
+  const int c = i / (96 * K1), r = i % (96 * K1), m = r / K1, j = r % K1;
+  const int v = (j / 8) ^ ((m >> 4) & 1);
+  out[i] = plain[(m * 3 + c) * K1 + 8 * v + j % 8];
+}
+
 template <typename T>
 __global__ void pack_stage_kernel(const float* __restrict__ w, T* __restrict__ out, int Mg, int Cg,
                                   int R, int BM, int64_t n) {
@@ -936,6 +948,7 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   const int G = gridDim.x, xcd = blockIdx.x % 8, per = G / 8, rem = G % 8;
   const int rank = xcd * per + min(xcd, rem) + blockIdx.x / 8;
   const int ntile = rank < ntiles ? (ntiles - rank + G - 1) / G : 0;
+  // wp: the stage-major weights, one contiguous block of 96 x WSL pieces per input channel.
   const __amdgpu_buffer_rsrc_t rsrc_w =
       __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(96 * 3 * K1 * sizeof(T)), 0x00020000);
   constexpr uint32_t OOB = 0x80000000u;
@@ -947,9 +960,8 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   uint32_t hoff[P::DH], woff[P::DW];
 #pragma unroll
   for (int i = 0; i < P::DW; ++i) {
-    const int q = (wave + 4 * i) * 64 + lane;
-    const int m = q / P::WSL, v = (q % P::WSL) ^ ((m >> 4) & 1);
-    woff[i] = m < 96 ? (uint32_t)((m * 3 * K1 + 8 * v) * sizeof(T)) : OOB;
+    const int q = (wave + 4 * i) * 64 + lane;  // piece q of a channel's block lands in LDS slot q
+    woff[i] = q < 96 * P::WSL ? (uint32_t)(q * 16) : OOB;
   }
   __amdgpu_buffer_rsrc_t rsrc_in;
   auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of tile t
@@ -969,7 +981,7 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
   auto load = [&](int buf, int c) {
     // The channel offset goes in the scalar offset, so the per-lane offsets stay in the same
     // registers for the whole tile (a lane past the plane keeps an offset the hardware drops).
-    const uint32_t ha = c * chan_bytes, wa = (uint32_t)(c * K1 * sizeof(T));
+    const uint32_t ha = c * chan_bytes, wa = (uint32_t)(c * 96 * K1 * sizeof(T));
 #pragma unroll
     for (int i = 0; i < P::DH; ++i)
       if (wave + 4 * i < P::NH) lds_direct16(rsrc_in, halo_buf(buf) + (wave + 4 * i) * 512, hoff[i], ha);
@@ -1147,8 +1159,8 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
   const T* wp = (const T*)((const char*)d_packed + L.w_off[layer - 1]);
-  // conv2..5 with 16-bit storage stream the stage-major copy
-  const T* ws = layer > 1 && L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
+  // the direct-load kernels (16-bit storage) stream the stage-major copy
+  const T* ws = L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
   const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
   if (layer == 1) {
     const int Ho = (H - 11) / 4 + 1, Wo = (W - 11) / 4 + 1;
@@ -1165,7 +1177,8 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
                           (int64_t)Ho * Wo * 96 * (int64_t)sizeof(T) < 0x7fffffffLL;
       if (direct) {
         const int grid = (int)std::min<int64_t>(blocks, 2 * device_cu_count());
-        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
+        if (ws == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
+        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, ws, bias, H, W, P, Ho, Wo, in_stride,
                                                    out_stride, tiles_x, tiles_y, (int)blocks);
       } else {
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
@@ -1211,9 +1224,10 @@ PackedLayout packed_layout(dn_dtype dt) {
   }
   for (int l = 0; l < 5; ++l) {
     L.s_off[l] = 0;
-    if (l == 0 || dt == DN_F32) continue;
+    if (dt == DN_F32) continue;
     L.s_off[l] = off;
-    off = align256(off + (size_t)L_M[l] * (L_C[l] / L_G[l]) * L_R[l] * L_R[l] * es);
+    off = align256(off + (l == 0 ? (size_t)96 * 3 * K1
+                                  : (size_t)L_M[l] * (L_C[l] / L_G[l]) * L_R[l] * L_R[l]) * es);
   }
   L.total = off;
   return L;
@@ -1243,7 +1257,14 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
         pack_conv_kernel<__bf16><<<nb, 256, 0, s>>>(d_w[l], (__bf16*)dst, L_M[l], Cg, RR);
     }
     copy_f32_kernel<<<(L_M[l] + 255) / 256, 256, 0, s>>>(d_b[l], (float*)(base + L.b_off[l]), L_M[l]);
-    if (L.s_off[l]) {
+    if (L.s_off[l] && l == 0) {
+      const int n = 96 * 3 * K1;
+      void* sd = base + L.s_off[0];
+      if (dt == DN_F16)
+        pack_conv1_stage_kernel<_Float16><<<(n + 255) / 256, 256, 0, s>>>((const _Float16*)dst, (_Float16*)sd);
+      if (dt == DN_BF16)
+        pack_conv1_stage_kernel<__bf16><<<(n + 255) / 256, 256, 0, s>>>((const __bf16*)dst, (__bf16*)sd);
+    } else if (L.s_off[l]) {
       const int Cg = L_C[l] / L_G[l], Mg = L_M[l] / L_G[l];
       const int64_t n = (int64_t)L_M[l] * Cg * L_R[l] * L_R[l];
       const unsigned nb = (unsigned)((n + 255) / 256);
