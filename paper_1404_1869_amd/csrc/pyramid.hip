@@ -11,6 +11,8 @@
 // ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers; only the blend is fp32.
 #include "common.h"
 
+#include <type_traits>
+
 namespace dn {
 namespace {
 
@@ -153,7 +155,11 @@ __device__ inline bool valid_item(const dn_scale_geom& g, const BatchGeom& bg) {
 
 // BATCH = false: planes of each image (a.s, pl), blocks z = image * pl.n + plane.  BATCH = true: the
 // planes of a cross-image packed batch (bg), blocks z = plane, each cell sampling its owner's image.
-template <typename T, bool BATCH>
+// Two consecutive pixels of the pixel image: 4-byte aligned (a dword-aligned 8-byte load).
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
+
+// PAIR (source width at least 2): the two taps of a source row are one 8-byte load.
+template <typename T, bool BATCH, bool PAIR>
 __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __restrict__ pix,
                                                            PyrArgs a, PyrPlanes pl, BatchGeom bg,
                                                            T* __restrict__ out, int tiles_x,
@@ -263,6 +269,12 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       wx[i] = border_weight(dx, a.pad, a.ramp);
       int c0, c1;  // c1 = min(c0 + 1, W - 1)
       src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, 1.0 / (2.0 * s.w), c0, c1, lx[i]);
+      // On the last source column (c1 = c0) the pair starts one column earlier with fraction 1:
+      // a + 1 (b - a) is exactly b for these small integers, the value the clamped tap gives.
+      if (PAIR && c1 == c0) {
+        c0 -= 1;
+        lx[i] = 1.f;
+      }
       sx0[i] = (uint32_t)c0;
       sx1[i] = (uint32_t)c1;
     }
@@ -284,8 +296,14 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     for (int i = 0; i < PX; ++i) {
       const RowEntry re = s_row[cl[i] * TROWS + r];
       const float wgt = re.wy * wx[i];
-      const uint32_t q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
-      const uint32_t q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
+      uint32_t q00, q01, q10, q11;
+      if constexpr (PAIR) {
+        const u32x2 t = *(const u32x2*)(P + re.r0 + sx0[i]), u = *(const u32x2*)(P + re.r1 + sx0[i]);
+        q00 = t.x, q01 = t.y, q10 = u.x, q11 = u.y;
+      } else {
+        q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
+        q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
+      }
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         const int sh = 8 * c;
@@ -331,12 +349,19 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
     bg.first = first;
     bg.list = list;
   }
-  auto go = [&](auto tag) {
+  auto go2 = [&](auto tag, auto pair) {
     using T = decltype(tag);
+    constexpr bool PAIR = decltype(pair)::value;
     if (batch)
-      build_planes_kernel<T, true><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+      build_planes_kernel<T, true, PAIR><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
     else
-      build_planes_kernel<T, false><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+      build_planes_kernel<T, false, PAIR><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+  };
+  auto go = [&](auto tag) {
+    if (a.W >= 2)
+      go2(tag, std::true_type{});
+    else
+      go2(tag, std::false_type{});
   };
   switch (dt) {
     case DN_F32: go(float{}); break;

@@ -80,6 +80,27 @@ def test_planes_strongly_reduced_wide_image(D, W, dt):
             assert np.all(np.abs(got - ref[j]) <= 0.5 * ulp(ref[j], dt) + 1e-3), f"plane {j}"
 
 
+@pytest.mark.parametrize("W", [1, 2, 3])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_planes_narrow_images(D, W, dt):
+    """Images 1-3 px wide, upscaled up to 40x: every plane column samples the last source column
+    (the clamped tap), with the two taps of a row loaded separately (W = 1) or as one pair."""
+    H = 5
+    img = synth.image(93 + W, H, W)
+    p = D.pyramid_params(3, 2, base_scale=40.0, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=256,
+                         plane_w=192, mean=synth.IMAGENET_MEAN)
+    planes, plan = D.densenet_build_pyramid(torch.from_numpy(img).cuda()[None], p, DTS[dt])
+    op = oracle.plan(H, W, 3, 2, 40.0, 0, 16, 256, 192)
+    ref = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    assert len(plan.planes) == op.n_planes
+    for j, d in enumerate(plan.planes):
+        got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        if dt == "f32":
+            assert np.max(np.abs(got - ref[j])) <= 1e-5 * 255, f"plane {j}"
+        else:
+            assert np.all(np.abs(got - ref[j]) <= 0.5 * ulp(ref[j], dt) + 1e-3), f"plane {j}"
+
+
 def test_smallest_plane_with_a_conv5_cell(D):
     # a 1 x 1 image with 13 px of zero padding is a 27 x 27 plane: conv5 is 1 x 1
     img = synth.image(5, 1, 1)
