@@ -69,7 +69,7 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, T* __restrict__ ou
 }
 
 // conv1, 16-bit types: per input channel c a contiguous block of 96 x 18 16-byte pieces in the order
-// of conv1_direct_kernel's LDS weight buffer: piece 18 m + p holds k = 8 (p ^ ((m >> 4) & 1)) .. + 7
+// of conv1_resident_kernel's LDS weights: piece 18 m + p holds k = 8 (p ^ ((m >> 4) & 1)) .. + 7
 // of channel m.  Read from the plain packed weights.
 template <typename T>
 __global__ void pack_conv1_stage_kernel(const T* __restrict__ plain, T* __restrict__ out) {
@@ -893,112 +893,112 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   }
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's epilogue
+
 // ------------------------------------------------------------------------------------------------
 // conv1 for 16-bit storage with direct global->LDS loads (plane width a multiple of 8, 16-byte
-// aligned planes).  Output tiles of 16 x 16 pixels x 96 channels; a workgroup of 4 waves (96 channels
-// x 64 pixels each) walks tiles with the grid's stride, and two workgroups share a CU (78 KB of LDS
-// each).  A stage is one input channel of one tile: its 72 x 72 input halo (each row nine 16-byte
-// slots of plane data and one zero slot) and its 96 x 144 packed weights (18 slots per output
-// channel; for channels 16..31 of every 32-channel group the two slots of each 32-byte pair are
-// swapped, so that the 32 lanes of a half-wave reading one k-step's 16 bytes of 32 channels hit
-// distinct slots modulo 512 bytes).  Stages run back to back across tiles: the next stage (next
-// channel, or the first channel of the workgroup's next tile) loads while the current one computes,
-// with one vmcnt wait and one barrier per stage; within a stage, each wave reads k-step ks + 1's
-// fragments from LDS while k-step ks's MFMAs run.  A tile's outputs leave through LDS, as whole
-// pixel rows.
+// aligned planes), weights resident, one independent pipeline per wave.  A workgroup of 8 waves (one
+// per CU, two waves per SIMD) loads all three input channels' stage-major weights (81 KB) into LDS
+// once: per output channel 18 slots of 16 bytes (k = 144 per input channel), the two slots of each
+// 32-byte pair swapped for channels 16..31 of every 32-channel group, so that the 32 lanes of a
+// half-wave reading one k-step's 16 bytes of 32 channels hit distinct slots modulo 512 bytes.  After
+// that every wave is its own worker with no workgroup barrier: it walks wave tiles of 4 x 16 output
+// pixels x 96 channels, and per stage (one input channel of one tile) loads the tile's 24 x 72 input
+// halo (rows of nine 16-byte slots of plane data and one zero slot) into one of its two private LDS
+// buffers while it computes the previous stage from the other, reading k-step ks + 1's fragments
+// while k-step ks's MFMAs run.  A wave that writes out a tile, or waits for a load, stalls only
+// itself; the other wave on its SIMD keeps the MFMAs busy.  A tile's outputs leave through LDS, as
+// whole 192-byte pixel rows.
 // ------------------------------------------------------------------------------------------------
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-struct Conv1D {
-  static constexpr int TH = 16, TW = 16, HR = 72;
-  static constexpr int HSL = 10, HS = HSL * 8;  // halo row: slots, elements
-  static constexpr int WSL = K1 / 8;            // weight slots per output channel
-  static constexpr int NH = 12, NW = 27;        // 1 KB load pieces per stage: halo, weights
-  static constexpr int DH = (NH + 3) / 4, DW = (NW + 3) / 4;  // pieces per wave, at most
-  static constexpr int HALO_E = NH * 512, W_E = NW * 512, STAGE_E = HALO_E + W_E;
-  static constexpr int SROW = 104;  // epilogue staging: elements per pixel row (96 + 8 padding)
+struct Conv1R {
+  static constexpr int TH = 4, TW = 16, HR = 4 * (TH - 1) + 12;  // wave tile; halo rows (k rows 0..11)
+  static constexpr int HSL = 10, HS = HSL * 8;   // halo row: slots, elements
+  static constexpr int WSL = K1 / 8;             // weight slots per output channel
+  static constexpr int NH = (HR * HSL + 63) / 64, NW = 27;  // 1 KB pieces: a halo, a channel's weights
+  static constexpr int DWL = (3 * NW + 7) / 8;   // weight pieces per wave (all channels, once)
+  static constexpr int HALO_E = NH * 512, WCH_E = NW * 512;
+  static constexpr int SROW = 104, SPX = 16;     // staging: elements per pixel row, pixels per round
+  static constexpr int HALO_OFF = 3 * WCH_E, BIAS_OFF = HALO_OFF + 8 * 2 * HALO_E;
+  static constexpr int LDS_E = BIAS_OFF + 2 * 96;  // the biases as 96 floats
 };
-constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's epilogue
-static_assert(4 * 32 * Conv1D::SROW <= Conv1D::STAGE_E, "epilogue staging fits one stage buffer");
-static_assert(Conv1D::NH * 64 >= Conv1D::HR * Conv1D::HSL, "halo pieces cover the halo");
-static_assert(Conv1D::NW * 64 >= 96 * Conv1D::WSL, "weight pieces cover the weights");
+static_assert(Conv1R::NW * 64 == 96 * Conv1R::WSL, "a channel's weights are whole pieces");
+static_assert(Conv1R::SPX * Conv1R::SROW <= Conv1R::HALO_E, "epilogue staging fits a halo buffer");
+static_assert((size_t)Conv1R::LDS_E * 2 <= 160 * 1024, "one workgroup's LDS fits the CU");
+
+// Keeps the compiler from moving this wave's LDS accesses across it (a wave's own LDS operations
+// execute in order).
+__device__ inline void wave_lds_order() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
 
 template <typename T>
-__global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
+__global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
-  using P = Conv1D;
+  using P = Conv1R;
   using Op = Mfma<T>;
   using frag = typename Op::frag;
   using hfrag = typename Op::half_frag;
   typedef T out4_t __attribute__((ext_vector_type(4)));
   typedef T vec8_t __attribute__((ext_vector_type(8)));
-  // One LDS object: the stage buffers, then the biases.  (A second __shared__ array made the
-  // compiler wait for every in-flight direct load before each LDS read, serializing the stages.)
-  __shared__ __align__(1024) T s_mem[2 * P::STAGE_E + 2 * 96];
-  float* s_bias = (float*)(s_mem + 2 * P::STAGE_E);
-  auto halo_buf = [&](int b) { return s_mem + b * P::STAGE_E; };
-  auto w_buf = [&](int b) { return s_mem + b * P::STAGE_E + P::HALO_E; };
+  __shared__ __align__(1024) T s_mem[P::LDS_E];
+  float* s_bias = (float*)(s_mem + P::BIAS_OFF);
   if (threadIdx.x < 96) s_bias[threadIdx.x] = bias[threadIdx.x];
-
-  // XCD-aware rank: workgroups are dispatched round-robin over the 8 XCDs; rank r of XCD x is
-  // x * (workgroups per XCD) + i, and rank r takes tiles r, r + G, ..., so the tiles in flight on
-  // one XCD at a time are neighbours and share its L2.
-  const int G = gridDim.x, xcd = blockIdx.x % 8, per = G / 8, rem = G % 8;
-  const int rank = xcd * per + min(xcd, rem) + blockIdx.x / 8;
-  const int ntile = rank < ntiles ? (ntiles - rank + G - 1) / G : 0;
-  // wp: the stage-major weights, one contiguous block of 96 x WSL pieces per input channel.
-  const __amdgpu_buffer_rsrc_t rsrc_w =
-      __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(96 * 3 * K1 * sizeof(T)), 0x00020000);
-  constexpr uint32_t OOB = 0x80000000u;
-  const uint32_t chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  // This lane's slot in each of its wave's pieces (piece wave + 4 i): byte offsets for channel 0.
-  uint32_t hoff[P::DH], woff[P::DW];
+  constexpr uint32_t OOB = 0x80000000u;
+
+  // Workers: workgroups are dispatched round-robin over the 8 XCDs, and rank r = x * (workgroups
+  // per XCD) + i of XCD x has the workers 8 r .. 8 r + 7; worker w takes wave tiles w, w + 8 G, ...:
+  // the workers in flight on one XCD hold neighbouring tiles, whose halos overlap in its L2.
+  const int G = gridDim.x, xcd = blockIdx.x % 8, per = G / 8, rem = G % 8;
+  const int rank = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int NWK = 8 * G, wk = 8 * rank + wave;
+  const int ntile = wk < ntiles ? (ntiles - wk + NWK - 1) / NWK : 0;
+
+  // All weights, once: piece q of the stage-major blob lands in LDS piece q.
+  {
+    const __amdgpu_buffer_rsrc_t rsrc_w =
+        __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(3 * 96 * K1 * sizeof(T)), 0x00020000);
 #pragma unroll
-  for (int i = 0; i < P::DW; ++i) {
-    const int q = (wave + 4 * i) * 64 + lane;  // piece q of a channel's block lands in LDS slot q
-    woff[i] = q < 96 * P::WSL ? (uint32_t)(q * 16) : OOB;
+    for (int i = 0; i < P::DWL; ++i) {
+      const int q = wave + 8 * i;
+      if (q < 3 * P::NW) lds_direct16(rsrc_w, s_mem + q * 512, (uint32_t)(q * 1024 + lane * 16));
+    }
   }
+  const uint32_t chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
+  auto hbuf = [&](int b) { return s_mem + P::HALO_OFF + (2 * wave + b) * P::HALO_E; };
+  uint32_t hoff[P::NH];
   __amdgpu_buffer_rsrc_t rsrc_in;
-  auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of tile t
+  auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of wave tile t
     const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
     rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + plane * in_stride), 0,
                                                 (int)(3 * chan_bytes), 0x00020000);
     const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
 #pragma unroll
-    for (int i = 0; i < P::DH; ++i) {
-      const int q = (wave + 4 * i) * 64 + lane;
+    for (int i = 0; i < P::NH; ++i) {
+      const int q = i * 64 + lane;
       const int row = q / P::HSL, r = q % P::HSL;
       const int iy = iy0 + row, ix = ix0 + 8 * r;
       const bool ok = row < P::HR && r < 9 && iy < H && ix < W;
       hoff[i] = ok ? (uint32_t)(((int64_t)iy * pitch + ix) * sizeof(T)) : OOB;
     }
   };
-  auto load = [&](int buf, int c) {
-    // The channel offset goes in the scalar offset, so the per-lane offsets stay in the same
-    // registers for the whole tile (a lane past the plane keeps an offset the hardware drops).
-    const uint32_t ha = c * chan_bytes, wa = (uint32_t)(c * 96 * K1 * sizeof(T));
+  auto load_halo = [&](int b, int c) {  // channel c of the current tile into buffer b
 #pragma unroll
-    for (int i = 0; i < P::DH; ++i)
-      if (wave + 4 * i < P::NH) lds_direct16(rsrc_in, halo_buf(buf) + (wave + 4 * i) * 512, hoff[i], ha);
-#pragma unroll
-    for (int i = 0; i < P::DW; ++i)
-      if (wave + 4 * i < P::NW) lds_direct16(rsrc_w, w_buf(buf) + (wave + 4 * i) * 512, woff[i], wa);
+    for (int i = 0; i < P::NH; ++i) lds_direct16(rsrc_in, hbuf(b) + i * 512, hoff[i], c * chan_bytes);
   };
 
-  // Lane bases: this lane's pixel (input row 4 prow + 2 half, column 4 pcol) per pixel tile, and its
-  // output channel's weight row at slot (half ^ swap); every k-step adds an offset common to all lanes.
   int lpix[2];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
-    const int idx = wave * 64 + b * 32 + l32;
+    const int idx = b * 32 + l32;
     lpix[b] = (4 * (idx / P::TW) + 2 * half) * P::HS + 4 * (idx % P::TW);
   }
   const int lw = 8 * (P::WSL * l32 + (half ^ ((l32 >> 4) & 1)));
+  // Lane bases: this lane's pixel (input row 4 prow + 2 half, column 4 pcol) per pixel tile, and its
+  // output channel's weight row at slot (half ^ swap); every k-step adds an offset common to all lanes.
   auto read = [&](const T* hs, const T* ws, int ks, frag* x, frag* w) {
     // k-step ks: rows ky, ky + 1 (ky = 4 (ks / 3) + 2 half), columns 4 (ks % 3) + 0..3
     const int o0 = 4 * (ks / 3) * P::HS + 4 * (ks % 3);
@@ -1019,84 +1019,90 @@ __global__ __launch_bounds__(256, 2) void conv1_direct_kernel(
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
 
   if (ntile > 0) {
-    set_tile(rank);
-    load(0, 0);
+    set_tile(wk);
+    load_halo(0, 0);
   }
   wait_vmem();
-  __syncthreads();
-  for (int j = 0; j < ntile; ++j) {
-    const int t = rank + j * G;
-#pragma unroll
-    for (int c = 0; c < 3; ++c) {
-      const int buf = (j + c) & 1;  // stage 3 j + c
-      if (c < 2) {
-        load(buf ^ 1, c + 1);
-      } else if (j + 1 < ntile) {
-        set_tile(t + G);
-        load(buf ^ 1, 0);
-      }
-      const T* hs = halo_buf(buf);
-      const T* ws = w_buf(buf);
+  __syncthreads();  // weights and biases are in LDS; from here on each wave runs on its own
+  for (int st = 0; st < 3 * ntile; ++st) {
+    const int j = st / 3, c = st - 3 * j;  // tile j of this worker, input channel c
+    if (st + 1 < 3 * ntile) {
+      const int nj = (st + 1) / 3, nc = st + 1 - 3 * nj;
+      if (nc == 0) set_tile(wk + nj * NWK);
+      load_halo((st + 1) & 1, nc);
+    }
+    T* hs = hbuf(st & 1);
+    const T* ws = s_mem + c * P::WCH_E;
+    {
       frag xr[2][2], wr[2][3];
       read(hs, ws, 0, xr[0], wr[0]);
 #pragma unroll
       for (int ks = 0; ks < K1 / 16; ++ks) {
         if (ks + 1 < K1 / 16) read(hs, ws, ks + 1, xr[(ks + 1) & 1], wr[(ks + 1) & 1]);
+        // raised wave priority while this k-step's MFMAs issue: the SIMD's other wave then issues
+        // its LDS reads, loads and epilogue work in between rather than ahead of them
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
           for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[ks & 1][mt], xr[ks & 1][b], acc[mt][b]);
+        __builtin_amdgcn_s_setprio(0);
       }
-      if (c == 2) {
-        // Epilogue: bias + ReLU, staged per wave in the stage buffer just consumed (once every wave
-        // has finished reading it), 32 pixels at a time with rows padded to 104 channels; then whole
-        // 192-byte pixel rows are written with 16-byte buffer stores.  Every lane issues all of
-        // them (a pixel outside the map stores at an offset past the plane, which the hardware
-        // drops), so the wave has exactly EPI_STORES stores in flight after the next stage's loads,
-        // and the stage-end wait below lets them drain while the next tile computes.
-        __syncthreads();
-        const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
-        T* dst = out + plane * out_stride;
-        const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)dst, 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)), 0x00020000);
-        T* stg = halo_buf(buf) + wave * (32 * P::SROW);
+    }
+    if (c == 2) {
+      // Epilogue of the tile: bias + ReLU; per 32-pixel MFMA tile, two rounds of 16 pixels staged
+      // in the halo buffer just consumed (rows of 104 channels), read back as whole pixel rows and
+      // written with 16-byte buffer stores that every lane issues (a pixel outside the map stores at
+      // an offset past the plane, which the hardware drops): EPI_STORES stores per lane.
+      const int t = wk + j * NWK;
+      const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
+      const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(out + plane * out_stride), 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)), 0x00020000);
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < 2; ++b) {
+        out4_t v[3][4];
 #pragma unroll
-          for (int mt = 0; mt < 3; ++mt)
+        for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int m = mt * 32 + 8 * q + 4 * half;
-              const f32x4 bv = *(const f32x4*)(s_bias + m);
-              out4_t v;
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 bv = *(const f32x4*)(s_bias + mt * 32 + 8 * q + 4 * half);
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                v[e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
-              *(out4_t*)(stg + l32 * P::SROW + m) = v;
-            }
+            for (int e = 0; e < 4; ++e) v[mt][q][e] = from_f32<T>(fmaxf(acc[mt][b][4 * q + e] + bv[e], 0.f));
+          }
 #pragma unroll
-          for (int it = 0; it < 6; ++it) {  // 32 pixels x 12 chunks of 8 channels
+        for (int ph = 0; ph < 2; ++ph) {
+          wave_lds_order();
+          if ((l32 >> 4) == ph) {
+#pragma unroll
+            for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                *(out4_t*)(hs + (l32 & 15) * P::SROW + mt * 32 + 8 * q + 4 * half) = v[mt][q];
+          }
+          wave_lds_order();
+#pragma unroll
+          for (int it = 0; it < 3; ++it) {  // 16 pixels x 12 chunks of 8 channels
             const int u = it * 64 + lane, p = u / 12, ch = u % 12;
-            const vec8_t v = *(const vec8_t*)(stg + p * P::SROW + 8 * ch);
-            const int idx = wave * 64 + b * 32 + p;
+            const vec8_t o = *(const vec8_t*)(hs + p * P::SROW + 8 * ch);
+            const int idx = b * 32 + 16 * ph + p;
             const int oy = ty * P::TH + idx / P::TW, ox = tx * P::TW + idx % P::TW;
             const uint32_t off = oy < Ho && ox < Wo
                                      ? (uint32_t)((((int64_t)oy * Wo + ox) * 96 + 8 * ch) * sizeof(T))
                                      : OOB;
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rsrc_out, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), rsrc_out, off, 0, 0);
           }
         }
-#pragma unroll
-        for (int a = 0; a < 3; ++a)
-#pragma unroll
-          for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
-        // Vector-memory operations retire in issue order: once no more than the epilogue's stores
-        // are outstanding, the next stage's loads (issued before them) have landed in LDS.
-        wait_vmem_but<EPI_STORES>();
-      } else {
-        wait_vmem();
       }
-      __syncthreads();
+      wave_lds_order();
+#pragma unroll
+      for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+      // Vector-memory operations retire in issue order: once no more than the epilogue's stores
+      // are outstanding, the next stage's halo loads (issued before them) have landed in LDS.
+      wait_vmem_but<EPI_STORES>();
+    } else {
+      wait_vmem();
     }
   }
 }
@@ -1176,10 +1182,14 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
                           (int64_t)3 * H * P * (int64_t)sizeof(T) < 0x7fffffffLL &&
                           (int64_t)Ho * Wo * 96 * (int64_t)sizeof(T) < 0x7fffffffLL;
       if (direct) {
-        const int grid = (int)std::min<int64_t>(blocks, 2 * device_cu_count());
         if (ws == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
-        conv1_direct_kernel<T><<<grid, 256, 0, s>>>(in, out, ws, bias, H, W, P, Ho, Wo, in_stride,
-                                                   out_stride, tiles_x, tiles_y, (int)blocks);
+        // wave tiles of 4 x 16 output pixels, 8 workers per workgroup, one workgroup per CU
+        const int wtx = (Wo + Conv1R::TW - 1) / Conv1R::TW, wty = (Ho + Conv1R::TH - 1) / Conv1R::TH;
+        const int64_t wtiles = (int64_t)wtx * wty * n;
+        if (wtiles > 0x7fffffff) return (int)hipErrorInvalidValue;
+        const int grid = (int)std::min<int64_t>((wtiles + 7) / 8, device_cu_count());
+        conv1_resident_kernel<T><<<grid, 512, 0, s>>>(in, out, ws, bias, H, W, P, Ho, Wo, in_stride,
+                                                     out_stride, wtx, wty, (int)wtiles);
       } else {
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
         conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,

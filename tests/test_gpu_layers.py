@@ -43,9 +43,10 @@ def oracle_weights(dt):
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 # Widths that are not multiples of 8 take the register-staged kernel, the others the direct-load one
-# (16-bit types); 1200 x 1200 is a full stitched plane.
+# (16-bit types); 1200 x 1200 is a full stitched plane, and four of them (1444 tiles) give every
+# worker of the direct-load kernel several tiles in a row.
 @pytest.mark.parametrize("shape", [(2, 227, 227), (1, 300, 263), (1, 83, 51), (2, 232, 240),
-                                   (3, 48, 64), (1, 11, 16), (1, 1200, 1200)])
+                                   (3, 48, 64), (1, 11, 16), (1, 1200, 1200), (4, 1200, 1200)])
 def test_conv1(D, dt, shape):
     n, H, W = shape
     rng = np.random.default_rng(H * 7 + W)
