@@ -216,28 +216,57 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
         }
         neg = (bits & 0x80008000u) != 0;
       }
-      // sq[2 + i] = a_i^2 for this thread's channels, two neighbours (or zeros) on each side
-      float sq[CPT + 4], pr[CPT + 3];
+      // xs[1 + c] = channel c of this thread (c = -1 .. CPT, the outer ones from the neighbours or
+      // zero); win[c] = sum of squares over channels c - 2 .. c + 2.
+      float win[CPT], xs[CPT + 2];
+      xs[0] = to_f32(lv[N - 1]);
+      xs[CPT + 1] = to_f32(rv[0]);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const float a = to_f32(lv[N - 2 + i]), b = to_f32(rv[i]);
-        sq[i] = a * a;
-        sq[CPT + 2 + i] = b * b;
+      for (int c = 0; c < CPT; ++c) xs[1 + c] = to_f32(v[c / N][c % N]);
+      if constexpr (sizeof(T) == 2) {
+        // Pair sums P_j = x_2j^2 + x_2j+1^2 (j = -1 .. CPT / 2, counting the neighbours' pairs), their
+        // neighbour sums Q_j = P_j + P_j+1, then window(2 i) = Q_i-1 + x_2i+2^2 and window(2 i + 1) =
+        // Q_i + x_2i-1^2: two and a half operations per channel.
+        constexpr int NP = CPT / 2;
+        float pp[NP + 2];  // pp[1 + j] = P_j
+        {
+          const float a = to_f32(lv[N - 2]), b = to_f32(rv[1]);
+          pp[0] = __builtin_fmaf(a, a, xs[0] * xs[0]);
+          pp[NP + 1] = __builtin_fmaf(b, b, xs[CPT + 1] * xs[CPT + 1]);
+        }
+#pragma unroll
+        for (int j = 0; j < NP; ++j) pp[1 + j] = __builtin_fmaf(xs[1 + 2 * j], xs[1 + 2 * j], xs[2 + 2 * j] * xs[2 + 2 * j]);
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+          win[2 * i] = __builtin_fmaf(xs[2 * i + 3], xs[2 * i + 3], pp[i] + pp[i + 1]);
+          win[2 * i + 1] = __builtin_fmaf(xs[2 * i], xs[2 * i], pp[i + 1] + pp[i + 2]);
+        }
+      } else {
+        // sq[2 + i] = a_i^2, pr[i] = sq[i] + sq[i + 1]: window(c) = pr[c] + pr[c + 2] + sq[c + 4]
+        float sq[CPT + 4], pr[CPT + 3];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const float a = to_f32(lv[N - 2 + i]), b = to_f32(rv[i]);
+          sq[i] = a * a;
+          sq[CPT + 2 + i] = b * b;
+        }
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+          const float a = to_f32(v[i / N][i % N]);
+          sq[2 + i] = a * a;
+        }
+#pragma unroll
+        for (int i = 0; i < CPT + 3; ++i) pr[i] = sq[i] + sq[i + 1];
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) win[c] = pr[c] + pr[c + 2] + sq[c + 4];
       }
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const float a = to_f32(v[i / N][i % N]);
-        sq[2 + i] = a * a;
-      }
-#pragma unroll
-      for (int i = 0; i < CPT + 3; ++i) pr[i] = sq[i] + sq[i + 1];
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
         vec_t r;
 #pragma unroll
         for (int e = 0; e < N; ++e) {
-          const int c = i * N + e;  // window sq[c .. c + 4]
-          float o = to_f32(v[i][e]) * lrn_scale(pr[c] + pr[c + 2] + sq[c + 4], alpha_n, beta, k);
+          const int c = i * N + e;
+          float o = xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k);
           if constexpr (OUT_SIGN && sizeof(T) == 2) {
             o = o + 0.0f;  // -0 -> +0
             neg |= o < 0.f;
