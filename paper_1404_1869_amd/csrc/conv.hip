@@ -1133,12 +1133,13 @@ int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* 
 // Per layer: channel block BM, MFMA tiles per wave along channels TM, waves per SIMD requested, and
 // the tile shape (100 rows + columns).  Chosen by timing each layer at the 96-plane batch shapes: two waves per
 // SIMD matter most; conv3/conv5 run best at three waves per SIMD; conv4's 192 channels per group run
-// best as one block of 3 x 32 channels per wave (7 LDS fragment reads per 12 MFMAs instead of 6 per 8);
-// 16 x 32 and 8 x 32 tiles (eight waves sharing each stage's weight row; less edge waste on 149-wide
-// maps) were 2-3 % slower for conv2 on pipeline activations, and waste 20 % more MFMA work on the
-// 74-wide maps of conv3..conv5.
+// best as one block of 3 x 32 channels per wave (7 LDS fragment reads per 12 MFMAs instead of 6 per 8).
+// conv2 takes 16 x 32 tiles of 64 channels (four waves of 64 channels x 128 pixels): each stage's
+// weight row then serves 512 pixels, which halves the weight loads per output against 16 x 16 tiles
+// of 128 channels (2 % faster; with 128 channels, eight waves per workgroup, 10 % slower).  On the
+// 74-wide maps of conv3..conv5, 32-wide tiles waste 20 % more MFMA work and were 25-30 % slower.
 #ifndef DN_CONV2_CFG
-#define DN_CONV2_CFG 128, 2, 2, 1616
+#define DN_CONV2_CFG 64, 2, 2, 1632
 #endif
 #ifndef DN_CONV3_CFG
 #define DN_CONV3_CFG 128, 2, 3, 1616
