@@ -722,14 +722,14 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   // MFMA pixel tile t of wave wn is the tile's (t WN + wn)-th 32-pixel tile: the waves along pixels
   // take the tiles in turn, so a partly filled bottom band splits its rows over them.
   auto gtile = [&](int t) { return t * Cf::WN + wn; };
-  int pix[TN];
-#pragma unroll
-  for (int t = 0; t < TN; ++t) {
-    const int idx = gtile(t) * 32 + l32;
-    pix[t] = Cf::halo_off(Cf::pix_row(idx), Cf::pix_col(idx), 0);
-  }
-  // Byte offsets (chunk 0, tap row 0) of this lane's slot in each of its wave's LDS pieces.
-  uint32_t hoff[DH], woff[DW];
+  // LDS offset of this lane's pixel in MFMA pixel tile t: pix0 + t DPIX (tile t of the wave lies
+  // t WN tiles further, i.e. 2 t WN / (TW / 16) halo rows down), so the reads take immediate offsets.
+  static_assert(Cf::WN % (Cf::TW / 16) == 0, "a wave's MFMA tiles are whole row pairs apart");
+  constexpr int DPIX = 2 * (Cf::WN / (Cf::TW / 16)) * Cf::RS;
+  const int pix0 = Cf::halo_off(Cf::pix_row(gtile(0) * 32 + l32), Cf::pix_col(gtile(0) * 32 + l32), 0);
+  // Byte offsets (chunk 0) of this lane's halo slot in each of its wave's LDS pieces; the chunk's
+  // offset goes in the scalar offset (a lane past the plane keeps an offset the hardware drops).
+  uint32_t hoff[DH];
 #pragma unroll
   for (int i = 0; i < DH; ++i) {
     const int q = (wave * DH + i) * 64 + lane;
@@ -738,22 +738,22 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     const bool ok = row < Cf::HH && r < 2 * Cf::HW && iy >= 0 && iy < H && ix >= 0 && ix < W;
     hoff[i] = ok ? (uint32_t)((((int64_t)iy * W + ix) * C + (r & 1) * 8) * sizeof(T)) : OOB;
   }
-#pragma unroll
-  for (int i = 0; i < DW; ++i) {
-    const int q = (wave * DW + i) * 64 + lane;  // piece q of a stage block lands in LDS slot q
-    woff[i] = q < WSLOTS ? (uint32_t)(q * 16) : OOB;
-  }
   auto load_halo = [&](int buf, int c0) {
 #pragma unroll
     for (int i = 0; i < DH; ++i)
-      lds_direct16(rsrc_in, halo_buf(buf) + (wave * DH + i) * 512,
-                   hoff[i] == OOB ? OOB : hoff[i] + (uint32_t)(c0 * sizeof(T)));
+      lds_direct16(rsrc_in, halo_buf(buf) + (wave * DH + i) * 512, hoff[i], (uint32_t)(c0 * sizeof(T)));
   };
+  // Weight piece p of a stage block lands in LDS piece p: lane offset 16 lane, the piece's and the
+  // stage's offsets in the scalar offset; the wave skips pieces past the block.
+  static_assert(WSLOTS % 64 == 0, "a stage's weights are whole 1 KB pieces");
+  const uint32_t lane16 = (uint32_t)lane * 16u;
   auto load_w = [&](int buf, int c0, int ky) {  // stage (chunk c0 / 16, kernel row ky)
     const uint32_t add = (uint32_t)(((c0 / Cf::CC) * R + ky) * WSLOTS * 16);
 #pragma unroll
-    for (int i = 0; i < DW; ++i)
-      lds_direct16(rsrc_w, wrow_buf(buf) + (wave * DW + i) * 512, woff[i] == OOB ? OOB : woff[i] + add);
+    for (int i = 0; i < DW; ++i) {
+      const int p = wave * DW + i;
+      if (p * 64 < WSLOTS) lds_direct16(rsrc_w, wrow_buf(buf) + p * 512, lane16, add + (uint32_t)p * 1024u);
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -792,7 +792,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
           typename Op::frag x[TNV], w[TM];
 #pragma unroll
           for (int t = 0; t < TNV; ++t)
-            x[t] = lds_frag16<T>(hs + pix[t] + ky * Cf::RS + kx * Cf::PS + half * 8);
+            x[t] = lds_frag16<T>(hs + pix0 + t * DPIX + ky * Cf::RS + kx * Cf::PS + half * 8);
 #pragma unroll
           for (int mt = 0; mt < TM; ++mt)
             w[mt] = lds_frag16<T>(ws + Cf::w_off(kx, wm * 32 * TM + mt * 32 + l32, half));
