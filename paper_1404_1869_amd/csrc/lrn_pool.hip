@@ -159,17 +159,15 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
 // LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 64 x 4 at 16-bit storage, 128 x 2 at
 // fp32) with the default window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
 // 16-byte loads at once (plus one neighbouring vector on each inner side when a pixel is split over
-// several threads), forms the five-channel sums of squares from pair sums (four adds and one multiply per
-// element), and stores the LRN result to LDS.  Pixels of the tile outside the map are stored as
+// several threads), forms the five-channel sums of squares from pair sums, and stores the LRN result
+// to LDS.  Pixels of the tile outside the map are stored as
 // -inf, so every pooled output then takes the max over its full 3 x 3 window from LDS, unrolled, with
 // no clipping tests.  Channel count and tile shape are compile-time constants, so no index
 // arithmetic needs a division.  With 16-bit storage, a tile whose LRN values are all >= +0 (the usual
 // case after ReLU) takes its maxima on the raw 16-bit patterns, two per instruction (for such values,
 // and the -inf fill, signed-integer order is the float order); any other tile takes them in fp32.
-// The tile's sign is read from the inputs' sign bits (LRN keeps the sign; -0 counts as negative) or,
-// with OUT_SIGN, from the LRN values themselves (-0 is stored as +0): the same decision up to -0, and
-// the faster schedule of the two as measured for each channel count.
-template <typename T, int C, int CPT, int TPH, int TPW, int WPE, bool OUT_SIGN>
+// The tile's sign is read from the inputs' sign bits (LRN keeps the sign; -0 counts as negative).
+template <typename T, int C, int CPT, int TPH, int TPW, int WPE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void lrn_pool_pixel_kernel(
                                                              const T* __restrict__ in,
                                                              T* __restrict__ out, int H, int W,
@@ -205,7 +203,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
       for (int i = 0; i < NV; ++i) v[i] = *(const vec_t*)(px + i * N);
       if (TPP > 1 && part > 0) lv = *(const vec_t*)(px - N);
       if (TPP > 1 && part + 1 < TPP) rv = *(const vec_t*)(px + CPT);
-      if constexpr (sizeof(T) == 2 && !OUT_SIGN) {
+      if constexpr (sizeof(T) == 2) {
         typedef uint32_t uvec_t __attribute__((ext_vector_type(N / 2)));
         uint32_t bits = 0;
 #pragma unroll
@@ -266,12 +264,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 #pragma unroll
         for (int e = 0; e < N; ++e) {
           const int c = i * N + e;
-          float o = xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k);
-          if constexpr (OUT_SIGN && sizeof(T) == 2) {
-            o = o + 0.0f;  // -0 -> +0
-            neg |= o < 0.f;
-          }
-          r[e] = from_f32<T>(o);
+          r[e] = from_f32<T>(xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k));
         }
         *(vec_t*)(d + i * N) = r;
       }
@@ -409,11 +402,11 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
     // Waves per SIMD the LDS tile allows (3 and 2 workgroups of 4 waves per CU): the compiler may use
     // the registers that occupancy leaves free for more independent work in flight.
     if (C == 96)
-      lrn_pool_pixel_kernel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE, false>
+      lrn_pool_pixel_kernel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE>
           <<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     else
-      lrn_pool_pixel_kernel<T, 256, F32 ? 128 : DN_LRN256_CPT, TH256, TW256, F32 ? 2 : DN_LRN256_WPE, true>
+      lrn_pool_pixel_kernel<T, 256, F32 ? 128 : DN_LRN256_CPT, TH256, TW256, F32 ? 2 : DN_LRN256_WPE>
           <<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
     return (int)hipGetLastError();
