@@ -934,7 +934,7 @@ template <typename T>
 __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
-    int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
+    int64_t out_stride, int tiles_x, int tiles_y, int ntiles, int zero_col_w) {
   using P = Conv1R;
   using Op = Mfma<T>;
   using frag = typename Op::frag;
@@ -971,11 +971,17 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   auto hbuf = [&](int b) { return s_mem + P::HALO_OFF + (2 * wave + b) * P::HALO_E; };
   uint32_t hoff[P::NH];
   __amdgpu_buffer_rsrc_t rsrc_in;
+  // Column W of the plane is the zero-weight tap (kx = 11) of the last output column when
+  // (W - 11) % 4 == 0.  With W % 8 != 0 its 16-byte slot starts inside the row and is loaded, so when
+  // rows are padded (pitch > W) the padding value would enter as 0 * x; zcol is then that column's
+  // position in the tile's halo (else -1) and the halo copy of it is overwritten with zeros.
+  int zcol = -1;
   auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of wave tile t
     const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
     rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + plane * in_stride), 0,
                                                 (int)(3 * chan_bytes), 0x00020000);
     const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
+    zcol = __builtin_amdgcn_readfirstlane(zero_col_w && W >= ix0 && W < ix0 + 72 ? W - ix0 : -1);
 #pragma unroll
     for (int i = 0; i < P::NH; ++i) {
       const int q = i * 64 + lane;
@@ -988,6 +994,13 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   auto load_halo = [&](int b, int c) {  // channel c of the current tile into buffer b
 #pragma unroll
     for (int i = 0; i < P::NH; ++i) lds_direct16(rsrc_in, hbuf(b) + i * 512, hoff[i], c * chan_bytes);
+  };
+  auto zero_col = [&](int b) {  // after buffer b's loads have landed
+    if (zcol >= 0) {
+      wave_lds_order();
+      if (lane < P::HR) hbuf(b)[lane * P::HS + zcol] = from_f32<T>(0.f);
+      wave_lds_order();
+    }
   };
 
   int lpix[2];
@@ -1024,6 +1037,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   }
   wait_vmem();
   __syncthreads();  // weights and biases are in LDS; from here on each wave runs on its own
+  zero_col(0);
   for (int st = 0; st < 3 * ntile; ++st) {
     const int j = st / 3, c = st - 3 * j;  // tile j of this worker, input channel c
     if (st + 1 < 3 * ntile) {
@@ -1104,6 +1118,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     } else {
       wait_vmem();
     }
+    zero_col((st + 1) & 1);
   }
 }
 
@@ -1190,7 +1205,8 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
         if (wtiles > 0x7fffffff) return (int)hipErrorInvalidValue;
         const int grid = (int)std::min<int64_t>((wtiles + 7) / 8, device_cu_count());
         conv1_resident_kernel<T><<<grid, 512, 0, s>>>(in, out, ws, bias, H, W, P, Ho, Wo, in_stride,
-                                                     out_stride, wtx, wty, (int)wtiles);
+                                                     out_stride, wtx, wty, (int)wtiles,
+                                                     (int)(W % 8 != 0 && P > W));
       } else {
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
         conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,

@@ -61,6 +61,22 @@ def ulp(x, dt):
     return 2.0 ** (e - mant)
 
 
+# fp32 error of a plane value before its final rounding to the storage type.  The builder (and the
+# crop-before warp) blends four uint8 taps in fp32: lerp-x twice, lerp-y, minus the mean pixel, times the
+# border weight.  Every intermediate is below 256 in magnitude, so each rounding costs at most
+# h = 2^-17 (half an fp32 ulp at 128..256); the fractions and weights are fp32 roundings of exact
+# rationals (relative error 2^-24, times values below 256: at most h each).  Counting terms:
+# lerp-x 3h per row, the lerp-y of the two rows 7h, the mean 8h, the border weight 15h < 2^-13.
+PLANE_FP32_ERR = 2.0 ** -13
+
+
+def plane_tol(ref, dt):
+    """Bound on |GPU plane value - fp64 oracle value|: the fp32 error above, plus half an ulp of the
+    storage type at the largest magnitude the fp32 value can have."""
+    ref = np.abs(np.asarray(ref, np.float64))
+    return 0.5 * ulp(ref + PLANE_FP32_ERR, dt) + PLANE_FP32_ERR
+
+
 def chw(nhwc):
     return np.ascontiguousarray(np.moveaxis(np.asarray(nhwc), -1, 0))
 

@@ -8,7 +8,7 @@ import pytest
 import oracle
 from paper_1404_1869_amd import configs as C
 from paper_1404_1869_amd import synth
-from tests.parity import assert_layer_close, chw, round_to, ulp
+from tests.parity import plane_tol, assert_layer_close, chw, round_to, ulp
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -49,10 +49,7 @@ def views(planes, plan):
 
 def check_planes(got, ref, dt):
     got = got.float().cpu().numpy().astype(np.float64)
-    if dt == "f32":
-        assert np.max(np.abs(got - ref)) <= 1e-5 * 255
-    else:
-        assert np.all(np.abs(got - ref) <= 0.5 * ulp(ref, dt) + 1e-3)
+    assert np.all(np.abs(got - ref) <= plane_tol(ref, dt))
 
 
 SMALL = [

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_1404_1869_amd import synth
-from tests.parity import assert_layer_close, chw, round_to, ulp
+from tests.parity import plane_tol, assert_layer_close, chw, round_to, ulp
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -74,10 +74,7 @@ def test_planes_strongly_reduced_wide_image(D, W, dt):
     assert len(plan.planes) == op.n_planes
     for j, d in enumerate(plan.planes):
         got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
-        if dt == "f32":
-            assert np.max(np.abs(got - ref[j])) <= 1e-5 * 255, f"plane {j}"
-        else:
-            assert np.all(np.abs(got - ref[j]) <= 0.5 * ulp(ref[j], dt) + 1e-3), f"plane {j}"
+        assert np.all(np.abs(got - ref[j]) <= plane_tol(ref[j], dt)), f"plane {j}"
 
 
 @pytest.mark.parametrize("W", [1, 2, 3])
@@ -95,10 +92,7 @@ def test_planes_narrow_images(D, W, dt):
     assert len(plan.planes) == op.n_planes
     for j, d in enumerate(plan.planes):
         got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
-        if dt == "f32":
-            assert np.max(np.abs(got - ref[j])) <= 1e-5 * 255, f"plane {j}"
-        else:
-            assert np.all(np.abs(got - ref[j]) <= 0.5 * ulp(ref[j], dt) + 1e-3), f"plane {j}"
+        assert np.all(np.abs(got - ref[j]) <= plane_tol(ref[j], dt)), f"plane {j}"
 
 
 def test_smallest_plane_with_a_conv5_cell(D):
@@ -224,7 +218,7 @@ def test_scale_and_plane_variants_end_to_end(D, spo, base, plane, dt):
     ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     for j, d in enumerate(pyra.plan.planes):
         got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
-        assert np.all(np.abs(got - ref_planes[j]) <= 0.5 * ulp(ref_planes[j], dt) + 1e-3), f"plane {j}"
+        assert np.all(np.abs(got - ref_planes[j]) <= plane_tol(ref_planes[j], dt)), f"plane {j}"
     maps = pyra.conv.conv5_maps()
     c5 = {}
     for j in range(op.n_planes):
@@ -253,10 +247,7 @@ def test_aspect_ratio_pyramids_end_to_end(D, dt):
     ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     for j, d in enumerate(pyra.plan.planes):
         got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
-        if dt == "f32":
-            assert np.max(np.abs(got - ref_planes[j])) <= 1e-5 * 255, f"plane {j}"
-        else:
-            assert np.all(np.abs(got - ref_planes[j]) <= 0.5 * ulp(ref_planes[j], dt) + 1e-3), f"plane {j}"
+        assert np.all(np.abs(got - ref_planes[j]) <= plane_tol(ref_planes[j], dt)), f"plane {j}"
     maps = pyra.conv.conv5_maps()
     c5 = []
     for j in range(op.n_planes):

@@ -124,3 +124,35 @@ def test_maxpool_exact(D, dt):
     out = D.densenet_maxpool(xg, DTS[dt]).float().cpu().numpy()
     for i in range(3):
         np.testing.assert_array_equal(chw(out[i]), oracle.maxpool(chw(x[i])))
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("W,pitch", [(227, 232), (235, 240), (229, 240)])
+def test_conv1_ignores_row_padding(D, dt, W, pitch):
+    """Planes whose rows are padded (pitch > width, width not a multiple of 8) take the direct-load
+    conv1; the padding columns hold NaN here and must not reach any output (for widths with
+    (W - 11) % 4 == 0 the last output column's zero-weight tap sits on column W).  The result equals
+    the same planes stored unpadded (which take the register-staged conv1) and the oracle."""
+    n, H = 3, 227
+    rng = np.random.default_rng(W + pitch)
+    x = round_to(rng.normal(0, 50, (n, 3, H, W)), dt)
+    padded = np.full((n, 3, H, pitch), np.nan, np.float32)
+    padded[..., :W] = x
+    outs = []
+    for arr, p in ((padded, pitch), (x, W)):
+        xg = torch.from_numpy(np.ascontiguousarray(arr)).to("cuda", TORCH_DT[dt]).reshape(-1)
+        desc = []
+        for i in range(n):
+            q = D.dn_plane_desc()
+            q.h, q.w, q.offset, q.pitch = H, W, i * 3 * H * p, p
+            desc.append(q)
+        cf = D.ConvFeatures(desc, DTS[dt], D.net_params(pool5=True), device="cuda")
+        cf(xg, packed(D, dt))
+        torch.cuda.synchronize()
+        outs.append([m.float().cpu().numpy() for m in cf.pool5_maps()])
+    w = oracle_weights(dt)
+    for i in range(n):
+        assert np.all(np.isfinite(outs[0][i])), f"NaN from the row padding reached plane {i}"
+        assert_layer_close(chw(outs[0][i]), chw(outs[1][i]), dt, f"padded vs unpadded [{i}]")
+        _, ref = oracle.net(x[i], w, pool5=True)
+        assert_layer_close(chw(outs[0][i]), ref, dt, f"padded pool5 [{i}]")
