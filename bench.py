@@ -7,7 +7,8 @@ on every stitched plane -> per-scale conv5 windows -> region windows for 2000 bo
 After the timed steps it also times the paper's per-window baseline (every box of one image warped to
 227 x 227 and run through the network on its own) and reports it beside the dense time per image, and
 the same batch with cross-image packing (the scales of all 16 images stitched together: 88 planes
-instead of 96), reported beside the headline, which keeps each image's own planes.
+instead of 96), reported beside the headline, which keeps each image's own planes, and the latency of
+one 25-scale pyramid of one image (fp16), launched eagerly and replayed from a captured graph.
 The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
 1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
 
@@ -51,6 +52,8 @@ def parse():
                     help="skip the per-window baseline (every box warped to 227 x 227 and run alone)")
     ap.add_argument("--no-packed", action="store_true",
                     help="skip the cross-image packed variant (the batch's scales stitched together)")
+    ap.add_argument("--no-single", action="store_true",
+                    help="skip the single-image latency figures (one 25-scale pyramid, fp16)")
     return ap.parse_args()
 
 
@@ -222,6 +225,8 @@ def main():
     if not args.no_packed and n_img > 1:
         result["cross_image_packing"] = cross_image(D, w, dt, imgs, boxes, box_img, packed, args.steps,
                                                     args.warmup, ms_per_step)
+    if not args.no_single and n_img > 1:
+        result["single_image"] = single_image(D, weights, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
     print(json.dumps(result), flush=True)
@@ -302,6 +307,96 @@ def cross_image(D, w, dt, imgs, boxes, box_img, packed, steps, warmup, per_image
             "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()}}
 
 
+def single_image(D, weights, steps, warmup):
+    """One 25-scale pyramid of one 768 x 1024 image (6 stitched 1200 x 1200 planes, fp16), the unit the
+    paper times (Sec. 3.4): ms per pyramid (build + conv stack) launched eagerly and replayed from a
+    captured graph of the same launches, the conv MFMA utilisation from a traced pass, and the 2000
+    region windows of the image timed on their own."""
+    import numpy as np
+    import torch
+
+    from paper_1404_1869_amd import configs as C
+    from paper_1404_1869_amd import synth, workmodel
+
+    w = C.XGA_25SCALE
+    dt = D.DTYPES[w.dtypes[0]]
+    dev = torch.device("cuda", 0)
+    img = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).to(dev)
+    packed = D.densenet_pack_weights(weights, dt)
+    params = D.params_for(w)
+    planes, plan = D.densenet_build_pyramid(img, params, dt)
+    cf = D.ConvFeatures(list(plan.planes), dt, D.net_params(pool5=False), device=dev)
+    c5d = list(cf.c5d)
+    boxes = torch.from_numpy(synth.boxes(w.box_seed or 105, 2000, w.H, w.W)).to(dev)
+    out = torch.empty((2000, 256 * 36), dtype=torch.float32, device=dev)
+    scale = torch.empty(2000, dtype=torch.int32, device=dev)
+    ppi = len(plan.planes)
+
+    def pyramid():
+        D.densenet_build_pyramid(img, params, dt, out=planes)
+        cf(planes, packed)
+
+    def regions():
+        D.densenet_region_windows(cf.conv5, c5d, dt, plan, w.pad, ppi, boxes, out=out, scale=scale)
+
+    def timed(fn, n):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    for _ in range(warmup):
+        pyramid()
+        regions()
+    torch.cuda.synchronize()
+    D.profile_start()
+    pyramid()
+    torch.cuda.synchronize()
+    kern = D.profile_stop()
+    eager_ms = timed(pyramid, steps)
+    regions_ms = timed(regions, steps)
+
+    # the same launches captured once into a graph (no allocation or memset inside), replayed
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pyramid()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pyramid()
+    for _ in range(warmup):
+        graph.replay()
+    graph_ms = timed(graph.replay, steps)
+
+    fl = workmodel.conv_flops(plan.planes[0].h, plan.planes[0].w)
+    conv_ms = sum(kern[k][1] / kern[k][0] for k in CONV_NAMES if k in kern)
+    conv_flops = sum(fl) * ppi
+    best = min(eager_ms, graph_ms)
+    return {"workload": w.name, "dtype": w.dtypes[0], "planes": ppi,
+            "ms_per_pyramid_eager": round(eager_ms, 4), "ms_per_pyramid_graph": round(graph_ms, 4),
+            "pyramids_per_s": round(1e3 / best, 2),
+            "conv_mfma_util": round(conv_flops / (conv_ms / 1e3) / 1e12 / PEAK_TFLOPS[w.dtypes[0]], 4),
+            "regions_2000_ms": round(regions_ms, 4),
+            "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()},
+            "paper_context": "Sec. 3.4, NVIDIA K20: one 25-scale pyramid in ~1 s"}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, n_planes_sample):
     """The oracle, as it stands, on a bounded sample of the workload: image 0's planes and its 2000
     region windows in full, its conv stack on `n_planes_sample` of its planes (a plane's cost depends
@@ -331,7 +426,7 @@ def cpu_baseline(w, n_planes_sample):
     t_reg = time.perf_counter() - t0
     per_pyr = t_build + p.n_planes * t_plane + t_reg
     return {"value": round(1.0 / per_pyr, 5), "unit": "pyramids/s", "cores": oracle.threads(),
-            "kind": "oracle",
+            "cpu": cpu_model(), "kind": "oracle",
             "sample": (f"image 0 of the workload: planes and 2000 region windows in full, conv stack "
                        f"on {n_planes_sample} of its {p.n_planes} 1200x1200 planes, extrapolated to "
                        f"{p.n_planes} planes ({per_pyr:.1f} s per pyramid)")}

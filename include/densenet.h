@@ -204,6 +204,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
  * ratio (ties to the smaller k; scales with an empty window skipped) is chosen, and S x S bilinear
  * samples at the bin centres of the box are read from that scale's conv5 window (coordinates clamped
  * to the window), all 256 channels: d_out[n][256 * S * S] fp32, flattened (channel, row, column).
+ * S must be in 1..8 (DN_E_UNSUPPORTED otherwise; the paper's windows are 6 x 6).
  * geom/n_scales: all pyramid entries; when they span several aspect ratios (geom[k].aspect > 0 for
  * some k, Sec. 3.3) the cost of entry k is multiplied by max(rho, 1/rho), rho = (sx bw)/(sy bh) the
  * box's aspect on that entry, so each box is read where it is closest to a target x target square.

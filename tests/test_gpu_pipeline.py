@@ -220,3 +220,45 @@ def test_region_windows_end_to_end(D):
     np.testing.assert_array_equal(ix.cpu().numpy(), idx)
     assert out.shape == (2000, 9216)
     assert_layer_close(out.cpu().numpy(), desc, "f16", "region descriptors")
+
+
+def test_graph_replay_equals_eager(D):
+    """The pyramid build and conv stack captured once into a graph (the library allocates nothing and
+    issues no memset, so its launches are capturable) and replayed several times, with eager work and
+    synchronisations in between: every replay's planes and conv5 maps equal the eager run's bit for
+    bit."""
+    w = C.XGA_25SCALE
+    dt = "f16"
+    img = torch.from_numpy(synth.image(w.seeds[0], w.H, w.W)).cuda()[None]
+    params = D.params_for(w)
+    planes, plan = D.densenet_build_pyramid(img, params, DTS[dt])
+    cf = D.ConvFeatures(list(plan.planes), DTS[dt], D.net_params())
+
+    def pyramid():
+        D.densenet_build_pyramid(img, params, DTS[dt], out=planes)
+        cf(planes, packed(D, dt))
+
+    pyramid()
+    torch.cuda.synchronize()
+    ref_planes = planes[:plan.image_elems].clone()
+    ref_c5 = cf.conv5.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pyramid()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pyramid()
+    other = D.densenet_build_pyramid(torch.from_numpy(synth.image(7, w.H, w.W)).cuda()[None], params,
+                                     DTS[dt])[0]
+    for rep in range(4):
+        planes.zero_()
+        cf.conv5.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(planes[:plan.image_elems], ref_planes), f"replay {rep}: planes"
+        assert torch.equal(cf.conv5, ref_c5), f"replay {rep}: conv5"
+        other.add_(1)                      # eager work between replays
+        torch.cuda.synchronize()
