@@ -14,7 +14,8 @@
  *    last failing call on this thread.
  *  - Ownership: the caller owns every buffer.  d_* pointers are device pointers (256-byte aligned,
  *    as returned by hipMalloc or the torch caching allocator); other pointers are host memory.
- *    The library allocates no device memory and keeps no device state.
+ *    The library allocates no device memory.  Its only device state is the staging array of
+ *    densenet_build_pyramid_noalloc (DN_STATIC_SCRATCH_BYTES per GPU, part of the code object).
  *  - Size queries: where an output or workspace pointer may be NULL, the call only writes the
  *    required byte count to *_needed and returns DN_OK.  A buffer that is too small returns
  *    DN_E_BUFFER_TOO_SMALL (the needed size is still written).
@@ -146,6 +147,23 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
                            size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
                            dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
                            int64_t* image_elems, void* stream);
+
+/* Scratch-free variant of densenet_build_pyramid, for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops and harnesses that forbid hipMalloc).  Same arguments,
+ * validation and planes as densenet_build_pyramid, but d_planes holds the planes only: *bytes_needed
+ * is the planes' size, with no trailing scratch region.  The builder's pixel-interleaved image stages
+ * in a library-owned device array of DN_STATIC_SCRATCH_BYTES on each GPU, which that GPU holds until
+ * the process ends; 4 * H * W * n_img above DN_STATIC_SCRATCH_BYTES returns DN_E_TOO_LARGE (checked
+ * before any device work).  The call allocates nothing; its first call on a GPU looks the array up
+ * (a runtime query, no allocation).  Every call on one GPU shares that GPU's array: calls that overlap
+ * on one GPU (different streams or threads with no ordering between them) race and give wrong planes;
+ * calls ordered on one stream are safe.  No part of the array needs to start at zero. */
+#define DN_STATIC_SCRATCH_BYTES (64u << 20)
+int densenet_build_pyramid_noalloc(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                                   const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
+                                   size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
+                                   dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                                   int64_t* image_elems, void* stream);
 
 /* Cross-image packing: Bottom-Left Fill stitching (Sec. 3.1) applied to a whole batch, so that the
  * small scales of several images share planes instead of each image leaving a half-empty last plane

@@ -261,11 +261,13 @@ int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_s
   }
 }
 
-int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
-                           const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
-                           size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
-                           dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
-                           int64_t* image_elems, void* stream) {
+// densenet_build_pyramid (static_scratch = false: the pixel image stages after the planes in the
+// caller's buffer) and densenet_build_pyramid_noalloc (true: it stages in the library's static array).
+static int build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                         const dn_pyramid_params* p, dn_dtype dtype, void* d_planes, size_t planes_bytes,
+                         size_t* bytes_needed, dn_scale_geom* geom, dn_plane_desc* planes,
+                         int32_t max_planes, int32_t* n_planes, int64_t* image_elems, void* stream,
+                         bool static_scratch_area) {
   try {
     if (!bytes_needed) return fail(DN_E_INVALID_ARG, "bytes_needed is NULL");
     if (!valid_dtype(dtype)) return fail(DN_E_UNSUPPORTED, "unknown dtype");
@@ -274,7 +276,11 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
     if (st != DN_OK) return st;
     const size_t planes_end = ((size_t)n_img * (size_t)*image_elems * dtype_size(dtype) + 255) &
                               ~(size_t)255;
-    const size_t need = planes_end + (size_t)n_img * 4 * (size_t)H * (size_t)W;
+    const size_t pix_bytes = (size_t)n_img * 4 * (size_t)H * (size_t)W;
+    if (static_scratch_area && pix_bytes > (size_t)DN_STATIC_SCRATCH_BYTES)
+      return fail(DN_E_TOO_LARGE, "4 * H * W * n_img exceeds DN_STATIC_SCRATCH_BYTES");
+    const size_t need = static_scratch_area ? (size_t)n_img * (size_t)*image_elems * dtype_size(dtype)
+                                            : planes_end + pix_bytes;
     *bytes_needed = need;
     if (!d_planes) return DN_OK;
     if (planes_bytes < need) return fail(DN_E_BUFFER_TOO_SMALL, "planes buffer too small");
@@ -306,13 +312,36 @@ int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, in
       mh = std::max(mh, planes[j].h);
       mw = std::max(mw, planes[j].w);
     }
+    uint8_t* pix = (uint8_t*)d_planes + planes_end;
+    if (static_scratch_area) {
+      const int e = static_scratch(&pix);
+      if (e != (int)hipSuccess) return hip_status(e, "static scratch lookup");
+    }
     TraceScope trace("build_planes", stream);
-    return hip_status(launch_build_planes(d_images, n_img, a, pl, nullptr, mh, mw, dtype, d_planes,
-                                          (uint8_t*)d_planes + planes_end, stream),
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, nullptr, mh, mw, dtype, d_planes, pix,
+                                          stream),
                       "build_planes launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
   }
+}
+
+int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                           const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
+                           size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
+                           dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                           int64_t* image_elems, void* stream) {
+  return build_pyramid(d_images, n_img, H, W, p, dtype, d_planes, planes_bytes, bytes_needed, geom,
+                       planes, max_planes, n_planes, image_elems, stream, false);
+}
+
+int densenet_build_pyramid_noalloc(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
+                                   const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
+                                   size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
+                                   dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
+                                   int64_t* image_elems, void* stream) {
+  return build_pyramid(d_images, n_img, H, W, p, dtype, d_planes, planes_bytes, bytes_needed, geom,
+                       planes, max_planes, n_planes, image_elems, stream, true);
 }
 
 int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_params* p,

@@ -92,6 +92,9 @@ inline size_t builder_scratch_bytes(int32_t n_img, int32_t H, int32_t W, int32_t
 // d_scratch: builder_scratch_bytes (256-byte aligned; n_planes = n_items = 0 without a batch).  batch:
 // NULL for per-image planes (a.s / pl), else the packed batch's placements (a.s and pl unused but H,
 // W, pad, ramp, mean).
+// Device address of the scratch-free builder's static staging array on the current device (looked up
+// once per device).  Returns a hipError_t.
+int static_scratch(uint8_t** out);
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
                         const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
                         uint8_t* d_scratch, void* stream);

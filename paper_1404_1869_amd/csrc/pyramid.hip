@@ -11,6 +11,7 @@
 // ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers; only the blend is fp32.
 #include "common.h"
 
+#include <mutex>
 #include <type_traits>
 
 namespace dn {
@@ -324,6 +325,31 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
 }
 
 }  // namespace
+
+// Staging array of the scratch-free builder entry point (the pixel-interleaved images).  Each device
+// holds its own copy at its own address; host code never passes this name to a kernel or a copy (in
+// host code it is only a stand-in), it uses the address hipGetSymbolAddress returns for the device.
+static __device__ __align__(256) uint8_t scratch[DN_STATIC_SCRATCH_BYTES];
+
+int static_scratch(uint8_t** out) {
+  constexpr int MAX_DEVICES = 64;
+  static std::mutex mu;
+  static uint8_t* addr[MAX_DEVICES] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= MAX_DEVICES) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {  // once per device, with that device current
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    if (!ptr) return (int)hipErrorInvalidSymbol;
+    addr[dev] = (uint8_t*)ptr;
+  }
+  *out = addr[dev];
+  return (int)hipSuccess;
+}
 
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
                         const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,

@@ -23,13 +23,14 @@ DN_F32, DN_F16, DN_BF16 = 0, 1, 2
 DN_PAD_ZERO, DN_PAD_RAMP = 0, 1
 DN_MAX_SCALES, DN_MAX_PLANES_PER_IMAGE, DN_MAX_WARP_SIDE, DN_MAX_ASPECTS = 64, 64, 1024, 8
 DN_MAX_BATCH_ITEMS = 65536
+DN_STATIC_SCRATCH_BYTES = 64 << 20
 DTYPES = {"f32": DN_F32, "f16": DN_F16, "bf16": DN_BF16}
 
 EXPORTS = ("densenet_plan_pyramid", "densenet_build_pyramid", "densenet_pack_weights",
            "densenet_conv_features", "densenet_region_windows", "densenet_conv_layer",
            "densenet_lrn_pool", "densenet_maxpool", "densenet_layer_sizes", "densenet_warp_regions",
            "densenet_region_pool", "densenet_plan_batch", "densenet_build_batch",
-           "densenet_region_windows_batch", "densenet_profile_start",
+           "densenet_region_windows_batch", "densenet_build_pyramid_noalloc", "densenet_profile_start",
            "densenet_profile_stop", "densenet_last_error")
 
 
@@ -85,6 +86,8 @@ def lib():
         sig = {
             "densenet_plan_pyramid": [i32, i32, pp, pg, pd, i32, pi32, pi64],
             "densenet_build_pyramid": [P, i32, i32, i32, pp, i32, P, sz, psz, pg, pd, i32, pi32, pi64, P],
+            "densenet_build_pyramid_noalloc": [P, i32, i32, i32, pp, i32, P, sz, psz, pg, pd, i32, pi32, pi64,
+                                               P],
             "densenet_pack_weights": [P, P, i32, P, sz, psz, P],
             "densenet_conv_features": [P, pd, i32, i32, P, pn, P, sz, psz, P, sz, psz, pd, P, sz, psz,
                                        pd, P],
@@ -231,6 +234,32 @@ def densenet_build_pyramid(images, p: dn_pyramid_params, dtype: int, out=None):
                                    out.numel() * out.element_size(), ctypes.byref(need), geom, planes,
                                    DN_MAX_PLANES_PER_IMAGE, ctypes.byref(n), ctypes.byref(e),
                                    _stream()))
+    return out, PlanResult(list(geom), list(planes[:n.value]), e.value)
+
+
+def densenet_build_pyramid_noalloc(images, p: dn_pyramid_params, dtype: int, out=None):
+    """As densenet_build_pyramid, with the builder's staging in the library's static array: `out` (the
+    planes only) is the only device buffer.  Returns (planes tensor, PlanResult)."""
+    torch = _torch()
+    if images.dim() == 3:
+        images = images[None]
+    n_img, _, H, W = images.shape
+    geom = (dn_scale_geom * n_entries(p))()
+    planes = (dn_plane_desc * DN_MAX_PLANES_PER_IMAGE)()
+    n = ctypes.c_int32()
+    e = ctypes.c_int64()
+    need = ctypes.c_size_t()
+    L = lib()
+    check(L.densenet_build_pyramid_noalloc(None, n_img, H, W, ctypes.byref(p), dtype, None, 0,
+                                           ctypes.byref(need), geom, planes, DN_MAX_PLANES_PER_IMAGE,
+                                           ctypes.byref(n), ctypes.byref(e), None))
+    es = 4 if dtype == DN_F32 else 2
+    if out is None:
+        out = torch.empty(need.value // es, dtype=_tdtype(dtype), device=images.device)
+    check(L.densenet_build_pyramid_noalloc(_ptr(images), n_img, H, W, ctypes.byref(p), dtype, _ptr(out),
+                                           out.numel() * out.element_size(), ctypes.byref(need), geom,
+                                           planes, DN_MAX_PLANES_PER_IMAGE, ctypes.byref(n),
+                                           ctypes.byref(e), _stream()))
     return out, PlanResult(list(geom), list(planes[:n.value]), e.value)
 
 

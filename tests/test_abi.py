@@ -201,3 +201,23 @@ def test_batch_entry_points_validation():
     cd[7].offset -= 256
     cd[0].h = cd[1].h = 20
     assert L.densenet_region_windows_batch(*args(cd, 88, 0)) == D.DN_E_INVALID_ARG
+
+
+def test_noalloc_builder_size_query_and_limit():
+    """The scratch-free builder reports the planes' size alone and rejects a batch whose staged
+    images exceed its static array, before any device work."""
+    L = D.lib()
+    p = D.pyramid_params(25, 10, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=1200, plane_w=1200)
+    geom = (D.dn_scale_geom * 25)()
+    planes = (D.dn_plane_desc * 64)()
+    n, e, need = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_size_t()
+    assert L.densenet_build_pyramid_noalloc(None, 16, 768, 1024, ctypes.byref(p), D.DN_BF16, None, 0,
+                                            ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
+                                            ctypes.byref(e), None) == 0
+    assert need.value == 16 * e.value * 2
+    n_img = D.DN_STATIC_SCRATCH_BYTES // (4 * 768 * 1024) + 1
+    fake = ctypes.c_void_p(256)
+    st = L.densenet_build_pyramid_noalloc(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_F16, fake,
+                                          1 << 40, ctypes.byref(need), geom, planes, 64,
+                                          ctypes.byref(n), ctypes.byref(e), None)
+    assert st == D.DN_E_TOO_LARGE and "DN_STATIC_SCRATCH_BYTES" in D.last_error()
