@@ -120,12 +120,7 @@ def main():
     params = D.params_for(w)
     planes, plan = D.densenet_build_pyramid(imgs, params, dt)
     ppi = len(plan.planes)
-    desc = []
-    for b in range(n_img):
-        for d in plan.planes:
-            q = D.dn_plane_desc()
-            q.h, q.w, q.offset = d.h, d.w, b * plan.image_elems + d.offset
-            desc.append(q)
+    desc = plan.image_descs(n_img)
     net = D.net_params(pool5=False)
     cf = D.ConvFeatures(desc, dt, net, device=dev)
     c5d = list(cf.c5d)

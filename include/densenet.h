@@ -23,8 +23,9 @@
  *    enqueued asynchronously on it; outputs are valid once the stream reaches that point.
  *  - dtypes: DN_F32, DN_F16, DN_BF16 select the storage and MFMA input type of planes and
  *    activations; accumulation is always fp32.  Region descriptors are always fp32.
- *  - Layouts: images are uint8 [n_img][3][H][W].  Planes are channel-major [3][PH][PW] per plane,
- *    packed back to back.  Activations and conv5 maps are channels-last [Hc][Wc][C] per plane, packed
+ *  - Layouts: images are uint8 [n_img][3][H][W].  Planes are channel-major [3][PH][pitch] per plane,
+ *    packed back to back, with rows of pitch = PW rounded up to a multiple of DN_PLANE_ROW_ALIGN
+ *    elements (columns PW .. pitch-1 hold 0).  Activations and conv5 maps are channels-last [Hc][Wc][C] per plane, packed
  *    back to back.
  */
 #ifndef DENSENET_H
@@ -51,6 +52,10 @@ typedef enum { DN_F32 = 0, DN_F16 = 1, DN_BF16 = 2 } dn_dtype;
 typedef enum { DN_PAD_ZERO = 0, DN_PAD_RAMP = 1 } dn_pad_mode;
 
 #define DN_MAX_SCALES 64 /* pyramid entries (scales x aspect ratios) */
+/* Row alignment of the planes the library plans and builds, in elements: every row of a plane then
+ * starts on a 128-byte boundary (256 at fp32) of a 256-byte aligned buffer, so no two workgroups of
+ * the builder write parts of one cache line. */
+#define DN_PLANE_ROW_ALIGN 64
 #define DN_MAX_PLANES_PER_IMAGE 64
 #define DN_MAX_ASPECTS 8
 
@@ -104,10 +109,11 @@ typedef struct {
 } dn_scale_geom;
 
 /* One plane or map: h x w pixels at `offset` elements from the start of its buffer.
- * pitch: elements between consecutive rows of a channel-major input plane of densenet_conv_features
- * (channels are h * pitch apart); 0 means w.  A pitch that is a multiple of 8 (16 bytes at 16-bit
- * storage) lets conv1 load plane rows directly into LDS whatever the width; the columns between w and
- * pitch are never read into a stored output.  Every other use ignores pitch and writes 0. */
+ * pitch: elements between consecutive rows of a channel-major plane (channels are h * pitch apart);
+ * 0 means w.  The planners and builders write pitch = w rounded up to a multiple of
+ * DN_PLANE_ROW_ALIGN; densenet_conv_features takes any pitch >= w (a multiple of 8 lets conv1 load
+ * plane rows directly into LDS whatever the width); the columns between w and pitch are never read
+ * into a stored output.  Maps (conv5, pool5) and every other use ignore pitch and write 0. */
 typedef struct {
   int32_t h, w;
   int64_t offset;
@@ -129,8 +135,8 @@ typedef struct {
 
 /* Geometry only (host, no device work): scales, sizes, stitching and conv5 windows for an H x W image.
  * Image sides are limited to 32768 px and scaled sides to 65535 px (DN_E_TOO_LARGE beyond).
- * geom: [n_scales] out.  planes: [max_planes] out, the planes of ONE image, offsets in elements of the
- * packed [3][PH][PW] planes; *image_elems = elements per image.  Returns DN_E_TOO_LARGE when a padded
+ * geom: [n_scales] out.  planes: [max_planes] out, the planes of ONE image (h, w, pitch and offset in
+ * elements of the packed [3][h][pitch] planes); *image_elems = elements per image.  Returns DN_E_TOO_LARGE when a padded
  * scale exceeds the stitching plane or the plane count exceeds max_planes. */
 int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_scale_geom* geom,
                           dn_plane_desc* planes, int32_t max_planes, int32_t* n_planes,
@@ -173,7 +179,8 @@ int densenet_build_pyramid_noalloc(const uint8_t* d_images, int32_t n_img, int32
  * image's entries, ties going to the smaller item index b * E + e.  p->plane_h and plane_w must be
  * positive.  geom: [n_img * E] out, entry e of image b at b * E + e, with .image = b, .k = e and .plane
  * counting over the batch.  planes: [max_planes] out, plane j of plane_h x plane_w at offset
- * j * 3 * plane_h * plane_w elements; *total_elems = elements of all planes.  Returns DN_E_TOO_LARGE
+ * j * 3 * plane_h * pitch elements, pitch = plane_w rounded up to a multiple of DN_PLANE_ROW_ALIGN;
+ * *total_elems = elements of all planes.  Returns DN_E_TOO_LARGE
  * when more than max_planes planes are needed (*n_planes still receives the count) or n_img * E
  * exceeds DN_MAX_BATCH_ITEMS. */
 #define DN_MAX_BATCH_ITEMS 65536
@@ -187,7 +194,7 @@ int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_pa
  * d_geom: a device copy of it (the kernel reads the placements there; upload it once per plan).
  * The host array is validated; an entry of d_geom that is not a placement inside a plane of this
  * batch is ignored by the kernel (its pixels stay background), so a stale copy gives wrong planes but
- * no out-of-bounds access.  d_planes: [n_planes][3][plane_h][plane_w] in `dtype`, followed by the
+ * no out-of-bounds access.  d_planes: [n_planes][3][plane_h][pitch] in `dtype`, followed by the
  * builder's scratch (the pixel image, 4 * H * W * n_img bytes, then per-plane item lists,
  * 4 * (n_planes + 1 + n_img * E) bytes, each part 256-byte aligned; contents afterwards unspecified),
  * or NULL for a size query into *bytes_needed.  n_img * H * W must be below 2^32 and n_planes at most

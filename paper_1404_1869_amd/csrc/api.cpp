@@ -249,10 +249,12 @@ int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_s
     std::copy(plan.scales.begin(), plan.scales.end(), geom);
     int64_t off = 0;
     for (int32_t j = 0; j < np; ++j) {
+      planes[j] = dn_plane_desc{};
       planes[j].h = plan.planes[j].h;
       planes[j].w = plan.planes[j].w;
+      planes[j].pitch = plane_pitch(plan.planes[j].w);
       planes[j].offset = off;
-      off += 3LL * plan.planes[j].h * plan.planes[j].w;
+      off += 3LL * plan.planes[j].h * planes[j].pitch;
     }
     *image_elems = off;
     return DN_OK;
@@ -312,14 +314,16 @@ static int build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int3
       mh = std::max(mh, planes[j].h);
       mw = std::max(mw, planes[j].w);
     }
+    int32_t max_scale_w = 0;
+    for (int k = 0; k < K; ++k) max_scale_w = std::max(max_scale_w, geom[k].w);
     uint8_t* pix = (uint8_t*)d_planes + planes_end;
     if (static_scratch_area) {
       const int e = static_scratch(&pix);
       if (e != (int)hipSuccess) return hip_status(e, "static scratch lookup");
     }
     TraceScope trace("build_planes", stream);
-    return hip_status(launch_build_planes(d_images, n_img, a, pl, nullptr, mh, mw, dtype, d_planes, pix,
-                                          stream),
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, nullptr, mh, mw, max_scale_w, dtype,
+                                          d_planes, pix, stream),
                       "build_planes launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
@@ -357,11 +361,12 @@ int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_pa
     *n_planes = np;
     if (np > max_planes) return fail(DN_E_TOO_LARGE, "more planes than max_planes");
     std::copy(items.begin(), items.end(), geom);
-    const int64_t pe = 3LL * p->plane_h * p->plane_w;
+    const int64_t pe = 3LL * p->plane_h * plane_pitch(p->plane_w);
     for (int32_t j = 0; j < np; ++j) {
       planes[j] = dn_plane_desc{};
       planes[j].h = p->plane_h;
       planes[j].w = p->plane_w;
+      planes[j].pitch = plane_pitch(p->plane_w);
       planes[j].offset = j * pe;
     }
     *total_elems = np * pe;
@@ -395,7 +400,7 @@ int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int3
     }
     if ((int64_t)n_img * H * W > 0xffffffffLL)
       return fail(DN_E_TOO_LARGE, "a packed batch is limited to 2^32 - 1 image pixels");
-    const int64_t pe = 3LL * p->plane_h * p->plane_w;
+    const int64_t pe = 3LL * p->plane_h * plane_pitch(p->plane_w);
     const size_t planes_end = ((size_t)n_planes * (size_t)pe * dtype_size(dtype) + 255) & ~(size_t)255;
     const size_t need = planes_end + builder_scratch_bytes(n_img, H, W, n_planes, (int32_t)(n_img * E));
     *bytes_needed = need;
@@ -413,9 +418,12 @@ int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int3
     for (int c = 0; c < 3; ++c) a.mean[c] = p->mean[c];
     PyrPlanes pl{};
     BatchGeom bg{d_geom, (int32_t)(n_img * E), n_img, n_planes, p->plane_h, p->plane_w, nullptr, nullptr};
+    int32_t max_scale_w = 0;
+    for (int64_t i = 0; i < n_img * E; ++i) max_scale_w = std::max(max_scale_w, geom[i].w);
     TraceScope trace("build_planes", stream);
-    return hip_status(launch_build_planes(d_images, n_img, a, pl, &bg, p->plane_h, p->plane_w, dtype,
-                                          d_planes, (uint8_t*)d_planes + planes_end, stream),
+    return hip_status(launch_build_planes(d_images, n_img, a, pl, &bg, p->plane_h, p->plane_w,
+                                          max_scale_w, dtype, d_planes, (uint8_t*)d_planes + planes_end,
+                                          stream),
                       "build_planes launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");

@@ -59,6 +59,10 @@ struct PyrArgs {
   uint8_t plane_first[DN_MAX_PLANES_PER_IMAGE];  // first entry of s[] on each plane
   uint8_t plane_count[DN_MAX_PLANES_PER_IMAGE];  // entries of s[] on each plane
 };
+// Row pitch of a plane w pixels wide: w rounded up to a multiple of DN_PLANE_ROW_ALIGN elements.
+__host__ __device__ inline int32_t plane_pitch(int32_t w) {
+  return (w + DN_PLANE_ROW_ALIGN - 1) / DN_PLANE_ROW_ALIGN * DN_PLANE_ROW_ALIGN;
+}
 struct PyrPlane {
   int32_t h, w;
   int64_t offset;
@@ -95,9 +99,11 @@ inline size_t builder_scratch_bytes(int32_t n_img, int32_t H, int32_t W, int32_t
 // Device address of the scratch-free builder's static staging array on the current device (looked up
 // once per device).  Returns a hipError_t.
 int static_scratch(uint8_t** out);
+// max_h, max_w: largest plane; max_scale_w: widest scaled image (selects the exact-integer
+// horizontal taps when at most 32767).
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
-                        uint8_t* d_scratch, void* stream);
+                        const BatchGeom* batch, int32_t max_h, int32_t max_w, int32_t max_scale_w,
+                        dn_dtype dt, void* d_out, uint8_t* d_scratch, void* stream);
 
 // Crop-before windows: n boxes warped to S x S channel-major planes (windows.hip).
 int launch_warp_regions(const uint8_t* d_img, int32_t n_img, int32_t H, int32_t W, const float* d_boxes,

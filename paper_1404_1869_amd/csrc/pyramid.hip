@@ -6,9 +6,12 @@
 // bilinear tap of all three channels is a single 4-byte load, and one image (3 MB at 768 x 1024) fits
 // an XCD's L2.  The builder then produces 4 plane pixels per thread, 64 columns apart, so that each
 // of a wave's gathers reads the taps of 64 consecutive pixels and each store writes 64 consecutive
-// pixels of a channel; a wave covers 256 columns.  Workgroups are ordered so that each XCD works
-// through a contiguous range of images and planes.  The half-pixel source coordinate
-// ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers; only the blend is fp32.
+// pixels of a channel; a wave covers 256 columns.  Plane rows are padded to a multiple of 64 elements
+// (written as 0), so every store instruction fills whole cache lines.  Workgroups are ordered so that
+// each XCD works through a contiguous range of images and planes.  The half-pixel source coordinate
+// ((2 y + 1) H - h) / (2 h) is formed exactly in 32-bit integers, the horizontal blend of a source
+// row is exact in integers (v_dot2_u32_u16 of the two taps with the weights 2 w - r and r), and only
+// the vertical blend, the centring and the border weight are fp32.
 #include "common.h"
 
 #include <mutex>
@@ -17,13 +20,10 @@
 namespace dn {
 namespace {
 
-// Tile shape (plane pixels per thread, rows per workgroup tile), compile-time settings chosen by
-// timing the 96-plane batch (2 or 8 pixels per thread and 8-row tiles were slower).
+// Plane pixels per thread, a compile-time setting chosen by timing the 96-plane batch (2 or 8 pixels
+// per thread were slower).
 #ifndef DN_BUILD_PX
 #define DN_BUILD_PX 4
-#endif
-#ifndef DN_BUILD_ROWS
-#define DN_BUILD_ROWS 16
 #endif
 constexpr int PX = DN_BUILD_PX;  // plane pixels per thread
 
@@ -54,15 +54,15 @@ __device__ inline float border_weight(int d, int pad, bool ramp) {
   return (float)(pad + 1 - d) / (float)(pad + 1);
 }
 
-// Workgroup tile: 16 plane rows x 64 * PX columns; each lane owns PX consecutive columns and the
-// four waves take the tile's rows in turn.  In stitched planes every rectangle edge is a multiple of
-// 16 px, and a per-scale plane is its scale's rectangle, so each 16 x 16 cell of a 16-row-aligned tile
-// has a single owner scale (or none).  Per tile the workgroup finds the owner of each of its 16 cells
-// and tabulates, per (cell, row), the two source rows, the row fraction and the row's border weight;
-// each lane computes its columns' source coordinates and border weights once and then only blends
-// per row.
-constexpr int TROWS = DN_BUILD_ROWS;     // rows per tile
-static_assert(16 % TROWS == 0 && TROWS % 4 == 0, "a tile's rows lie in one row of 16-px cells");
+// Workgroup tile: NBANDS bands of 16 plane rows x 64 * PX columns (4 bands on large launches, 1 where
+// a launch has too few tiles to fill the chip).  In stitched planes every rectangle edge
+// is a multiple of 16 px, and a per-scale plane is its scale's rectangle, so each 16 x 16 cell of a
+// band has a single owner scale (or none).  Per tile the workgroup finds the owners of its cells and
+// tabulates, per (cell, row), the two source rows, the row fraction and the row's border weight.  The
+// four waves take the tile's rows in turn (wave w: rows w, w + 4, ...), so at any time they read the
+// same few source rows; a lane computes its columns' taps for the first band and again only where
+// a later band's owner differs.
+constexpr int BAND = 16;                 // rows per band (one row of 16-px cells)
 constexpr int TCELLS = 64 * PX / 16;     // 16-px cells per tile row
 
 // Pixel image: pix[b][y][x] = R | G << 8 | B << 16, one thread per pixel (any width), or per 4 pixels
@@ -154,22 +154,46 @@ __device__ inline bool valid_item(const dn_scale_geom& g, const BatchGeom& bg) {
          g.y >= 0 && g.x >= 0 && g.y <= bg.PH - g.rh && g.x <= bg.PW - g.rw;
 }
 
+
+// PAIR (source width at least 2): the two taps of a source row are one 8-byte load.
+
 // BATCH = false: planes of each image (a.s, pl), blocks z = image * pl.n + plane.  BATCH = true: the
 // planes of a cross-image packed batch (bg), blocks z = plane, each cell sampling its owner's image.
 // Two consecutive pixels of the pixel image: 4-byte aligned (a dword-aligned 8-byte load).
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
-// PAIR (source width at least 2): the two taps of a source row are one 8-byte load.
-template <typename T, bool BATCH, bool PAIR>
+// Keeps the compiler from moving this wave's LDS accesses across it (a wave's own LDS operations
+// execute in order).
+__device__ inline void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
+// Horizontal taps of one source row, exact in integers: for the 4-byte pixels q0 (left) and q1
+// (right), channel c gives I0 (Dx - rx) + I1 rx = Dx ((1 - lx) I0 + lx I1), with the column fraction
+// lx = rx / Dx, Dx = 2 w (at most 65535) and the weights packed as u16 pairs (Dx - rx) | rx << 16.
+// v_perm_b32 places byte c of q0 and of q1 in the two 16-bit halves of one dword.
+template <int C>
+__device__ inline uint32_t taps_x(uint32_t q0, uint32_t q1, uint32_t wts) {
+  constexpr uint32_t sel = 0x0c000c00u | ((4u + C) << 16) | (uint32_t)C;
+  const uint32_t pair = __builtin_amdgcn_perm(q1, q0, sel);
+  return __builtin_amdgcn_udot2(__builtin_bit_cast(u16x2, pair), __builtin_bit_cast(u16x2, wts), 0u,
+                                false);
+}
+
+// PAIR (source width at least 2): the two taps of a source row are one 8-byte load.  XDOT (every
+// scale at most 32767 px wide): horizontal taps in exact integers (taps_x); otherwise an fp32 lerp.
+template <typename T, bool BATCH, bool PAIR, bool XDOT, int NBANDS>
 __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __restrict__ pix,
                                                            PyrArgs a, PyrPlanes pl, BatchGeom bg,
                                                            T* __restrict__ out, int tiles_x,
                                                            int tiles_y) {
-  static_assert(TCELLS <= 256, "one owner search per thread");
-  __shared__ int s_own[TCELLS];
-  __shared__ PyrScale s_sc[TCELLS];  // owner's rectangle, per cell
-  __shared__ int s_img[TCELLS];      // owner's image, per cell
-  __shared__ RowEntry s_row[TCELLS * TROWS];
+  constexpr int TROWS = NBANDS * BAND;    // rows of the tile
+  constexpr int NCELL = NBANDS * TCELLS;  // cells of the tile, band-major
+  static_assert(NCELL <= 256 && (NCELL * BAND) % 256 == 0, "one cell per thread");
+  __shared__ int s_own[NCELL];
+  __shared__ PyrScale s_sc[NCELL];   // owner's rectangle, per cell
+  __shared__ double s_inv[NCELL];    // 1 / (2 h) of the owner, per cell
+  __shared__ uint32_t s_img[NCELL];  // owner's image offset (pixels), per cell
+  __shared__ RowEntry s_row[NCELL * BAND];
   // XCD-aware order over a flat grid: XCD x takes a contiguous range of (image, plane, row tile,
   // column tile) indices, so the tiles in flight on one XCD read the same image from its L2.
   const int nbk = gridDim.x, xcd = blockIdx.x % 8, per = nbk / 8, rem = nbk % 8;
@@ -180,42 +204,49 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   const int z = bid / tiles_y;
   const int b = BATCH ? 0 : z / pl.n, j = BATCH ? z : z - b * pl.n;
   const int PH = BATCH ? bg.PH : pl.p[j].h, PW = BATCH ? bg.PW : pl.p[j].w;
-  const int tx0 = gx * 64 * PX, ty0 = gy * TROWS;
-  if (tx0 >= PW || ty0 >= PH) return;  // uniform per workgroup
+  const int PP = plane_pitch(PW);  // row pitch; columns PW .. PP - 1 are written as 0
+  const int ty0 = gy * TROWS;
+  const int tx0 = gx * 64 * PX;
+  if (tx0 >= PP || ty0 >= PH) return;  // uniform per workgroup
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
 
+  // Owners of the tile's cells (cell c = band * TCELLS + column).
   if constexpr (BATCH) {
-    // Rectangles never overlap and their edges are multiples of 16, so each cell of this 16-row band
-    // has at most one owner among the items on plane j.
-    if (tid < TCELLS) s_own[tid] = -1;
+    // Rectangles never overlap and their edges are multiples of 16, so each cell has at most one
+    // owner among the items on plane j.
+    if (tid < NCELL) s_own[tid] = -1;
     __syncthreads();
     for (int i = bg.first[j] + tid; i < bg.first[j + 1]; i += 256) {
       const int e = bg.list[i];
       const dn_scale_geom& g = bg.geom[e];
-      if (g.plane != j || !valid_item(g, bg) || ty0 < g.y || ty0 >= g.y + g.rh) continue;
+      if (g.plane != j || !valid_item(g, bg)) continue;
+      const int r_lo = max(0, (g.y - ty0) / 16), r_hi = min(NBANDS, (g.y + g.rh - ty0) / 16);
       const int c_lo = max(0, (g.x - tx0) / 16), c_hi = min(TCELLS, (g.x + g.rw - tx0) / 16);
-      for (int c = c_lo; c < c_hi; ++c) s_own[c] = e;
+      for (int r = r_lo; r < r_hi; ++r)
+        for (int c = c_lo; c < c_hi; ++c) s_own[r * TCELLS + c] = e;
     }
     __syncthreads();
-    if (tid < TCELLS) {
+    if (tid < NCELL) {
       const int e = s_own[tid];
-      if (e >= 0 && tx0 + 16 * tid < PW) {
+      const int cy = ty0 + 16 * (tid / TCELLS), cx = tx0 + 16 * (tid % TCELLS);
+      if (e >= 0 && cx < PW && cy < PH) {
         const dn_scale_geom& g = bg.geom[e];
         s_sc[tid] = PyrScale{g.plane, g.y, g.x, g.rh, g.rw, g.h, g.w};
-        s_img[tid] = g.image;
+        s_img[tid] = (uint32_t)g.image * (uint32_t)a.H * (uint32_t)a.W;
+        s_inv[tid] = 1.0 / (2.0 * g.h);
       } else {
         s_own[tid] = -1;
       }
     }
   } else {
     const int f0 = a.plane_first[j], f1 = f0 + a.plane_count[j];
-    if (tid < TCELLS) {
-      const int cx = tx0 + 16 * tid;
+    if (tid < NCELL) {
+      const int cy = ty0 + 16 * (tid / TCELLS), cx = tx0 + 16 * (tid % TCELLS);
       int owner = -1;
-      for (int e = f0; e < f1 && cx < PW; ++e) {
+      for (int e = f0; e < f1 && cx < PW && cy < PH; ++e) {
         const PyrScale& s = a.s[e];
-        if (ty0 >= s.y && ty0 < s.y + s.rh && cx >= s.x && cx < s.x + s.rw) {
+        if (cy >= s.y && cy < s.y + s.rh && cx >= s.x && cx < s.x + s.rw) {
           owner = e;
           break;
         }
@@ -223,13 +254,17 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       s_own[tid] = owner;
       if (owner >= 0) {
         s_sc[tid] = a.s[owner];
-        s_img[tid] = b;
+        s_img[tid] = 0u;
+        s_inv[tid] = 1.0 / (2.0 * a.s[owner].h);
       }
     }
   }
   __syncthreads();
-  for (int ent = tid; ent < TCELLS * TROWS; ent += 256) {
-    const int cell = ent / TROWS, r = ent % TROWS, y = ty0 + r;
+  // Row table: entry (cell, r) for row 16 band + r of the tile.
+#pragma unroll
+  for (int k = 0; k < NCELL * BAND / 256; ++k) {
+    const int ent = k * 256 + tid, cell = ent / BAND, r = ent % BAND;
+    const int y = ty0 + 16 * (cell / TCELLS) + r;
     RowEntry re{0u, 0u, 0.f, 0.f};
     if (s_own[cell] >= 0 && y < PH) {
       const PyrScale& s = s_sc[cell];
@@ -237,12 +272,11 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       const int dy = max(0, max(-vy, vy - (s.h - 1)));
       re.wy = border_weight(dy, a.pad, a.ramp);
       int sy0, sy1;
-      src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, 1.0 / (2.0 * s.h), sy0, sy1, re.ly);
+      src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, s_inv[cell], sy0, sy1, re.ly);
       // a packed batch reads the owner's image: its offset is folded into the row offsets, so the
       // pixel loads keep one base address for the whole workgroup
-      const uint32_t img_off = BATCH ? (uint32_t)s_img[cell] * (uint32_t)a.H * (uint32_t)a.W : 0u;
-      re.r0 = img_off + (uint32_t)sy0 * (uint32_t)a.W;
-      re.r1 = img_off + (uint32_t)sy1 * (uint32_t)a.W;
+      re.r0 = s_img[cell] + (uint32_t)sy0 * (uint32_t)a.W;
+      re.r1 = s_img[cell] + (uint32_t)sy1 * (uint32_t)a.W;
     }
     s_row[ent] = re;
   }
@@ -250,78 +284,139 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
 
   // This lane's columns x_i = tx0 + lane + 64 i: each gather instruction of a wave then reads the
   // taps of 64 consecutive plane pixels (few cache lines), and each store writes 64 consecutive
-  // pixels of one channel.  Per column: its cell, border weight, source columns and fraction.
-  int cl[PX];
+  // pixels of one channel.  Per column: its owner, border weight, first source column and the
+  // horizontal weights (XDOT: u16 pair and 1 / Dx; else the fp32 fraction lx).
   bool inside[PX];
-  float wx[PX], lx[PX];
-  uint32_t sx0[PX], sx1[PX];
-#pragma unroll
-  for (int i = 0; i < PX; ++i) {
-    const int xl = lane + 64 * i, x = tx0 + xl;
-    cl[i] = xl >> 4;
-    inside[i] = x < PW;
+  int own[PX];
+  float wx[PX], hx[PX];  // border weight; 1 / Dx (XDOT) or the column fraction lx
+  uint32_t sx0[PX], sx1[PX], wts[PX];
+  auto column_taps = [&](int i, int cell) {
+    const int x = tx0 + lane + 64 * i;
     wx[i] = 0.f;
-    lx[i] = 0.f;
+    hx[i] = XDOT ? 1.f : 0.f;
     sx0[i] = sx1[i] = 0u;
-    if (inside[i] && s_own[cl[i]] >= 0) {
-      const PyrScale& s = s_sc[cl[i]];
+    wts[i] = 0u;
+    if (own[i] >= 0) {
+      const PyrScale& s = s_sc[cell];
       const int ux = x - s.x - a.pad;
       const int dx = max(0, max(-ux, ux - (s.w - 1)));
       wx[i] = border_weight(dx, a.pad, a.ramp);
-      int c0, c1;  // c1 = min(c0 + 1, W - 1)
-      src_coord(min(max(ux, 0), s.w - 1), a.W, s.w, 1.0 / (2.0 * s.w), c0, c1, lx[i]);
-      // On the last source column (c1 = c0) the pair starts one column earlier with fraction 1:
-      // a + 1 (b - a) is exactly b for these small integers, the value the clamped tap gives.
+      // half-pixel source column ((2 u + 1) W - w) / (2 w), clamped at 0: c0 and remainder rx
+      const int u = min(max(ux, 0), s.w - 1);
+      const int64_t num = (int64_t)(2 * u + 1) * a.W - s.w;
+      const uint32_t n = num > 0 ? (uint32_t)num : 0u, d = 2u * (uint32_t)s.w;
+      uint32_t rx;
+      int c0 = (int)udiv_exact(n, d, 1.0 / (double)d, rx);
+      const int c1 = min(c0 + 1, a.W - 1);
+      // On the last source column (c1 = c0) the pair starts one column earlier with all the weight
+      // on its right tap, the value the clamped tap gives.
       if (PAIR && c1 == c0) {
         c0 -= 1;
-        lx[i] = 1.f;
+        rx = d;
       }
       sx0[i] = (uint32_t)c0;
       sx1[i] = (uint32_t)c1;
+      if constexpr (XDOT) {
+        wts[i] = (d - rx) | (rx << 16);
+        hx[i] = 1.f / (float)d;
+      } else {
+        hx[i] = (float)((double)rx / (double)d);
+      }
     }
+  };
+#pragma unroll
+  for (int i = 0; i < PX; ++i) {
+    inside[i] = tx0 + lane + 64 * i < PP;
+    own[i] = -2;  // nothing computed yet
   }
   const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
-  T* o = out + (BATCH ? (int64_t)j * 3 * PH * PW : (int64_t)b * pl.image_elems + pl.p[j].offset);
-  const int64_t plane = (int64_t)PH * PW;
+  T* o = out + (BATCH ? (int64_t)j * 3 * PH * PP : (int64_t)b * pl.image_elems + pl.p[j].offset);
+  const int64_t plane = (int64_t)PH * PP;
+  const float mean[3] = {a.mean[0], a.mean[1], a.mean[2]};
 
-  // Rows wave, wave + 4, ... of the tile, unrolled so that the taps of several rows are in flight.
-  // Every pixel reads its four taps (background pixels and pixels outside a scale's border read valid
-  // pixels, with weight 0), so the loads carry no per-pixel branch.
+  // A row's taps (4 pixels per lane) and its per-pixel row fraction and weight.
+  struct RowTaps {
+    uint32_t q[PX][4];  // (row 0, col 0), (row 0, col 1), (row 1, col 0), (row 1, col 1)
+    float ly[PX], wgt[PX];
+  };
+  auto fetch = [&](int band, int r, RowTaps& t) {
 #pragma unroll
-  for (int rr = 0; rr < TROWS / 4; ++rr) {
-    const int r = wave + 4 * rr;
-    const int y = ty0 + r;
-    if (y >= PH) break;  // uniform per wave
+    for (int i = 0; i < PX; ++i) {
+      const int cell = band * TCELLS + ((lane + 64 * i) >> 4);
+      const RowEntry re = s_row[cell * BAND + r];
+      t.ly[i] = re.ly;
+      t.wgt[i] = re.wy * wx[i];
+      if constexpr (PAIR) {
+        const u32x2 a0 = *(const u32x2*)(P + (re.r0 + sx0[i]));
+        const u32x2 a1 = *(const u32x2*)(P + (re.r1 + sx0[i]));
+        t.q[i][0] = a0.x, t.q[i][1] = a0.y, t.q[i][2] = a1.x, t.q[i][3] = a1.y;
+      } else {
+        t.q[i][0] = P[re.r0 + sx0[i]], t.q[i][1] = P[re.r0 + sx1[i]];
+        t.q[i][2] = P[re.r1 + sx0[i]], t.q[i][3] = P[re.r1 + sx1[i]];
+      }
+    }
+  };
+  //   XDOT: the two rows' taps T0, T1 are exact integers below 2^24 (so exact in fp32); the value is
+  //   ((T0 + ly (T1 - T0)) / Dx - mean) * weight, as fma(ly, T1 - T0, T0), fma(., 1 / Dx, -mean)
+  //   and a product.  Otherwise the fp32 lerps run on the fraction lx.
+  auto emit = [&](int y, const RowTaps& t) {
     float v[PX][3];
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      const RowEntry re = s_row[cl[i] * TROWS + r];
-      const float wgt = re.wy * wx[i];
-      uint32_t q00, q01, q10, q11;
-      if constexpr (PAIR) {
-        const u32x2 t = *(const u32x2*)(P + re.r0 + sx0[i]), u = *(const u32x2*)(P + re.r1 + sx0[i]);
-        q00 = t.x, q01 = t.y, q10 = u.x, q11 = u.y;
-      } else {
-        q00 = P[re.r0 + sx0[i]], q01 = P[re.r0 + sx1[i]];
-        q10 = P[re.r1 + sx0[i]], q11 = P[re.r1 + sx1[i]];
-      }
+      const uint32_t q00 = t.q[i][0], q01 = t.q[i][1], q10 = t.q[i][2], q11 = t.q[i][3];
+      if constexpr (XDOT) {
+        const uint32_t t0[3] = {taps_x<0>(q00, q01, wts[i]), taps_x<1>(q00, q01, wts[i]),
+                                taps_x<2>(q00, q01, wts[i])};
+        const uint32_t t1[3] = {taps_x<0>(q10, q11, wts[i]), taps_x<1>(q10, q11, wts[i]),
+                                taps_x<2>(q10, q11, wts[i])};
 #pragma unroll
-      for (int c = 0; c < 3; ++c) {
-        const int sh = 8 * c;
-        const float i00 = (float)((q00 >> sh) & 255u), i01 = (float)((q01 >> sh) & 255u);
-        const float i10 = (float)((q10 >> sh) & 255u), i11 = (float)((q11 >> sh) & 255u);
-        const float top = i00 + lx[i] * (i01 - i00), bot = i10 + lx[i] * (i11 - i10);
-        v[i][c] = (top + re.ly * (bot - top) - a.mean[c]) * wgt;
+        for (int c = 0; c < 3; ++c) {
+          const float f0 = (float)t0[c], f1 = (float)t1[c];
+          const float vr = __builtin_fmaf(t.ly[i], f1 - f0, f0);
+          v[i][c] = __builtin_fmaf(vr, hx[i], -mean[c]) * t.wgt[i];
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+          const int sh = 8 * c;
+          const float i00 = (float)((q00 >> sh) & 255u), i01 = (float)((q01 >> sh) & 255u);
+          const float i10 = (float)((q10 >> sh) & 255u), i11 = (float)((q11 >> sh) & 255u);
+          const float top = i00 + hx[i] * (i01 - i00), bot = i10 + hx[i] * (i11 - i10);
+          v[i][c] = (top + t.ly[i] * (bot - top) - mean[c]) * t.wgt[i];
+        }
       }
     }
-    T* orow = o + (int64_t)y * PW + tx0 + lane;
+    T* orow = o + (int64_t)y * PP + tx0 + lane;
 #pragma unroll
     for (int c = 0; c < 3; ++c)
 #pragma unroll
       for (int i = 0; i < PX; ++i)
         if (inside[i]) orow[c * plane + 64 * i] = from_f32<T>(v[i][c]);
-  }
+  };
 
+  // Per band: refresh the columns whose owner changed, then the wave's 4 rows of the band.
+  for (int band = 0; band < NBANDS; ++band) {
+    const int yb = ty0 + BAND * band;
+    if (yb >= PH) break;  // uniform
+#pragma unroll
+    for (int i = 0; i < PX; ++i) {
+      const int cell = band * TCELLS + ((lane + 64 * i) >> 4);
+      const int o_new = inside[i] ? s_own[cell] : -1;
+      if (o_new != own[i]) {
+        own[i] = o_new;
+        column_taps(i, cell);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < BAND / 4; ++k) {
+      const int r = wave + 4 * k;
+      if (yb + r < PH) {
+        RowTaps t;
+        fetch(band, r, t);
+        emit(yb + r, t);
+      }
+    }
+  }
 }
 
 }  // namespace
@@ -352,16 +447,20 @@ int static_scratch(uint8_t** out) {
 }
 
 int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, const PyrPlanes& pl,
-                        const BatchGeom* batch, int32_t max_h, int32_t max_w, dn_dtype dt, void* d_out,
-                        uint8_t* d_scratch, void* stream) {
+                        const BatchGeom* batch, int32_t max_h, int32_t max_w, int32_t max_scale_w,
+                        dn_dtype dt, void* d_out, uint8_t* d_scratch, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   uint32_t* pix = (uint32_t*)d_scratch;
   if (a.W % 4 == 0)
     pixel_image4_kernel<<<dim3((a.W / 4 + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
   else
     pixel_image_kernel<<<dim3((a.W + 255) / 256, a.H, n_img), 256, 0, s>>>(d_img, a.H, a.W, pix);
-  const int tiles_x = (max_w + 64 * PX - 1) / (64 * PX), tiles_y = (max_h + TROWS - 1) / TROWS;
-  const int64_t nblk = (int64_t)tiles_x * tiles_y * (batch ? batch->n_planes : n_img * pl.n);
+  // 64-row tiles (4 bands) where that still gives at least 4096 workgroups, else 16-row tiles
+  const int tiles_x = (plane_pitch(max_w) + 64 * PX - 1) / (64 * PX);
+  const int64_t n_pl = batch ? batch->n_planes : (int64_t)n_img * pl.n;
+  const bool tall = (int64_t)tiles_x * ((max_h + 4 * BAND - 1) / (4 * BAND)) * n_pl >= 4096;
+  const int tiles_y = tall ? (max_h + 4 * BAND - 1) / (4 * BAND) : (max_h + BAND - 1) / BAND;
+  const int64_t nblk = (int64_t)tiles_x * tiles_y * n_pl;
   if (nblk > 0x7fffffff) return (int)hipErrorInvalidValue;
   const unsigned grid = (unsigned)nblk;
   BatchGeom bg = batch ? *batch : BatchGeom{};
@@ -375,13 +474,30 @@ int launch_build_planes(const uint8_t* d_img, int32_t n_img, const PyrArgs& a, c
     bg.first = first;
     bg.list = list;
   }
-  auto go2 = [&](auto tag, auto pair) {
+  // exact integer horizontal taps need 2 w <= 65535 (u16 weights) for every scale
+  const bool xdot = max_scale_w <= 32767;
+  auto go4 = [&](auto tag, auto pair, auto xd, auto nbands) {
     using T = decltype(tag);
-    constexpr bool PAIR = decltype(pair)::value;
+    constexpr bool PAIR = decltype(pair)::value, XDOT = decltype(xd)::value;
+    constexpr int NB = decltype(nbands)::value;
     if (batch)
-      build_planes_kernel<T, true, PAIR><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+      build_planes_kernel<T, true, PAIR, XDOT, NB>
+          <<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
     else
-      build_planes_kernel<T, false, PAIR><<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+      build_planes_kernel<T, false, PAIR, XDOT, NB>
+          <<<grid, 256, 0, s>>>(pix, a, pl, bg, (T*)d_out, tiles_x, tiles_y);
+  };
+  auto go3 = [&](auto tag, auto pair, auto xd) {
+    if (tall)
+      go4(tag, pair, xd, std::integral_constant<int, 4>{});
+    else
+      go4(tag, pair, xd, std::integral_constant<int, 1>{});
+  };
+  auto go2 = [&](auto tag, auto pair) {
+    if (xdot)
+      go3(tag, pair, std::true_type{});
+    else
+      go3(tag, pair, std::false_type{});
   };
   auto go = [&](auto tag) {
     if (a.W >= 2)

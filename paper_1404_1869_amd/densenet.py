@@ -201,6 +201,25 @@ class PlanResult:
     def scale_array(self) -> np.ndarray:
         return np.array([[g.s, g.sy, g.sx] for g in self.geom], np.float64)
 
+    def image_descs(self, n_img: int) -> list:
+        """Descriptors of the planes of n_img images built with this plan (image b's planes at
+        b * image_elems), image-major, for densenet_conv_features."""
+        out = []
+        for b in range(n_img):
+            for d in self.planes:
+                q = dn_plane_desc()
+                q.h, q.w, q.pitch, q.offset = d.h, d.w, d.pitch, b * self.image_elems + d.offset
+                out.append(q)
+        return out
+
+
+def plane_view(planes, d: dn_plane_desc, base: int = 0):
+    """[3][h][w] view of the plane that descriptor d places in the flat planes tensor (rows d.pitch
+    elements apart), shifted by base elements."""
+    pitch = d.pitch or d.w
+    o = base + d.offset
+    return planes[o:o + 3 * d.h * pitch].view(3, d.h, pitch)[:, :, :d.w]
+
 
 def densenet_plan_pyramid(H: int, W: int, p: dn_pyramid_params) -> PlanResult:
     geom = (dn_scale_geom * n_entries(p))()
@@ -301,7 +320,7 @@ class BatchPlan:
 
 def densenet_build_batch(images, plan: BatchPlan, dtype: int, out=None):
     """images: uint8 device tensor [n_img][3][H][W] -> the packed batch's planes (flat tensor; plane j
-    at j * 3 * plane_h * plane_w, followed by the builder's scratch)."""
+    at j * 3 * plane_h * pitch, followed by the builder's scratch; views: plane_view(out, plan.planes[j]))."""
     torch = _torch()
     n_img, _, H, W = images.shape
     assert (n_img, H, W) == (plan.n_img, plan.H, plan.W), "images do not match the plan"
@@ -549,13 +568,7 @@ def convnet_featpyramid(images, p: dn_pyramid_params, packed, dtype: int, net=No
     net = net or net_params()
     planes, plan = densenet_build_pyramid(images, p, dtype)
     n_img = images.shape[0]
-    desc = []
-    for b in range(n_img):
-        for d in plan.planes:
-            q = dn_plane_desc()
-            q.h, q.w, q.offset = d.h, d.w, b * plan.image_elems + d.offset
-            desc.append(q)
-    cf = densenet_conv_features(planes, desc, dtype, packed, net)
+    cf = densenet_conv_features(planes, plan.image_descs(n_img), dtype, packed, net)
     maps = cf.conv5_maps()
     feat = []
     npl = len(plan.planes)

@@ -51,7 +51,7 @@ def test_size_queries_without_device():
     assert L.densenet_build_pyramid(None, 16, 768, 1024, ctypes.byref(p), D.DN_BF16, None, 0,
                                     ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
                                     ctypes.byref(e), None) == 0
-    assert n.value == 6 and e.value == 6 * 3 * 1200 * 1200
+    assert n.value == 6 and e.value == 6 * 3 * 1200 * 1216   # rows padded to 1216 elements
     # the planes, then the builder's scratch (4 bytes per image pixel) 256-byte aligned after them
     full = (16 * e.value * 2 + 255) // 256 * 256 + 16 * 4 * 768 * 1024
     assert need.value == full
@@ -155,7 +155,7 @@ def test_batch_entry_points_validation():
     n, e = ctypes.c_int32(), ctypes.c_int64()
     assert L.densenet_plan_batch(n_img, 768, 1024, ctypes.byref(p), geom, planes, 200, ctypes.byref(n),
                                  ctypes.byref(e)) == D.DN_OK
-    assert n.value == 88 and e.value == 88 * 3 * 1200 * 1200
+    assert n.value == 88 and e.value == 88 * 3 * 1200 * 1216
     assert L.densenet_plan_batch(n_img, 768, 1024, ctypes.byref(p), geom, planes, 50, ctypes.byref(n),
                                  ctypes.byref(e)) == D.DN_E_TOO_LARGE and n.value == 88
     q = D.pyramid_params(25, 10, pad=16)                       # no stitching planes
@@ -172,7 +172,7 @@ def test_batch_entry_points_validation():
     need = ctypes.c_size_t()
     assert L.densenet_build_batch(None, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, None, 88,
                                   None, 0, ctypes.byref(need), None) == D.DN_OK
-    assert need.value == (88 * 3 * 1200 * 1200 * 2 + 255) // 256 * 256 + n_img * 4 * 768 * 1024 + \
+    assert need.value == (88 * 3 * 1200 * 1216 * 2 + 255) // 256 * 256 + n_img * 4 * 768 * 1024 + \
         4 * (88 + 1 + n_img * E)
     fake = ctypes.c_void_p(256)
     assert L.densenet_build_batch(fake, n_img, 768, 1024, ctypes.byref(p), D.DN_BF16, geom, fake, 88, fake,

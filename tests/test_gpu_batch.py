@@ -42,9 +42,8 @@ def oplan_batch(n_img, w):
                              aspects=list(w.aspects) or None)
 
 
-def views(planes, plan):
-    PH, PW = plan.params.plane_h, plan.params.plane_w
-    return [planes[j * 3 * PH * PW:(j + 1) * 3 * PH * PW].view(3, PH, PW) for j in range(plan.n_planes)]
+def views(D, planes, plan):
+    return [D.plane_view(planes, plan.planes[j]) for j in range(plan.n_planes)]
 
 
 def check_planes(got, ref, dt):
@@ -75,7 +74,7 @@ def test_packed_planes(D, n_img, w, dt):
     planes = D.densenet_build_batch(torch.from_numpy(imgs).cuda(), plan, DTS[dt])
     torch.cuda.synchronize()
     ref = oracle.build_planes(imgs, ref_plan, w.pad_mode, w.mean)
-    for j, v in enumerate(views(planes, plan)):
+    for j, v in enumerate(views(D, planes, plan)):
         check_planes(v, ref[j], dt)
 
 
@@ -86,7 +85,7 @@ def test_packed_rectangles_equal_per_image_rectangles_full_batch(D):
     imgs = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).cuda()
     plan = D.BatchPlan(16, w.H, w.W, D.params_for(w))
     assert plan.n_planes == 88
-    pk = views(D.densenet_build_batch(imgs, plan, DTS["bf16"]), plan)
+    pk = views(D, D.densenet_build_batch(imgs, plan, DTS["bf16"]), plan)
     own, own_plan = D.densenet_build_pyramid(imgs, D.params_for(w), DTS["bf16"])
     torch.cuda.synchronize()
     covered = torch.zeros((88, 1200, 1200), dtype=torch.bool, device="cuda")
@@ -94,8 +93,7 @@ def test_packed_rectangles_equal_per_image_rectangles_full_batch(D):
         for e in range(plan.E):
             g1, gb = own_plan.geom[e], plan.entry(b, e)
             d = own_plan.planes[g1.plane]
-            o = b * own_plan.image_elems + d.offset
-            src = own[o:o + 3 * d.h * d.w].view(3, d.h, d.w)[:, g1.y:g1.y + g1.rh, g1.x:g1.x + g1.rw]
+            src = D.plane_view(own, d, b * own_plan.image_elems)[:, g1.y:g1.y + g1.rh, g1.x:g1.x + g1.rw]
             dst = pk[gb.plane][:, gb.y:gb.y + gb.rh, gb.x:gb.x + gb.rw]
             assert torch.equal(src, dst), (b, e)
             covered[gb.plane, gb.y:gb.y + gb.rh, gb.x:gb.x + gb.rw] = True

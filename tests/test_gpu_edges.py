@@ -61,9 +61,8 @@ def test_ragged_image_small_stitched_planes(D, dt):
 @pytest.mark.parametrize("W", [4000, 3999])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_planes_strongly_reduced_wide_image(D, W, dt):
-    """Scales 0.3 .. 0.106 of a 4000-px-wide image: at the two smaller ones a wave's 256 plane
-    columns need more source columns than the builder stages, so those taps are gathered from the
-    image directly; rows of 4000 px start on 4-byte boundaries, rows of 3999 px do not."""
+    """Scales 0.3 .. 0.106 of a 4000-px-wide image: a wave's 256 plane columns span up to 2400
+    source columns; rows of 4000 px start on 4-byte boundaries, rows of 3999 px do not."""
     H = 40
     img = synth.image(91, H, W)
     p = D.pyramid_params(4, 2, base_scale=0.3, pad=16, pad_mode=D.DN_PAD_RAMP, plane_h=64,
@@ -73,7 +72,26 @@ def test_planes_strongly_reduced_wide_image(D, W, dt):
     ref = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     assert len(plan.planes) == op.n_planes
     for j, d in enumerate(plan.planes):
-        got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        got = D.plane_view(planes, d).float().cpu().numpy()
+        assert np.all(np.abs(got - ref[j]) <= plane_tol(ref[j], dt)), f"plane {j}"
+
+
+@pytest.mark.parametrize("W,base", [(32767, 1.0), (16384, 2.0), (17000, 2.0)])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_planes_widest_scales(D, W, base, dt):
+    """Scaled widths up to 32767 px take exact integer horizontal taps (weights 2 w - rx and rx as
+    16-bit integers: 32767 and 32768 px wide scales sit on either side of that limit); a pyramid with
+    a wider scale (34000 px) blends its columns in fp32 instead.  Per-scale planes, ramp border."""
+    H = 3
+    img = synth.image(95, H, W)
+    p = D.pyramid_params(2, 2, base_scale=base, pad=16, pad_mode=D.DN_PAD_RAMP,
+                         mean=synth.IMAGENET_MEAN)
+    planes, plan = D.densenet_build_pyramid(torch.from_numpy(img).cuda()[None], p, DTS[dt])
+    op = oracle.plan(H, W, 2, 2, base, 0, 16, 0, 0)
+    ref = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
+    assert len(plan.planes) == op.n_planes
+    for j, d in enumerate(plan.planes):
+        got = D.plane_view(planes, d).float().cpu().numpy()
         assert np.all(np.abs(got - ref[j]) <= plane_tol(ref[j], dt)), f"plane {j}"
 
 
@@ -91,7 +109,7 @@ def test_planes_narrow_images(D, W, dt):
     ref = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     assert len(plan.planes) == op.n_planes
     for j, d in enumerate(plan.planes):
-        got = planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        got = D.plane_view(planes, d).float().cpu().numpy()
         assert np.all(np.abs(got - ref[j]) <= plane_tol(ref[j], dt)), f"plane {j}"
 
 
@@ -217,7 +235,7 @@ def test_scale_and_plane_variants_end_to_end(D, spo, base, plane, dt):
     assert len(pyra.plan.planes) == op.n_planes
     ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     for j, d in enumerate(pyra.plan.planes):
-        got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        got = D.plane_view(pyra.planes, d).float().cpu().numpy()
         assert np.all(np.abs(got - ref_planes[j]) <= plane_tol(ref_planes[j], dt)), f"plane {j}"
     maps = pyra.conv.conv5_maps()
     c5 = {}
@@ -246,7 +264,7 @@ def test_aspect_ratio_pyramids_end_to_end(D, dt):
     assert len(pyra.plan.geom) == K * len(r) and len(pyra.plan.planes) == op.n_planes
     ref_planes = oracle.build_planes(img, op, 1, synth.IMAGENET_MEAN)
     for j, d in enumerate(pyra.plan.planes):
-        got = pyra.planes[d.offset:d.offset + 3 * d.h * d.w].view(3, d.h, d.w).float().cpu().numpy()
+        got = D.plane_view(pyra.planes, d).float().cpu().numpy()
         assert np.all(np.abs(got - ref_planes[j]) <= plane_tol(ref_planes[j], dt)), f"plane {j}"
     maps = pyra.conv.conv5_maps()
     c5 = []

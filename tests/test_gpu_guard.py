@@ -78,16 +78,6 @@ def guard_conv(cf):
     return guards
 
 
-def image_descs(D, plan, n_img):
-    out = []
-    for b in range(n_img):
-        for d in plan.planes:
-            q = D.dn_plane_desc()
-            q.h, q.w, q.offset = d.h, d.w, b * plan.image_elems + d.offset
-            out.append(q)
-    return out
-
-
 @pytest.mark.parametrize("w,dt,n_img", [(C.XGA_25SCALE, "f16", 2), (C.VGA_8SCALE, "f32", 1),
                                         (C.VGA_8SCALE, "f16", 1), (C.ALEXNET_227, "f32", 1)],
                          ids=lambda v: getattr(v, "name", v))
@@ -101,7 +91,7 @@ def test_guarded_pyramid_conv_and_regions(D, w, dt, n_img):
     pix = n_img * plan.image_elems
     assert torch.equal(planes[:pix], ref_planes[:pix])
 
-    desc = image_descs(D, plan, n_img)
+    desc = plan.image_descs(n_img)
     net = D.net_params(pool5=True)
     ref_cf = D.ConvFeatures(desc, DTS[dt], net)
     ref_cf(ref_planes, packed(D, dt))

@@ -69,11 +69,10 @@ def gpu_planes(D, w, dt, imgs):
     return planes, plan
 
 
-def plane_views(planes, plan, b):
+def plane_views(D, planes, plan, b):
     out = []
     for d in plan.planes:
-        o = b * plan.image_elems + d.offset
-        out.append(planes[o:o + 3 * d.h * d.w].view(3, d.h, d.w))
+        out.append(D.plane_view(planes, d, b * plan.image_elems))
     return out
 
 
@@ -91,7 +90,7 @@ def test_planes(D, w, dt):
     p = oplan(w)
     ref = oracle.build_planes(img, p, w.pad_mode, w.mean)
     assert len(plan.planes) == p.n_planes
-    for j, v in enumerate(plane_views(planes, plan, 0)):
+    for j, v in enumerate(plane_views(D, planes, plan, 0)):
         check_planes(v, ref[j], dt)
 
 
@@ -102,7 +101,7 @@ def test_planes_batch_first_and_last(D):
     p = oplan(w)
     for b in (0, 15):
         ref = oracle.build_planes(imgs[b], p, w.pad_mode, w.mean)
-        for j, v in enumerate(plane_views(planes, plan, b)):
+        for j, v in enumerate(plane_views(D, planes, plan, b)):
             check_planes(v, ref[j], "bf16")
 
 

@@ -30,7 +30,10 @@ def test_plan_bit_exact_vs_oracle(w):
     np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, [*range(12), 14]])
     np.testing.assert_array_equal(lib.scale_array(), ref.gd)   # bitwise equal fp64
     assert [(p.h, p.w) for p in lib.planes] == ref.plane_sizes
-    off = np.cumsum([0] + [3 * h * w for h, w in ref.plane_sizes])
+    # rows padded to a multiple of 64 elements
+    pitch = [(w_ + 63) // 64 * 64 for _, w_ in ref.plane_sizes]
+    assert [p.pitch for p in lib.planes] == pitch
+    off = np.cumsum([0] + [3 * h * p for (h, _), p in zip(ref.plane_sizes, pitch)])
     assert [p.offset for p in lib.planes] == list(off[:-1])
     assert lib.image_elems == off[-1]
 
@@ -62,9 +65,10 @@ def test_batch_plan_bit_exact_vs_oracle(n_img, w):
     assert lib.n_planes == ref.n_planes
     np.testing.assert_array_equal(lib.geom_array(), ref.gi[:, [*range(12), 14, 15]])
     np.testing.assert_array_equal(np.array([[g.s, g.sy, g.sx] for g in lib.geom]), ref.gd)
-    pe = 3 * w.plane_h * w.plane_w
-    assert [(p.h, p.w, p.offset) for p in lib.planes] == [(w.plane_h, w.plane_w, j * pe)
-                                                          for j in range(ref.n_planes)]
+    pitch = (w.plane_w + 63) // 64 * 64
+    pe = 3 * w.plane_h * pitch
+    assert [(p.h, p.w, p.pitch, p.offset) for p in lib.planes] == [(w.plane_h, w.plane_w, pitch, j * pe)
+                                                                   for j in range(ref.n_planes)]
     assert lib.total_elems == ref.n_planes * pe
 
 
