@@ -671,7 +671,9 @@ __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece
                                            16, voff, soff, 0, 0);
 }
 
-template <typename T, int R, int BM, int TM, int OCC, int TS>
+// BMP: the channel block the stage-major weight copy is cut in (a multiple of BM); a workgroup's BM
+// channels are a sub-block of one such block.
+template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP>
 __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_direct_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
@@ -681,7 +683,8 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   static_assert(!Cf::F32 && (TM == 2 || TM == 3), "direct-load path is for 16-bit storage");
   constexpr int pad = (R - 1) / 2;
   constexpr int TN = Cf::TN, NW = Cf::WM * Cf::WN;
-  constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2;
+  static_assert(BMP % BM == 0, "a channel block is a sub-block of the weight copy's block");
+  constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2, WSLOTS_P = R * BMP * 2;
   constexpr int DH = Pieces<16>::count(HSLOTS, NW), DW = Pieces<16>::count(WSLOTS, NW);
   constexpr int HALO_E = DH * NW * 512, W_E = DW * NW * 512;  // elements (2 bytes)
   constexpr int PIPE_E = 2 * HALO_E + 2 * W_E;
@@ -707,12 +710,15 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   const int g = mb / mpg, m0 = (mb % mpg) * BM;
   const int oy0 = ty * Cf::TH, ox0 = tx * Cf::TW;
   const T* src = in + plane * in_stride + g * Cg;
-  // This channel block's stage-major weights: one contiguous block of WSLOTS 16-byte pieces per stage.
-  const T* wg = wp + (int64_t)mb * (Cg / Cf::CC) * R * (WSLOTS * 8);
+  // The stage-major weights of the enclosing BMP-channel block: per stage one contiguous block of
+  // WSLOTS_P 16-byte pieces, [kernel column][BMP channels][2 slots]; this workgroup's channels start
+  // msub channels into it.
+  const int mbp = g * (Mg / BMP) + m0 / BMP, msub = m0 % BMP;
+  const T* wg = wp + (int64_t)mbp * (Cg / Cf::CC) * R * (WSLOTS_P * 8);
   const __amdgpu_buffer_rsrc_t rsrc_in = __builtin_amdgcn_make_buffer_rsrc(
       (void*)src, 0, (int)(((int64_t)H * W * C - g * Cg) * sizeof(T)), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)wg, 0, (int)((int64_t)(Cg / Cf::CC) * R * WSLOTS * 16), 0x00020000);
+      (void*)wg, 0, (int)((int64_t)(Cg / Cf::CC) * R * WSLOTS_P * 16), 0x00020000);
   constexpr uint32_t OOB = 0x80000000u;
 
   const int tid = threadIdx.x;
@@ -748,11 +754,13 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   static_assert(WSLOTS % 64 == 0, "a stage's weights are whole 1 KB pieces");
   const uint32_t lane16 = (uint32_t)lane * 16u;
   auto load_w = [&](int buf, int c0, int ky) {  // stage (chunk c0 / 16, kernel row ky)
-    const uint32_t add = (uint32_t)(((c0 / Cf::CC) * R + ky) * WSLOTS * 16);
+    const uint32_t add = (uint32_t)(((c0 / Cf::CC) * R + ky) * WSLOTS_P * 16);
 #pragma unroll
     for (int i = 0; i < DW; ++i) {
-      const int p = wave * DW + i;
-      if (p * 64 < WSLOTS) lds_direct16(rsrc_w, wrow_buf(buf) + p * 512, lane16, add + (uint32_t)p * 1024u);
+      const int p = wave * DW + i;  // piece p: kernel column p / (BM / 32), channels 32 (p % (BM / 32))
+      const uint32_t src = BMP == BM ? (uint32_t)p * 1024u
+                                     : (uint32_t)(((p / (BM / 32)) * BMP + msub + 32 * (p % (BM / 32))) * 32);
+      if (p * 64 < WSLOTS) lds_direct16(rsrc_w, wrow_buf(buf) + p * 512, lane16, add + src);
     }
   };
 
@@ -1122,7 +1130,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   }
 }
 
-template <typename T, int R, int BM, int TM, int OCC, int TS>
+template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM>
 int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, int n, int H,
                 int W, int C, int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
   using Cf = ConvCfg<T, R, BM, TM, TS>;
@@ -1139,7 +1147,7 @@ int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* 
     // buffer descriptors address one plane with 32-bit byte offsets
     if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
     if (wstage == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
-    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP><<<(unsigned)blocks, Cf::NT, 0, s>>>(
         in, out, wstage, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   }
   return (int)hipGetLastError();
@@ -1173,6 +1181,17 @@ struct CfgBM {
 // Channel block of the direct-load kernel per layer (the stage-major weight copy is cut in these).
 constexpr int L_BM[5] = {0, CfgBM<DN_CONV2_CFG>::BM, CfgBM<DN_CONV3_CFG>::BM, CfgBM<DN_CONV4_CFG>::BM,
                          CfgBM<DN_CONV5_CFG>::BM};
+
+// A launch of the per-layer configuration with fewer workgroups than two rounds of the chip's
+// resident slots (CUs x workgroups per CU) leaves CUs idle; such launches (one image's planes) take
+// 64-channel blocks of 16 x 16 pixels instead, three to six times as many workgroups.
+template <int BM_, int TM_, int OCC_, int TS_>
+bool small_launch(int n, int H, int W, int M) {
+  const int64_t blocks = (int64_t)((W + TS_ % 100 - 1) / (TS_ % 100)) * ((H + TS_ / 100 - 1) / (TS_ / 100)) *
+                         (M / BM_) * n;
+  const int per_cu = OCC_ * 4 / (BM_ / (32 * TM_) * (TS_ / 100) * (TS_ % 100) / 128);
+  return blocks < 2LL * device_cu_count() * (per_cu > 0 ? per_cu : 1);
+}
 
 template <typename T>
 int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
@@ -1221,12 +1240,21 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
       return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 3:
+      if (!std::is_same<T, float>::value && small_launch<DN_CONV3_CFG>(n, H, W, L_M[li]))
+        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[2]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+                                                          L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 5:
+      if (!std::is_same<T, float>::value && small_launch<DN_CONV5_CFG>(n, H, W, L_M[li]))
+        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[4]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+                                                          L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 4:
+      if (!std::is_same<T, float>::value && small_launch<DN_CONV4_CFG>(n, H, W, L_M[li]))
+        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[3]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+                                                          L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
   }

@@ -76,6 +76,23 @@ def test_conv_s1(D, dt, layer, shape):
         assert_layer_close(chw(out[i]), ref, dt, f"conv{layer} {shape}[{i}]")
 
 
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("layer", [3, 4, 5])
+def test_conv_s1_many_planes(D, dt, layer):
+    """128 planes: enough workgroups for the per-layer configuration of large launches (the small
+    launches above take 64-channel sub-blocks); first, middle and last planes against the oracle."""
+    n, H, W = 128, 19, 40
+    M, C, R, s, p, G = LAYERS[layer - 1]
+    rng = np.random.default_rng(layer * 77)
+    x = round_to(np.abs(rng.normal(0, 3, (n, H, W, C))), dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_conv_layer(layer, xg, n, H, W, DTS[dt], packed(D, dt)).float().cpu().numpy()
+    w, b = oracle_weights(dt)[layer - 1]
+    for i in (0, 63, 127):
+        ref = oracle.conv2d(chw(x[i]), w, b, s, p, G, True)
+        assert_layer_close(chw(out[i]), ref, dt, f"conv{layer} {n} planes [{i}]")
+
+
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("C,shape", [(96, (2, 55, 55)), (256, (1, 27, 26)), (96, (1, 298, 31)),
                                      (256, (2, 4, 3))])
