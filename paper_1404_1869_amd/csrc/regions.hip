@@ -54,8 +54,9 @@ __device__ inline RegScale entry(const RegArgs& a, const RegBatch& bt, int img, 
 }
 
 // POOL = false: bilinear samples at the bin centres; POOL = true: per-channel max over each bin's cells.
-// BATCH = true: the maps of a cross-image packed batch (bt), else per-image maps (a).
-template <typename T, bool POOL, bool BATCH>
+// BATCH = true: the maps of a cross-image packed batch (bt), else per-image maps (a).  SC: the window
+// side S as a compile-time constant (6, the paper's windows), or 0 to take it from a.S.
+template <typename T, bool POOL, bool BATCH, int SC>
 __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict__ maps, RegArgs a,
                                                              RegBatch bt,
                                                              const float* __restrict__ boxes,
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
   __shared__ float s_ly[MAX_S], s_lx[MAX_S];
   const int r = blockIdx.x;
-  const int S = a.S, C = a.C, SS = S * S;
+  const int S = SC ? SC : a.S, C = a.C, SS = S * S;
   const int tid = threadIdx.x;
   const double x1 = boxes[4 * r + 0], y1 = boxes[4 * r + 1], x2 = boxes[4 * r + 2],
                y2 = boxes[4 * r + 3];
@@ -214,8 +215,8 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
             const int q = 4 * k + e;
             const float v00 = to_f32(a[it][0][q]), v01 = to_f32(a[it][1][q]);
             const float v10 = to_f32(a[it][2][q]), v11 = to_f32(a[it][3][q]);
-            const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
-            o[e] = top + ly * (bot - top);
+            const float top = __builtin_fmaf(lx, v01 - v00, v00), bot = __builtin_fmaf(lx, v11 - v10, v10);
+            o[e] = __builtin_fmaf(ly, bot - top, top);
           }
           float* d = s_row + bin * RSTR + c0 + 4 * k;
           *(float2*)d = make_float2(o[0], o[1]);
@@ -260,8 +261,8 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
           const int q = 4 * k + e;
           const float v00 = to_f32(a00[q]), v01 = to_f32(a01[q]);
           const float v10 = to_f32(a10[q]), v11 = to_f32(a11[q]);
-          const float top = v00 + lx * (v01 - v00), bot = v10 + lx * (v11 - v10);
-          o[e] = top + ly * (bot - top);
+          const float top = __builtin_fmaf(lx, v01 - v00, v00), bot = __builtin_fmaf(lx, v11 - v10, v10);
+          o[e] = __builtin_fmaf(ly, bot - top, top);
         }
         float* d = s_row + bin * RSTR + c0 + 4 * k;  // natural channel order, 8-byte aligned
         *(float2*)d = make_float2(o[0], o[1]);
@@ -309,8 +310,12 @@ int launch(const void* d_conv5, dn_dtype dt, const RegArgs& a, const RegBatch& b
   const size_t lds = sizeof(float) * (size_t)(a.C + 2) * a.S * a.S;
   auto go = [&](auto tag) {
     using T = decltype(tag);
-    region_windows_kernel<T, POOL, BATCH><<<n, 256, lds, s>>>((const T*)d_conv5, a, bt, d_boxes,
-                                                              d_box_img, d_out, d_scale, d_idx);
+    if (a.S == 6)
+      region_windows_kernel<T, POOL, BATCH, 6><<<n, 256, lds, s>>>((const T*)d_conv5, a, bt, d_boxes,
+                                                                   d_box_img, d_out, d_scale, d_idx);
+    else
+      region_windows_kernel<T, POOL, BATCH, 0><<<n, 256, lds, s>>>((const T*)d_conv5, a, bt, d_boxes,
+                                                                   d_box_img, d_out, d_scale, d_idx);
   };
   switch (dt) {
     case DN_F32: go(float{}); break;
