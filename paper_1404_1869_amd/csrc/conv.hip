@@ -665,6 +665,13 @@ __device__ inline void wait_vmem_but() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
 
+// Output stores are non-temporal: the next layer reads a batch's maps only after this launch has
+// written all of them, so they need not stay in the caches next to this layer's inputs.
+template <typename V>
+__device__ inline void store_out(const V& v, V* p) {
+  __builtin_nontemporal_store(v, p);
+}
+
 __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece, uint32_t voff,
                                     uint32_t soff = 0) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds_piece,
@@ -863,7 +870,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
           const int idx = gtile(p >> 5) * 32 + (p & 31);
           const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
           if (oy < H && ox < W)
-            *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j) = v;
+            store_out(v, (vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j));
         }
       }
     }
@@ -895,13 +902,14 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
         const vec8_t v = *(const vec8_t*)(stg + p * SROW + 8 * ch);
         const int idx = gtile(t) * 32 + p;
         const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
-        if (oy < H && ox < W) *(vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch) = v;
+        if (oy < H && ox < W) store_out(v, (vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch));
       }
     }
   }
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int OUT_CPOL = 2;  // cache policy of conv1's output stores: non-temporal
 constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's epilogue
 
 // ------------------------------------------------------------------------------------------------
@@ -1111,7 +1119,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
             const uint32_t off = oy < Ho && ox < Wo
                                      ? (uint32_t)((((int64_t)oy * Wo + ox) * 96 + 8 * ch) * sizeof(T))
                                      : OOB;
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), rsrc_out, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), rsrc_out, off, 0, OUT_CPOL);
           }
         }
       }

@@ -391,7 +391,8 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     for (int c = 0; c < 3; ++c)
 #pragma unroll
       for (int i = 0; i < PX; ++i)
-        if (inside[i]) orow[c * plane + 64 * i] = from_f32<T>(v[i][c]);
+        if (inside[i])  // non-temporal: conv1 reads the planes only after the whole batch is built
+          __builtin_nontemporal_store(from_f32<T>(v[i][c]), orow + c * plane + 64 * i);
   };
 
   // Per band: refresh the columns whose owner changed, then the wave's 4 rows of the band.
