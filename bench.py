@@ -175,7 +175,8 @@ def main():
     work["lrn_pool1"] = ("hbm", (sd[0] ** 2 + sd[1] ** 2) * 96 * es * n_planes)
     work["lrn_pool2"] = ("hbm", (sd[2] ** 2 + sd[3] ** 2) * 256 * es * n_planes)
     work["build_planes"] = ("hbm", 3 * w.H * w.W * n_img + 3 * PH * PW * es * n_planes)
-    work["region_windows"] = ("hbm", n_boxes * (256 * 36 * 4 + 36 * 4 * 256 * es))
+    # descriptors written once, conv5 maps read once
+    work["region_windows"] = ("hbm", n_boxes * 256 * 36 * 4 + n_planes * sd[4] ** 2 * 256 * es)
     kind, units = work[dominant]
     launches, tot_ms = live[dominant]
     avg_s = tot_ms / launches / 1e3
