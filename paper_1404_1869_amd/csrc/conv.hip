@@ -384,6 +384,24 @@ int device_cu_count() {
 // next chunk's halo) is already in flight into registers; it is written to the other buffers after
 // the stage's MFMAs, and one barrier per stage publishes it.
 // ------------------------------------------------------------------------------------------------
+// Slots (16 bytes) that collide modulo 512 bytes when the 32 lanes of a half-wave read pixels
+// (r, c), r < 16, c < 2, of a halo whose rows are rs slots apart (two slots per pixel).
+constexpr int colpair_collisions(int rs) {
+  int n = 0;
+  for (int a = 0; a < 32; ++a)
+    for (int b = 0; b < a; ++b)
+      if ((((a & 15) * rs + 2 * (a >> 4)) - ((b & 15) * rs + 2 * (b >> 4))) % 32 == 0) {
+        ++n;
+        break;
+      }
+  return n;
+}
+// Padding slots per 16-bit halo row: odd (so the two rows of a 2 x 16 MFMA tile fall on slots of
+// opposite parity), and of 1 and 3 the one with fewer collisions for 16 x 2 MFMA tiles.
+constexpr int halo_row_pad(int hw) {
+  return colpair_collisions(2 * hw + 3) < colpair_collisions(2 * hw + 1) ? 3 : 1;
+}
+
 template <typename T, int R, int BM, int TM, int TS>
 struct ConvCfg {
   // Tile of TH x TW output pixels, TS = 100 TH + TW (TW 16 or 32, TH TW a multiple of 256) for 16-bit
@@ -403,11 +421,13 @@ struct ConvCfg {
   static_assert(WM * 32 * TM == BM, "channel block must be whole wave tiles");
   // LDS layout.  16-bit types: a pixel (or an output channel's weight row) is 32 bytes, two 16-byte
   // slots.  The 32 lanes of a half-wave read 16 bytes each and must hit distinct slots modulo 512
-  // bytes: a halo row is padded by one slot, so the two tile rows a half-wave reads land on slots of
-  // opposite parity; the weight rows of channels 16..31 of a 32-channel group swap their two slots.
-  // fp32: a pixel or channel row is CC + 1 floats.
+  // bytes: a halo row is padded by an odd number of slots (RP), so the two tile rows a half-wave
+  // reads land on slots of opposite parity; the weight rows of channels 16..31 of a 32-channel group
+  // swap their two slots.  fp32: a pixel or channel row is CC + 1 floats.
   static constexpr int PS = F32 ? CC + 1 : CC;          // pixel stride (elements)
-  static constexpr int RS = F32 ? HW * PS : HW * PS + 8;  // halo row stride (elements)
+  static constexpr int RP = F32 ? 0 : halo_row_pad(HW);  // halo row padding (16-byte slots)
+  static constexpr int RSS = 2 * HW + RP;                // 16-bit halo row stride (slots)
+  static constexpr int RS = F32 ? HW * PS : HW * PS + 8 * RP;  // halo row stride (elements)
   static constexpr int HALO_E = HH * RS, W_E = R * BM * PS;
   static constexpr int STAGE_E = F32 ? 0 : WM * WN * 32 * TN * 64;  // epilogue staging
   static constexpr int LDS_E = (2 * HALO_E + 2 * W_E) > STAGE_E ? (2 * HALO_E + 2 * W_E) : STAGE_E;
@@ -691,7 +711,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   constexpr int pad = (R - 1) / 2;
   constexpr int TN = Cf::TN, NW = Cf::WM * Cf::WN;
   static_assert(BMP % BM == 0, "a channel block is a sub-block of the weight copy's block");
-  constexpr int HSLOTS = Cf::HH * (2 * Cf::HW + 1), WSLOTS = R * BM * 2, WSLOTS_P = R * BMP * 2;
+  constexpr int HSLOTS = Cf::HH * Cf::RSS, WSLOTS = R * BM * 2, WSLOTS_P = R * BMP * 2;
   constexpr int DH = Pieces<16>::count(HSLOTS, NW), DW = Pieces<16>::count(WSLOTS, NW);
   constexpr int HALO_E = DH * NW * 512, W_E = DW * NW * 512;  // elements (2 bytes)
   constexpr int PIPE_E = 2 * HALO_E + 2 * W_E;
@@ -735,18 +755,30 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   // MFMA pixel tile t of wave wn is the tile's (t WN + wn)-th 32-pixel tile: the waves along pixels
   // take the tiles in turn, so a partly filled bottom band splits its rows over them.
   auto gtile = [&](int t) { return t * Cf::WN + wn; };
+  // Two layouts of the tile's pixels over the MFMA tiles.  Row layout: each MFMA tile is 2 rows x 16
+  // columns (pix_row / pix_col).  Column-pair layout, for a tile cut by the map's right edge (cv < TW
+  // columns in the map): MFMA tile m is the 16 rows of columns 2 m and 2 m + 1 (lane l: row l % 16,
+  // column 2 m + l / 16), so only ceil(cv / 2) MFMA tiles are computed instead of all TW / 16 column
+  // blocks.  A tile takes the layout with fewer MFMA tiles holding a map pixel (ties: rows).
+  const int cv = min(Cf::TW, W - ox0), rv = min(Cf::TH, H - oy0);
+  const int n_rows = ((rv + 1) / 2) * (Cf::TW / 16), n_cols = (cv + 1) / 2;
+  const bool colpair = Cf::TH == 16 && n_cols < n_rows;
+  const int n_mt = colpair ? n_cols : n_rows;  // MFMA tiles holding a map pixel: tiles 0 .. n_mt - 1
+  auto out_row = [&](int idx) { return colpair ? (idx & 15) : Cf::pix_row(idx); };
+  auto out_col = [&](int idx) { return colpair ? 2 * (idx >> 5) + ((idx >> 4) & 1) : Cf::pix_col(idx); };
   // LDS offset of this lane's pixel in MFMA pixel tile t: pix0 + t DPIX (tile t of the wave lies
-  // t WN tiles further, i.e. 2 t WN / (TW / 16) halo rows down), so the reads take immediate offsets.
+  // t WN tiles further: 2 t WN / (TW / 16) halo rows down, or 2 t WN columns right), so the reads
+  // take immediate offsets.
   static_assert(Cf::WN % (Cf::TW / 16) == 0, "a wave's MFMA tiles are whole row pairs apart");
-  constexpr int DPIX = 2 * (Cf::WN / (Cf::TW / 16)) * Cf::RS;
-  const int pix0 = Cf::halo_off(Cf::pix_row(gtile(0) * 32 + l32), Cf::pix_col(gtile(0) * 32 + l32), 0);
+  constexpr int DPIX_R = 2 * (Cf::WN / (Cf::TW / 16)) * Cf::RS, DPIX_C = 2 * Cf::WN * Cf::PS;
+  const int pix0 = Cf::halo_off(out_row(gtile(0) * 32 + l32), out_col(gtile(0) * 32 + l32), 0);
   // Byte offsets (chunk 0) of this lane's halo slot in each of its wave's LDS pieces; the chunk's
   // offset goes in the scalar offset (a lane past the plane keeps an offset the hardware drops).
   uint32_t hoff[DH];
 #pragma unroll
   for (int i = 0; i < DH; ++i) {
     const int q = (wave * DH + i) * 64 + lane;
-    const int row = q / (2 * Cf::HW + 1), r = q % (2 * Cf::HW + 1);
+    const int row = q / Cf::RSS, r = q % Cf::RSS;
     const int iy = oy0 - pad + row, ix = ox0 - pad + r / 2;
     const bool ok = row < Cf::HH && r < 2 * Cf::HW && iy >= 0 && iy < H && ix >= 0 && ix < W;
     hoff[i] = ok ? (uint32_t)((((int64_t)iy * W + ix) * C + (r & 1) * 8) * sizeof(T)) : OOB;
@@ -778,16 +810,16 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     for (int t = 0; t < TN; ++t) acc[a][t] = f32x16{};
 
   const int nchunks = Cg / Cf::CC, nst = nchunks * R;
-  // MFMA pixel tiles of this wave that hold a pixel of the map: a prefix of its TN tiles, since the
-  // tiles are in row order.  Below the map's last row (the bottom band of tiles) the wave runs a
-  // stage loop that skips the empty tiles' reads and MFMAs; every wave still issues its share of the
-  // loads and reaches the same barriers.
+  // MFMA pixel tiles of this wave that hold a pixel of the map: a prefix of its TN tiles.  In a
+  // tile cut by the map's bottom or right edge the wave runs a stage loop that skips the empty
+  // tiles' reads and MFMAs; every wave still issues its share of the loads and reaches the same
+  // barriers.
   int tnv = 0;
 #pragma unroll
-  for (int t = 0; t < TN; ++t) tnv += oy0 + Cf::pix_row(gtile(t) * 32) < H ? 1 : 0;
+  for (int t = 0; t < TN; ++t) tnv += gtile(t) < n_mt ? 1 : 0;
   tnv = __builtin_amdgcn_readfirstlane(tnv);
-  auto stage_loop = [&](auto tnv_c) {
-    constexpr int TNV = decltype(tnv_c)::value;
+  auto stage_loop = [&](auto tnv_c, auto dpix_c) {
+    constexpr int TNV = decltype(tnv_c)::value, DPIX = decltype(dpix_c)::value;
     load_halo(0, 0);
     load_w(0, 0, 0);
     wait_vmem();
@@ -822,12 +854,24 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     }
   };
   static_assert(TN == 4, "stage loop variants cover 0..4 tiles");
-  switch (tnv) {
-    case 4: stage_loop(std::integral_constant<int, 4>{}); break;
-    case 3: stage_loop(std::integral_constant<int, 3>{}); break;
-    case 2: stage_loop(std::integral_constant<int, 2>{}); break;
-    case 1: stage_loop(std::integral_constant<int, 1>{}); break;
-    default: stage_loop(std::integral_constant<int, 0>{}); break;
+  using RowL = std::integral_constant<int, DPIX_R>;
+  using ColL = std::integral_constant<int, DPIX_C>;
+  if (colpair) {
+    switch (tnv) {
+      case 4: stage_loop(std::integral_constant<int, 4>{}, ColL{}); break;
+      case 3: stage_loop(std::integral_constant<int, 3>{}, ColL{}); break;
+      case 2: stage_loop(std::integral_constant<int, 2>{}, ColL{}); break;
+      case 1: stage_loop(std::integral_constant<int, 1>{}, ColL{}); break;
+      default: stage_loop(std::integral_constant<int, 0>{}, ColL{}); break;
+    }
+  } else {
+    switch (tnv) {
+      case 4: stage_loop(std::integral_constant<int, 4>{}, RowL{}); break;
+      case 3: stage_loop(std::integral_constant<int, 3>{}, RowL{}); break;
+      case 2: stage_loop(std::integral_constant<int, 2>{}, RowL{}); break;
+      case 1: stage_loop(std::integral_constant<int, 1>{}, RowL{}); break;
+      default: stage_loop(std::integral_constant<int, 0>{}, RowL{}); break;
+    }
   }
 
   typedef T vec8_t __attribute__((ext_vector_type(8)));
@@ -868,7 +912,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
           const int key = (p & 7) ^ ((p >> 3) & 3);
           const vec8_t v = *(const vec8_t*)(stg + p * 64 + ((j ^ key) * 8));
           const int idx = gtile(p >> 5) * 32 + (p & 31);
-          const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
+          const int oy = oy0 + out_row(idx), ox = ox0 + out_col(idx);
           if (oy < H && ox < W)
             store_out(v, (vec8_t*)(dst + ((int64_t)oy * W + ox) * M + g * Mg + m0 + wm * 64 + 8 * j));
         }
@@ -901,7 +945,7 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
         const int u = it * 64 + lane, p = u / NCH, ch = u % NCH;
         const vec8_t v = *(const vec8_t*)(stg + p * SROW + 8 * ch);
         const int idx = gtile(t) * 32 + p;
-        const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
+        const int oy = oy0 + out_row(idx), ox = ox0 + out_col(idx);
         if (oy < H && ox < W) store_out(v, (vec8_t*)(dst + ((int64_t)oy * W + ox) * M + mw + 8 * ch));
       }
     }
