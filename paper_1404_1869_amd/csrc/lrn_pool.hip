@@ -14,6 +14,9 @@
 // (k + alpha/n * s)^-beta is evaluated as exp2(-beta * log2(.)) on the hardware transcendental units;
 // the argument is >= k > 0.
 //
+// With 16-bit storage, C = 256 (after conv2) walks column strips instead of tiles, so that each input
+// element's LRN is computed about once rather than once per tile whose windows reach it.
+//
 // The pool-then-LRN order uses a simple kernel with one thread per output element.
 #include <type_traits>
 
@@ -40,21 +43,15 @@ constexpr int VECB = 16;  // bytes per channel vector
 #ifndef DN_LRN96_WPE
 #define DN_LRN96_WPE 3
 #endif
-// Per-pixel kernel configurations for 16-bit storage (channels per thread, output tile rows and
-// columns, waves per SIMD), chosen by timing each layer on the 96-plane batch: C = 96 keeps a whole
-// pixel per thread; C = 256 splits a pixel over 4 threads, so a thread needs half the registers
-// and 4 waves per SIMD fit (lrn_pool2 0.40 -> 0.35 ms against 2 threads per pixel).
-#ifndef DN_LRN256_CPT
-#define DN_LRN256_CPT 64
-#endif
-#ifndef DN_LRN256_TH
-#define DN_LRN256_TH 3
-#endif
-#ifndef DN_LRN256_TW
-#define DN_LRN256_TW 4
-#endif
-#ifndef DN_LRN256_WPE
-#define DN_LRN256_WPE 4
+// The tile kernel's configuration at C = 96 for 16-bit storage (channels per thread, output tile rows
+// and columns, waves per SIMD), chosen by timing on the 96-plane batch: a whole pixel per thread.
+// Strip kernel configuration for C = 256 and 16-bit storage: channels per thread, pooled columns and
+// rows per workgroup, waves per SIMD (the LDS ring admits 4 workgroups per CU).  Chosen by timing on
+// the 96-plane batch (lrn_pool2 0.334 -> 0.313 ms against the tile kernel; 16 rows 0.315 ms).  At
+// C = 96 the tile kernel stays: a whole pixel per thread (12 loads in flight, no neighbour vectors)
+// with 1.14x recomputation beat the strips (0.43 against 0.46-0.50 ms).
+#ifndef DN_STRIP256
+#define DN_STRIP256 32, 7, 8, 4
 #endif
 constexpr int MAX_HALF = 8;
 
@@ -156,8 +153,82 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
   }
 }
 
-// LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 64 x 4 at 16-bit storage, 128 x 2 at
-// fp32) with the default window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
+// LRN (window n = 5) of CPT consecutive channels c0 .. c0 + CPT - 1 of one pixel: v holds them, lv
+// the vector just below c0 and rv the vector just above (zero beyond the channel range, which equals
+// clipping the window).  The fp32 results go to res.
+template <typename T, int CPT>
+__device__ inline void lrn_values(const typename Vec<T>::type* v, const typename Vec<T>::type& lv,
+                                  const typename Vec<T>::type& rv, float* res, float alpha_n, float beta,
+                                  float k) {
+  constexpr int N = Vec<T>::N;
+  // xs[1 + c] = channel c of this thread (c = -1 .. CPT, the outer ones from the neighbours or
+  // zero); win[c] = sum of squares over channels c - 2 .. c + 2.
+  float win[CPT], xs[CPT + 2];
+  xs[0] = to_f32(lv[N - 1]);
+  xs[CPT + 1] = to_f32(rv[0]);
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) xs[1 + c] = to_f32(v[c / N][c % N]);
+  if constexpr (sizeof(T) == 2) {
+    // Pair sums P_j = x_2j^2 + x_2j+1^2 (j = -1 .. CPT / 2, counting the neighbours' pairs), their
+    // neighbour sums Q_j = P_j + P_j+1, then window(2 i) = Q_i-1 + x_2i+2^2 and window(2 i + 1) =
+    // Q_i + x_2i-1^2: two and a half operations per channel.
+    constexpr int NP = CPT / 2;
+    float pp[NP + 2];  // pp[1 + j] = P_j
+    {
+      const float a = to_f32(lv[N - 2]), b = to_f32(rv[1]);
+      pp[0] = __builtin_fmaf(a, a, xs[0] * xs[0]);
+      pp[NP + 1] = __builtin_fmaf(b, b, xs[CPT + 1] * xs[CPT + 1]);
+    }
+#pragma unroll
+    for (int j = 0; j < NP; ++j) pp[1 + j] = __builtin_fmaf(xs[1 + 2 * j], xs[1 + 2 * j], xs[2 + 2 * j] * xs[2 + 2 * j]);
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      win[2 * i] = __builtin_fmaf(xs[2 * i + 3], xs[2 * i + 3], pp[i] + pp[i + 1]);
+      win[2 * i + 1] = __builtin_fmaf(xs[2 * i], xs[2 * i], pp[i + 1] + pp[i + 2]);
+    }
+  } else {
+    // sq[2 + i] = a_i^2, pr[i] = sq[i] + sq[i + 1]: window(c) = pr[c] + pr[c + 2] + sq[c + 4]
+    float sq[CPT + 4], pr[CPT + 3];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const float a = to_f32(lv[N - 2 + i]), b = to_f32(rv[i]);
+      sq[i] = a * a;
+      sq[CPT + 2 + i] = b * b;
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const float a = to_f32(v[i / N][i % N]);
+      sq[2 + i] = a * a;
+    }
+#pragma unroll
+    for (int i = 0; i < CPT + 3; ++i) pr[i] = sq[i] + sq[i + 1];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) win[c] = pr[c] + pr[c + 2] + sq[c + 4];
+  }
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) res[c] = xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k);
+}
+
+// The same, rounded to the storage type and stored to d.
+template <typename T, int CPT>
+__device__ inline void lrn_channels(const typename Vec<T>::type* v, const typename Vec<T>::type& lv,
+                                    const typename Vec<T>::type& rv, T* d, float alpha_n, float beta,
+                                    float k) {
+  constexpr int N = Vec<T>::N, NV = CPT / N;
+  typedef typename Vec<T>::type vec_t;
+  float res[CPT];
+  lrn_values<T, CPT>(v, lv, rv, res, alpha_n, beta, k);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    vec_t r;
+#pragma unroll
+    for (int e = 0; e < N; ++e) r[e] = from_f32<T>(res[i * N + e]);
+    *(vec_t*)(d + i * N) = r;
+  }
+}
+
+// LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 128 x 2 at fp32) with the default
+// window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
 // 16-byte loads at once (plus one neighbouring vector on each inner side when a pixel is split over
 // several threads), forms the five-channel sums of squares from pair sums, and stores the LRN result
 // to LDS.  Pixels of the tile outside the map are stored as
@@ -214,60 +285,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
         }
         neg = (bits & 0x80008000u) != 0;
       }
-      // xs[1 + c] = channel c of this thread (c = -1 .. CPT, the outer ones from the neighbours or
-      // zero); win[c] = sum of squares over channels c - 2 .. c + 2.
-      float win[CPT], xs[CPT + 2];
-      xs[0] = to_f32(lv[N - 1]);
-      xs[CPT + 1] = to_f32(rv[0]);
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) xs[1 + c] = to_f32(v[c / N][c % N]);
-      if constexpr (sizeof(T) == 2) {
-        // Pair sums P_j = x_2j^2 + x_2j+1^2 (j = -1 .. CPT / 2, counting the neighbours' pairs), their
-        // neighbour sums Q_j = P_j + P_j+1, then window(2 i) = Q_i-1 + x_2i+2^2 and window(2 i + 1) =
-        // Q_i + x_2i-1^2: two and a half operations per channel.
-        constexpr int NP = CPT / 2;
-        float pp[NP + 2];  // pp[1 + j] = P_j
-        {
-          const float a = to_f32(lv[N - 2]), b = to_f32(rv[1]);
-          pp[0] = __builtin_fmaf(a, a, xs[0] * xs[0]);
-          pp[NP + 1] = __builtin_fmaf(b, b, xs[CPT + 1] * xs[CPT + 1]);
-        }
-#pragma unroll
-        for (int j = 0; j < NP; ++j) pp[1 + j] = __builtin_fmaf(xs[1 + 2 * j], xs[1 + 2 * j], xs[2 + 2 * j] * xs[2 + 2 * j]);
-#pragma unroll
-        for (int i = 0; i < NP; ++i) {
-          win[2 * i] = __builtin_fmaf(xs[2 * i + 3], xs[2 * i + 3], pp[i] + pp[i + 1]);
-          win[2 * i + 1] = __builtin_fmaf(xs[2 * i], xs[2 * i], pp[i + 1] + pp[i + 2]);
-        }
-      } else {
-        // sq[2 + i] = a_i^2, pr[i] = sq[i] + sq[i + 1]: window(c) = pr[c] + pr[c + 2] + sq[c + 4]
-        float sq[CPT + 4], pr[CPT + 3];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const float a = to_f32(lv[N - 2 + i]), b = to_f32(rv[i]);
-          sq[i] = a * a;
-          sq[CPT + 2 + i] = b * b;
-        }
-#pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-          const float a = to_f32(v[i / N][i % N]);
-          sq[2 + i] = a * a;
-        }
-#pragma unroll
-        for (int i = 0; i < CPT + 3; ++i) pr[i] = sq[i] + sq[i + 1];
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) win[c] = pr[c] + pr[c + 2] + sq[c + 4];
-      }
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        vec_t r;
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-          const int c = i * N + e;
-          r[e] = from_f32<T>(xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k));
-        }
-        *(vec_t*)(d + i * N) = r;
-      }
+      lrn_channels<T, CPT>(v, lv, rv, d, alpha_n, beta, k);
     } else {
       vec_t f;
 #pragma unroll
@@ -319,6 +337,146 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 #pragma unroll
     for (int i = 0; i < N; ++i) r[i] = from_f32<T>(m[i]);
     *(vec_t*)(out + plane * out_stride + ((int64_t)oy * Wo + ox) * C + g * N) = r;
+  }
+}
+
+// LRN then pool on column strips, for 16-bit storage and the default window (n = 5).  A workgroup
+// owns TPW pooled columns and SR pooled rows of one plane; it walks its output rows top to bottom.
+// For output row oy it computes the LRN of input rows 2 oy + 1 and 2 oy + 2 over the strip's 2 TPW + 1
+// input columns (one thread per (row, pixel, CPT channels)) into a ring of five LDS rows, and pools
+// rows 2 oy .. 2 oy + 2 of the ring; row 2 oy came from the previous output row.  Each input element's
+// LRN is thus computed once per strip, apart from the one column two strips share and the one row two
+// row blocks share ((2 TPW + 1) / (2 TPW) x (2 SR + 1) / (2 SR) of the map's elements, against
+// (2 TPH + 1)(2 TPW + 1) / (4 TPH TPW) for a workgroup tile of TPH x TPW outputs).  One barrier per
+// output row: the ring's five rows keep the rows being written apart from the three being pooled.
+// The next output row's input vectors are loaded into registers before the current row's LRN, so
+// their latency overlaps the LRN, the barrier and the pooling.  Every thread issues the same loads
+// and one store per output row, with no branches around them (addresses outside the map are
+// clamped into it and their values discarded; threads without a pooling task repeat the strip's
+// last one), so the compiler's vector-memory waits count exactly.  Pixels outside the map are stored
+// as -inf.  The maxima are taken on the raw 16-bit patterns when the pooled rows' LRN values are all
+// >= +0, else in fp32, as in the tile kernel.
+template <typename T, int C, int CPT, int TPW, int SR, int WPE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void lrn_pool_strip_kernel(
+    const T* __restrict__ in, T* __restrict__ out, int H, int W, int Ho, int Wo, int strips_x,
+    int strips_y, int64_t in_stride, int64_t out_stride, float alpha_n, float beta, float k) {
+  constexpr int N = Vec<T>::N;
+  constexpr int NV = CPT / N, TPP = C / CPT, G = C / N, CS = C + N;
+  constexpr int IW = 2 * TPW + 1, NSLOT = 5;
+  static_assert(sizeof(T) == 2, "16-bit storage");
+  static_assert(CPT % N == 0 && C % CPT == 0, "channel split must be whole vectors");
+  static_assert(2 * IW * TPP <= 256 && TPW * G <= 256, "one thread per (row, pixel, part) and per task");
+  typedef typename Vec<T>::type vec_t;
+  typedef short svec_t __attribute__((ext_vector_type(N)));
+  typedef uint32_t uvec_t __attribute__((ext_vector_type(N / 2)));
+  __shared__ __align__(16) T s[NSLOT * IW * CS];
+
+  int bid = blockIdx.x;
+  const int sx = bid % strips_x;
+  bid /= strips_x;
+  const int sy = bid % strips_y;
+  const int plane = bid / strips_y;
+  const int ox0 = sx * TPW, oy0 = sy * SR, ix0 = 2 * ox0;
+  const int nrows = min(SR, Ho - oy0);
+  const T* src = in + plane * in_stride;
+  T* dst = out + plane * out_stride;
+
+  const int tid = threadIdx.x;
+  const int r = min(tid / (IW * TPP), 1), rem = tid % (IW * TPP), px = rem / TPP, part = rem % TPP;
+  const bool worker = tid < 2 * IW * TPP;
+  const int x = ix0 + px, xc = min(x, W - 1);
+  const bool col_ok = worker && x < W;
+  // This thread's input vectors of one row: its CPT channels and the vectors just below and above
+  // them (zero at the ends of the channel range).
+  struct Row {
+    vec_t v[NV], lv, rv;
+  };
+  auto load_row = [&](int y) {
+    Row a;
+    const T* p = src + ((int64_t)min(y, H - 1) * W + xc) * C + part * CPT;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) a.v[i] = *(const vec_t*)(p + i * N);
+    a.lv = *(const vec_t*)(p - (part > 0 ? N : 0));
+    a.rv = *(const vec_t*)(p + (part + 1 < TPP ? CPT : 0));
+    return a;
+  };
+  // LRN of row y's vectors into ring row `slot` (-inf outside the map).  Returns whether an input
+  // sign bit was set (LRN keeps the sign; -0 counts as negative).
+  auto lrn_row = [&](const Row& a, int y, int slot) -> bool {
+    T* d = s + (slot * IW + px) * CS + part * CPT;
+    if (col_ok && y < H) {
+      uint32_t bits = 0;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const uvec_t u = __builtin_bit_cast(uvec_t, a.v[i]);
+#pragma unroll
+        for (int j = 0; j < N / 2; ++j) bits |= u[j];
+      }
+      const vec_t lv = part > 0 ? a.lv : vec_t{}, rv = part + 1 < TPP ? a.rv : vec_t{};
+      lrn_channels<T, CPT>(a.v, lv, rv, d, alpha_n, beta, k);
+      return (bits & 0x80008000u) != 0;
+    }
+    if (worker) {
+      vec_t f;
+#pragma unroll
+      for (int e = 0; e < N; ++e) f[e] = from_f32<T>(-INFINITY);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) *(vec_t*)(d + i * N) = f;
+    }
+    return false;
+  };
+  // Pooling task of this thread: pooled column q of the strip, channel vector g (threads past the
+  // tasks, and columns past the map, repeat the strip's last column in the map).
+  const int task = min(tid, TPW * G - 1);
+  const int q = min(task / G, Wo - 1 - ox0), g = task % G;
+
+  // Ring rows of input rows 2 oy, 2 oy + 1, 2 oy + 2 (input row y sits in ring row y mod 5).
+  int s0 = (2 * oy0) % NSLOT;
+  bool neg;
+  {
+    const Row top = load_row(2 * oy0);  // the first window's top row (threads of row 0)
+    neg = r == 0 ? lrn_row(top, 2 * oy0, s0) : false;
+  }
+  Row cur = load_row(2 * oy0 + 1 + r);
+  bool prev_any = false;
+  for (int i = 0; i < nrows; ++i) {
+    const int oy = oy0 + i;
+    const Row nxt = load_row(2 * oy + 3 + r);
+    const int s1 = s0 == NSLOT - 1 ? 0 : s0 + 1, s2 = s1 == NSLOT - 1 ? 0 : s1 + 1;
+    neg |= lrn_row(cur, 2 * oy + 1 + r, r ? s2 : s1);
+    const bool any = __syncthreads_or(neg) != 0;
+    const bool fp = any || prev_any;  // rows 2 oy + 1, 2 oy + 2 and (previous pass) row 2 oy
+    prev_any = any;
+    neg = false;
+    const T* b[3] = {s + (s0 * IW + 2 * q) * CS + g * N, s + (s1 * IW + 2 * q) * CS + g * N,
+                     s + (s2 * IW + 2 * q) * CS + g * N};
+    vec_t res;
+    if (!fp) {
+      svec_t m = *(const svec_t*)b[0];
+#pragma unroll
+      for (int wy = 0; wy < 3; ++wy)
+#pragma unroll
+        for (int wx = 0; wx < 3; ++wx)
+          if (wy || wx) m = __builtin_elementwise_max(m, *(const svec_t*)(b[wy] + wx * CS));
+      res = __builtin_bit_cast(vec_t, m);
+    } else {
+      float m[N];
+#pragma unroll
+      for (int e = 0; e < N; ++e) m[e] = -INFINITY;
+#pragma unroll
+      for (int wy = 0; wy < 3; ++wy)
+#pragma unroll
+        for (int wx = 0; wx < 3; ++wx) {
+          const vec_t v = *(const vec_t*)(b[wy] + wx * CS);
+#pragma unroll
+          for (int e = 0; e < N; ++e) m[e] = fmaxf(m[e], to_f32(v[e]));
+        }
+#pragma unroll
+      for (int e = 0; e < N; ++e) res[e] = from_f32<T>(m[e]);
+    }
+    *(vec_t*)(dst + ((int64_t)oy * Wo + ox0 + q) * C + g * N) = res;
+    cur = nxt;
+    s0 = s2;
   }
 }
 
@@ -391,24 +549,38 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
   // Per-pixel kernel for the two channel counts of the network with the default window (n = 5).
   // Tiles: the largest whose input pixels fit one thread each (per part) and whose LDS tile stays
   // within 64 KB.
+  if constexpr (sizeof(T) == 2) {
+    if (lrn && hn == 2 && C == 256) {
+      const int cfg[4] = {DN_STRIP256};
+      const int TPW = cfg[1], SR = cfg[2];
+      const int strips_x = (Wo + TPW - 1) / TPW, strips_y = (Ho + SR - 1) / SR;
+      const int64_t blocks = (int64_t)strips_x * strips_y * n;
+      if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+      lrn_pool_strip_kernel<T, 256, DN_STRIP256><<<(unsigned)blocks, 256, 0, s>>>(
+          in, out, H, W, Ho, Wo, strips_x, strips_y, in_stride, out_stride, an, beta, k);
+      return (int)hipGetLastError();
+    }
+  }
   if (lrn && hn == 2 && (C == 96 || C == 256)) {
+    // (16-bit storage reaches this only for C = 96: C = 256 takes the strip kernel above)
     constexpr bool F32 = sizeof(T) == 4;
-    constexpr int TH96 = F32 ? 4 : DN_LRN96_TH, TW96 = F32 ? 7 : DN_LRN96_TW, TH256 = F32 ? 2 : DN_LRN256_TH,
-                  TW256 = F32 ? 5 : DN_LRN256_TW;
+    constexpr int TH96 = F32 ? 4 : DN_LRN96_TH, TW96 = F32 ? 7 : DN_LRN96_TW, TH256 = 2, TW256 = 5;
     const int TPH = C == 96 ? TH96 : TH256, TPW = C == 96 ? TW96 : TW256;
     const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
     const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
     if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
     // Waves per SIMD the LDS tile allows (3 and 2 workgroups of 4 waves per CU): the compiler may use
     // the registers that occupancy leaves free for more independent work in flight.
-    if (C == 96)
+    if (C == 96) {
       lrn_pool_pixel_kernel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE>
           <<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
-    else
-      lrn_pool_pixel_kernel<T, 256, F32 ? 128 : DN_LRN256_CPT, TH256, TW256, F32 ? 2 : DN_LRN256_WPE>
-          <<<(unsigned)blocks, 256, 0, s>>>(
+    } else if constexpr (F32) {
+      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256, 2><<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+    } else {
+      return (int)hipErrorInvalidValue;
+    }
     return (int)hipGetLastError();
   }
   int TPH, TPW;
