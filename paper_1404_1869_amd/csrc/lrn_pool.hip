@@ -14,8 +14,9 @@
 // (k + alpha/n * s)^-beta is evaluated as exp2(-beta * log2(.)) on the hardware transcendental units;
 // the argument is >= k > 0.
 //
-// With 16-bit storage, C = 256 (after conv2) walks column strips instead of tiles, so that each input
-// element's LRN is computed about once rather than once per tile whose windows reach it.
+// With 16-bit storage, C = 256 (after conv2) walks column strips instead of tiles on large launches,
+// so that each input element's LRN is computed about once rather than once per tile whose windows
+// reach it.
 //
 // The pool-then-LRN order uses a simple kernel with one thread per output element.
 #include <type_traits>
@@ -53,6 +54,18 @@ constexpr int VECB = 16;  // bytes per channel vector
 #ifndef DN_STRIP256
 #define DN_STRIP256 32, 7, 8, 4
 #endif
+int device_cus() {
+  static int n = 0;
+  if (!n) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
 constexpr int MAX_HALF = 8;
 
 template <typename T>
@@ -155,12 +168,13 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
 
 // LRN (window n = 5) of CPT consecutive channels c0 .. c0 + CPT - 1 of one pixel: v holds them, lv
 // the vector just below c0 and rv the vector just above (zero beyond the channel range, which equals
-// clipping the window).  The fp32 results go to res.
+// clipping the window).  The results go to d in the storage type.
 template <typename T, int CPT>
-__device__ inline void lrn_values(const typename Vec<T>::type* v, const typename Vec<T>::type& lv,
-                                  const typename Vec<T>::type& rv, float* res, float alpha_n, float beta,
-                                  float k) {
-  constexpr int N = Vec<T>::N;
+__device__ inline void lrn_channels(const typename Vec<T>::type* v, const typename Vec<T>::type& lv,
+                                    const typename Vec<T>::type& rv, T* d, float alpha_n, float beta,
+                                    float k) {
+  constexpr int N = Vec<T>::N, NV = CPT / N;
+  typedef typename Vec<T>::type vec_t;
   // xs[1 + c] = channel c of this thread (c = -1 .. CPT, the outer ones from the neighbours or
   // zero); win[c] = sum of squares over channels c - 2 .. c + 2.
   float win[CPT], xs[CPT + 2];
@@ -206,29 +220,19 @@ __device__ inline void lrn_values(const typename Vec<T>::type* v, const typename
     for (int c = 0; c < CPT; ++c) win[c] = pr[c] + pr[c + 2] + sq[c + 4];
   }
 #pragma unroll
-  for (int c = 0; c < CPT; ++c) res[c] = xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k);
-}
-
-// The same, rounded to the storage type and stored to d.
-template <typename T, int CPT>
-__device__ inline void lrn_channels(const typename Vec<T>::type* v, const typename Vec<T>::type& lv,
-                                    const typename Vec<T>::type& rv, T* d, float alpha_n, float beta,
-                                    float k) {
-  constexpr int N = Vec<T>::N, NV = CPT / N;
-  typedef typename Vec<T>::type vec_t;
-  float res[CPT];
-  lrn_values<T, CPT>(v, lv, rv, res, alpha_n, beta, k);
-#pragma unroll
   for (int i = 0; i < NV; ++i) {
     vec_t r;
 #pragma unroll
-    for (int e = 0; e < N; ++e) r[e] = from_f32<T>(res[i * N + e]);
+    for (int e = 0; e < N; ++e) {
+      const int c = i * N + e;
+      r[e] = from_f32<T>(xs[1 + c] * lrn_scale(win[c], alpha_n, beta, k));
+    }
     *(vec_t*)(d + i * N) = r;
   }
 }
 
-// LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 128 x 2 at fp32) with the default
-// window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
+// LRN then pool for C = CPT * TPP channels (96 = 96 x 1; 256 = 64 x 4 at 16-bit storage, 128 x 2 at
+// fp32) with the default window n = 5: every thread owns CPT consecutive channels of one input pixel.  It issues all of their
 // 16-byte loads at once (plus one neighbouring vector on each inner side when a pixel is split over
 // several threads), forms the five-channel sums of squares from pair sums, and stores the LRN result
 // to LDS.  Pixels of the tile outside the map are stored as
@@ -556,6 +560,15 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
       const int strips_x = (Wo + TPW - 1) / TPW, strips_y = (Ho + SR - 1) / SR;
       const int64_t blocks = (int64_t)strips_x * strips_y * n;
       if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+      // Launches of fewer strips than two rounds of the chip's resident slots (one image's planes:
+      // about 660) take the tile kernel's 2850 shorter workgroups instead (29 against 31-37 us).
+      if (blocks < 2LL * 4 * device_cus()) {
+        const int tiles_x = (Wo + 3) / 4, tiles_y = (Ho + 2) / 3;
+        const int64_t tb = (int64_t)tiles_x * tiles_y * n;
+        lrn_pool_pixel_kernel<T, 256, 64, 3, 4, 4><<<(unsigned)tb, 256, 0, s>>>(
+            in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+        return (int)hipGetLastError();
+      }
       lrn_pool_strip_kernel<T, 256, DN_STRIP256><<<(unsigned)blocks, 256, 0, s>>>(
           in, out, H, W, Ho, Wo, strips_x, strips_y, in_stride, out_stride, an, beta, k);
       return (int)hipGetLastError();

@@ -114,6 +114,27 @@ def test_lrn_pool(D, dt, C, shape, lrn_first):
             assert np.max(np.abs(chw(out[i]) - ref) / np.maximum(np.abs(ref), 1e-3)) < 2e-5
 
 
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_lrn_pool2_strips_many_planes(D, dt):
+    """20 planes of conv2's 149 x 149 x 256 maps: a launch large enough for the column-strip kernel
+    (one image's planes take the tile kernel).  Sampled planes against the oracle, and every plane
+    bit-identical to the same plane pooled alone (the tile kernel: the same arithmetic per element)."""
+    n, H, W, C = 20, 149, 149, 256
+    g = torch.Generator().manual_seed(256 + H)
+    x = (torch.randn((n, H, W, C), generator=g) * 30).abs()
+    x[7] = -x[7]                       # one plane of negative values pools in fp32
+    xg = x.to("cuda", TORCH_DT[dt]).contiguous()
+    del x
+    out = D.densenet_lrn_pool(xg, DTS[dt], D.net_params())
+    for i in (0, 7, 19):
+        xi = xg[i].float().cpu().numpy()
+        ref = oracle.maxpool(oracle.lrn(chw(xi)))
+        assert_layer_close(chw(out[i].float().cpu().numpy()), ref, dt, f"lrn_pool2 strips [{i}]")
+    for i in (0, 7, 13, 19):
+        one = D.densenet_lrn_pool(xg[i:i + 1].contiguous(), DTS[dt], D.net_params())
+        assert torch.equal(one[0].view(torch.int16), out[i].view(torch.int16)), f"plane {i}"
+
+
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("C", [96, 256])
 def test_lrn_pool_signed_and_zero_inputs(D, dt, C):
