@@ -282,16 +282,20 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   }
   __syncthreads();
 
-  // This lane's columns x_i = tx0 + lane + 64 i: each gather instruction of a wave then reads the
-  // taps of 64 consecutive plane pixels (few cache lines), and each store writes 64 consecutive
-  // pixels of one channel.  Per column: its owner, border weight, first source column and the
+  // This lane's columns: pairs of neighbours, x_i = tx0 + 128 (i / 2) + 2 lane + i % 2, so each
+  // store instruction of a wave writes a pair of one channel per lane (128 consecutive pixels), the
+  // two pixels of a pair share their cell's row entry, and each gather instruction reads the taps of
+  // 64 pixels two columns apart.  Per column: its owner, border weight, first source column and the
   // horizontal weights (XDOT: u16 pair and 1 / Dx; else the fp32 fraction lx).
+  static_assert(PX % 2 == 0, "pairs of neighbouring columns");
+  auto col_of = [&](int i) { return tx0 + 128 * (i / 2) + 2 * lane + (i % 2); };
+  auto cell_of = [&](int band, int i) { return band * TCELLS + ((128 * (i / 2) + 2 * lane) >> 4); };
   bool inside[PX];
   int own[PX];
   float wx[PX], hx[PX];  // border weight; 1 / Dx (XDOT) or the column fraction lx
   uint32_t sx0[PX], sx1[PX], wts[PX];
   auto column_taps = [&](int i, int cell) {
-    const int x = tx0 + lane + 64 * i;
+    const int x = col_of(i);
     wx[i] = 0.f;
     hx[i] = XDOT ? 1.f : 0.f;
     sx0[i] = sx1[i] = 0u;
@@ -326,7 +330,7 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   };
 #pragma unroll
   for (int i = 0; i < PX; ++i) {
-    inside[i] = tx0 + lane + 64 * i < PP;
+    inside[i] = col_of(i) < PP;
     own[i] = -2;  // nothing computed yet
   }
   const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
@@ -339,11 +343,15 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     uint32_t q[PX][4];  // (row 0, col 0), (row 0, col 1), (row 1, col 0), (row 1, col 1)
     float ly[PX], wgt[PX];
   };
+  // live[p]: some lane of the wave has a pixel of pair p in a scale's rectangle (wave-uniform); a
+  // pair that is background in every lane of the wave loads nothing and stores zeros.
+  bool live[PX / 2];
   auto fetch = [&](int band, int r, RowTaps& t) {
+    RowEntry re;
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      const int cell = band * TCELLS + ((lane + 64 * i) >> 4);
-      const RowEntry re = s_row[cell * BAND + r];
+      if (!live[i / 2]) continue;
+      if (i % 2 == 0) re = s_row[cell_of(band, i) * BAND + r];  // one entry per pair
       t.ly[i] = re.ly;
       t.wgt[i] = re.wy * wx[i];
       if constexpr (PAIR) {
@@ -363,6 +371,10 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     float v[PX][3];
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
+      if (!live[i / 2]) {
+        v[i][0] = v[i][1] = v[i][2] = 0.f;
+        continue;
+      }
       const uint32_t q00 = t.q[i][0], q01 = t.q[i][1], q10 = t.q[i][2], q11 = t.q[i][3];
       if constexpr (XDOT) {
         const uint32_t t0[3] = {taps_x<0>(q00, q01, wts[i]), taps_x<1>(q00, q01, wts[i]),
@@ -386,13 +398,18 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
         }
       }
     }
-    T* orow = o + (int64_t)y * PP + tx0 + lane;
+    typedef T pair_t __attribute__((ext_vector_type(2)));
+    T* orow = o + (int64_t)y * PP + tx0 + 2 * lane;
 #pragma unroll
     for (int c = 0; c < 3; ++c)
 #pragma unroll
-      for (int i = 0; i < PX; ++i)
-        if (inside[i])  // non-temporal: conv1 reads the planes only after the whole batch is built
-          __builtin_nontemporal_store(from_f32<T>(v[i][c]), orow + c * plane + 64 * i);
+      for (int i = 0; i < PX; i += 2)
+        if (inside[i]) {  // non-temporal: conv1 reads the planes only after the whole batch is built
+          pair_t pv;
+          pv[0] = from_f32<T>(v[i][c]);
+          pv[1] = from_f32<T>(v[i + 1][c]);
+          __builtin_nontemporal_store(pv, (pair_t*)(orow + c * plane + 64 * i));
+        }
   };
 
   // Per band: refresh the columns whose owner changed, then the wave's 4 rows of the band.
@@ -401,13 +418,15 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     if (yb >= PH) break;  // uniform
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      const int cell = band * TCELLS + ((lane + 64 * i) >> 4);
+      const int cell = cell_of(band, i);
       const int o_new = inside[i] ? s_own[cell] : -1;
       if (o_new != own[i]) {
         own[i] = o_new;
         column_taps(i, cell);
       }
     }
+#pragma unroll
+    for (int i = 0; i < PX; i += 2) live[i / 2] = __builtin_amdgcn_ballot_w64(own[i] >= 0 || own[i + 1] >= 0) != 0;
 #pragma unroll
     for (int k = 0; k < BAND / 4; ++k) {
       const int r = wave + 4 * k;
