@@ -147,7 +147,8 @@ int densenet_plan_pyramid(int32_t H, int32_t W, const dn_pyramid_params* p, dn_s
  * `dtype`, image b's plane j at b * image_elems + planes[j].offset, or NULL for a size query.
  * *bytes_needed (and so planes_bytes) also covers a trailing scratch region after the planes
  * (4 * H * W * n_img bytes, 256-byte aligned) that the call uses while it runs; its contents
- * afterwards are unspecified.  geom/planes/n_planes/image_elems as densenet_plan_pyramid. */
+ * afterwards are unspecified.  geom/planes/n_planes/image_elems as densenet_plan_pyramid.  An image is
+ * limited to 2^30 - 1 pixels and a plane (3 * h * pitch elements) to 2^31 - 1 bytes (DN_E_TOO_LARGE). */
 int densenet_build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                            const dn_pyramid_params* p, dn_dtype dtype, void* d_planes,
                            size_t planes_bytes, size_t* bytes_needed, dn_scale_geom* geom,
@@ -197,8 +198,8 @@ int densenet_plan_batch(int32_t n_img, int32_t H, int32_t W, const dn_pyramid_pa
  * no out-of-bounds access.  d_planes: [n_planes][3][plane_h][pitch] in `dtype`, followed by the
  * builder's scratch (the pixel image, 4 * H * W * n_img bytes, then per-plane item lists,
  * 4 * (n_planes + 1 + n_img * E) bytes, each part 256-byte aligned; contents afterwards unspecified),
- * or NULL for a size query into *bytes_needed.  n_img * H * W must be below 2^32 and n_planes at most
- * 16384 (DN_E_TOO_LARGE). */
+ * or NULL for a size query into *bytes_needed.  n_img * H * W must be below 2^30, a plane's
+ * 3 * plane_h * pitch elements below 2^31 bytes, and n_planes at most 16384 (DN_E_TOO_LARGE). */
 int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int32_t W,
                          const dn_pyramid_params* p, dn_dtype dtype, const dn_scale_geom* geom,
                          const dn_scale_geom* d_geom, int32_t n_planes, void* d_planes,

@@ -276,6 +276,11 @@ static int build_pyramid(const uint8_t* d_images, int32_t n_img, int32_t H, int3
     if (n_img <= 0) return fail(DN_E_INVALID_ARG, "n_img must be positive");
     int st = densenet_plan_pyramid(H, W, p, geom, planes, max_planes, n_planes, image_elems);
     if (st != DN_OK) return st;
+    // the builder addresses an image's pixels (4 bytes each) and a plane with 32-bit byte offsets
+    if ((int64_t)H * W >= (1LL << 30)) return fail(DN_E_TOO_LARGE, "an image is limited to 2^30 - 1 pixels");
+    for (int j = 0; j < *n_planes; ++j)
+      if (3LL * planes[j].h * planes[j].pitch * (int64_t)dtype_size(dtype) >= (1LL << 31))
+        return fail(DN_E_TOO_LARGE, "a plane is limited to 2^31 - 1 bytes");
     const size_t planes_end = ((size_t)n_img * (size_t)*image_elems * dtype_size(dtype) + 255) &
                               ~(size_t)255;
     const size_t pix_bytes = (size_t)n_img * 4 * (size_t)H * (size_t)W;
@@ -398,9 +403,13 @@ int densenet_build_batch(const uint8_t* d_images, int32_t n_img, int32_t H, int3
       os << "a packed batch is limited to " << MAX_INDEX_PLANES << " planes";
       return fail(DN_E_TOO_LARGE, os.str());
     }
-    if ((int64_t)n_img * H * W > 0xffffffffLL)
-      return fail(DN_E_TOO_LARGE, "a packed batch is limited to 2^32 - 1 image pixels");
+    // the builder addresses the batch's pixel images (4 bytes per pixel) and a plane with 32-bit
+    // byte offsets
+    if ((int64_t)n_img * H * W >= (1LL << 30))
+      return fail(DN_E_TOO_LARGE, "a packed batch is limited to 2^30 - 1 image pixels");
     const int64_t pe = 3LL * p->plane_h * plane_pitch(p->plane_w);
+    if (pe * (int64_t)dtype_size(dtype) >= (1LL << 31))
+      return fail(DN_E_TOO_LARGE, "a plane is limited to 2^31 - 1 bytes");
     const size_t planes_end = ((size_t)n_planes * (size_t)pe * dtype_size(dtype) + 255) & ~(size_t)255;
     const size_t need = planes_end + builder_scratch_bytes(n_img, H, W, n_planes, (int32_t)(n_img * E));
     *bytes_needed = need;

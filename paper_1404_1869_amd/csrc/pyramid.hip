@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256) void pixel_image4_kernel(const uint8_t* __rest
 }
 
 struct RowEntry {
-  uint32_t r0, r1;  // source row offsets sy0 * W, sy1 * W (pixels; plus image * H * W in a packed batch)
+  uint32_t r0, r1;  // byte offsets of source rows sy0, sy1 (plus image * 4 H W in a packed batch)
   float ly, wy;     // row fraction, row border weight (0: background)
 };
 
@@ -274,9 +274,9 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       int sy0, sy1;
       src_coord(min(max(vy, 0), s.h - 1), a.H, s.h, s_inv[cell], sy0, sy1, re.ly);
       // a packed batch reads the owner's image: its offset is folded into the row offsets, so the
-      // pixel loads keep one base address for the whole workgroup
-      re.r0 = s_img[cell] + (uint32_t)sy0 * (uint32_t)a.W;
-      re.r1 = s_img[cell] + (uint32_t)sy1 * (uint32_t)a.W;
+      // pixel loads keep one buffer descriptor for the whole workgroup
+      re.r0 = 4u * (s_img[cell] + (uint32_t)sy0 * (uint32_t)a.W);
+      re.r1 = 4u * (s_img[cell] + (uint32_t)sy1 * (uint32_t)a.W);
     }
     s_row[ent] = re;
   }
@@ -318,8 +318,8 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
         c0 -= 1;
         rx = d;
       }
-      sx0[i] = (uint32_t)c0;
-      sx1[i] = (uint32_t)c1;
+      sx0[i] = 4u * (uint32_t)c0;  // byte offsets
+      sx1[i] = 4u * (uint32_t)c1;
       if constexpr (XDOT) {
         wts[i] = (d - rx) | (rx << 16);
         hx[i] = 1.f / (float)d;
@@ -333,9 +333,21 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     inside[i] = col_of(i) < PP;
     own[i] = -2;  // nothing computed yet
   }
+  constexpr uint32_t OOB = 0x80000000u;  // a store offset past any plane: dropped by the hardware
+  uint32_t soff_lane[PX / 2];  // byte offset of pair p in a plane row (OOB past the pitch)
+#pragma unroll
+  for (int i = 0; i < PX; i += 2)
+    soff_lane[i / 2] = inside[i] ? (uint32_t)((tx0 + 128 * (i / 2) + 2 * lane) * (int)sizeof(T)) : OOB;
+  // Buffer descriptors: the pixel image(s) (below 2^32 bytes, so 32-bit byte offsets reach every
+  // pixel) and this plane (below 2^31 bytes).  A store lane past the row pitch takes an offset past
+  // the plane's size, which the hardware drops.
   const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
   T* o = out + (BATCH ? (int64_t)j * 3 * PH * PP : (int64_t)b * pl.image_elems + pl.p[j].offset);
   const int64_t plane = (int64_t)PH * PP;
+  const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)P, 0, (int)(4u * (uint32_t)(BATCH ? bg.n_img : 1) * (uint32_t)a.H * (uint32_t)a.W), 0x00020000);
+  const __amdgpu_buffer_rsrc_t ro =
+      __builtin_amdgcn_make_buffer_rsrc((void*)o, 0, (int)(3 * plane * (int64_t)sizeof(T)), 0x00020000);
   const float mean[3] = {a.mean[0], a.mean[1], a.mean[2]};
 
   // A row's taps (4 pixels per lane) and its per-pixel row fraction and weight.
@@ -355,12 +367,14 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       t.ly[i] = re.ly;
       t.wgt[i] = re.wy * wx[i];
       if constexpr (PAIR) {
-        const u32x2 a0 = *(const u32x2*)(P + (re.r0 + sx0[i]));
-        const u32x2 a1 = *(const u32x2*)(P + (re.r1 + sx0[i]));
+        const u32x2 a0 = __builtin_amdgcn_raw_buffer_load_b64(rp, re.r0 + sx0[i], 0, 0);
+        const u32x2 a1 = __builtin_amdgcn_raw_buffer_load_b64(rp, re.r1 + sx0[i], 0, 0);
         t.q[i][0] = a0.x, t.q[i][1] = a0.y, t.q[i][2] = a1.x, t.q[i][3] = a1.y;
       } else {
-        t.q[i][0] = P[re.r0 + sx0[i]], t.q[i][1] = P[re.r0 + sx1[i]];
-        t.q[i][2] = P[re.r1 + sx0[i]], t.q[i][3] = P[re.r1 + sx1[i]];
+        t.q[i][0] = __builtin_amdgcn_raw_buffer_load_b32(rp, re.r0 + sx0[i], 0, 0);
+        t.q[i][1] = __builtin_amdgcn_raw_buffer_load_b32(rp, re.r0 + sx1[i], 0, 0);
+        t.q[i][2] = __builtin_amdgcn_raw_buffer_load_b32(rp, re.r1 + sx0[i], 0, 0);
+        t.q[i][3] = __builtin_amdgcn_raw_buffer_load_b32(rp, re.r1 + sx1[i], 0, 0);
       }
     }
   };
@@ -399,17 +413,21 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
       }
     }
     typedef T pair_t __attribute__((ext_vector_type(2)));
-    T* orow = o + (int64_t)y * PP + tx0 + 2 * lane;
 #pragma unroll
-    for (int c = 0; c < 3; ++c)
+    for (int c = 0; c < 3; ++c) {
+      const uint32_t soff = (uint32_t)((c * plane + (int64_t)y * PP) * (int64_t)sizeof(T));
 #pragma unroll
-      for (int i = 0; i < PX; i += 2)
-        if (inside[i]) {  // non-temporal: conv1 reads the planes only after the whole batch is built
-          pair_t pv;
-          pv[0] = from_f32<T>(v[i][c]);
-          pv[1] = from_f32<T>(v[i + 1][c]);
-          __builtin_nontemporal_store(pv, (pair_t*)(orow + c * plane + 64 * i));
-        }
+      for (int i = 0; i < PX; i += 2) {
+        pair_t pv;
+        pv[0] = from_f32<T>(v[i][c]);
+        pv[1] = from_f32<T>(v[i + 1][c]);
+        // non-temporal (aux 2): conv1 reads the planes only after the whole batch is built
+        if constexpr (sizeof(T) == 2)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, pv), ro, soff_lane[i / 2], soff, 2);
+        else
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, pv), ro, soff_lane[i / 2], soff, 2);
+      }
+    }
   };
 
   // Per band: refresh the columns whose owner changed, then the wave's 4 rows of the band.

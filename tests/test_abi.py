@@ -221,3 +221,27 @@ def test_noalloc_builder_size_query_and_limit():
                                           1 << 40, ctypes.byref(need), geom, planes, 64,
                                           ctypes.byref(n), ctypes.byref(e), None)
     assert st == D.DN_E_TOO_LARGE and "DN_STATIC_SCRATCH_BYTES" in D.last_error()
+
+
+def test_builder_offset_limits():
+    """The builder addresses pixel images and planes with 32-bit byte offsets: an image (or a packed
+    batch) of 2^30 pixels and a plane of 2^31 bytes are rejected before any device work."""
+    L = D.lib()
+    geom = (D.dn_scale_geom * 4096)()
+    planes = (D.dn_plane_desc * 64)()
+    n, e, need = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_size_t()
+    p = D.pyramid_params(1, 10, pad=16)
+    q = lambda side: L.densenet_build_pyramid(None, 1, side, side, ctypes.byref(p), D.DN_BF16, None, 0,
+                                              ctypes.byref(need), geom, planes, 64, ctypes.byref(n),
+                                              ctypes.byref(e), None)
+    assert q(32768) == D.DN_E_TOO_LARGE and "2^30" in D.last_error()      # 2^30 pixels
+    assert q(32767) == D.DN_E_TOO_LARGE and "2^31" in D.last_error()      # one 32799^2 plane, 6.4 GB
+    assert q(16384) == D.DN_OK                                            # 16416 x 16448 x 3 x 2 B
+    pb = D.pyramid_params(25, 10, pad=16, plane_h=1200, plane_w=1200)
+    assert L.densenet_build_batch(None, 1024, 1024, 1024, ctypes.byref(pb), D.DN_BF16, geom, None, 88,
+                                  None, 0, ctypes.byref(need), None) == D.DN_E_TOO_LARGE
+    assert "2^30" in D.last_error()
+    big = D.pyramid_params(25, 10, pad=16, plane_h=16384, plane_w=16384)
+    assert L.densenet_build_batch(None, 1, 1024, 1024, ctypes.byref(big), D.DN_F32, geom, None, 1,
+                                  None, 0, ctypes.byref(need), None) == D.DN_E_TOO_LARGE
+    assert "2^31" in D.last_error()
