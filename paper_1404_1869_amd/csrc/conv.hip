@@ -402,14 +402,14 @@ constexpr int halo_row_pad(int hw) {
   return colpair_collisions(2 * hw + 3) < colpair_collisions(2 * hw + 1) ? 3 : 1;
 }
 
-template <typename T, int R, int BM, int TM, int TS>
+template <typename T, int R, int BM, int TM, int TS, int TN_ = 4>
 struct ConvCfg {
   // Tile of TH x TW output pixels, TS = 100 TH + TW (TW 16 or 32, TH TW a multiple of 256) for 16-bit
   // storage; fp32 uses 16 x 16.
   static constexpr bool F32_ = std::is_same<T, float>::value;
   static constexpr int TH = F32_ ? 16 : TS / 100, TW = F32_ ? 16 : TS % 100, CC = 16;
   static_assert((TW == 16 || TW == 32) && TH % 2 == 0 && (TH * TW) % 256 == 0, "tile shape");
-  static constexpr int TN = 4;                     // 32-pixel MFMA tiles per wave (128 pixels)
+  static constexpr int TN = TN_;                   // 32-pixel MFMA tiles per wave (32 TN pixels)
   static constexpr int HH = TH + R - 1, HW = TW + R - 1;
   static constexpr bool F32 = std::is_same<T, float>::value;
   static constexpr int WM = BM / (32 * TM), WN = (TH * TW) / (32 * TN);
@@ -442,9 +442,9 @@ struct ConvCfg {
   }
 };
 
-template <typename T, int BM, int TM, int TS>
+template <typename T, int BM, int TM, int TS, int TN = 4>
 constexpr int conv_threads() {
-  return 64 * (BM / (32 * TM)) * (std::is_same<T, float>::value ? 256 : (TS / 100) * (TS % 100)) / 128;
+  return 64 * (BM / (32 * TM)) * (std::is_same<T, float>::value ? 256 : (TS / 100) * (TS % 100)) / (32 * TN);
 }
 
 template <typename T, int R, int BM, int TM, int OCC, int TS>
@@ -699,13 +699,13 @@ __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece
 }
 
 // BMP: the channel block the stage-major weight copy is cut in (a multiple of BM); a workgroup's BM
-// channels are a sub-block of one such block.
-template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP>
-__global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_direct_kernel(
+// channels are a sub-block of one such block.  TN_: 32-pixel MFMA tiles per wave.
+template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP, int TN_>
+__global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void conv_s1_direct_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
-  using Cf = ConvCfg<T, R, BM, TM, TS>;
+  using Cf = ConvCfg<T, R, BM, TM, TS, TN_>;
   using Op = Mfma<T>;
   static_assert(!Cf::F32 && (TM == 2 || TM == 3), "direct-load path is for 16-bit storage");
   constexpr int pad = (R - 1) / 2;
@@ -853,26 +853,22 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
       __syncthreads();
     }
   };
-  static_assert(TN == 4, "stage loop variants cover 0..4 tiles");
+  static_assert(TN >= 1 && TN <= 4, "stage loop variants cover 0..4 tiles");
   using RowL = std::integral_constant<int, DPIX_R>;
   using ColL = std::integral_constant<int, DPIX_C>;
-  if (colpair) {
+  auto run_layout = [&](auto layout) {
     switch (tnv) {
-      case 4: stage_loop(std::integral_constant<int, 4>{}, ColL{}); break;
-      case 3: stage_loop(std::integral_constant<int, 3>{}, ColL{}); break;
-      case 2: stage_loop(std::integral_constant<int, 2>{}, ColL{}); break;
-      case 1: stage_loop(std::integral_constant<int, 1>{}, ColL{}); break;
-      default: stage_loop(std::integral_constant<int, 0>{}, ColL{}); break;
+      case 4: if constexpr (TN >= 4) stage_loop(std::integral_constant<int, 4>{}, layout); break;
+      case 3: if constexpr (TN >= 3) stage_loop(std::integral_constant<int, 3>{}, layout); break;
+      case 2: if constexpr (TN >= 2) stage_loop(std::integral_constant<int, 2>{}, layout); break;
+      case 1: stage_loop(std::integral_constant<int, 1>{}, layout); break;
+      default: stage_loop(std::integral_constant<int, 0>{}, layout); break;
     }
-  } else {
-    switch (tnv) {
-      case 4: stage_loop(std::integral_constant<int, 4>{}, RowL{}); break;
-      case 3: stage_loop(std::integral_constant<int, 3>{}, RowL{}); break;
-      case 2: stage_loop(std::integral_constant<int, 2>{}, RowL{}); break;
-      case 1: stage_loop(std::integral_constant<int, 1>{}, RowL{}); break;
-      default: stage_loop(std::integral_constant<int, 0>{}, RowL{}); break;
-    }
-  }
+  };
+  if (colpair)
+    run_layout(ColL{});
+  else
+    run_layout(RowL{});
 
   typedef T vec8_t __attribute__((ext_vector_type(8)));
   T* dst = out + plane * out_stride;
@@ -1182,10 +1178,10 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   }
 }
 
-template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM>
+template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM, int TN = 4>
 int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, int n, int H,
                 int W, int C, int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
-  using Cf = ConvCfg<T, R, BM, TM, TS>;
+  using Cf = ConvCfg<T, R, BM, TM, TS, TN>;
   const int Cg = C / G, Mg = M / G;
   const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
   if (Mg % BM) return (int)hipErrorInvalidValue;  // whole channel blocks per group
@@ -1199,7 +1195,7 @@ int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* 
     // buffer descriptors address one plane with 32-bit byte offsets
     if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
     if (wstage == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
-    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP, TN><<<(unsigned)blocks, Cf::NT, 0, s>>>(
         in, out, wstage, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
   }
   return (int)hipGetLastError();
@@ -1237,6 +1233,13 @@ constexpr int L_BM[5] = {0, CfgBM<DN_CONV2_CFG>::BM, CfgBM<DN_CONV3_CFG>::BM, Cf
 // A launch of the per-layer configuration with fewer workgroups than two rounds of the chip's
 // resident slots (CUs x workgroups per CU) leaves CUs idle; such launches (one image's planes) take
 // 64-channel blocks of 16 x 16 pixels instead, three to six times as many workgroups.
+// Small launches: 64-channel blocks of 16 x 16 pixels whose waves own DN_SMALL_TN MFMA pixel tiles.
+#ifndef DN_SMALL_TN
+#define DN_SMALL_TN 2
+#endif
+#ifndef DN_SMALL_OCC
+#define DN_SMALL_OCC 3
+#endif
 template <int BM_, int TM_, int OCC_, int TS_>
 bool small_launch(int n, int H, int W, int M) {
   const int64_t blocks = (int64_t)((W + TS_ % 100 - 1) / (TS_ % 100)) * ((H + TS_ / 100 - 1) / (TS_ / 100)) *
@@ -1293,19 +1296,19 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
                                              in_stride, out_stride, s);
     case 3:
       if (!std::is_same<T, float>::value && small_launch<DN_CONV3_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[2]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[2], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
                                                           L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 5:
       if (!std::is_same<T, float>::value && small_launch<DN_CONV5_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[4]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[4], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
                                                           L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
     case 4:
       if (!std::is_same<T, float>::value && small_launch<DN_CONV4_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, 2, 1616, L_BM[3]>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
+        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[3], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
                                                           L_M[li], in_stride, out_stride, s);
       return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
                                              in_stride, out_stride, s);
