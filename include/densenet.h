@@ -235,7 +235,8 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
  * some k, Sec. 3.3) the cost of entry k is multiplied by max(rho, 1/rho), rho = (sx bw)/(sy bh) the
  * box's aspect on that entry, so each box is read where it is closest to a target x target square.
  * conv5_desc: [n_img * planes_per_img] maps from densenet_conv_features (image b's plane j at index
- * b * planes_per_img + j), channels-last with 256 channels, offsets multiples of 16 bytes.  d_box_img: nullable [n] image index per box (NULL => image 0).
+ * b * planes_per_img + j), channels-last with 256 channels, offsets multiples of 16 bytes, each map
+ * below 2^31 bytes (DN_E_TOO_LARGE).  d_box_img: nullable [n] image index per box (NULL => image 0).
  * d_scale: [n] chosen scale, -1 for a box with a non-finite or non-positive side (its row is 0).
  * d_idx: nullable [n][S][S][2] int32 (i0, j0) conv5 cell of each sample's top-left neighbour.
  * With n == 0 nothing is launched and d_boxes, d_out, d_scale may be NULL.

@@ -104,9 +104,13 @@ static int region_call(const void* d_conv5, const dn_plane_desc* conv5_desc, int
     a.C = 256;
     a.target = (double)target;
     const int64_t vec = 16 / (int64_t)dtype_size(conv5_dtype);
-    for (int32_t i = 0; i < n_maps; ++i)
+    for (int32_t i = 0; i < n_maps; ++i) {
       if (conv5_desc[i].offset < 0 || conv5_desc[i].offset % vec)
         return fail(DN_E_INVALID_ARG, "conv5 map offsets must be multiples of 16 bytes");
+      // the kernel addresses a map with 32-bit byte offsets
+      if ((int64_t)conv5_desc[i].h * conv5_desc[i].w * 256 * (int64_t)dtype_size(conv5_dtype) >= (1LL << 31))
+        return fail(DN_E_TOO_LARGE, "a conv5 map is limited to 2^31 - 1 bytes");
+    }
     for (int32_t j = 0; j < planes_per_img; ++j) {
       a.map_off[j] = conv5_desc[j].offset - conv5_desc[0].offset;
       a.map_w[j] = conv5_desc[j].w;
@@ -180,6 +184,8 @@ static int region_batch_call(const void* d_conv5, const dn_plane_desc* conv5_des
     const int64_t stride = n_maps > 1 ? conv5_desc[1].offset - d0.offset : 0;
     if (d0.h <= 0 || d0.w <= 0 || (n_maps > 1 && stride < (int64_t)d0.h * d0.w * 256))
       return fail(DN_E_INVALID_ARG, "conv5 maps must be non-empty and not overlap");
+    if ((int64_t)d0.h * d0.w * 256 * (int64_t)dtype_size(conv5_dtype) >= (1LL << 31))
+      return fail(DN_E_TOO_LARGE, "a conv5 map is limited to 2^31 - 1 bytes");
     for (int32_t j = 0; j < n_maps; ++j) {
       const dn_plane_desc& d = conv5_desc[j];
       if (d.h != d0.h || d.w != d0.w || d.offset != d0.offset + j * stride || d.offset < 0 || d.offset % vec)

@@ -68,6 +68,8 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   extern __shared__ __align__(16) float s_row[];  // S * S rows of C + 2 floats
   __shared__ int s_i0[MAX_S], s_j0[MAX_S], s_i1[MAX_S], s_j1[MAX_S];
   __shared__ float s_ly[MAX_S], s_lx[MAX_S];
+  // byte offsets of the sample rows i0, i1 and columns j0, j1 within the map (below 2^31 bytes)
+  __shared__ uint32_t s_ro0[MAX_S], s_ro1[MAX_S], s_co0[MAX_S], s_co1[MAX_S];
   const int r = blockIdx.x;
   const int S = SC ? SC : a.S, C = a.C, SS = S * S;
   const int tid = threadIdx.x;
@@ -119,6 +121,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
     return;
   }
   const RegScale sc = entry<BATCH>(a, bt, img, best);
+  const int Wc = BATCH ? bt.map_w : a.map_w[sc.plane];
   if (POOL && tid < 2 * S) {
     const bool row = tid < S;
     const int t = row ? tid : tid - S;
@@ -161,16 +164,19 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       s_i0[t] = i0;
       s_i1[t] = i1;
       s_ly[t] = lam;
+      s_ro0[t] = (uint32_t)i0 * (uint32_t)Wc * (uint32_t)(C * sizeof(T));
+      s_ro1[t] = (uint32_t)i1 * (uint32_t)Wc * (uint32_t)(C * sizeof(T));
     } else {
       s_j0[t] = i0;
       s_j1[t] = i1;
       s_lx[t] = lam;
+      s_co0[t] = (uint32_t)i0 * (uint32_t)(C * sizeof(T));
+      s_co1[t] = (uint32_t)i1 * (uint32_t)(C * sizeof(T));
     }
   }
   __syncthreads();
   const T* F = BATCH ? maps + (int64_t)sc.plane * bt.map_stride
                      : maps + (int64_t)img * a.image_stride + a.map_off[sc.plane];
-  const int Wc = BATCH ? bt.map_w : a.map_w[sc.plane];
   // Each thread blends VT consecutive channels (one 16-byte vector per neighbour cell); C / VT
   // threads cover a bin, and the workgroup's groups of C / VT threads take different bins.  The
   // results are staged bin-major, one row of C + 2 floats per bin in channel order (8-byte writes),
@@ -186,19 +192,23 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
   constexpr int MAXIT = 5;  // bins per thread whose loads are all issued before any blend
   if (!POOL && grp < groups && SS <= MAXIT * groups) {
     // Bilinear bins, up to MAXIT per thread (S <= 6 with 16-bit maps): all 4 MAXIT cell vectors are
-    // in flight at once, then blended.
+    // in flight at once (buffer loads at the bins' byte offsets: one add each), then blended with the
+    // four bilinear weights of the bin.
     const int c0 = lt * VT;
+    const uint32_t cb = (uint32_t)(c0 * sizeof(T));
+    const __amdgpu_buffer_rsrc_t rf = __builtin_amdgcn_make_buffer_rsrc((void*)F, 0, 0x7fffffff, 0x00020000);
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     vec_t a[MAXIT][4];
 #pragma unroll
     for (int it = 0; it < MAXIT; ++it) {
       const int bin = grp + it * groups;
       if (bin < SS) {
         const int u = bin / S, v = bin - u * S;
-        const int i0 = s_i0[u], i1 = s_i1[u], j0 = s_j0[v], j1 = s_j1[v];
-        a[it][0] = *(const vec_t*)(F + ((int64_t)i0 * Wc + j0) * C + c0);
-        a[it][1] = *(const vec_t*)(F + ((int64_t)i0 * Wc + j1) * C + c0);
-        a[it][2] = *(const vec_t*)(F + ((int64_t)i1 * Wc + j0) * C + c0);
-        a[it][3] = *(const vec_t*)(F + ((int64_t)i1 * Wc + j1) * C + c0);
+        const uint32_t r0 = s_ro0[u] + cb, r1 = s_ro1[u] + cb, q0 = s_co0[v], q1 = s_co1[v];
+        a[it][0] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rf, r0 + q0, 0, 0));
+        a[it][1] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rf, r0 + q1, 0, 0));
+        a[it][2] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rf, r1 + q0, 0, 0));
+        a[it][3] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rf, r1 + q1, 0, 0));
       }
     }
 #pragma unroll
@@ -206,7 +216,8 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
       const int bin = grp + it * groups;
       if (bin < SS) {
         const int u = bin / S, v = bin - u * S;
-        const float ly = s_ly[u], lx = s_lx[v];
+        const float ly = s_ly[u], lx = s_lx[v], my = 1.f - ly, mx = 1.f - lx;
+        const float w00 = my * mx, w01 = my * lx, w10 = ly * mx, w11 = ly * lx;
 #pragma unroll
         for (int k = 0; k < NQ; ++k) {
           f32x4 o;
@@ -215,8 +226,7 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
             const int q = 4 * k + e;
             const float v00 = to_f32(a[it][0][q]), v01 = to_f32(a[it][1][q]);
             const float v10 = to_f32(a[it][2][q]), v11 = to_f32(a[it][3][q]);
-            const float top = __builtin_fmaf(lx, v01 - v00, v00), bot = __builtin_fmaf(lx, v11 - v10, v10);
-            o[e] = __builtin_fmaf(ly, bot - top, top);
+            o[e] = __builtin_fmaf(w11, v11, __builtin_fmaf(w10, v10, __builtin_fmaf(w01, v01, w00 * v00)));
           }
           float* d = s_row + bin * RSTR + c0 + 4 * k;
           *(float2*)d = make_float2(o[0], o[1]);
