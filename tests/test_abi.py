@@ -245,3 +245,20 @@ def test_builder_offset_limits():
     assert L.densenet_build_batch(None, 1, 1024, 1024, ctypes.byref(big), D.DN_F32, geom, None, 1,
                                   None, 0, ctypes.byref(need), None) == D.DN_E_TOO_LARGE
     assert "2^31" in D.last_error()
+
+
+def test_region_map_size_limit():
+    """Region windows address a conv5 map with 32-bit byte offsets: a map of 2^31 bytes is rejected
+    before any device work, per image and in a packed batch."""
+    L = D.lib()
+    fake = ctypes.c_void_p(256)
+    geom = (D.dn_scale_geom * 1)()
+    geom[0].plane, geom[0].r0, geom[0].r1, geom[0].c0, geom[0].c1 = 0, 0, 0, 0, 0
+    d = (D.dn_plane_desc * 1)()
+    d[0].h, d[0].w, d[0].offset = 2048, 2048, 0          # 2048 * 2048 * 256 * 2 B = 2^31
+    st = L.densenet_region_windows(fake, d, 1, D.DN_BF16, geom, 1, 16, 1, fake, None, 1,
+                                   ctypes.c_float(227.0), 6, fake, fake, None, None)
+    assert st == D.DN_E_TOO_LARGE and "2^31" in D.last_error()
+    d[0].h = 2047
+    assert L.densenet_region_windows(fake, d, 1, D.DN_BF16, geom, 1, 16, 1, fake, None, 0,
+                                     ctypes.c_float(227.0), 6, fake, fake, None, None) == D.DN_OK
