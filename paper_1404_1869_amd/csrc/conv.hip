@@ -68,16 +68,26 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, T* __restrict__ ou
   out[i] = from_f32<T>(w[((int64_t)m * Cg + c) * RR + t]);
 }
 
-// conv1, 16-bit types: per input channel c a contiguous block of 96 x 18 16-byte pieces in the order
-// of conv1_resident_kernel's LDS weights: piece 18 m + p holds k = 8 (p ^ ((m >> 4) & 1)) .. + 7
-// of channel m.  Read from the plain packed weights.
+// conv1, 16-bit types, for conv1_resident_kernel: the 3 x 11 x 11 taps of an output channel as 99
+// units of 4 taps (input channel c, kernel row r, columns 4 cb .. 4 cb + 3, the column 11 of the last
+// block zero), unit u = 33 c + 11 cb + r, packed into 25 k-steps of 16: k-step j holds units 4 j .. 4 j
+// + 3 (a zero unit past 98), k = 8 h + 4 s + e taking unit 4 j + 2 h + s, column 4 cb + e.  Layout
+// [25][96][16] in the order of the kernel's LDS weights: the two 16-byte slots of a channel's k-step
+// are swapped for channels 16..31 of every 32-channel group.
+constexpr int C1_UNITS = 99, C1_KSTEPS = (C1_UNITS + 3) / 4;
 template <typename T>
-__global__ void pack_conv1_stage_kernel(const T* __restrict__ plain, T* __restrict__ out) {
+__global__ void pack_conv1_resident_kernel(const float* __restrict__ w, T* __restrict__ out) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 96 * 3 * K1) return;
-  const int c = i / (96 * K1), r = i % (96 * K1), m = r / K1, j = r % K1;
-  const int v = (j / 8) ^ ((m >> 4) & 1);
-  out[i] = plain[(m * 3 + c) * K1 + 8 * v + j % 8];
+  if (i >= C1_KSTEPS * 96 * 16) return;
+  const int j = i / (96 * 16), m = (i / 16) % 96, kk = i % 16;
+  const int h = (kk / 8) ^ ((m >> 4) & 1), sx = (kk % 8) / 4, e = kk % 4;
+  const int u = 4 * j + 2 * h + sx;
+  float v = 0.f;
+  if (u < C1_UNITS) {
+    const int c = u / 33, cb = (u % 33) / 11, r = (u % 33) % 11, kx = 4 * cb + e;
+    if (kx < 11) v = w[((m * 3 + c) * 11 + r) * 11 + kx];
+  }
+  out[i] = from_f32<T>(v);
 }
 
 template <typename T>
@@ -955,36 +965,57 @@ constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's 
 // ------------------------------------------------------------------------------------------------
 // conv1 for 16-bit storage with direct global->LDS loads (plane width a multiple of 8, 16-byte
 // aligned planes), weights resident, one independent pipeline per wave.  A workgroup of 8 waves (one
-// per CU, two waves per SIMD) loads all three input channels' stage-major weights (81 KB) into LDS
-// once: per output channel 18 slots of 16 bytes (k = 144 per input channel), the two slots of each
-// 32-byte pair swapped for channels 16..31 of every 32-channel group, so that the 32 lanes of a
-// half-wave reading one k-step's 16 bytes of 32 channels hit distinct slots modulo 512 bytes.  After
-// that every wave is its own worker with no workgroup barrier: it walks wave tiles of 4 x 16 output
-// pixels x 96 channels, and per stage (one input channel of one tile) loads the tile's 24 x 72 input
-// halo (rows of nine 16-byte slots of plane data and one zero slot) into one of its two private LDS
-// buffers while it computes the previous stage from the other, reading k-step ks + 1's fragments
-// while k-step ks's MFMAs run.  A wave that writes out a tile, or waits for a load, stalls only
+// per CU, two waves per SIMD) loads all weights (75 KB) into LDS once, as 25 k-steps of 16 (the 363
+// taps of an output channel as 99 units of 4 taps: see pack_conv1_resident_kernel) x 96 channels x
+// two 16-byte slots, the slots swapped for channels 16..31 of every 32-channel group, so that the 32
+// lanes of a half-wave reading one k-step's 16 bytes of 32 channels hit distinct slots modulo 512
+// bytes.  After that every wave is its own worker with no workgroup barrier: it walks wave tiles of 4
+// x 16 output pixels x 96 channels, and per stage (one input channel of one tile) loads the tile's 24
+// x 72 input halo (rows of nine 16-byte slots of plane data and one zero slot) into one of its two
+// private LDS buffers while it computes from the other, reading k-step j + 1's fragments while k-step
+// j's MFMAs run.  Stage c runs k-steps 0..7, 8..15 or 16..24; k-steps 8 and 16 hold units of two
+// input channels, so they run first in their stage, from both buffers, before the next stage's halo
+// load reuses the older one.  A wave that writes out a tile, or waits for a load, stalls only
 // itself; the other wave on its SIMD keeps the MFMAs busy.  A tile's outputs leave through LDS, as
 // whole 192-byte pixel rows.
 // ------------------------------------------------------------------------------------------------
 struct Conv1R {
   static constexpr int TH = 4, TW = 16, HR = 4 * (TH - 1) + 12;  // wave tile; halo rows (k rows 0..11)
   static constexpr int HSL = 10, HS = HSL * 8;   // halo row: slots, elements
-  static constexpr int WSL = K1 / 8;             // weight slots per output channel
-  static constexpr int NH = (HR * HSL + 63) / 64, NW = 27;  // 1 KB pieces: a halo, a channel's weights
-  static constexpr int DWL = (3 * NW + 7) / 8;   // weight pieces per wave (all channels, once)
-  static constexpr int HALO_E = NH * 512, WCH_E = NW * 512;
+  static constexpr int NH = (HR * HSL + 63) / 64;  // 1 KB pieces of a halo
+  static constexpr int KSE = 96 * 16;            // elements of one k-step's weights
+  static constexpr int WP = C1_KSTEPS * KSE / 512;  // 1 KB pieces of all weights
+  static constexpr int DWL = (WP + 7) / 8;       // weight pieces per wave (all weights, once)
+  static constexpr int HALO_E = NH * 512;
   static constexpr int SROW = 104, SPX = 16;     // staging: elements per pixel row, pixels per round
-  static constexpr int HALO_OFF = 3 * WCH_E, BIAS_OFF = HALO_OFF + 8 * 2 * HALO_E;
+  static constexpr int HALO_OFF = WP * 512, BIAS_OFF = HALO_OFF + 8 * 2 * HALO_E;
   static constexpr int LDS_E = BIAS_OFF + 2 * 96;  // the biases as 96 floats
+  // unit u of a tile's k-steps: input channel, and its LDS offset (row r, columns 4 cb ..) in the halo
+  __host__ __device__ static constexpr int uchan(int u) { return u < C1_UNITS ? u / 33 : 2; }
+  __host__ __device__ static constexpr int uoff(int u) {
+    return u < C1_UNITS ? ((u % 33) % 11) * HS + 4 * ((u % 33) / 11) : uoff(C1_UNITS - 1);
+  }
+  __host__ __device__ static constexpr int kchan(int j) { return j < 8 ? 0 : (j < 16 ? 1 : 2); }  // stage
 };
-static_assert(Conv1R::NW * 64 == 96 * Conv1R::WSL, "a channel's weights are whole pieces");
+static_assert(Conv1R::WP * 512 == C1_KSTEPS * Conv1R::KSE, "the weights are whole pieces");
+static_assert(Conv1R::uchan(4 * 8) == 0 && Conv1R::uchan(4 * 8 + 1) == 1 && Conv1R::uchan(4 * 16 + 1) == 1 &&
+                  Conv1R::uchan(4 * 16 + 2) == 2,
+              "k-steps 8 and 16 are the only ones that span two input channels");
 static_assert(Conv1R::SPX * Conv1R::SROW <= Conv1R::HALO_E, "epilogue staging fits a halo buffer");
 static_assert((size_t)Conv1R::LDS_E * 2 <= 160 * 1024, "one workgroup's LDS fits the CU");
 
 // Keeps the compiler from moving this wave's LDS accesses across it (a wave's own LDS operations
 // execute in order).
 __device__ inline void wave_lds_order() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
+// f(integral_constant<I>) for I = B .. E - 1, in order.
+template <int B, int E, typename F>
+__device__ inline void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 template <typename T>
 __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
@@ -1013,14 +1044,14 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   const int NWK = 8 * G, wk = 8 * rank + wave;
   const int ntile = wk < ntiles ? (ntiles - wk + NWK - 1) / NWK : 0;
 
-  // All weights, once: piece q of the stage-major blob lands in LDS piece q.
+  // All weights, once: piece q of the k-step blob lands in LDS piece q.
   {
-    const __amdgpu_buffer_rsrc_t rsrc_w =
-        __builtin_amdgcn_make_buffer_rsrc((void*)wp, 0, (int)(3 * 96 * K1 * sizeof(T)), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)wp, 0, (int)(C1_KSTEPS * P::KSE * sizeof(T)), 0x00020000);
 #pragma unroll
     for (int i = 0; i < P::DWL; ++i) {
       const int q = wave + 8 * i;
-      if (q < 3 * P::NW) lds_direct16(rsrc_w, s_mem + q * 512, (uint32_t)(q * 1024 + lane * 16));
+      if (q < P::WP) lds_direct16(rsrc_w, s_mem + q * 512, (uint32_t)(q * 1024 + lane * 16));
     }
   }
   const uint32_t chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
@@ -1059,26 +1090,39 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     }
   };
 
-  int lpix[2];
+  int lpix[2], lpix2[2];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int idx = b * 32 + l32;
-    lpix[b] = (4 * (idx / P::TW) + 2 * half) * P::HS + 4 * (idx % P::TW);
+    lpix[b] = 4 * (idx / P::TW) * P::HS + 4 * (idx % P::TW);
+    lpix2[b] = lpix[b] + 2 * half * P::HS;
   }
-  const int lw = 8 * (P::WSL * l32 + (half ^ ((l32 >> 4) & 1)));
-  // Lane bases: this lane's pixel (input row 4 prow + 2 half, column 4 pcol) per pixel tile, and its
-  // output channel's weight row at slot (half ^ swap); every k-step adds an offset common to all lanes.
-  auto read = [&](const T* hs, const T* ws, int ks, frag* x, frag* w) {
-    // k-step ks: rows ky, ky + 1 (ky = 4 (ks / 3) + 2 half), columns 4 (ks % 3) + 0..3
-    const int o0 = 4 * (ks / 3) * P::HS + 4 * (ks % 3);
+  const int lw = 16 * l32 + 8 * (half ^ ((l32 >> 4) & 1));
+  // Lane bases: this lane's pixel (input row 4 prow, column 4 pcol) per pixel tile (lpix2: two rows
+  // further in the upper half-wave), and its output channel's weight slot (half ^ swap).  k-step J:
+  // lane half h reads units 4 J + 2 h (the fragment's low 8 bytes) and 4 J + 2 h + 1 (high); hp holds
+  // the previous input channel's halo, hs the stage's.
+  auto read = [&](auto jc, const T* hp, const T* hs, frag* x, frag* w) {
+    constexpr int J = decltype(jc)::value, CS = P::kchan(J);
+    hfrag hv[2][2];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const hfrag lo = *(const hfrag*)(hs + lpix[b] + o0);
-      const hfrag hi = *(const hfrag*)(hs + lpix[b] + o0 + P::HS);
-      x[b] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    for (int sx = 0; sx < 2; ++sx) {
+      const int u0 = 4 * J + sx, u1 = 4 * J + 2 + sx;
+      const bool p0 = P::uchan(u0) != CS, p1 = P::uchan(u1) != CS;
+      const int o0 = P::uoff(u0), o1 = P::uoff(u1);
+      if (!p0 && !p1 && o1 - o0 == 2 * P::HS) {  // the usual case: the upper half two rows down
+#pragma unroll
+        for (int b = 0; b < 2; ++b) hv[b][sx] = *(const hfrag*)(hs + lpix2[b] + o0);
+      } else {
+        const T* bh = half ? (p1 ? hp : hs) + o1 : (p0 ? hp : hs) + o0;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) hv[b][sx] = *(const hfrag*)(bh + lpix[b]);
+      }
     }
 #pragma unroll
-    for (int mt = 0; mt < 3; ++mt) w[mt] = *(const frag*)(ws + lw + 8 * (P::WSL * 32 * mt + 2 * ks));
+    for (int b = 0; b < 2; ++b) x[b] = __builtin_shufflevector(hv[b][0], hv[b][1], 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+    for (int mt = 0; mt < 3; ++mt) w[mt] = *(const frag*)(s_mem + J * P::KSE + 512 * mt + lw);
   };
 
   f32x16 acc[3][2];
@@ -1094,36 +1138,58 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   wait_vmem();
   __syncthreads();  // weights and biases are in LDS; from here on each wave runs on its own
   zero_col(0);
-  for (int st = 0; st < 3 * ntile; ++st) {
-    const int j = st / 3, c = st - 3 * j;  // tile j of this worker, input channel c
-    if (st + 1 < 3 * ntile) {
-      const int nj = (st + 1) / 3, nc = st + 1 - 3 * nj;
-      if (nc == 0) set_tile(wk + nj * NWK);
-      load_halo((st + 1) & 1, nc);
-    }
-    T* hs = hbuf(st & 1);
-    const T* ws = s_mem + c * P::WCH_E;
-    {
+  // One tile per iteration, its three stages in straight-line code.  Channel 0 and channel 2 of tile
+  // j sit in buffer X = j & 1, channel 1 in the other, Y; a stage's load of the next stage's channel
+  // goes to the buffer its own k-steps no longer read.
+  for (int j = 0; j < ntile; ++j) {
+    T* hx = hbuf(j & 1);
+    T* hy = hbuf((j + 1) & 1);
+    // k-steps J0 .. J1 - 1 of stage J0's channel (halo in hs, the previous channel's in hp); the next
+    // stage's load (issue) follows k-step J0's MFMAs, which have then consumed any fragment of hp.
+    auto ksteps = [&](auto j0c, auto j1c, const T* hp, const T* hs, auto&& issue) {
+      constexpr int J0 = decltype(j0c)::value, J1 = decltype(j1c)::value;
       frag xr[2][2], wr[2][3];
-      read(hs, ws, 0, xr[0], wr[0]);
-#pragma unroll
-      for (int ks = 0; ks < K1 / 16; ++ks) {
-        if (ks + 1 < K1 / 16) read(hs, ws, ks + 1, xr[(ks + 1) & 1], wr[(ks + 1) & 1]);
+      read(std::integral_constant<int, J0>{}, hp, hs, xr[0], wr[0]);
+      auto body = [&](auto jc) {
+        constexpr int J = decltype(jc)::value, B = (J - J0) & 1;
+        if constexpr (J + 1 < J1) read(std::integral_constant<int, J + 1>{}, hp, hs, xr[B ^ 1], wr[B ^ 1]);
         // raised wave priority while this k-step's MFMAs issue: the SIMD's other wave then issues
         // its LDS reads, loads and epilogue work in between rather than ahead of them
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[ks & 1][mt], xr[ks & 1][b], acc[mt][b]);
+          for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[B][mt], xr[B][b], acc[mt][b]);
         __builtin_amdgcn_s_setprio(0);
+        if constexpr (J == J0) {
+          wave_lds_order();
+          issue();
+        }
+      };
+      static_for<J0, J1>(body);
+    };
+    // stage 0: channel 0 in X; channel 1 loads into Y
+    ksteps(std::integral_constant<int, 0>{}, std::integral_constant<int, 8>{}, hy, hx, [&] { load_halo((j + 1) & 1, 1); });
+    wait_vmem();
+    zero_col((j + 1) & 1);
+    // stage 1: channel 1 in Y (k-step 8 also reads channel 0 in X); channel 2 loads into X
+    ksteps(std::integral_constant<int, 8>{}, std::integral_constant<int, 16>{}, hx, hy, [&] { load_halo(j & 1, 2); });
+    wait_vmem();
+    zero_col(j & 1);
+    // stage 2: channel 2 in X (k-step 16 also reads channel 1 in Y); the next tile's channel 0
+    // loads into Y, the next tile's X
+    ksteps(std::integral_constant<int, 16>{}, std::integral_constant<int, C1_KSTEPS>{}, hy, hx, [&] {
+      if (j + 1 < ntile) {
+        set_tile(wk + (j + 1) * NWK);
+        load_halo((j + 1) & 1, 0);
       }
-    }
-    if (c == 2) {
+    });
+    {
       // Epilogue of the tile: bias + ReLU; per 32-pixel MFMA tile, two rounds of 16 pixels staged
-      // in the halo buffer just consumed (rows of 104 channels), read back as whole pixel rows and
-      // written with 16-byte buffer stores that every lane issues (a pixel outside the map stores at
-      // an offset past the plane, which the hardware drops): EPI_STORES stores per lane.
+      // in X, just consumed (rows of 104 channels), read back as whole pixel rows and written with
+      // 16-byte buffer stores that every lane issues (a pixel outside the map stores at an offset
+      // past the plane, which the hardware drops): EPI_STORES stores per lane.
+      T* hs = hx;
       const int t = wk + j * NWK;
       const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
       const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
@@ -1169,12 +1235,10 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
 #pragma unroll
         for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
       // Vector-memory operations retire in issue order: once no more than the epilogue's stores
-      // are outstanding, the next stage's halo loads (issued before them) have landed in LDS.
+      // are outstanding, the next tile's halo loads (issued before them) have landed in LDS.
       wait_vmem_but<EPI_STORES>();
-    } else {
-      wait_vmem();
     }
-    zero_col((st + 1) & 1);
+    zero_col((j + 1) & 1);
   }
 }
 
@@ -1336,7 +1400,7 @@ PackedLayout packed_layout(dn_dtype dt) {
     L.s_off[l] = 0;
     if (dt == DN_F32) continue;
     L.s_off[l] = off;
-    off = align256(off + (l == 0 ? (size_t)96 * 3 * K1
+    off = align256(off + (l == 0 ? (size_t)C1_KSTEPS * 96 * 16
                                   : (size_t)L_M[l] * (L_C[l] / L_G[l]) * L_R[l] * L_R[l]) * es);
   }
   L.total = off;
@@ -1368,12 +1432,12 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
     }
     copy_f32_kernel<<<(L_M[l] + 255) / 256, 256, 0, s>>>(d_b[l], (float*)(base + L.b_off[l]), L_M[l]);
     if (L.s_off[l] && l == 0) {
-      const int n = 96 * 3 * K1;
+      const int n = C1_KSTEPS * 96 * 16;
       void* sd = base + L.s_off[0];
       if (dt == DN_F16)
-        pack_conv1_stage_kernel<_Float16><<<(n + 255) / 256, 256, 0, s>>>((const _Float16*)dst, (_Float16*)sd);
+        pack_conv1_resident_kernel<_Float16><<<(n + 255) / 256, 256, 0, s>>>(d_w[0], (_Float16*)sd);
       if (dt == DN_BF16)
-        pack_conv1_stage_kernel<__bf16><<<(n + 255) / 256, 256, 0, s>>>((const __bf16*)dst, (__bf16*)sd);
+        pack_conv1_resident_kernel<__bf16><<<(n + 255) / 256, 256, 0, s>>>(d_w[0], (__bf16*)sd);
     } else if (L.s_off[l]) {
       const int Cg = L_C[l] / L_G[l], Mg = L_M[l] / L_G[l];
       const int64_t n = (int64_t)L_M[l] * Cg * L_R[l] * L_R[l];
