@@ -8,7 +8,7 @@ import pytest
 import oracle
 from paper_1404_1869_amd import configs as C
 from paper_1404_1869_amd import synth
-from tests.parity import plane_tol, assert_layer_close, hwc, ulp
+from tests.parity import BARS, plane_tol, assert_layer_close, hwc, ulp
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -128,7 +128,9 @@ def test_warp_regions_row_pitch(D, dt):
 
 def test_conv_features_row_pitch_matches_packed_rows(D):
     """The same windows as pitch-232 planes (conv1 loads rows straight into LDS) and as packed 227-wide
-    planes (register-staged conv1) give the same pool5 descriptors."""
+    planes (register-staged conv1) give the same pool5 descriptors, up to the order of conv1's fp32
+    accumulation (the two kernels group the 363 taps into MFMA k-steps differently): a wrong row pitch
+    or padding read would differ by far more."""
     boxes = synth.boxes(107, 24, WL.H, WL.W)
     x, b = torch.from_numpy(IMGS).cuda(), torch.from_numpy(boxes).cuda()
     pk = packed(D, "bf16")
@@ -141,4 +143,8 @@ def test_conv_features_row_pitch_matches_packed_rows(D):
         desc.append(q)
     cf = D.densenet_conv_features(win, desc, DTS["bf16"], pk, D.net_params(pool5=True))
     c = torch.stack([m.float() for m in cf.pool5_maps()])
-    torch.testing.assert_close(a, c, rtol=0, atol=0)
+    d = (a - c).abs()
+    rms = c.pow(2).mean().sqrt()
+    # the bf16 layer bar (a one-ulp difference at the largest values is ~0.05 rms), and most equal
+    assert torch.isfinite(a).all() and d.max() <= BARS["bf16"] * rms, (d.max().item(), rms.item())
+    assert (d > 0).float().mean() < 0.1
