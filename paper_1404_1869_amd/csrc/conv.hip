@@ -960,7 +960,18 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void con
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int OUT_CPOL = 2;  // cache policy of conv1's output stores: non-temporal
-constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's epilogue
+// conv1's MFMA pixel tiles per wave (Conv1R): 2, chosen by timing on the 96-plane batch (4, one wave per
+// SIMD with 30 % fewer LDS bytes per MFMA, took 0.82-0.84 ms against 0.646: a lone wave does not hide
+// its own LDS and load latency).
+#ifndef DN_CONV1_PT
+#define DN_CONV1_PT 2
+#endif
+// Wait until at most N (< 64) vector-memory accesses of this wave are outstanding.
+template <int N>
+__device__ inline void wait_vmem_upto() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
 
 // ------------------------------------------------------------------------------------------------
 // conv1 for 16-bit storage with direct global->LDS loads (plane width a multiple of 8, 16-byte
@@ -979,16 +990,21 @@ constexpr int EPI_STORES = 2 * 6;  // 16-byte stores per lane in a conv1 tile's 
 // itself; the other wave on its SIMD keeps the MFMAs busy.  A tile's outputs leave through LDS, as
 // whole 192-byte pixel rows.
 // ------------------------------------------------------------------------------------------------
+// PT: 32-pixel MFMA tiles per wave (2: wave tiles of 4 x 16 pixels, 8 waves per workgroup, two per
+// SIMD; 4: 8 x 16 pixels, 4 waves, one per SIMD, 30 % fewer LDS bytes per MFMA).
+template <int PT>
 struct Conv1R {
-  static constexpr int TH = 4, TW = 16, HR = 4 * (TH - 1) + 12;  // wave tile; halo rows (k rows 0..11)
+  static constexpr int NWV = PT == 2 ? 8 : 4;    // waves (workers) per workgroup
+  static constexpr int TH = 2 * PT, TW = 16, HR = 4 * (TH - 1) + 12;  // wave tile; halo rows (k 0..11)
+  static constexpr int EPI_STORES = PT * 6;      // 16-byte stores per lane in a tile's epilogue
   static constexpr int HSL = 10, HS = HSL * 8;   // halo row: slots, elements
   static constexpr int NH = (HR * HSL + 63) / 64;  // 1 KB pieces of a halo
   static constexpr int KSE = 96 * 16;            // elements of one k-step's weights
   static constexpr int WP = C1_KSTEPS * KSE / 512;  // 1 KB pieces of all weights
-  static constexpr int DWL = (WP + 7) / 8;       // weight pieces per wave (all weights, once)
+  static constexpr int DWL = (WP + NWV - 1) / NWV;  // weight pieces per wave (all weights, once)
   static constexpr int HALO_E = NH * 512;
   static constexpr int SROW = 104, SPX = 16;     // staging: elements per pixel row, pixels per round
-  static constexpr int HALO_OFF = WP * 512, BIAS_OFF = HALO_OFF + 8 * 2 * HALO_E;
+  static constexpr int HALO_OFF = WP * 512, BIAS_OFF = HALO_OFF + NWV * 2 * HALO_E;
   static constexpr int LDS_E = BIAS_OFF + 2 * 96;  // the biases as 96 floats
   // unit u of a tile's k-steps: input channel, and its LDS offset (row r, columns 4 cb ..) in the halo
   __host__ __device__ static constexpr int uchan(int u) { return u < C1_UNITS ? u / 33 : 2; }
@@ -997,12 +1013,13 @@ struct Conv1R {
   }
   __host__ __device__ static constexpr int kchan(int j) { return j < 8 ? 0 : (j < 16 ? 1 : 2); }  // stage
 };
-static_assert(Conv1R::WP * 512 == C1_KSTEPS * Conv1R::KSE, "the weights are whole pieces");
-static_assert(Conv1R::uchan(4 * 8) == 0 && Conv1R::uchan(4 * 8 + 1) == 1 && Conv1R::uchan(4 * 16 + 1) == 1 &&
-                  Conv1R::uchan(4 * 16 + 2) == 2,
+static_assert(Conv1R<2>::WP * 512 == C1_KSTEPS * Conv1R<2>::KSE, "the weights are whole pieces");
+static_assert(Conv1R<2>::uchan(4 * 8) == 0 && Conv1R<2>::uchan(4 * 8 + 1) == 1 &&
+                  Conv1R<2>::uchan(4 * 16 + 1) == 1 && Conv1R<2>::uchan(4 * 16 + 2) == 2,
               "k-steps 8 and 16 are the only ones that span two input channels");
-static_assert(Conv1R::SPX * Conv1R::SROW <= Conv1R::HALO_E, "epilogue staging fits a halo buffer");
-static_assert((size_t)Conv1R::LDS_E * 2 <= 160 * 1024, "one workgroup's LDS fits the CU");
+static_assert(Conv1R<2>::SPX * Conv1R<2>::SROW <= Conv1R<2>::HALO_E, "epilogue staging fits a halo buffer");
+static_assert((size_t)Conv1R<2>::LDS_E * 2 <= 160 * 1024, "one workgroup's LDS fits the CU");
+static_assert((size_t)Conv1R<4>::LDS_E * 2 <= 160 * 1024, "one workgroup's LDS fits the CU");
 
 // Keeps the compiler from moving this wave's LDS accesses across it (a wave's own LDS operations
 // execute in order).
@@ -1017,12 +1034,13 @@ __device__ inline void static_for(F&& f) {
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
+template <typename T, int PT>
+__global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
     int64_t out_stride, int tiles_x, int tiles_y, int ntiles, int zero_col_w) {
-  using P = Conv1R;
+  using P = Conv1R<PT>;
+  constexpr int NWV = P::NWV;
   using Op = Mfma<T>;
   using frag = typename Op::frag;
   using hfrag = typename Op::half_frag;
@@ -1037,11 +1055,12 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   constexpr uint32_t OOB = 0x80000000u;
 
   // Workers: workgroups are dispatched round-robin over the 8 XCDs, and rank r = x * (workgroups
-  // per XCD) + i of XCD x has the workers 8 r .. 8 r + 7; worker w takes wave tiles w, w + 8 G, ...:
-  // the workers in flight on one XCD hold neighbouring tiles, whose halos overlap in its L2.
+  // per XCD) + i of XCD x has the workers NWV r .. NWV r + NWV - 1; worker w takes wave tiles w,
+  // w + NWV G, ...: the workers in flight on one XCD hold neighbouring tiles, whose halos overlap in
+  // its L2.
   const int G = gridDim.x, xcd = blockIdx.x % 8, per = G / 8, rem = G % 8;
   const int rank = xcd * per + min(xcd, rem) + blockIdx.x / 8;
-  const int NWK = 8 * G, wk = 8 * rank + wave;
+  const int NWK = NWV * G, wk = NWV * rank + wave;
   const int ntile = wk < ntiles ? (ntiles - wk + NWK - 1) / NWK : 0;
 
   // All weights, once: piece q of the k-step blob lands in LDS piece q.
@@ -1050,7 +1069,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
         (void*)wp, 0, (int)(C1_KSTEPS * P::KSE * sizeof(T)), 0x00020000);
 #pragma unroll
     for (int i = 0; i < P::DWL; ++i) {
-      const int q = wave + 8 * i;
+      const int q = wave + NWV * i;
       if (q < P::WP) lds_direct16(rsrc_w, s_mem + q * 512, (uint32_t)(q * 1024 + lane * 16));
     }
   }
@@ -1090,9 +1109,9 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     }
   };
 
-  int lpix[2], lpix2[2];
+  int lpix[PT], lpix2[PT];
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < PT; ++b) {
     const int idx = b * 32 + l32;
     lpix[b] = 4 * (idx / P::TW) * P::HS + 4 * (idx % P::TW);
     lpix2[b] = lpix[b] + 2 * half * P::HS;
@@ -1104,7 +1123,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
   // the previous input channel's halo, hs the stage's.
   auto read = [&](auto jc, const T* hp, const T* hs, frag* x, frag* w) {
     constexpr int J = decltype(jc)::value, CS = P::kchan(J);
-    hfrag hv[2][2];
+    hfrag hv[PT][2];
 #pragma unroll
     for (int sx = 0; sx < 2; ++sx) {
       const int u0 = 4 * J + sx, u1 = 4 * J + 2 + sx;
@@ -1112,24 +1131,24 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
       const int o0 = P::uoff(u0), o1 = P::uoff(u1);
       if (!p0 && !p1 && o1 - o0 == 2 * P::HS) {  // the usual case: the upper half two rows down
 #pragma unroll
-        for (int b = 0; b < 2; ++b) hv[b][sx] = *(const hfrag*)(hs + lpix2[b] + o0);
+        for (int b = 0; b < PT; ++b) hv[b][sx] = *(const hfrag*)(hs + lpix2[b] + o0);
       } else {
         const T* bh = half ? (p1 ? hp : hs) + o1 : (p0 ? hp : hs) + o0;
 #pragma unroll
-        for (int b = 0; b < 2; ++b) hv[b][sx] = *(const hfrag*)(bh + lpix[b]);
+        for (int b = 0; b < PT; ++b) hv[b][sx] = *(const hfrag*)(bh + lpix[b]);
       }
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) x[b] = __builtin_shufflevector(hv[b][0], hv[b][1], 0, 1, 2, 3, 4, 5, 6, 7);
+    for (int b = 0; b < PT; ++b) x[b] = __builtin_shufflevector(hv[b][0], hv[b][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
     for (int mt = 0; mt < 3; ++mt) w[mt] = *(const frag*)(s_mem + J * P::KSE + 512 * mt + lw);
   };
 
-  f32x16 acc[3][2];
+  f32x16 acc[3][PT];
 #pragma unroll
   for (int a = 0; a < 3; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < PT; ++b) acc[a][b] = f32x16{};
 
   if (ntile > 0) {
     set_tile(wk);
@@ -1148,7 +1167,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
     // stage's load (issue) follows k-step J0's MFMAs, which have then consumed any fragment of hp.
     auto ksteps = [&](auto j0c, auto j1c, const T* hp, const T* hs, auto&& issue) {
       constexpr int J0 = decltype(j0c)::value, J1 = decltype(j1c)::value;
-      frag xr[2][2], wr[2][3];
+      frag xr[2][PT], wr[2][3];
       read(std::integral_constant<int, J0>{}, hp, hs, xr[0], wr[0]);
       auto body = [&](auto jc) {
         constexpr int J = decltype(jc)::value, B = (J - J0) & 1;
@@ -1159,7 +1178,7 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
 #pragma unroll
         for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
-          for (int b = 0; b < 2; ++b) acc[mt][b] = Op::mma(wr[B][mt], xr[B][b], acc[mt][b]);
+          for (int b = 0; b < PT; ++b) acc[mt][b] = Op::mma(wr[B][mt], xr[B][b], acc[mt][b]);
         __builtin_amdgcn_s_setprio(0);
         if constexpr (J == J0) {
           wave_lds_order();
@@ -1188,14 +1207,14 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
       // Epilogue of the tile: bias + ReLU; per 32-pixel MFMA tile, two rounds of 16 pixels staged
       // in X, just consumed (rows of 104 channels), read back as whole pixel rows and written with
       // 16-byte buffer stores that every lane issues (a pixel outside the map stores at an offset
-      // past the plane, which the hardware drops): EPI_STORES stores per lane.
+      // past the plane, which the hardware drops): P::EPI_STORES stores per lane.
       T* hs = hx;
       const int t = wk + j * NWK;
       const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
       const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
           (void*)(out + plane * out_stride), 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)), 0x00020000);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < PT; ++b) {
         out4_t v[3][4];
 #pragma unroll
         for (int mt = 0; mt < 3; ++mt)
@@ -1233,10 +1252,10 @@ __global__ __launch_bounds__(512, 1) void conv1_resident_kernel(
 #pragma unroll
       for (int a = 0; a < 3; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+        for (int b = 0; b < PT; ++b) acc[a][b] = f32x16{};
       // Vector-memory operations retire in issue order: once no more than the epilogue's stores
       // are outstanding, the next tile's halo loads (issued before them) have landed in LDS.
-      wait_vmem_but<EPI_STORES>();
+      wait_vmem_upto<P::EPI_STORES>();
     }
     zero_col((j + 1) & 1);
   }
@@ -1338,13 +1357,14 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
       if (direct) {
         if (ws == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
         // wave tiles of 4 x 16 output pixels, 8 workers per workgroup, one workgroup per CU
-        const int wtx = (Wo + Conv1R::TW - 1) / Conv1R::TW, wty = (Ho + Conv1R::TH - 1) / Conv1R::TH;
+        using R1 = Conv1R<DN_CONV1_PT>;
+        const int wtx = (Wo + R1::TW - 1) / R1::TW, wty = (Ho + R1::TH - 1) / R1::TH;
         const int64_t wtiles = (int64_t)wtx * wty * n;
         if (wtiles > 0x7fffffff) return (int)hipErrorInvalidValue;
-        const int grid = (int)std::min<int64_t>((wtiles + 7) / 8, device_cu_count());
-        conv1_resident_kernel<T><<<grid, 512, 0, s>>>(in, out, ws, bias, H, W, P, Ho, Wo, in_stride,
-                                                     out_stride, wtx, wty, (int)wtiles,
-                                                     (int)(W % 8 != 0 && P > W));
+        const int grid = (int)std::min<int64_t>((wtiles + R1::NWV - 1) / R1::NWV, device_cu_count());
+        conv1_resident_kernel<T, DN_CONV1_PT><<<grid, 64 * R1::NWV, 0, s>>>(
+            in, out, ws, bias, H, W, P, Ho, Wo, in_stride, out_stride, wtx, wty, (int)wtiles,
+            (int)(W % 8 != 0 && P > W));
       } else {
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
         conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
