@@ -114,6 +114,25 @@ def test_lrn_pool(D, dt, C, shape, lrn_first):
             assert np.max(np.abs(chw(out[i]) - ref) / np.maximum(np.abs(ref), 1e-3)) < 2e-5
 
 
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("C", [96, 256])
+@pytest.mark.parametrize("beta,k", [(0.75, 1.0), (0.5, 1.0), (0.75, 2.0), (0.75, 0.5)])
+def test_lrn_pool_power_paths(D, dt, C, beta, k):
+    """(k + alpha/n s)^-beta for other beta and k than AlexNet's, and activations from 0 to ~500 (every
+    third row 8x larger, sums of squares far past the usual range), against the oracle."""
+    n, H, W = 1, 29, 33
+    rng = np.random.default_rng(C + 11)
+    x = np.abs(rng.normal(0, 30, (n, H, W, C)))
+    x[:, ::3] *= 8.0                   # every third row large: sums of squares far past 12 500
+    x = round_to(x, dt)
+    xg = torch.from_numpy(x).to("cuda", TORCH_DT[dt]).contiguous()
+    out = D.densenet_lrn_pool(xg, DTS[dt], D.net_params(beta=beta, k=k)).float().cpu().numpy()
+    ref = oracle.maxpool(oracle.lrn(chw(x[0]), beta=beta, k=k))
+    assert_layer_close(chw(out[0]), ref, dt, f"lrn_pool C={C} beta={beta} k={k}")
+    if dt == "f32":
+        assert np.max(np.abs(chw(out[0]) - ref) / np.maximum(np.abs(ref), 1e-3)) < 2e-5
+
+
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 def test_lrn_pool2_strips_many_planes(D, dt):
     """20 planes of conv2's 149 x 149 x 256 maps: a launch large enough for the column-strip kernel
