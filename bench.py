@@ -8,7 +8,9 @@ After the timed steps it also times the paper's per-window baseline (every box o
 227 x 227 and run through the network on its own) and reports it beside the dense time per image, and
 the same batch with cross-image packing (the scales of all 16 images stitched together: 88 planes
 instead of 96), reported beside the headline, which keeps each image's own planes, and the latency of
-one 25-scale pyramid of one image (fp16), launched eagerly and replayed from a captured graph.
+one 25-scale pyramid of one image (fp16), launched eagerly and replayed from a captured graph, and
+the workloads that give each scale its own plane (480 x 640 at 8 scales in fp16 and fp32, 227 x 227
+at 2 scales in fp32), whose planes of different sizes share one launch per layer.
 The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
 1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
 
@@ -54,6 +56,8 @@ def parse():
                     help="skip the cross-image packed variant (the batch's scales stitched together)")
     ap.add_argument("--no-single", action="store_true",
                     help="skip the single-image latency figures (one 25-scale pyramid, fp16)")
+    ap.add_argument("--no-per-scale", action="store_true",
+                    help="skip the per-scale-plane workloads (480x640 at 8 scales, 227x227 at 2)")
     return ap.parse_args()
 
 
@@ -223,6 +227,8 @@ def main():
                                                     args.warmup, ms_per_step)
     if not args.no_single and n_img > 1:
         result["single_image"] = single_image(D, weights, args.steps, args.warmup)
+    if not args.no_per_scale and n_img > 1:
+        result["per_scale_planes"] = per_scale_planes(D, weights, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
     print(json.dumps(result), flush=True)
@@ -381,6 +387,59 @@ def single_image(D, weights, steps, warmup):
             "regions_2000_ms": round(regions_ms, 4),
             "kernels_ms": {k: round(v[1] / v[0], 4) for k, v in kern.items()},
             "paper_context": "Sec. 3.4, NVIDIA K20: one 25-scale pyramid in ~1 s"}
+
+
+def per_scale_planes(D, weights, steps, warmup):
+    """The workloads that give each scale its own plane (Sec. 3.1 without stitching): a 480 x 640 image
+    at 8 scales (8 plane sizes; fp16 and fp32) and a 227 x 227 image at 2 scales with pool5 (fp32).
+    Per workload: ms per pyramid (build + conv stack, eager, inputs resident), pyramids/s, and the conv
+    MFMA utilisation against the dtype's peak (algorithmic conv work of every plane over the summed
+    conv kernel time of traced pyramids).  Every layer is one launch over all plane sizes."""
+    import torch
+
+    from paper_1404_1869_amd import configs as C
+    from paper_1404_1869_amd import synth, workmodel
+
+    dev = torch.device("cuda", 0)
+    out = {}
+    for w in (C.VGA_8SCALE, C.ALEXNET_227):
+        img = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).to(dev)
+        params = D.params_for(w)
+        res = {}
+        for dtn in w.dtypes:
+            dt = D.DTYPES[dtn]
+            packed = D.densenet_pack_weights(weights, dt)
+            planes, plan = D.densenet_build_pyramid(img, params, dt)
+            cf = D.ConvFeatures(list(plan.planes), dt, D.net_params(pool5=w.pool5), device=dev)
+
+            def pyramid():
+                D.densenet_build_pyramid(img, params, dt, out=planes)
+                cf(planes, packed)
+
+            for _ in range(warmup):
+                pyramid()
+            torch.cuda.synchronize()
+            D.profile_start()
+            for _ in range(steps):
+                pyramid()
+            torch.cuda.synchronize()
+            kern = D.profile_stop()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(steps):
+                pyramid()
+            b.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b) / steps
+            conv_ms = sum(kern[k][1] for k in CONV_NAMES if k in kern) / steps
+            flops = sum(sum(workmodel.conv_flops(d.h, d.w)) for d in plan.planes)
+            res[dtn] = {"planes": [f"{d.h}x{d.w}" for d in plan.planes], "ms_per_pyramid": round(ms, 4),
+                        "pyramids_per_s": round(1e3 / ms, 2),
+                        "conv_launches_per_pyramid": round(sum(kern[k][0] for k in CONV_NAMES if k in kern)
+                                                           / steps, 2),
+                        "conv_mfma_util": round(flops / (conv_ms / 1e3) / 1e12 / PEAK_TFLOPS[dtn], 4)}
+        out[w.name] = res
+    return out
 
 
 def cpu_model() -> str:

@@ -212,9 +212,12 @@ int densenet_pack_weights(const float* const* d_w, const float* const* d_b, dn_d
                           void* d_packed, size_t packed_bytes, size_t* bytes_needed, void* stream);
 
 /* Planes -> conv5 maps (+ pool5), the whole conv stack (Sec. 3).  planes: [n_planes] descriptors of
- * the planes to run (offsets into d_planes, elements of `dtype`); consecutive planes of equal size
- * whose offsets are evenly spaced run in one launch per layer.  d_packed from densenet_pack_weights
- * with the same dtype.  d_workspace: scratch of ws_bytes (NULL => size query into *ws_needed).
+ * the planes to run (offsets into d_planes, elements of `dtype`), of any sizes.  Consecutive planes
+ * of equal size whose offsets are evenly spaced form a run; each layer is one launch over up to 16
+ * runs (more runs take more launches), so planes of different sizes (one plane per scale, several
+ * images) share their launches.  d_packed from densenet_pack_weights with the same dtype.
+ * d_workspace: scratch of ws_bytes (NULL => size query into *ws_needed): two buffers, each holding
+ * one layer's maps of all planes back to back.
  * d_conv5: out, per plane [Hc][Wc][256] packed back to back (descs in conv5_desc[n_planes]).
  * d_pool5: nullable; when net->pool5 it receives [Hp][Wp][256] per plane (descs in pool5_desc).
  * *conv5_needed / *pool5_needed receive the output sizes in bytes (size query when d_conv5 == NULL). */

@@ -46,8 +46,8 @@ static bool stack_shape(int32_t H, int32_t W, StackShape& s) {
   return s.h[6] > 0 && s.w[6] > 0;
 }
 
-// Planes grouped into runs of equal size and pitch and evenly spaced offsets (one launch per layer
-// per run).
+// Planes grouped into runs of equal size and pitch and evenly spaced offsets (the runs of a layer
+// share its launches).
 struct Run {
   int32_t first, count, h, w, pitch;
   int64_t stride;  // elements between consecutive planes (0 for a run of one)
@@ -482,9 +482,8 @@ int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, i
     const int64_t out_stride = (int64_t)Ms[layer - 1] * Ho * Wo;
     static const char* names[5] = {"conv1", "conv2", "conv3", "conv4", "conv5"};
     TraceScope trace(names[layer - 1], stream);
-    return hip_status(launch_conv(layer, d_in, n, H, W, in_stride, W, dtype, d_packed, d_out,
-                                  out_stride, stream),
-                      "conv launch");
+    const MapRun run{n, H, W, W, 0, in_stride, 0, out_stride};
+    return hip_status(launch_conv(layer, d_in, &run, 1, dtype, d_packed, d_out, stream), "conv launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
   }
@@ -502,9 +501,10 @@ int densenet_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t
     if (!(net->lrn_k > 0)) return fail(DN_E_INVALID_ARG, "lrn_k must be positive");
     const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
     TraceScope trace(C == 96 ? "lrn_pool1" : "lrn_pool2", stream);
-    return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, true,
-                                      net->lrn_before_pool != 0, net->lrn_alpha, net->lrn_beta,
-                                      net->lrn_k, net->lrn_n, d_out, (int64_t)C * Ho * Wo, stream),
+    const MapRun run{n, H, W, 0, 0, (int64_t)C * H * W, 0, (int64_t)C * Ho * Wo};
+    return hip_status(launch_lrn_pool(d_in, &run, 1, C, dtype, true, net->lrn_before_pool != 0,
+                                      net->lrn_alpha, net->lrn_beta, net->lrn_k, net->lrn_n, d_out,
+                                      stream),
                       "lrn_pool launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
@@ -519,8 +519,8 @@ int densenet_maxpool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t 
     if (n <= 0 || H < 2 || W < 2 || C <= 0) return fail(DN_E_INVALID_ARG, "bad sizes");
     const int64_t Ho = (H - 2) / 2 + 1, Wo = (W - 2) / 2 + 1;
     TraceScope trace("pool5", stream);
-    return hip_status(launch_lrn_pool(d_in, n, H, W, C, (int64_t)C * H * W, dtype, false, false, 0,
-                                      0, 1, 1, d_out, (int64_t)C * Ho * Wo, stream),
+    const MapRun run{n, H, W, 0, 0, (int64_t)C * H * W, 0, (int64_t)C * Ho * Wo};
+    return hip_status(launch_lrn_pool(d_in, &run, 1, C, dtype, false, false, 0, 0, 1, 1, d_out, stream),
                       "maxpool launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
@@ -549,9 +549,8 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
     if (net->pool5 && (!pool5_needed || !pool5_desc))
       return fail(DN_E_INVALID_ARG, "pool5 requested without pool5_needed / pool5_desc");
     const size_t es = dtype_size(dtype);
-    // Output layout and workspace: two ping-pong buffers sized for the largest run.
+    // Output layout: the conv5 (and pool5) maps in plane order.
     int64_t c5_off = 0, p5_off = 0;
-    size_t ws_a = 0, ws_b = 0;
     for (int32_t i = 0; i < n_planes; ++i) {
       StackShape s;
       if (planes[i].h <= 0 || planes[i].w <= 0 || planes[i].offset < 0 ||
@@ -571,16 +570,27 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
         p5_off += 256 * s.h[7] * s.w[7];
       }
     }
+    // Each layer is one launch over all runs (planes of different sizes included): the runs' maps of
+    // a layer are packed one after another in the workspace's two ping-pong buffers, A (conv1,
+    // conv2, conv3 outputs) and B (pool1, pool2, conv4 outputs).
     const std::vector<Run> runs = make_runs(planes, n_planes);
-    for (const Run& r : runs) {
-      StackShape s;
-      stack_shape(r.h, r.w, s);
-      const size_t a = std::max({96 * s.h[0] * s.w[0], 256 * s.h[2] * s.w[2], 384 * s.h[4] * s.w[4]});
-      const size_t b = std::max({96 * s.h[1] * s.w[1], 256 * s.h[3] * s.w[3], 384 * s.h[5] * s.w[5]});
-      ws_a = std::max(ws_a, (size_t)r.count * a * es);
-      ws_b = std::max(ws_b, (size_t)r.count * b * es);
+    const size_t nr = runs.size();
+    std::vector<StackShape> shp(nr);
+    std::vector<int64_t> oa1(nr), ob1(nr), oa2(nr), ob2(nr), oa3(nr), ob4(nr);
+    int64_t a1 = 0, b1 = 0, a2 = 0, b2 = 0, a3 = 0, b4 = 0;
+    for (size_t i = 0; i < nr; ++i) {
+      StackShape& s = shp[i];
+      stack_shape(runs[i].h, runs[i].w, s);
+      const int64_t n = runs[i].count;
+      oa1[i] = a1, a1 += n * 96 * s.h[0] * s.w[0];
+      ob1[i] = b1, b1 += n * 96 * s.h[1] * s.w[1];
+      oa2[i] = a2, a2 += n * 256 * s.h[2] * s.w[2];
+      ob2[i] = b2, b2 += n * 256 * s.h[3] * s.w[3];
+      oa3[i] = a3, a3 += n * 384 * s.h[4] * s.w[4];
+      ob4[i] = b4, b4 += n * 384 * s.h[5] * s.w[5];
     }
-    ws_a = (ws_a + 255) & ~(size_t)255;
+    const size_t ws_a = ((size_t)std::max({a1, a2, a3}) * es + 255) & ~(size_t)255;
+    const size_t ws_b = (size_t)std::max({b1, b2, b4}) * es;
     *ws_needed = ws_a + ws_b;
     *conv5_needed = (size_t)c5_off * es;
     if (net->pool5) *pool5_needed = (size_t)p5_off * es;
@@ -595,63 +605,69 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
     char* A = (char*)d_workspace;
     char* B = A + ws_a;
     const bool lf = net->lrn_before_pool != 0;
-    for (const Run& r : runs) {
-      StackShape s;
-      stack_shape(r.h, r.w, s);
+    const float al = net->lrn_alpha, be = net->lrn_beta, kk = net->lrn_k;
+    const int ln = net->lrn_n;
+    // Per layer and run: planes, input size, input/output offsets and strides (elements).
+    std::vector<MapRun> c1(nr), l1(nr), c2(nr), l2(nr), c3(nr), c4(nr), c5(nr), q5(nr);
+    for (size_t i = 0; i < nr; ++i) {
+      const Run& r = runs[i];
+      const StackShape& s = shp[i];
       const int n = r.count;
-      const char* in = (const char*)d_planes + planes[r.first].offset * es;
-      const int64_t sp = r.count > 1 ? r.stride : 3LL * r.h * r.pitch;
-      const int64_t H0 = r.h, W0 = r.w;
       const int64_t s1 = 96 * s.h[0] * s.w[0], p1 = 96 * s.h[1] * s.w[1];
       const int64_t s2 = 256 * s.h[2] * s.w[2], p2 = 256 * s.h[3] * s.w[3];
       const int64_t s3 = 384 * s.h[4] * s.w[4], s4 = 384 * s.h[5] * s.w[5];
-      const int64_t s5 = 256 * s.h[6] * s.w[6], q5 = 256 * s.h[7] * s.w[7];
-      char* c5 = (char*)d_conv5 + conv5_desc[r.first].offset * es;
+      const int64_t s5 = 256 * s.h[6] * s.w[6];
       const int h0 = (int)s.h[0], w0 = (int)s.w[0], h1 = (int)s.h[1], w1 = (int)s.w[1];
       const int h2 = (int)s.h[2], w2 = (int)s.w[2], h3 = (int)s.h[3], w3 = (int)s.w[3];
       const int h4 = (int)s.h[4], w4 = (int)s.w[4], h6 = (int)s.h[6], w6 = (int)s.w[6];
-      const float al = net->lrn_alpha, be = net->lrn_beta, kk = net->lrn_k;
-      const int ln = net->lrn_n;
-      int st;
-      if ((st = run_step("conv1", stream, [&] {
-             return launch_conv(1, in, n, (int)H0, (int)W0, sp, r.pitch, dtype, d_packed, A, s1,
-                                stream);
+      const int64_t sp = r.count > 1 ? r.stride : 3LL * r.h * r.pitch;
+      const int64_t o5 = conv5_desc[r.first].offset;
+      c1[i] = MapRun{n, r.h, r.w, r.pitch, planes[r.first].offset, sp, oa1[i], s1};
+      l1[i] = MapRun{n, h0, w0, 0, oa1[i], s1, ob1[i], p1};
+      c2[i] = MapRun{n, h1, w1, 0, ob1[i], p1, oa2[i], s2};
+      l2[i] = MapRun{n, h2, w2, 0, oa2[i], s2, ob2[i], p2};
+      c3[i] = MapRun{n, h3, w3, 0, ob2[i], p2, oa3[i], s3};
+      c4[i] = MapRun{n, h4, w4, 0, oa3[i], s3, ob4[i], s4};
+      c5[i] = MapRun{n, h4, w4, 0, ob4[i], s4, o5, s5};
+      if (net->pool5)
+        q5[i] = MapRun{n, h6, w6, 0, o5, s5, pool5_desc[r.first].offset, 256 * s.h[7] * s.w[7]};
+    }
+    const int n_runs = (int)nr;
+    int st;
+    if ((st = run_step("conv1", stream, [&] {
+           return launch_conv(1, d_planes, c1.data(), n_runs, dtype, d_packed, A, stream);
+         })))
+      return st;
+    if ((st = run_step("lrn_pool1", stream, [&] {
+           return launch_lrn_pool(A, l1.data(), n_runs, 96, dtype, true, lf, al, be, kk, ln, B, stream);
+         })))
+      return st;
+    if ((st = run_step("conv2", stream, [&] {
+           return launch_conv(2, B, c2.data(), n_runs, dtype, d_packed, A, stream);
+         })))
+      return st;
+    if ((st = run_step("lrn_pool2", stream, [&] {
+           return launch_lrn_pool(A, l2.data(), n_runs, 256, dtype, true, lf, al, be, kk, ln, B, stream);
+         })))
+      return st;
+    if ((st = run_step("conv3", stream, [&] {
+           return launch_conv(3, B, c3.data(), n_runs, dtype, d_packed, A, stream);
+         })))
+      return st;
+    if ((st = run_step("conv4", stream, [&] {
+           return launch_conv(4, A, c4.data(), n_runs, dtype, d_packed, B, stream);
+         })))
+      return st;
+    if ((st = run_step("conv5", stream, [&] {
+           return launch_conv(5, B, c5.data(), n_runs, dtype, d_packed, d_conv5, stream);
+         })))
+      return st;
+    if (net->pool5) {
+      if ((st = run_step("pool5", stream, [&] {
+             return launch_lrn_pool(d_conv5, q5.data(), n_runs, 256, dtype, false, false, 0, 0, 1, 1,
+                                    d_pool5, stream);
            })))
         return st;
-      if ((st = run_step("lrn_pool1", stream, [&] {
-             return launch_lrn_pool(A, n, h0, w0, 96, s1, dtype, true, lf, al, be, kk, ln, B, p1,
-                                    stream);
-           })))
-        return st;
-      if ((st = run_step("conv2", stream, [&] {
-             return launch_conv(2, B, n, h1, w1, p1, 0, dtype, d_packed, A, s2, stream);
-           })))
-        return st;
-      if ((st = run_step("lrn_pool2", stream, [&] {
-             return launch_lrn_pool(A, n, h2, w2, 256, s2, dtype, true, lf, al, be, kk, ln, B, p2,
-                                    stream);
-           })))
-        return st;
-      if ((st = run_step("conv3", stream, [&] {
-             return launch_conv(3, B, n, h3, w3, p2, 0, dtype, d_packed, A, s3, stream);
-           })))
-        return st;
-      if ((st = run_step("conv4", stream, [&] {
-             return launch_conv(4, A, n, h4, w4, s3, 0, dtype, d_packed, B, s4, stream);
-           })))
-        return st;
-      if ((st = run_step("conv5", stream, [&] {
-             return launch_conv(5, B, n, h4, w4, s4, 0, dtype, d_packed, c5, s5, stream);
-           })))
-        return st;
-      if (net->pool5) {
-        char* p5 = (char*)d_pool5 + pool5_desc[r.first].offset * es;
-        if ((st = run_step("pool5", stream, [&] {
-               return launch_lrn_pool(c5, n, h6, w6, 256, s5, dtype, false, false, 0, 0, 1, 1, p5,
-                                      q5, stream);
-             })))
-          return st;
-      }
     }
     return DN_OK;
   } catch (...) {

@@ -120,16 +120,76 @@ PackedLayout packed_layout(dn_dtype dt);
 int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dtype dt, void* d_packed,
                         void* stream);
 
-// One conv layer (1..5) with bias and ReLU over n equal planes spaced in_stride / out_stride elements.
-// in_pitch: row pitch (elements) of layer 1's channel-major input planes (>= W); ignored otherwise.
-int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                int32_t in_pitch, dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride,
-                void* stream);
+// A run of a layer launch: n planes of one size, H x W at the layer's input; plane i reads at in_off +
+// i in_stride and writes at out_off + i out_stride (elements from the launch's base pointers).  pitch:
+// row pitch of conv1's channel-major input planes (>= W, or 0 for W); ignored by the other layers.
+struct MapRun {
+  int32_t n, H, W, pitch;
+  int64_t in_off, in_stride, out_off, out_stride;
+};
 
-// LRN + pool (order by lrn_first), or plain pool when lrn == false.  Channels-last maps.
-int launch_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in_stride,
-                    dn_dtype dt, bool lrn, bool lrn_first, float alpha, float beta, float k,
-                    int32_t lrn_n, void* d_out, int64_t out_stride, void* stream);
+// The runs of one launch as the kernels see them (passed by value): run r owns the launch's
+// workgroups (or wave tiles) first .. first of run r + 1 - 1, its planes' tiles in the kernel's own
+// order; Ho x Wo is the layer's output size.  A launch of more runs than MAX_RUNS is issued as
+// several launches.
+constexpr int MAX_RUNS = 16;
+struct KRun {
+  int32_t first, H, W, pitch, Ho, Wo, tiles_x, tiles_y;
+  int64_t in_off, in_stride, out_off, out_stride;
+};
+struct KRuns {
+  int32_t count;
+  KRun r[MAX_RUNS];
+};
+#if defined(__HIPCC__)
+// Run of workgroup (or tile) index b: the last run whose first index is at most b.  The table sits in
+// the kernel arguments; a wave-uniform index reads its fields with scalar loads.  MULTI = false: a
+// launch of one run, whose fields then sit at fixed offsets like plain scalar arguments (no loads
+// per tile, whose waits would also drain a kernel's LDS pipeline).
+template <bool MULTI = true>
+__device__ inline int run_of(const KRuns& t, int b) {
+  if constexpr (!MULTI) {
+    return 0;
+  } else {
+    int k = 0;
+#pragma unroll
+    for (int i = 1; i < MAX_RUNS; ++i) k = (i < t.count && b >= t.r[i].first) ? i : k;
+    return __builtin_amdgcn_readfirstlane(k);
+  }
+}
+#endif
+// The kernel table of runs [0, n) (n <= MAX_RUNS): geometry(k) sets k's Ho, Wo, tiles_x and tiles_y
+// from its input size and returns the workgroups (or tiles) of one plane.  Returns the launch's
+// total, or -1 when it is empty or passes 2^31 - 1.
+template <typename G>
+inline int64_t fill_kruns(const MapRun* runs, int n, KRuns& t, G&& geometry) {
+  t = KRuns{};
+  t.count = n;
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    KRun& k = t.r[i];
+    k.first = (int32_t)total;
+    k.H = runs[i].H, k.W = runs[i].W, k.pitch = runs[i].pitch > 0 ? runs[i].pitch : runs[i].W;
+    k.in_off = runs[i].in_off, k.in_stride = runs[i].in_stride;
+    k.out_off = runs[i].out_off, k.out_stride = runs[i].out_stride;
+    const int64_t per = geometry(k);
+    if (per <= 0 || runs[i].n <= 0) return -1;
+    total += per * runs[i].n;
+    if (total > 0x7fffffffLL) return -1;
+  }
+  return total > 0 ? total : -1;
+}
+
+// One conv layer (1..5) with bias and ReLU over the planes of `runs` (any number of runs; one launch
+// per MAX_RUNS of them).
+int launch_conv(int layer, const void* d_in, const MapRun* runs, int32_t n_runs, dn_dtype dt,
+                const void* d_packed, void* d_out, void* stream);
+
+// LRN + pool (order by lrn_first), or plain pool when lrn == false, over the channels-last maps of
+// `runs` (one launch per MAX_RUNS runs).
+int launch_lrn_pool(const void* d_in, const MapRun* runs, int32_t n_runs, int32_t C, dn_dtype dt,
+                    bool lrn, bool lrn_first, float alpha, float beta, float k, int32_t lrn_n,
+                    void* d_out, void* stream);
 
 struct RegScale {
   int32_t plane, y, x, r0, r1, c0, c1;

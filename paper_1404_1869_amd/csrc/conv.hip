@@ -145,15 +145,20 @@ struct Conv1Cfg {
 template <typename T>
 __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T* __restrict__ out,
                                                     const T* __restrict__ wp,
-                                                    const float* __restrict__ bias, int H, int W,
-                                                    int P, int Ho, int Wo, int64_t in_stride,
-                                                    int64_t out_stride, int tiles_x, int tiles_y) {
+                                                    const float* __restrict__ bias, KRuns runs) {
   using C = Conv1Cfg<T>;
   using Op = Mfma<T>;
   __shared__ T s_in[C::HR * C::HS];
   __shared__ T s_w[96 * C::WS];
 
   int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
+  const int P = rn.pitch, Ho = rn.Ho, Wo = rn.Wo;
   const int tx = bid % tiles_x;
   bid /= tiles_x;
   const int ty = bid % tiles_y;
@@ -245,8 +250,7 @@ struct Conv1P {
 template <typename T>
 __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
-    int64_t out_stride, int tiles_x, int tiles_y, int ntiles) {
+    const float* __restrict__ bias, KRuns runs, int ntiles) {
   using P = Conv1P<T>;
   using Op = Mfma<T>;
   typedef T vec8 __attribute__((ext_vector_type(8)));
@@ -266,11 +270,13 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     const int idx = wave * 64 + t * 32 + l32;
     lpix[t] = 4 * (idx / P::TW) * P::HS + 4 * (idx % P::TW);
   }
-  const bool vec_ok = (W % 8) == 0 && (pitch % 8) == 0;
   vec8 hreg[P::HPER];
   auto load_halo = [&](int t) {
-    const int tx = t % tiles_x, r = t / tiles_x, ty = r % tiles_y, plane = r / tiles_y;
-    const T* src = in + plane * in_stride;
+    const KRun& rn = runs.r[run_of(runs, t)];
+    const int H = rn.H, W = rn.W, pitch = rn.pitch, tl = t - rn.first;
+    const bool vec_ok = (W % 8) == 0 && (pitch % 8) == 0;
+    const int tx = tl % rn.tiles_x, r = tl / rn.tiles_x, ty = r % rn.tiles_y, plane = r / rn.tiles_y;
+    const T* src = in + rn.in_off + plane * rn.in_stride;
     const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
 #pragma unroll
     for (int i = 0; i < P::HPER; ++i) {
@@ -344,8 +350,10 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
     }
     if (tn < ntiles) store_halo(buf ^ 1);
     // epilogue: bias + ReLU, 4 consecutive channels per store
-    const int tx = t % tiles_x, r = t / tiles_x, ty = r % tiles_y, plane = r / tiles_y;
-    T* dst = out + plane * out_stride;
+    const KRun& rn = runs.r[run_of(runs, t)];
+    const int Ho = rn.Ho, Wo = rn.Wo, tl = t - rn.first;
+    const int tx = tl % rn.tiles_x, r = tl / rn.tiles_x, ty = r % rn.tiles_y, plane = r / rn.tiles_y;
+    T* dst = out + rn.out_off + plane * rn.out_stride;
 #pragma unroll
     for (int mt = 0; mt < 3; ++mt)
 #pragma unroll
@@ -460,8 +468,7 @@ constexpr int conv_threads() {
 template <typename T, int R, int BM, int TM, int OCC, int TS>
 __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
-    int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
+    const float* __restrict__ bias, KRuns runs, int C, int Cg, int M, int Mg, int mblocks) {
   using Cf = ConvCfg<T, R, BM, TM, TS>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
@@ -478,6 +485,12 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   // one tile first, then neighbouring tiles) then share that XCD's L2.
   const int nb = gridDim.x, xcd = blockIdx.x % 8, per = nb / 8, rem = nb % 8;
   int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
   const int mb = bid % mblocks;
   bid /= mblocks;
   const int tx = bid % tiles_x;
@@ -709,12 +722,12 @@ __device__ inline void lds_direct16(__amdgpu_buffer_rsrc_t rsrc, void* lds_piece
 }
 
 // BMP: the channel block the stage-major weight copy is cut in (a multiple of BM); a workgroup's BM
-// channels are a sub-block of one such block.  TN_: 32-pixel MFMA tiles per wave.
-template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP, int TN_>
+// channels are a sub-block of one such block.  TN_: 32-pixel MFMA tiles per wave.  MULTI: the launch
+// holds several runs (else run 0 only).
+template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP, int TN_, bool MULTI>
 __global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void conv_s1_direct_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int C, int Cg, int M, int Mg, int64_t in_stride,
-    int64_t out_stride, int tiles_x, int tiles_y, int mblocks) {
+    const float* __restrict__ bias, KRuns runs, int C, int Cg, int M, int Mg, int mblocks) {
   using Cf = ConvCfg<T, R, BM, TM, TS, TN_>;
   using Op = Mfma<T>;
   static_assert(!Cf::F32 && (TM == 2 || TM == 3), "direct-load path is for 16-bit storage");
@@ -737,6 +750,12 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void con
 
   const int nb = gridDim.x, xcd = blockIdx.x % 8, per = nb / 8, rem = nb % 8;
   int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const KRun& rn = runs.r[run_of<MULTI>(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
   const int mb = bid % mblocks;
   bid /= mblocks;
   const int tx = bid % tiles_x;
@@ -1034,11 +1053,10 @@ __device__ inline void static_for(F&& f) {
   }
 }
 
-template <typename T, int PT>
+template <typename T, int PT, bool MULTI>
 __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, int H, int W, int pitch, int Ho, int Wo, int64_t in_stride,
-    int64_t out_stride, int tiles_x, int tiles_y, int ntiles, int zero_col_w) {
+    const float* __restrict__ bias, KRuns runs, int ntiles) {
   using P = Conv1R<PT>;
   constexpr int NWV = P::NWV;
   using Op = Mfma<T>;
@@ -1073,7 +1091,7 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
       if (q < P::WP) lds_direct16(rsrc_w, s_mem + q * 512, (uint32_t)(q * 1024 + lane * 16));
     }
   }
-  const uint32_t chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
+  uint32_t chan_bytes = 0;  // bytes of one input channel of the current tile's plane
   auto hbuf = [&](int b) { return s_mem + P::HALO_OFF + (2 * wave + b) * P::HALO_E; };
   uint32_t hoff[P::NH];
   __amdgpu_buffer_rsrc_t rsrc_in;
@@ -1083,10 +1101,14 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
   // position in the tile's halo (else -1) and the halo copy of it is overwritten with zeros.
   int zcol = -1;
   auto set_tile = [&](int t) {  // input descriptor and halo slot offsets of wave tile t
-    const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
-    rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + plane * in_stride), 0,
+    const KRun& rn = runs.r[run_of<MULTI>(runs, t)];
+    const int H = rn.H, W = rn.W, pitch = rn.pitch, tl = t - rn.first;
+    const int tx = tl % rn.tiles_x, rr = tl / rn.tiles_x, ty = rr % rn.tiles_y, plane = rr / rn.tiles_y;
+    chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
+    rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + rn.in_off + plane * rn.in_stride), 0,
                                                 (int)(3 * chan_bytes), 0x00020000);
     const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
+    const bool zero_col_w = W % 8 != 0 && pitch > W;
     zcol = __builtin_amdgcn_readfirstlane(zero_col_w && W >= ix0 && W < ix0 + 72 ? W - ix0 : -1);
 #pragma unroll
     for (int i = 0; i < P::NH; ++i) {
@@ -1210,9 +1232,12 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
       // past the plane, which the hardware drops): P::EPI_STORES stores per lane.
       T* hs = hx;
       const int t = wk + j * NWK;
-      const int tx = t % tiles_x, rr = t / tiles_x, ty = rr % tiles_y, plane = rr / tiles_y;
+      const KRun& rn = runs.r[run_of<MULTI>(runs, t)];
+      const int Ho = rn.Ho, Wo = rn.Wo, tl = t - rn.first;
+      const int tx = tl % rn.tiles_x, rr = tl / rn.tiles_x, ty = rr % rn.tiles_y, plane = rr / rn.tiles_y;
       const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)(out + plane * out_stride), 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)), 0x00020000);
+          (void*)(out + rn.out_off + plane * rn.out_stride), 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)),
+          0x00020000);
 #pragma unroll
       for (int b = 0; b < PT; ++b) {
         out4_t v[3][4];
@@ -1262,24 +1287,34 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
 }
 
 template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM, int TN = 4>
-int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, int n, int H,
-                int W, int C, int G, int M, int64_t in_stride, int64_t out_stride, hipStream_t s) {
+int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, const MapRun* runs,
+                int n_runs, int C, int G, int M, hipStream_t s) {
   using Cf = ConvCfg<T, R, BM, TM, TS, TN>;
   const int Cg = C / G, Mg = M / G;
-  const int tiles_x = (W + Cf::TW - 1) / Cf::TW, tiles_y = (H + Cf::TH - 1) / Cf::TH;
   if (Mg % BM) return (int)hipErrorInvalidValue;  // whole channel blocks per group
   const int mblocks = G * (Mg / BM);
-  const int64_t blocks = (int64_t)tiles_x * tiles_y * mblocks * n;
-  if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+  KRuns kr;
+  const int64_t blocks = fill_kruns(runs, n_runs, kr, [&](KRun& k) {
+    k.Ho = k.H, k.Wo = k.W;
+    k.tiles_x = (k.W + Cf::TW - 1) / Cf::TW, k.tiles_y = (k.H + Cf::TH - 1) / Cf::TH;
+    return (int64_t)k.tiles_x * k.tiles_y * mblocks;
+  });
+  if (blocks <= 0) return (int)hipErrorInvalidValue;
   if constexpr (Cf::F32 || (TM != 2 && TM != 3)) {
-    conv_s1_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(
-        in, out, wp, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+    conv_s1_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(in, out, wp, bias, kr, C, Cg,
+                                                                           M, Mg, mblocks);
   } else {
     // buffer descriptors address one plane with 32-bit byte offsets
-    if ((int64_t)H * W * C * (int64_t)sizeof(T) >= 0x7fffffffLL) return (int)hipErrorInvalidValue;
+    for (int i = 0; i < n_runs; ++i)
+      if ((int64_t)runs[i].H * runs[i].W * C * (int64_t)sizeof(T) >= 0x7fffffffLL)
+        return (int)hipErrorInvalidValue;
     if (wstage == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
-    conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP, TN><<<(unsigned)blocks, Cf::NT, 0, s>>>(
-        in, out, wstage, bias, H, W, C, Cg, M, Mg, in_stride, out_stride, tiles_x, tiles_y, mblocks);
+    if (n_runs == 1)
+      conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP, TN, false><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+          in, out, wstage, bias, kr, C, Cg, M, Mg, mblocks);
+    else
+      conv_s1_direct_kernel<T, R, BM, TM, OCC, TS, BMP, TN, true><<<(unsigned)blocks, Cf::NT, 0, s>>>(
+          in, out, wstage, bias, kr, C, Cg, M, Mg, mblocks);
   }
   return (int)hipGetLastError();
 }
@@ -1324,17 +1359,18 @@ constexpr int L_BM[5] = {0, CfgBM<DN_CONV2_CFG>::BM, CfgBM<DN_CONV3_CFG>::BM, Cf
 #define DN_SMALL_OCC 3
 #endif
 template <int BM_, int TM_, int OCC_, int TS_>
-bool small_launch(int n, int H, int W, int M) {
-  const int64_t blocks = (int64_t)((W + TS_ % 100 - 1) / (TS_ % 100)) * ((H + TS_ / 100 - 1) / (TS_ / 100)) *
-                         (M / BM_) * n;
+bool small_launch(const MapRun* runs, int n_runs, int M) {
+  int64_t blocks = 0;
+  for (int i = 0; i < n_runs; ++i)
+    blocks += (int64_t)((runs[i].W + TS_ % 100 - 1) / (TS_ % 100)) *
+              ((runs[i].H + TS_ / 100 - 1) / (TS_ / 100)) * (M / BM_) * runs[i].n;
   const int per_cu = OCC_ * 4 / (BM_ / (32 * TM_) * (TS_ / 100) * (TS_ % 100) / 128);
   return blocks < 2LL * device_cu_count() * (per_cu > 0 ? per_cu : 1);
 }
 
 template <typename T>
-int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                  int32_t P, const void* d_packed, void* d_out, int64_t out_stride, const PackedLayout& L,
-                  hipStream_t s) {
+int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, const void* d_packed,
+                  void* d_out, const PackedLayout& L, hipStream_t s) {
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
   const T* wp = (const T*)((const char*)d_packed + L.w_off[layer - 1]);
@@ -1342,61 +1378,75 @@ int conv_dispatch(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, 
   const T* ws = L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
   const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
   if (layer == 1) {
-    const int Ho = (H - 11) / 4 + 1, Wo = (W - 11) / 4 + 1;
-    const int tiles_x = (Wo + 15) / 16, tiles_y = (Ho + 15) / 16;
-    const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
-    if (blocks <= 0 || blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    KRuns kr;
+    auto tiles16 = [](KRun& k) {  // tiles of 16 x 16 output pixels
+      k.Ho = (k.H - 11) / 4 + 1, k.Wo = (k.W - 11) / 4 + 1;
+      k.tiles_x = (k.Wo + 15) / 16, k.tiles_y = (k.Ho + 15) / 16;
+      return (int64_t)k.tiles_x * k.tiles_y;
+    };
     if constexpr (std::is_same<T, float>::value) {
-      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
-                                                      out_stride, tiles_x, tiles_y);
+      const int64_t blocks = fill_kruns(runs, n_runs, kr, tiles16);
+      if (blocks <= 0) return (int)hipErrorInvalidValue;
+      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, kr);
     } else {
       // Direct loads take 16-byte slots of plane rows at 32-bit byte offsets within one plane.
-      const bool direct = P % 8 == 0 && in_stride % 8 == 0 && ((uintptr_t)in & 15) == 0 &&
-                          (int64_t)3 * H * P * (int64_t)sizeof(T) < 0x7fffffffLL &&
-                          (int64_t)Ho * Wo * 96 * (int64_t)sizeof(T) < 0x7fffffffLL;
+      bool direct = ((uintptr_t)in & 15) == 0;
+      for (int i = 0; i < n_runs; ++i) {
+        const MapRun& r = runs[i];
+        const int64_t Ho = (r.H - 11) / 4 + 1, Wo = (r.W - 11) / 4 + 1;
+        const int64_t pitch = r.pitch > 0 ? r.pitch : r.W;
+        direct = direct && pitch % 8 == 0 && r.in_stride % 8 == 0 && r.in_off % 8 == 0 &&
+                 3 * r.H * pitch * (int64_t)sizeof(T) < 0x7fffffffLL &&
+                 Ho * Wo * 96 * (int64_t)sizeof(T) < 0x7fffffffLL;
+      }
       if (direct) {
         if (ws == wp) return (int)hipErrorInvalidValue;  // the stage-major weight copy is required
         // wave tiles of 4 x 16 output pixels, 8 workers per workgroup, one workgroup per CU
         using R1 = Conv1R<DN_CONV1_PT>;
-        const int wtx = (Wo + R1::TW - 1) / R1::TW, wty = (Ho + R1::TH - 1) / R1::TH;
-        const int64_t wtiles = (int64_t)wtx * wty * n;
-        if (wtiles > 0x7fffffff) return (int)hipErrorInvalidValue;
+        const int64_t wtiles = fill_kruns(runs, n_runs, kr, [](KRun& k) {
+          k.Ho = (k.H - 11) / 4 + 1, k.Wo = (k.W - 11) / 4 + 1;
+          k.tiles_x = (k.Wo + R1::TW - 1) / R1::TW, k.tiles_y = (k.Ho + R1::TH - 1) / R1::TH;
+          return (int64_t)k.tiles_x * k.tiles_y;
+        });
+        if (wtiles <= 0) return (int)hipErrorInvalidValue;
         const int grid = (int)std::min<int64_t>((wtiles + R1::NWV - 1) / R1::NWV, device_cu_count());
-        conv1_resident_kernel<T, DN_CONV1_PT><<<grid, 64 * R1::NWV, 0, s>>>(
-            in, out, ws, bias, H, W, P, Ho, Wo, in_stride, out_stride, wtx, wty, (int)wtiles,
-            (int)(W % 8 != 0 && P > W));
+        if (n_runs == 1)
+          conv1_resident_kernel<T, DN_CONV1_PT, false><<<grid, 64 * R1::NWV, 0, s>>>(in, out, ws, bias, kr,
+                                                                                    (int)wtiles);
+        else
+          conv1_resident_kernel<T, DN_CONV1_PT, true><<<grid, 64 * R1::NWV, 0, s>>>(in, out, ws, bias, kr,
+                                                                                   (int)wtiles);
       } else {
+        const int64_t blocks = fill_kruns(runs, n_runs, kr, tiles16);
+        if (blocks <= 0) return (int)hipErrorInvalidValue;
         const int grid = (int)std::min<int64_t>(blocks, device_cu_count());
-        conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, H, W, P, Ho, Wo, in_stride,
-                                                       out_stride, tiles_x, tiles_y, (int)blocks);
+        conv1_persistent_kernel<T><<<grid, 256, 0, s>>>(in, out, wp, bias, kr, (int)blocks);
       }
     }
     return (int)hipGetLastError();
   }
   const int li = layer - 1;
+  constexpr bool F32 = std::is_same<T, float>::value;
+#define DN_RUN_ARGS in, out, wp, ws, bias, runs, n_runs, L_C[li], L_G[li], L_M[li], s
+#define DN_SMALL_CFG(l) 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[l], DN_SMALL_TN
   switch (layer) {
     case 2:
-      return run_conv_s1<T, 5, DN_CONV2_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
-                                             in_stride, out_stride, s);
+      return run_conv_s1<T, 5, DN_CONV2_CFG>(DN_RUN_ARGS);
     case 3:
-      if (!std::is_same<T, float>::value && small_launch<DN_CONV3_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[2], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
-                                                          L_M[li], in_stride, out_stride, s);
-      return run_conv_s1<T, 3, DN_CONV3_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
-                                             in_stride, out_stride, s);
-    case 5:
-      if (!std::is_same<T, float>::value && small_launch<DN_CONV5_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[4], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
-                                                          L_M[li], in_stride, out_stride, s);
-      return run_conv_s1<T, 3, DN_CONV5_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
-                                             in_stride, out_stride, s);
+      if (!F32 && small_launch<DN_CONV3_CFG>(runs, n_runs, L_M[li]))
+        return run_conv_s1<T, DN_SMALL_CFG(2)>(DN_RUN_ARGS);
+      return run_conv_s1<T, 3, DN_CONV3_CFG>(DN_RUN_ARGS);
     case 4:
-      if (!std::is_same<T, float>::value && small_launch<DN_CONV4_CFG>(n, H, W, L_M[li]))
-        return run_conv_s1<T, 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[3], DN_SMALL_TN>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li],
-                                                          L_M[li], in_stride, out_stride, s);
-      return run_conv_s1<T, 3, DN_CONV4_CFG>(in, out, wp, ws, bias, n, H, W, L_C[li], L_G[li], L_M[li],
-                                             in_stride, out_stride, s);
+      if (!F32 && small_launch<DN_CONV4_CFG>(runs, n_runs, L_M[li]))
+        return run_conv_s1<T, DN_SMALL_CFG(3)>(DN_RUN_ARGS);
+      return run_conv_s1<T, 3, DN_CONV4_CFG>(DN_RUN_ARGS);
+    case 5:
+      if (!F32 && small_launch<DN_CONV5_CFG>(runs, n_runs, L_M[li]))
+        return run_conv_s1<T, DN_SMALL_CFG(4)>(DN_RUN_ARGS);
+      return run_conv_s1<T, 3, DN_CONV5_CFG>(DN_RUN_ARGS);
   }
+#undef DN_SMALL_CFG
+#undef DN_RUN_ARGS
   return (int)hipErrorInvalidValue;
 }
 
@@ -1472,22 +1522,22 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
   return (int)hipGetLastError();
 }
 
-int launch_conv(int layer, const void* d_in, int32_t n, int32_t H, int32_t W, int64_t in_stride,
-                int32_t in_pitch, dn_dtype dt, const void* d_packed, void* d_out, int64_t out_stride,
-                void* stream) {
+int launch_conv(int layer, const void* d_in, const MapRun* runs, int32_t n_runs, dn_dtype dt,
+                const void* d_packed, void* d_out, void* stream) {
   const PackedLayout L = packed_layout(dt);
   hipStream_t s = (hipStream_t)stream;
-  const int32_t P = layer == 1 && in_pitch > 0 ? in_pitch : W;
-  switch (dt) {
-    case DN_F32:
-      return conv_dispatch<float>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride, L, s);
-    case DN_F16:
-      return conv_dispatch<_Float16>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride,
-                                     L, s);
-    case DN_BF16:
-      return conv_dispatch<__bf16>(layer, d_in, n, H, W, in_stride, P, d_packed, d_out, out_stride, L, s);
+  if (layer < 1 || layer > 5 || n_runs <= 0) return (int)hipErrorInvalidValue;
+  for (int i0 = 0; i0 < n_runs; i0 += MAX_RUNS) {  // one launch per MAX_RUNS runs
+    const int nr = std::min(MAX_RUNS, n_runs - i0);
+    int st = (int)hipErrorInvalidValue;
+    switch (dt) {
+      case DN_F32: st = conv_dispatch<float>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
+      case DN_F16: st = conv_dispatch<_Float16>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
+      case DN_BF16: st = conv_dispatch<__bf16>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
+    }
+    if (st) return st;
   }
-  return (int)hipErrorInvalidValue;
+  return 0;
 }
 
 }  // namespace dn

@@ -19,6 +19,7 @@
 // reach it.
 //
 // The pool-then-LRN order uses a simple kernel with one thread per output element.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -76,11 +77,9 @@ struct Vec {
 
 template <typename T, bool LRN, int HN>
 __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict__ in,
-                                                            T* __restrict__ out, int H, int W, int C,
-                                                            int Ho, int Wo, int TPH, int TPW,
-                                                            int tiles_x, int tiles_y,
-                                                            int64_t in_stride, int64_t out_stride,
-                                                            float alpha_n, float beta, float k) {
+                                                            T* __restrict__ out, KRuns runs, int C,
+                                                            int TPH, int TPW, float alpha_n,
+                                                            float beta, float k) {
   constexpr int N = Vec<T>::N;
   static_assert(HN <= N && HN <= MAX_HALF, "the channel window must fit one neighbouring vector");
   typedef typename Vec<T>::type vec_t;
@@ -90,6 +89,12 @@ __global__ __launch_bounds__(256) void lrn_pool_tile_kernel(const T* __restrict_
   const int G = C / N;   // channel vectors per pixel
 
   int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, Ho = rn.Ho, Wo = rn.Wo, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
   const int tx = bid % tiles_x;
   bid /= tiles_x;
   const int ty = bid % tiles_y;
@@ -242,14 +247,11 @@ __device__ inline void lrn_channels(const typename Vec<T>::type* v, const typena
 // case after ReLU) takes its maxima on the raw 16-bit patterns, two per instruction (for such values,
 // and the -inf fill, signed-integer order is the float order); any other tile takes them in fp32.
 // The tile's sign is read from the inputs' sign bits (LRN keeps the sign; -0 counts as negative).
-template <typename T, int C, int CPT, int TPH, int TPW, int WPE>
+template <typename T, int C, int CPT, int TPH, int TPW, int WPE, bool MULTI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void lrn_pool_pixel_kernel(
                                                              const T* __restrict__ in,
-                                                             T* __restrict__ out, int H, int W,
-                                                             int Ho, int Wo, int tiles_x,
-                                                             int tiles_y, int64_t in_stride,
-                                                             int64_t out_stride, float alpha_n,
-                                                             float beta, float k) {
+                                                             T* __restrict__ out, KRuns runs,
+                                                             float alpha_n, float beta, float k) {
   constexpr int N = Vec<T>::N;
   constexpr int NV = CPT / N, TPP = C / CPT, G = C / N, CS = C + N;
   constexpr int IW = 2 * TPW + 1, NP = (2 * TPH + 1) * IW;
@@ -259,6 +261,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
   __shared__ __align__(16) T s[NP * CS];
 
   int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of<MULTI>(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, Ho = rn.Ho, Wo = rn.Wo, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
   const int tx = bid % tiles_x;
   bid /= tiles_x;
   const int ty = bid % tiles_y;
@@ -362,8 +370,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 // >= +0, else in fp32, as in the tile kernel.
 template <typename T, int C, int CPT, int TPW, int SR, int WPE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE))) void lrn_pool_strip_kernel(
-    const T* __restrict__ in, T* __restrict__ out, int H, int W, int Ho, int Wo, int strips_x,
-    int strips_y, int64_t in_stride, int64_t out_stride, float alpha_n, float beta, float k) {
+    const T* __restrict__ in, T* __restrict__ out, KRuns runs, float alpha_n, float beta, float k) {
   constexpr int N = Vec<T>::N;
   constexpr int NV = CPT / N, TPP = C / CPT, G = C / N, CS = C + N;
   constexpr int IW = 2 * TPW + 1, NSLOT = 5;
@@ -376,6 +383,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
   __shared__ __align__(16) T s[NSLOT * IW * CS];
 
   int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, Ho = rn.Ho, Wo = rn.Wo, strips_x = rn.tiles_x, strips_y = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
   const int sx = bid % strips_x;
   bid /= strips_x;
   const int sy = bid % strips_y;
@@ -487,18 +500,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 // Pool first, then LRN of the pooled vector: one thread per output element.
 template <typename T>
 __global__ __launch_bounds__(256) void pool_lrn_kernel(const T* __restrict__ in, T* __restrict__ out,
-                                                       int H, int W, int C, int Ho, int Wo,
-                                                       int64_t in_stride, int64_t out_stride,
-                                                       int64_t total, float alpha_n, float beta,
+                                                       KRuns runs, int C, float alpha_n, float beta,
                                                        float k, int half_n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= total) return;
-  const int c = (int)(i % C);
-  int64_t r = i / C;
-  const int ox = (int)(r % Wo);
-  r /= Wo;
-  const int oy = (int)(r % Ho);
-  const int plane = (int)(r / Ho);
+  // run r: tiles_x workgroups of 256 output elements per plane
+  int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int H = rn.H, W = rn.W, Ho = rn.Ho, Wo = rn.Wo, tiles_x = rn.tiles_x, tiles_y_unused = rn.tiles_y;
+  const int64_t in_stride = rn.in_stride, out_stride = rn.out_stride;
+  in += rn.in_off;
+  out += rn.out_off;
+  (void)tiles_y_unused;
+  const int plane = bid / tiles_x, i = (bid % tiles_x) * 256 + (int)threadIdx.x;
+  if (i >= Ho * Wo * C) return;
+  const int c = i % C, ox = (i / C) % Wo, oy = i / C / Wo;
   const T* src = in + plane * in_stride;
   const int y0 = 2 * oy, y1 = min(y0 + 3, H), x0 = 2 * ox, x1 = min(x0 + 3, W);
   const int clo = max(0, c - half_n), chi = min(C - 1, c + half_n);
@@ -530,22 +545,44 @@ void pick_tile(int C, int& TPH, int& TPW) {
   TPH = TPW = 0;
 }
 
+// The per-pixel kernel over the runs of kr: the single-run variant when there is one.
+template <typename T, int C, int CPT, int TPH, int TPW, int WPE>
+void pixel(int64_t blocks, hipStream_t s, const T* in, T* out, const KRuns& kr, float an, float beta,
+           float k) {
+  if (kr.count == 1)
+    lrn_pool_pixel_kernel<T, C, CPT, TPH, TPW, WPE, false><<<(unsigned)blocks, 256, 0, s>>>(in, out, kr, an,
+                                                                                          beta, k);
+  else
+    lrn_pool_pixel_kernel<T, C, CPT, TPH, TPW, WPE, true><<<(unsigned)blocks, 256, 0, s>>>(in, out, kr, an,
+                                                                                         beta, k);
+}
+
 template <typename T>
-int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in_stride, bool lrn,
-        bool lrn_first, float alpha, float beta, float k, int32_t lrn_n, void* d_out,
-        int64_t out_stride, hipStream_t s) {
-  const int Ho = H >= 2 ? (H - 2) / 2 + 1 : 0, Wo = W >= 2 ? (W - 2) / 2 + 1 : 0;
-  if (n <= 0 || Ho <= 0 || Wo <= 0) return (int)hipErrorInvalidValue;
+int run(const void* d_in, const MapRun* runs, int n_runs, int32_t C, bool lrn, bool lrn_first,
+        float alpha, float beta, float k, int32_t lrn_n, void* d_out, hipStream_t s) {
+  for (int i = 0; i < n_runs; ++i)
+    if (runs[i].n <= 0 || runs[i].H < 2 || runs[i].W < 2) return (int)hipErrorInvalidValue;
   const float an = alpha / (float)lrn_n;
   const int hn = lrn_n / 2;
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
+  KRuns kr;
+  // Per run: the pooled size and tiles of TPH x TPW output pixels.
+  auto tiles = [&](int TPH, int TPW) {
+    return fill_kruns(runs, n_runs, kr, [=](KRun& q) {
+      q.Ho = (q.H - 2) / 2 + 1, q.Wo = (q.W - 2) / 2 + 1;
+      q.tiles_x = (q.Wo + TPW - 1) / TPW, q.tiles_y = (q.Ho + TPH - 1) / TPH;
+      return (int64_t)q.tiles_x * q.tiles_y;
+    });
+  };
   if (lrn && !lrn_first) {
-    const int64_t total = (int64_t)n * Ho * Wo * C;
-    const int64_t blocks = (total + 255) / 256;
-    if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
-    pool_lrn_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, H, W, C, Ho, Wo, in_stride,
-                                                       out_stride, total, an, beta, k, hn);
+    const int64_t blocks = fill_kruns(runs, n_runs, kr, [=](KRun& q) {
+      q.Ho = (q.H - 2) / 2 + 1, q.Wo = (q.W - 2) / 2 + 1;
+      q.tiles_x = (int)(((int64_t)q.Ho * q.Wo * C + 255) / 256), q.tiles_y = 1;
+      return (int64_t)q.tiles_x;
+    });
+    if (blocks <= 0) return (int)hipErrorInvalidValue;
+    pool_lrn_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, kr, C, an, beta, k, hn);
     return (int)hipGetLastError();
   }
   constexpr int N = Vec<T>::N;
@@ -557,20 +594,17 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
     if (lrn && hn == 2 && C == 256) {
       const int cfg[4] = {DN_STRIP256};
       const int TPW = cfg[1], SR = cfg[2];
-      const int strips_x = (Wo + TPW - 1) / TPW, strips_y = (Ho + SR - 1) / SR;
-      const int64_t blocks = (int64_t)strips_x * strips_y * n;
-      if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+      const int64_t blocks = tiles(SR, TPW);  // strips of SR rows x TPW columns
+      if (blocks <= 0) return (int)hipErrorInvalidValue;
       // Launches of fewer strips than two rounds of the chip's resident slots (one image's planes:
       // about 660) take the tile kernel's 2850 shorter workgroups instead (29 against 31-37 us).
       if (blocks < 2LL * 4 * device_cus()) {
-        const int tiles_x = (Wo + 3) / 4, tiles_y = (Ho + 2) / 3;
-        const int64_t tb = (int64_t)tiles_x * tiles_y * n;
-        lrn_pool_pixel_kernel<T, 256, 64, 3, 4, 4><<<(unsigned)tb, 256, 0, s>>>(
-            in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+        const int64_t tb = tiles(3, 4);
+        if (tb <= 0) return (int)hipErrorInvalidValue;
+        pixel<T, 256, 64, 3, 4, 4>(tb, s, in, out, kr, an, beta, k);
         return (int)hipGetLastError();
       }
-      lrn_pool_strip_kernel<T, 256, DN_STRIP256><<<(unsigned)blocks, 256, 0, s>>>(
-          in, out, H, W, Ho, Wo, strips_x, strips_y, in_stride, out_stride, an, beta, k);
+      lrn_pool_strip_kernel<T, 256, DN_STRIP256><<<(unsigned)blocks, 256, 0, s>>>(in, out, kr, an, beta, k);
       return (int)hipGetLastError();
     }
   }
@@ -578,19 +612,15 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
     // (16-bit storage reaches this only for C = 96: C = 256 takes the strip kernel above)
     constexpr bool F32 = sizeof(T) == 4;
     constexpr int TH96 = F32 ? 4 : DN_LRN96_TH, TW96 = F32 ? 7 : DN_LRN96_TW, TH256 = 2, TW256 = 5;
-    const int TPH = C == 96 ? TH96 : TH256, TPW = C == 96 ? TW96 : TW256;
-    const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
-    const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
-    if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+    const int64_t blocks = C == 96 ? tiles(TH96, TW96) : tiles(TH256, TW256);
+    if (blocks <= 0) return (int)hipErrorInvalidValue;
     // Waves per SIMD the LDS tile allows (3 and 2 workgroups of 4 waves per CU): the compiler may use
     // the registers that occupancy leaves free for more independent work in flight.
     if (C == 96) {
-      lrn_pool_pixel_kernel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE>
-          <<<(unsigned)blocks, 256, 0, s>>>(
-          in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+      pixel<T, 96, F32 ? 96 : DN_LRN96_CPT, TH96, TW96, F32 ? 3 : DN_LRN96_WPE>(blocks, s, in, out, kr, an,
+                                                                               beta, k);
     } else if constexpr (F32) {
-      lrn_pool_pixel_kernel<T, 256, 128, TH256, TW256, 2><<<(unsigned)blocks, 256, 0, s>>>(
-          in, out, H, W, Ho, Wo, tiles_x, tiles_y, in_stride, out_stride, an, beta, k);
+      pixel<T, 256, 128, TH256, TW256, 2>(blocks, s, in, out, kr, an, beta, k);
     } else {
       return (int)hipErrorInvalidValue;
     }
@@ -599,11 +629,10 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
   int TPH, TPW;
   pick_tile<T>(C, TPH, TPW);
   if (!TPH) return (int)hipErrorInvalidValue;
-  const int tiles_x = (Wo + TPW - 1) / TPW, tiles_y = (Ho + TPH - 1) / TPH;
-  const int64_t blocks = (int64_t)tiles_x * tiles_y * n;
-  if (blocks > 0x7fffffff) return (int)hipErrorInvalidValue;
+  const int64_t blocks = tiles(TPH, TPW);
+  if (blocks <= 0) return (int)hipErrorInvalidValue;
   const size_t lds = (size_t)(2 * TPH + 1) * (2 * TPW + 1) * (C + N) * sizeof(T);
-#define DN_TILE_ARGS in, out, H, W, C, Ho, Wo, TPH, TPW, tiles_x, tiles_y, in_stride, out_stride, an, beta, k
+#define DN_TILE_ARGS in, out, kr, C, TPH, TPW, an, beta, k
   if (!lrn) {
     lrn_pool_tile_kernel<T, false, 0><<<(unsigned)blocks, 256, lds, s>>>(DN_TILE_ARGS);
   } else {
@@ -622,22 +651,28 @@ int run(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in
 
 }  // namespace
 
-int launch_lrn_pool(const void* d_in, int32_t n, int32_t H, int32_t W, int32_t C, int64_t in_stride,
-                    dn_dtype dt, bool lrn, bool lrn_first, float alpha, float beta, float k,
-                    int32_t lrn_n, void* d_out, int64_t out_stride, void* stream) {
+int launch_lrn_pool(const void* d_in, const MapRun* runs, int32_t n_runs, int32_t C, dn_dtype dt,
+                    bool lrn, bool lrn_first, float alpha, float beta, float k, int32_t lrn_n,
+                    void* d_out, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  switch (dt) {
-    case DN_F32:
-      return run<float>(d_in, n, H, W, C, in_stride, lrn, lrn_first, alpha, beta, k, lrn_n, d_out,
-                        out_stride, s);
-    case DN_F16:
-      return run<_Float16>(d_in, n, H, W, C, in_stride, lrn, lrn_first, alpha, beta, k, lrn_n, d_out,
-                           out_stride, s);
-    case DN_BF16:
-      return run<__bf16>(d_in, n, H, W, C, in_stride, lrn, lrn_first, alpha, beta, k, lrn_n, d_out,
-                         out_stride, s);
+  if (n_runs <= 0) return (int)hipErrorInvalidValue;
+  for (int i0 = 0; i0 < n_runs; i0 += MAX_RUNS) {  // one launch per MAX_RUNS runs
+    const int nr = std::min(MAX_RUNS, n_runs - i0);
+    int st = (int)hipErrorInvalidValue;
+    switch (dt) {
+      case DN_F32:
+        st = run<float>(d_in, runs + i0, nr, C, lrn, lrn_first, alpha, beta, k, lrn_n, d_out, s);
+        break;
+      case DN_F16:
+        st = run<_Float16>(d_in, runs + i0, nr, C, lrn, lrn_first, alpha, beta, k, lrn_n, d_out, s);
+        break;
+      case DN_BF16:
+        st = run<__bf16>(d_in, runs + i0, nr, C, lrn, lrn_first, alpha, beta, k, lrn_n, d_out, s);
+        break;
+    }
+    if (st) return st;
   }
-  return (int)hipErrorInvalidValue;
+  return 0;
 }
 
 }  // namespace dn

@@ -1,0 +1,67 @@
+"""GPU: one launch per layer over planes of several sizes (Sec. 3.1 per-scale planes, several images).
+The planes of three images' 8-scale pyramids, image-major, form 24 runs of one plane each, so every
+layer takes two launches of a run table (16 + 8 runs); each plane's conv5 and pool5 maps must equal,
+bit for bit, the maps of that plane run through the stack on its own.  All storage types and both LRN
+orders; the workspace the call asks for is checked against the sum of the runs' layer maps."""
+import numpy as np
+import pytest
+
+from paper_1404_1869_amd import configs as C
+from paper_1404_1869_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DTS = {"f32": 0, "f16": 1, "bf16": 2}
+W7 = synth.weights(7)
+
+
+@pytest.fixture(scope="module")
+def D():
+    from paper_1404_1869_amd import densenet
+    assert torch.cuda.is_available()
+    densenet.lib()
+    return densenet
+
+
+_packed = {}
+
+
+def packed(D, dt):
+    if dt not in _packed:
+        ws = [(torch.from_numpy(w).cuda(), torch.from_numpy(b).cuda()) for w, b in W7]
+        _packed[dt] = D.densenet_pack_weights(ws, DTS[dt])
+    return _packed[dt]
+
+
+def pyramid(D, dt, n_img, H, W):
+    """n_img images, 8 scales at 2^-0.25 from longest side 512, each scale its own plane."""
+    w = C.Workload("runs", H, W, tuple(300 + i for i in range(n_img)), 8, 4, base_longest_side=512,
+                   pad=16, pad_mode=0)
+    imgs = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).cuda()
+    planes, plan = D.densenet_build_pyramid(imgs, D.params_for(w), DTS[dt])
+    return planes, plan.image_descs(n_img)
+
+
+@pytest.mark.parametrize("dt,lrn_first", [("f32", True), ("f16", True), ("bf16", True), ("f16", False)])
+def test_mixed_sizes_one_launch_per_layer(D, dt, lrn_first):
+    planes, descs = pyramid(D, dt, 3, 240, 320)
+    assert len(descs) == 24 and len({(d.h, d.w) for d in descs}) == 8
+    net = D.net_params(pool5=True, lrn_before_pool=lrn_first)
+    cf = D.ConvFeatures(descs, DTS[dt], net, device="cuda")
+    cf(planes, packed(D, dt))
+    torch.cuda.synchronize()
+    # workspace: two ping-pong buffers each holding a layer's maps of all runs back to back
+    es = 4 if dt == "f32" else 2
+    hw = [D.layer_sizes(d.h, d.w) for d in descs]
+    a = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 0), (256, 2), (384, 4)))
+    b = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 1), (256, 3), (384, 5)))
+    assert cf.workspace.numel() == (a * es + 255) // 256 * 256 + b * es
+    c5, p5 = cf.conv5_maps(), cf.pool5_maps()
+    for i, d in enumerate(descs):
+        one = D.ConvFeatures([d], DTS[dt], net, device="cuda")
+        one(planes, packed(D, dt))
+        torch.cuda.synchronize()
+        assert torch.equal(one.conv5_maps()[0], c5[i]), f"plane {i} ({d.h}x{d.w}) conv5"
+        assert torch.equal(one.pool5_maps()[0], p5[i]), f"plane {i} ({d.h}x{d.w}) pool5"
+        assert torch.isfinite(c5[i].float()).all() and c5[i].float().abs().max() > 0
