@@ -142,6 +142,21 @@ struct KRuns {
   KRun r[MAX_RUNS];
 };
 #if defined(__HIPCC__)
+// Buffer resource for `bytes` bytes from p (raw buffer, 32-bit offsets; an offset at or past `bytes`
+// reads 0 and drops a store).  p and bytes must be wave-uniform: they are taken from the first active
+// lane, so the descriptor stays in scalar registers.  Built from values the compiler cannot prove
+// uniform, a descriptor lands in vector registers and every buffer instruction that uses it is
+// wrapped in a loop over the distinct descriptors of the wave (one pass when they agree).
+__device__ inline __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  // The builtin returns a signed int: each word goes back through uint32_t, so the low word is
+  // zero-extended (sign-extending it would corrupt the high word of an address with bit 31 set).
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(lo | hi << 32), 0,
+                                           __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000);
+}
+
 // Run of workgroup (or tile) index b: the last run whose first index is at most b.  The table sits in
 // the kernel arguments; a wave-uniform index reads its fields with scalar loads.  MULTI = false: a
 // launch of one run, whose fields then sit at fixed offsets like plain scalar arguments (no loads

@@ -771,10 +771,9 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void con
   // msub channels into it.
   const int mbp = g * (Mg / BMP) + m0 / BMP, msub = m0 % BMP;
   const T* wg = wp + (int64_t)mbp * (Cg / Cf::CC) * R * (WSLOTS_P * 8);
-  const __amdgpu_buffer_rsrc_t rsrc_in = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)src, 0, (int)(((int64_t)H * W * C - g * Cg) * sizeof(T)), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)wg, 0, (int)((int64_t)(Cg / Cf::CC) * R * WSLOTS_P * 16), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_in =
+      uniform_rsrc(src, (uint32_t)(((int64_t)H * W * C - g * Cg) * sizeof(T)));
+  const __amdgpu_buffer_rsrc_t rsrc_w = uniform_rsrc(wg, (uint32_t)((Cg / Cf::CC) * R * WSLOTS_P * 16));
   constexpr uint32_t OOB = 0x80000000u;
 
   const int tid = threadIdx.x;
@@ -821,11 +820,13 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS, TN_>()), OCC) void con
   // stage's offsets in the scalar offset; the wave skips pieces past the block.
   static_assert(WSLOTS % 64 == 0, "a stage's weights are whole 1 KB pieces");
   const uint32_t lane16 = (uint32_t)lane * 16u;
+  // (the wave index as a scalar: the piece offsets go in the scalar offset operand)
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   auto load_w = [&](int buf, int c0, int ky) {  // stage (chunk c0 / 16, kernel row ky)
     const uint32_t add = (uint32_t)(((c0 / Cf::CC) * R + ky) * WSLOTS_P * 16);
 #pragma unroll
     for (int i = 0; i < DW; ++i) {
-      const int p = wave * DW + i;  // piece p: kernel column p / (BM / 32), channels 32 (p % (BM / 32))
+      const int p = wave_s * DW + i;  // piece p: kernel column p / (BM / 32), channels 32 (p % (BM / 32))
       const uint32_t src = BMP == BM ? (uint32_t)p * 1024u
                                      : (uint32_t)(((p / (BM / 32)) * BMP + msub + 32 * (p % (BM / 32))) * 32);
       if (p * 64 < WSLOTS) lds_direct16(rsrc_w, wrow_buf(buf) + p * 512, lane16, add + src);
@@ -1068,7 +1069,7 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
   float* s_bias = (float*)(s_mem + P::BIAS_OFF);
   if (threadIdx.x < 96) s_bias[threadIdx.x] = bias[threadIdx.x];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, l32 = lane & 31;
   constexpr uint32_t OOB = 0x80000000u;
 
@@ -1083,8 +1084,7 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
 
   // All weights, once: piece q of the k-step blob lands in LDS piece q.
   {
-    const __amdgpu_buffer_rsrc_t rsrc_w = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)wp, 0, (int)(C1_KSTEPS * P::KSE * sizeof(T)), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc_w = uniform_rsrc(wp, (uint32_t)(C1_KSTEPS * P::KSE * sizeof(T)));
 #pragma unroll
     for (int i = 0; i < P::DWL; ++i) {
       const int q = wave + NWV * i;
@@ -1105,8 +1105,7 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
     const int H = rn.H, W = rn.W, pitch = rn.pitch, tl = t - rn.first;
     const int tx = tl % rn.tiles_x, rr = tl / rn.tiles_x, ty = rr % rn.tiles_y, plane = rr / rn.tiles_y;
     chan_bytes = (uint32_t)((int64_t)H * pitch * sizeof(T));
-    rsrc_in = __builtin_amdgcn_make_buffer_rsrc((void*)(in + rn.in_off + plane * rn.in_stride), 0,
-                                                (int)(3 * chan_bytes), 0x00020000);
+    rsrc_in = uniform_rsrc(in + rn.in_off + plane * rn.in_stride, 3 * chan_bytes);
     const int iy0 = 4 * P::TH * ty, ix0 = 4 * P::TW * tx;
     const bool zero_col_w = W % 8 != 0 && pitch > W;
     zcol = __builtin_amdgcn_readfirstlane(zero_col_w && W >= ix0 && W < ix0 + 72 ? W - ix0 : -1);
@@ -1235,9 +1234,8 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
       const KRun& rn = runs.r[run_of<MULTI>(runs, t)];
       const int Ho = rn.Ho, Wo = rn.Wo, tl = t - rn.first;
       const int tx = tl % rn.tiles_x, rr = tl / rn.tiles_x, ty = rr % rn.tiles_y, plane = rr / rn.tiles_y;
-      const __amdgpu_buffer_rsrc_t rsrc_out = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)(out + rn.out_off + plane * rn.out_stride), 0, (int)((int64_t)Ho * Wo * 96 * sizeof(T)),
-          0x00020000);
+      const __amdgpu_buffer_rsrc_t rsrc_out =
+          uniform_rsrc(out + rn.out_off + plane * rn.out_stride, (uint32_t)((int64_t)Ho * Wo * 96 * sizeof(T)));
 #pragma unroll
       for (int b = 0; b < PT; ++b) {
         out4_t v[3][4];

@@ -344,10 +344,9 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   const uint32_t* P = pix + (BATCH ? 0 : (int64_t)b * a.H * a.W);
   T* o = out + (BATCH ? (int64_t)j * 3 * PH * PP : (int64_t)b * pl.image_elems + pl.p[j].offset);
   const int64_t plane = (int64_t)PH * PP;
-  const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)P, 0, (int)(4u * (uint32_t)(BATCH ? bg.n_img : 1) * (uint32_t)a.H * (uint32_t)a.W), 0x00020000);
-  const __amdgpu_buffer_rsrc_t ro =
-      __builtin_amdgcn_make_buffer_rsrc((void*)o, 0, (int)(3 * plane * (int64_t)sizeof(T)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rp =
+      uniform_rsrc(P, 4u * (uint32_t)(BATCH ? bg.n_img : 1) * (uint32_t)a.H * (uint32_t)a.W);
+  const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(o, (uint32_t)(3 * plane * (int64_t)sizeof(T)));
   const float mean[3] = {a.mean[0], a.mean[1], a.mean[2]};
 
   // A row's taps (4 pixels per lane) and its per-pixel row fraction and weight.
@@ -415,7 +414,9 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     typedef T pair_t __attribute__((ext_vector_type(2)));
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
-      const uint32_t soff = (uint32_t)((c * plane + (int64_t)y * PP) * (int64_t)sizeof(T));
+      // uniform per wave (plane, row and channel are): a scalar offset, not a per-lane one
+      const uint32_t soff =
+          __builtin_amdgcn_readfirstlane((uint32_t)((c * plane + (int64_t)y * PP) * (int64_t)sizeof(T)));
 #pragma unroll
       for (int i = 0; i < PX; i += 2) {
         pair_t pv;
