@@ -303,6 +303,13 @@ template <typename T>
 __device__ inline float to_f32(T x) {
   return (float)x;
 }
+// Two values rounded to T (nearest even) as a packed pair: one v_cvt_pk_bf16_f32 for bf16.
+template <typename T>
+__device__ inline T __attribute__((ext_vector_type(2))) from_f32x2(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef T t2 __attribute__((ext_vector_type(2)));
+  return __builtin_convertvector(f2{a, b}, t2);
+}
 
 }  // namespace dn
 #endif

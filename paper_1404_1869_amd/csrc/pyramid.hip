@@ -62,6 +62,15 @@ __device__ inline float border_weight(int d, int pad, bool ramp) {
 // four waves take the tile's rows in turn (wave w: rows w, w + 4, ...), so at any time they read the
 // same few source rows; a lane computes its columns' taps for the first band and again only where
 // a later band's owner differs.
+// f(integral_constant<I>) for I = B .. E - 1, in order.
+template <int B, int E, typename F>
+__device__ inline void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 constexpr int BAND = 16;                 // rows per band (one row of 16-px cells)
 constexpr int TCELLS = 64 * PX / 16;     // 16-px cells per tile row
 
@@ -355,13 +364,16 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
     float ly[PX], wgt[PX];
   };
   // live[p]: some lane of the wave has a pixel of pair p in a scale's rectangle (wave-uniform); a
-  // pair that is background in every lane of the wave loads nothing and stores zeros.
+  // pair that is background in every lane of the wave loads nothing and stores zeros.  A row is
+  // emitted by a variant compiled for its wave's live pattern (LIVE bit p: pair p), so no value is
+  // merged across live and background paths.
   bool live[PX / 2];
-  auto fetch = [&](int band, int r, RowTaps& t) {
+  auto fetch = [&](auto live_c, int band, int r, RowTaps& t) {
+    constexpr int LIVE = decltype(live_c)::value;
     RowEntry re;
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      if (!live[i / 2]) continue;
+      if (!((LIVE >> (i / 2)) & 1)) continue;
       if (i % 2 == 0) re = s_row[cell_of(band, i) * BAND + r];  // one entry per pair
       t.ly[i] = re.ly;
       t.wgt[i] = re.wy * wx[i];
@@ -380,11 +392,12 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
   //   XDOT: the two rows' taps T0, T1 are exact integers below 2^24 (so exact in fp32); the value is
   //   ((T0 + ly (T1 - T0)) / Dx - mean) * weight, as fma(ly, T1 - T0, T0), fma(., 1 / Dx, -mean)
   //   and a product.  Otherwise the fp32 lerps run on the fraction lx.
-  auto emit = [&](int y, const RowTaps& t) {
+  auto emit = [&](auto live_c, int y, const RowTaps& t) {
+    constexpr int LIVE = decltype(live_c)::value;
     float v[PX][3];
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
-      if (!live[i / 2]) {
+      if (!((LIVE >> (i / 2)) & 1)) {
         v[i][0] = v[i][1] = v[i][2] = 0.f;
         continue;
       }
@@ -419,9 +432,7 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
           __builtin_amdgcn_readfirstlane((uint32_t)((c * plane + (int64_t)y * PP) * (int64_t)sizeof(T)));
 #pragma unroll
       for (int i = 0; i < PX; i += 2) {
-        pair_t pv;
-        pv[0] = from_f32<T>(v[i][c]);
-        pv[1] = from_f32<T>(v[i + 1][c]);
+        const pair_t pv = from_f32x2<T>(v[i][c], v[i + 1][c]);
         // non-temporal (aux 2): conv1 reads the planes only after the whole batch is built
         if constexpr (sizeof(T) == 2)
           __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, pv), ro, soff_lane[i / 2], soff, 2);
@@ -444,17 +455,26 @@ __global__ __launch_bounds__(256) void build_planes_kernel(const uint32_t* __res
         column_taps(i, cell);
       }
     }
+    int lm = 0;  // live pattern of the band (wave-uniform)
 #pragma unroll
-    for (int i = 0; i < PX; i += 2) live[i / 2] = __builtin_amdgcn_ballot_w64(own[i] >= 0 || own[i + 1] >= 0) != 0;
-#pragma unroll
-    for (int k = 0; k < BAND / 4; ++k) {
-      const int r = wave + 4 * k;
-      if (yb + r < PH) {
-        RowTaps t;
-        fetch(band, r, t);
-        emit(yb + r, t);
-      }
+    for (int i = 0; i < PX; i += 2) {
+      live[i / 2] = __builtin_amdgcn_ballot_w64(own[i] >= 0 || own[i + 1] >= 0) != 0;
+      lm |= live[i / 2] ? 1 << (i / 2) : 0;
     }
+    auto rows = [&](auto live_c) {
+#pragma unroll
+      for (int k = 0; k < BAND / 4; ++k) {
+        const int r = wave + 4 * k;
+        if (yb + r < PH) {
+          RowTaps t;
+          fetch(live_c, band, r, t);
+          emit(live_c, yb + r, t);
+        }
+      }
+    };
+    static_for<0, 1 << (PX / 2)>([&](auto c) {
+      if (lm == decltype(c)::value) rows(c);
+    });
   }
 }
 
