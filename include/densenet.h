@@ -217,7 +217,8 @@ int densenet_pack_weights(const float* const* d_w, const float* const* d_b, dn_d
  * runs (more runs take more launches), so planes of different sizes (one plane per scale, several
  * images) share their launches.  d_packed from densenet_pack_weights with the same dtype.
  * d_workspace: scratch of ws_bytes (NULL => size query into *ws_needed): two buffers, each holding
- * one layer's maps of all planes back to back.
+ * one layer's maps of all planes back to back, and for fp32 launches too small to fill the GPU
+ * (whose workgroups then split the input channels) room for their partial sums.
  * d_conv5: out, per plane [Hc][Wc][256] packed back to back (descs in conv5_desc[n_planes]).
  * d_pool5: nullable; when net->pool5 it receives [Hp][Wp][256] per plane (descs in pool5_desc).
  * *conv5_needed / *pool5_needed receive the output sizes in bytes (size query when d_conv5 == NULL). */

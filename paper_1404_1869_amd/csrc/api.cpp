@@ -483,7 +483,8 @@ int densenet_conv_layer(int32_t layer, const void* d_in, int32_t n, int32_t H, i
     static const char* names[5] = {"conv1", "conv2", "conv3", "conv4", "conv5"};
     TraceScope trace(names[layer - 1], stream);
     const MapRun run{n, H, W, W, 0, in_stride, 0, out_stride};
-    return hip_status(launch_conv(layer, d_in, &run, 1, dtype, d_packed, d_out, stream), "conv launch");
+    return hip_status(launch_conv(layer, d_in, &run, 1, dtype, d_packed, d_out, nullptr, 0, stream),
+                      "conv launch");
   } catch (...) {
     return fail(DN_E_INTERNAL, "unexpected exception");
   }
@@ -589,24 +590,6 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
       oa3[i] = a3, a3 += n * 384 * s.h[4] * s.w[4];
       ob4[i] = b4, b4 += n * 384 * s.h[5] * s.w[5];
     }
-    const size_t ws_a = ((size_t)std::max({a1, a2, a3}) * es + 255) & ~(size_t)255;
-    const size_t ws_b = (size_t)std::max({b1, b2, b4}) * es;
-    *ws_needed = ws_a + ws_b;
-    *conv5_needed = (size_t)c5_off * es;
-    if (net->pool5) *pool5_needed = (size_t)p5_off * es;
-    if (!d_conv5) return DN_OK;
-    if (!d_planes || !d_packed) return fail(DN_E_INVALID_ARG, "null device pointer");
-    if (!d_workspace || ws_bytes < *ws_needed)
-      return fail(DN_E_BUFFER_TOO_SMALL, "workspace too small");
-    if (conv5_bytes < *conv5_needed) return fail(DN_E_BUFFER_TOO_SMALL, "conv5 buffer too small");
-    if (net->pool5 && (!d_pool5 || pool5_bytes < *pool5_needed))
-      return fail(DN_E_BUFFER_TOO_SMALL, "pool5 buffer too small");
-
-    char* A = (char*)d_workspace;
-    char* B = A + ws_a;
-    const bool lf = net->lrn_before_pool != 0;
-    const float al = net->lrn_alpha, be = net->lrn_beta, kk = net->lrn_k;
-    const int ln = net->lrn_n;
     // Per layer and run: planes, input size, input/output offsets and strides (elements).
     std::vector<MapRun> c1(nr), l1(nr), c2(nr), l2(nr), c3(nr), c4(nr), c5(nr), q5(nr);
     for (size_t i = 0; i < nr; ++i) {
@@ -633,9 +616,33 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
         q5[i] = MapRun{n, h6, w6, 0, o5, s5, pool5_desc[r.first].offset, 256 * s.h[7] * s.w[7]};
     }
     const int n_runs = (int)nr;
+    // C: partial sums of the fp32 conv launches too small to fill the chip (0 bytes otherwise)
+    const size_t ws_c = std::max({conv_part_bytes(2, c2.data(), n_runs, dtype),
+                                  conv_part_bytes(3, c3.data(), n_runs, dtype),
+                                  conv_part_bytes(4, c4.data(), n_runs, dtype),
+                                  conv_part_bytes(5, c5.data(), n_runs, dtype)});
+    const size_t ws_a = ((size_t)std::max({a1, a2, a3}) * es + 255) & ~(size_t)255;
+    const size_t ws_b = ((size_t)std::max({b1, b2, b4}) * es + 255) & ~(size_t)255;
+    *ws_needed = ws_a + ws_b + ws_c;
+    *conv5_needed = (size_t)c5_off * es;
+    if (net->pool5) *pool5_needed = (size_t)p5_off * es;
+    if (!d_conv5) return DN_OK;
+    if (!d_planes || !d_packed) return fail(DN_E_INVALID_ARG, "null device pointer");
+    if (!d_workspace || ws_bytes < *ws_needed)
+      return fail(DN_E_BUFFER_TOO_SMALL, "workspace too small");
+    if (conv5_bytes < *conv5_needed) return fail(DN_E_BUFFER_TOO_SMALL, "conv5 buffer too small");
+    if (net->pool5 && (!d_pool5 || pool5_bytes < *pool5_needed))
+      return fail(DN_E_BUFFER_TOO_SMALL, "pool5 buffer too small");
+
+    char* A = (char*)d_workspace;
+    char* B = A + ws_a;
+    char* Cp = B + ws_b;
+    const bool lf = net->lrn_before_pool != 0;
+    const float al = net->lrn_alpha, be = net->lrn_beta, kk = net->lrn_k;
+    const int ln = net->lrn_n;
     int st;
     if ((st = run_step("conv1", stream, [&] {
-           return launch_conv(1, d_planes, c1.data(), n_runs, dtype, d_packed, A, stream);
+           return launch_conv(1, d_planes, c1.data(), n_runs, dtype, d_packed, A, Cp, ws_c, stream);
          })))
       return st;
     if ((st = run_step("lrn_pool1", stream, [&] {
@@ -643,7 +650,7 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
          })))
       return st;
     if ((st = run_step("conv2", stream, [&] {
-           return launch_conv(2, B, c2.data(), n_runs, dtype, d_packed, A, stream);
+           return launch_conv(2, B, c2.data(), n_runs, dtype, d_packed, A, Cp, ws_c, stream);
          })))
       return st;
     if ((st = run_step("lrn_pool2", stream, [&] {
@@ -651,15 +658,15 @@ int densenet_conv_features(const void* d_planes, const dn_plane_desc* planes, in
          })))
       return st;
     if ((st = run_step("conv3", stream, [&] {
-           return launch_conv(3, B, c3.data(), n_runs, dtype, d_packed, A, stream);
+           return launch_conv(3, B, c3.data(), n_runs, dtype, d_packed, A, Cp, ws_c, stream);
          })))
       return st;
     if ((st = run_step("conv4", stream, [&] {
-           return launch_conv(4, A, c4.data(), n_runs, dtype, d_packed, B, stream);
+           return launch_conv(4, A, c4.data(), n_runs, dtype, d_packed, B, Cp, ws_c, stream);
          })))
       return st;
     if ((st = run_step("conv5", stream, [&] {
-           return launch_conv(5, B, c5.data(), n_runs, dtype, d_packed, d_conv5, stream);
+           return launch_conv(5, B, c5.data(), n_runs, dtype, d_packed, d_conv5, Cp, ws_c, stream);
          })))
       return st;
     if (net->pool5) {

@@ -196,9 +196,12 @@ inline int64_t fill_kruns(const MapRun* runs, int n, KRuns& t, G&& geometry) {
 }
 
 // One conv layer (1..5) with bias and ReLU over the planes of `runs` (any number of runs; one launch
-// per MAX_RUNS of them).
+// per MAX_RUNS of them).  d_part: conv_part_bytes(...) bytes of device workspace for the partial sums
+// of fp32 launches too small to fill the chip, which then split their input channels (NULL or too
+// small: no split).
 int launch_conv(int layer, const void* d_in, const MapRun* runs, int32_t n_runs, dn_dtype dt,
-                const void* d_packed, void* d_out, void* stream);
+                const void* d_packed, void* d_out, void* d_part, size_t part_bytes, void* stream);
+size_t conv_part_bytes(int layer, const MapRun* runs, int32_t n_runs, dn_dtype dt);
 
 // LRN + pool (order by lrn_first), or plain pool when lrn == false, over the channels-last maps of
 // `runs` (one launch per MAX_RUNS runs).

@@ -465,10 +465,15 @@ constexpr int conv_threads() {
   return 64 * (BM / (32 * TM)) * (std::is_same<T, float>::value ? 256 : (TS / 100) * (TS % 100)) / (32 * TN);
 }
 
+// ksplit > 1 (fp32 launches too small to fill the chip): the launch is ksplit copies of its base
+// workgroups; copy ks runs the input-channel chunks [ks nchunks / ksplit, (ks + 1) nchunks / ksplit)
+// and writes its raw sums (no bias, no ReLU) to part + ks part_slice at the output's element offsets;
+// split_reduce_kernel then adds the copies in order.
 template <typename T, int R, int BM, int TM, int OCC, int TS>
 __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
-    const float* __restrict__ bias, KRuns runs, int C, int Cg, int M, int Mg, int mblocks) {
+    const float* __restrict__ bias, KRuns runs, int C, int Cg, int M, int Mg, int mblocks, int ksplit,
+    int base, float* __restrict__ part, int64_t part_slice) {
   using Cf = ConvCfg<T, R, BM, TM, TS>;
   using Op = Mfma<T>;
   constexpr int pad = (R - 1) / 2;
@@ -485,6 +490,8 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
   // one tile first, then neighbouring tiles) then share that XCD's L2.
   const int nb = gridDim.x, xcd = blockIdx.x % 8, per = nb / 8, rem = nb % 8;
   int bid = xcd * per + min(xcd, rem) + blockIdx.x / 8;
+  const int ks = bid / base;
+  bid -= ks * base;
   const KRun& rn = runs.r[run_of(runs, bid)];
   bid -= rn.first;
   const int H = rn.H, W = rn.W, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
@@ -609,21 +616,48 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
     }
   };
 
-  const int nchunks = Cg / Cf::CC, nst = nchunks * R;
-  load_halo(0);
-  load_w(0, 0);
-  store_halo(0);
-  store_w(0);
+  // this workgroup's chunks [c_lo, c_hi) (all of them without a split): stages c_lo R .. c_hi R - 1
+  const int nchunks = Cg / Cf::CC;
+  const int c_lo = ks * nchunks / ksplit, c_hi = (ks + 1) * nchunks / ksplit;
+  const int st0 = c_lo * R, st1 = c_hi * R;
+  load_halo(c_lo * Cf::CC);
+  load_w(c_lo * Cf::CC, 0);
+  store_halo(c_lo & 1);
+  store_w(st0 & 1);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
+  for (int st = st0; st < st1; ++st) {
     const int chunk = st / R, ky = st - chunk * R;
-    const bool more = st + 1 < nst, next_chunk = chunk + 1 < nchunks;
+    const bool more = st + 1 < st1, next_chunk = chunk + 1 < c_hi;
     if (more) load_w(((st + 1) / R) * Cf::CC, (st + 1) % R);
     if (ky == 0 && next_chunk) load_halo((chunk + 1) * Cf::CC);
     compute(chunk & 1, st & 1, ky);
     if (more) store_w((st + 1) & 1);
     if (ky == R - 1 && next_chunk) store_halo((chunk + 1) & 1);
     __syncthreads();
+  }
+
+  if constexpr (Cf::F32) {
+    if (ksplit > 1) {  // raw partial sums of this split
+      float* pd = part + ks * part_slice + rn.out_off + plane * out_stride;
+#pragma unroll
+      for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int m = g * Mg + m0 + wm * 32 * TM + mt * 32 + 8 * q + 4 * half;
+#pragma unroll
+          for (int t = 0; t < TN; ++t) {
+            const int idx = wn * 32 * TN + t * 32 + l32;
+            const int oy = oy0 + Cf::pix_row(idx), ox = ox0 + Cf::pix_col(idx);
+            if (oy < H && ox < W) {
+              f32x4 r;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) r[e] = acc[mt][t][4 * q + e];
+              *(f32x4*)(pd + ((int64_t)oy * W + ox) * M + m) = r;
+            }
+          }
+        }
+      return;
+    }
   }
 
   // Epilogue: D[m][pixel]; register group q of MFMA tile mt holds channels 32 mt + 8 q + 4 half + 0..3
@@ -683,6 +717,30 @@ __global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_
         }
       }
   }
+}
+
+// Sum of the ksplit partial copies of a split fp32 conv launch, in copy order, plus bias, then ReLU:
+// run r has tiles_x workgroups of 256 four-channel groups per plane (Ho x Wo x M outputs).
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part,
+                                                           int64_t part_slice, int ksplit,
+                                                           const float* __restrict__ bias,
+                                                           float* __restrict__ out, KRuns runs, int M) {
+  int bid = blockIdx.x;
+  const KRun& rn = runs.r[run_of(runs, bid)];
+  bid -= rn.first;
+  const int plane = bid / rn.tiles_x, v = (bid % rn.tiles_x) * 256 + (int)threadIdx.x;
+  if ((int64_t)v * 4 >= (int64_t)rn.Ho * rn.Wo * M) return;
+  const int64_t o = rn.out_off + plane * rn.out_stride + (int64_t)v * 4;
+  f32x4 acc = *(const f32x4*)(part + o);
+  for (int k = 1; k < ksplit; ++k) {
+    const f32x4 p = *(const f32x4*)(part + k * part_slice + o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] += p[e];
+  }
+  const f32x4 b = *(const f32x4*)(bias + (v * 4) % M);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc[e] = fmaxf(acc[e] + b[e], 0.f);
+  *(f32x4*)(out + o) = acc;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -1284,9 +1342,12 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
   }
 }
 
+// part / part_bytes: workspace for the partial sums of a split fp32 launch (may be NULL: no split);
+// part_need non-NULL: only report the bytes this launch would use there (0 without a split).
 template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM, int TN = 4>
 int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* bias, const MapRun* runs,
-                int n_runs, int C, int G, int M, hipStream_t s) {
+                int n_runs, int C, int G, int M, float* part, size_t part_bytes, size_t* part_need,
+                hipStream_t s) {
   using Cf = ConvCfg<T, R, BM, TM, TS, TN>;
   const int Cg = C / G, Mg = M / G;
   if (Mg % BM) return (int)hipErrorInvalidValue;  // whole channel blocks per group
@@ -1299,9 +1360,53 @@ int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* 
   });
   if (blocks <= 0) return (int)hipErrorInvalidValue;
   if constexpr (Cf::F32 || (TM != 2 && TM != 3)) {
-    conv_s1_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)blocks, Cf::NT, 0, s>>>(in, out, wp, bias, kr, C, Cg,
-                                                                           M, Mg, mblocks);
+    // fp32 launches of fewer workgroups than CUs may split their input channels over ks <= nchunks
+    // copies: a lone workgroup's whole K loop would otherwise set the launch's time.  ks minimises
+    // rounds(ks) / ks + 0.15 [ks > 1] + 0.02 ks blocks / CUs, rounds(ks) = ceil(ks blocks / CUs) (one
+    // fp32 workgroup per CU at a time): the launch's rounds of shorter workgroups, plus the reduction
+    // and the partial sums' traffic, which grows with the copies and the launch's output (fitted to
+    // timed launches of the 227 x 227 and the 8-scale 480 x 640 pyramids).
+    int ks = 1;
+    int64_t span = 0;  // elements of one partial copy: the launch's output extent
+    if constexpr (Cf::F32) {
+      const int64_t cus = device_cu_count();
+      if (blocks < cus) {
+        double best = 1.0;
+        for (int k = 2; k <= Cg / Cf::CC; ++k) {
+          const double cost =
+              (double)((k * blocks + cus - 1) / cus) / k + 0.15 + 0.02 * k * (double)blocks / cus;
+          if (cost < best) best = cost, ks = k;
+        }
+      }
+      for (int i = 0; i < n_runs; ++i)
+        span = std::max(span, runs[i].out_off + runs[i].n * runs[i].out_stride);
+      span = (span + 63) / 64 * 64;
+    }
+    const size_t need = ks > 1 ? (size_t)ks * (size_t)span * sizeof(float) : 0;
+    if (part_need) {
+      *part_need = need;
+      return 0;
+    }
+    if (ks > 1 && (!part || part_bytes < need)) ks = 1;
+    conv_s1_kernel<T, R, BM, TM, OCC, TS><<<(unsigned)(blocks * ks), Cf::NT, 0, s>>>(
+        in, out, wp, bias, kr, C, Cg, M, Mg, mblocks, ks, (int)blocks, part, span);
+    if constexpr (Cf::F32) {
+      if (ks > 1) {
+        KRuns rr;
+        const int64_t rb = fill_kruns(runs, n_runs, rr, [&](KRun& k) {
+          k.Ho = k.H, k.Wo = k.W;
+          k.tiles_x = (int)(((int64_t)k.H * k.W * M / 4 + 255) / 256), k.tiles_y = 1;
+          return (int64_t)k.tiles_x;
+        });
+        if (rb <= 0) return (int)hipErrorInvalidValue;
+        split_reduce_kernel<<<(unsigned)rb, 256, 0, s>>>(part, span, ks, bias, out, rr, M);
+      }
+    }
   } else {
+    if (part_need) {
+      *part_need = 0;
+      return 0;
+    }
     // buffer descriptors address one plane with 32-bit byte offsets
     for (int i = 0; i < n_runs; ++i)
       if ((int64_t)runs[i].H * runs[i].W * C * (int64_t)sizeof(T) >= 0x7fffffffLL)
@@ -1368,7 +1473,8 @@ bool small_launch(const MapRun* runs, int n_runs, int M) {
 
 template <typename T>
 int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, const void* d_packed,
-                  void* d_out, const PackedLayout& L, hipStream_t s) {
+                  void* d_out, float* part, size_t part_bytes, size_t* part_need, const PackedLayout& L,
+                  hipStream_t s) {
   const T* in = (const T*)d_in;
   T* out = (T*)d_out;
   const T* wp = (const T*)((const char*)d_packed + L.w_off[layer - 1]);
@@ -1376,6 +1482,10 @@ int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, c
   const T* ws = L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
   const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
   if (layer == 1) {
+    if (part_need) {  // conv1 does not split
+      *part_need = 0;
+      return 0;
+    }
     KRuns kr;
     auto tiles16 = [](KRun& k) {  // tiles of 16 x 16 output pixels
       k.Ho = (k.H - 11) / 4 + 1, k.Wo = (k.W - 11) / 4 + 1;
@@ -1425,7 +1535,7 @@ int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, c
   }
   const int li = layer - 1;
   constexpr bool F32 = std::is_same<T, float>::value;
-#define DN_RUN_ARGS in, out, wp, ws, bias, runs, n_runs, L_C[li], L_G[li], L_M[li], s
+#define DN_RUN_ARGS in, out, wp, ws, bias, runs, n_runs, L_C[li], L_G[li], L_M[li], part, part_bytes, part_need, s
 #define DN_SMALL_CFG(l) 3, 64, 2, DN_SMALL_OCC, 1616, L_BM[l], DN_SMALL_TN
   switch (layer) {
     case 2:
@@ -1520,22 +1630,50 @@ int launch_pack_weights(const float* const* d_w, const float* const* d_b, dn_dty
   return (int)hipGetLastError();
 }
 
-int launch_conv(int layer, const void* d_in, const MapRun* runs, int32_t n_runs, dn_dtype dt,
-                const void* d_packed, void* d_out, void* stream) {
+// One launch per MAX_RUNS runs (the partial-sum workspace is reused by each in turn), or with
+// part_need: the largest workspace any of them would use.
+static int conv_part_bytes_or_launch(int layer, const void* d_in, const MapRun* runs, int32_t n_runs,
+                                     dn_dtype dt, const void* d_packed, void* d_out, void* d_part,
+                                     size_t part_bytes, size_t* part_need, void* stream) {
   const PackedLayout L = packed_layout(dt);
   hipStream_t s = (hipStream_t)stream;
   if (layer < 1 || layer > 5 || n_runs <= 0) return (int)hipErrorInvalidValue;
-  for (int i0 = 0; i0 < n_runs; i0 += MAX_RUNS) {  // one launch per MAX_RUNS runs
+  if (part_need) *part_need = 0;
+  float* part = (float*)d_part;
+  for (int i0 = 0; i0 < n_runs; i0 += MAX_RUNS) {
     const int nr = std::min(MAX_RUNS, n_runs - i0);
+    size_t need = 0;
+    size_t* q = part_need ? &need : nullptr;
     int st = (int)hipErrorInvalidValue;
     switch (dt) {
-      case DN_F32: st = conv_dispatch<float>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
-      case DN_F16: st = conv_dispatch<_Float16>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
-      case DN_BF16: st = conv_dispatch<__bf16>(layer, d_in, runs + i0, nr, d_packed, d_out, L, s); break;
+      case DN_F32:
+        st = conv_dispatch<float>(layer, d_in, runs + i0, nr, d_packed, d_out, part, part_bytes, q, L, s);
+        break;
+      case DN_F16:
+        st = conv_dispatch<_Float16>(layer, d_in, runs + i0, nr, d_packed, d_out, part, part_bytes, q, L, s);
+        break;
+      case DN_BF16:
+        st = conv_dispatch<__bf16>(layer, d_in, runs + i0, nr, d_packed, d_out, part, part_bytes, q, L, s);
+        break;
     }
     if (st) return st;
+    if (part_need) *part_need = std::max(*part_need, need);
   }
   return 0;
+}
+
+int launch_conv(int layer, const void* d_in, const MapRun* runs, int32_t n_runs, dn_dtype dt,
+                const void* d_packed, void* d_out, void* d_part, size_t part_bytes, void* stream) {
+  return conv_part_bytes_or_launch(layer, d_in, runs, n_runs, dt, d_packed, d_out, d_part, part_bytes,
+                                   nullptr, stream);
+}
+
+size_t conv_part_bytes(int layer, const MapRun* runs, int32_t n_runs, dn_dtype dt) {
+  size_t need = 0;
+  if (conv_part_bytes_or_launch(layer, nullptr, runs, n_runs, dt, nullptr, nullptr, nullptr, 0, &need,
+                                nullptr))
+    return 0;
+  return need;
 }
 
 }  // namespace dn

@@ -1,8 +1,10 @@
 """GPU: one launch per layer over planes of several sizes (Sec. 3.1 per-scale planes, several images).
 The planes of three images' 8-scale pyramids, image-major, form 24 runs of one plane each, so every
 layer takes two launches of a run table (16 + 8 runs); each plane's conv5 and pool5 maps must equal,
-bit for bit, the maps of that plane run through the stack on its own.  All storage types and both LRN
-orders; the workspace the call asks for is checked against the sum of the runs' layer maps."""
+bit for bit (fp32: to 1e-5, as fp32 launches too small to fill the GPU split their sums, in an order
+that depends on the launch), the maps of that plane run through the stack on its own.  All storage
+types and both LRN orders; the workspace the call asks for is checked against the sum of the runs'
+layer maps."""
 import numpy as np
 import pytest
 
@@ -51,17 +53,29 @@ def test_mixed_sizes_one_launch_per_layer(D, dt, lrn_first):
     cf = D.ConvFeatures(descs, DTS[dt], net, device="cuda")
     cf(planes, packed(D, dt))
     torch.cuda.synchronize()
-    # workspace: two ping-pong buffers each holding a layer's maps of all runs back to back
+    # workspace: two ping-pong buffers each holding a layer's maps of all runs back to back (fp32:
+    # plus the partial sums of launches that split their input channels)
     es = 4 if dt == "f32" else 2
     hw = [D.layer_sizes(d.h, d.w) for d in descs]
     a = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 0), (256, 2), (384, 4)))
     b = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 1), (256, 3), (384, 5)))
-    assert cf.workspace.numel() == (a * es + 255) // 256 * 256 + b * es
+    ab = (a * es + 255) // 256 * 256 + (b * es + 255) // 256 * 256
+    if dt == "f32":
+        assert cf.workspace.numel() >= ab
+    else:
+        assert cf.workspace.numel() == ab
     c5, p5 = cf.conv5_maps(), cf.pool5_maps()
     for i, d in enumerate(descs):
         one = D.ConvFeatures([d], DTS[dt], net, device="cuda")
         one(planes, packed(D, dt))
         torch.cuda.synchronize()
-        assert torch.equal(one.conv5_maps()[0], c5[i]), f"plane {i} ({d.h}x{d.w}) conv5"
-        assert torch.equal(one.pool5_maps()[0], p5[i]), f"plane {i} ({d.h}x{d.w}) pool5"
+        if dt == "f32":
+            # fp32 launches too small to fill the GPU split their input channels, and how many
+            # splits a plane gets depends on the launch it is in: sums in another order
+            for g, r, what in ((one.conv5_maps()[0], c5[i], "conv5"), (one.pool5_maps()[0], p5[i], "pool5")):
+                assert torch.allclose(g, r, rtol=1e-5, atol=1e-5 * float(r.abs().max())), \
+                    f"plane {i} ({d.h}x{d.w}) {what}"
+        else:
+            assert torch.equal(one.conv5_maps()[0], c5[i]), f"plane {i} ({d.h}x{d.w}) conv5"
+            assert torch.equal(one.pool5_maps()[0], p5[i]), f"plane {i} ({d.h}x{d.w}) pool5"
         assert torch.isfinite(c5[i].float()).all() and c5[i].float().abs().max() > 0
