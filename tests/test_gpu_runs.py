@@ -79,3 +79,36 @@ def test_mixed_sizes_one_launch_per_layer(D, dt, lrn_first):
             assert torch.equal(one.conv5_maps()[0], c5[i]), f"plane {i} ({d.h}x{d.w}) conv5"
             assert torch.equal(one.pool5_maps()[0], p5[i]), f"plane {i} ({d.h}x{d.w}) pool5"
         assert torch.isfinite(c5[i].float()).all() and c5[i].float().abs().max() > 0
+
+
+def test_fp32_split_launches_match_layer_by_layer(D):
+    """The 227 x 227 pyramid in fp32 (Sec. 3.1, one plane per scale): densenet_conv_features splits
+    its small conv2-5 launches over input-channel copies (the workspace holds their partial sums);
+    the same planes through densenet_conv_layer / densenet_lrn_pool / densenet_maxpool, which never
+    split, must agree to 1e-5."""
+    w = C.ALEXNET_227
+    f32 = DTS["f32"]
+    img = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).cuda()
+    planes, plan = D.densenet_build_pyramid(img, D.params_for(w), f32)
+    net = D.net_params(pool5=True)
+    pk = packed(D, "f32")
+    for d in plan.planes:
+        cf = D.ConvFeatures([d], f32, net, device="cuda")
+        hw = D.layer_sizes(d.h, d.w)
+        ab = sum((max(c * hw[i][0] * hw[i][1] for c, i in pairs) * 4 + 255) // 256 * 256
+                 for pairs in (((96, 0), (256, 2), (384, 4)), ((96, 1), (256, 3), (384, 5))))
+        assert cf.workspace.numel() > ab, "the small fp32 launches should take partial-sum space"
+        cf(planes, pk)
+        x = D.plane_view(planes, d).contiguous().unsqueeze(0)
+        a = D.densenet_conv_layer(1, x, 1, d.h, d.w, f32, pk)
+        a = D.densenet_lrn_pool(a, f32, net)
+        for layer in (2, 3, 4, 5):
+            a = D.densenet_conv_layer(layer, a, 1, a.shape[1], a.shape[2], f32, pk)
+            if layer == 2:
+                a = D.densenet_lrn_pool(a, f32, net)
+        p5 = D.densenet_maxpool(a, f32)
+        torch.cuda.synchronize()
+        for got, ref, what in ((cf.conv5_maps()[0], a[0], "conv5"), (cf.pool5_maps()[0], p5[0], "pool5")):
+            assert got.shape == ref.shape
+            assert torch.allclose(got, ref, rtol=1e-5, atol=1e-5 * float(ref.abs().max())), (d.h, what)
+            assert float(ref.abs().max()) > 0
