@@ -142,16 +142,21 @@ struct Conv1Cfg {
   static constexpr int WS = K1 + 1;
 };
 
+// ksplit > 1: as conv_s1_kernel's split, over the three input channels.
 template <typename T>
 __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T* __restrict__ out,
                                                     const T* __restrict__ wp,
-                                                    const float* __restrict__ bias, KRuns runs) {
+                                                    const float* __restrict__ bias, KRuns runs,
+                                                    int ksplit, int base, float* __restrict__ part,
+                                                    int64_t part_slice) {
   using C = Conv1Cfg<T>;
   using Op = Mfma<T>;
   __shared__ T s_in[C::HR * C::HS];
   __shared__ T s_w[96 * C::WS];
 
   int bid = blockIdx.x;
+  const int copy = bid / base;  // split copy: input channels [3 copy / ksplit, 3 (copy + 1) / ksplit)
+  bid -= copy * base;
   const KRun& rn = runs.r[run_of(runs, bid)];
   bid -= rn.first;
   const int H = rn.H, W = rn.W, tiles_x = rn.tiles_x, tiles_y = rn.tiles_y;
@@ -182,7 +187,7 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
 #pragma unroll
     for (int t = 0; t < 2; ++t) acc[a][t] = f32x16{};
 
-  for (int c = 0; c < 3; ++c) {
+  for (int c = copy * 3 / ksplit; c < (copy + 1) * 3 / ksplit; ++c) {
     __syncthreads();
     const T* sc = src + (int64_t)c * H * P;
     for (int e = threadIdx.x; e < C::HR * C::HR; e += 256) {
@@ -212,6 +217,21 @@ __global__ __launch_bounds__(256) void conv1_kernel(const T* __restrict__ in, T*
     }
   }
 
+  if (ksplit > 1) {  // raw partial sums of this split
+    float* pd = part + copy * part_slice + rn.out_off + plane * out_stride;
+#pragma unroll
+    for (int mt = 0; mt < 3; ++mt)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int i = 8 * (r >> 2) + 4 * half + (r & 3);
+          const int idx = wave * 64 + t * 32 + i;
+          const int oy = oy0 + idx / C::TW, ox = ox0 + idx % C::TW;
+          if (oy < Ho && ox < Wo) pd[((int64_t)oy * Wo + ox) * 96 + mt * 32 + l32] = acc[mt][t][r];
+        }
+    return;
+  }
   T* dst = out + plane * out_stride;
 #pragma unroll
   for (int mt = 0; mt < 3; ++mt) {
@@ -1342,6 +1362,33 @@ __global__ __launch_bounds__(64 * Conv1R<PT>::NWV, 1) void conv1_resident_kernel
   }
 }
 
+// Copies an fp32 launch of `blocks` workgroups splits its input channels over (at most max_copies):
+// the ks minimising rounds(ks) / ks + 0.15 [ks > 1] + 0.02 ks blocks / CUs, rounds(ks) =
+// ceil(ks blocks / CUs) (one fp32 workgroup per CU at a time): the launch's rounds of shorter
+// workgroups, plus the reduction and the partial sums' traffic, which grows with the copies and the
+// launch's output (fitted to timed launches of the 227 x 227 and the 8-scale 480 x 640 pyramids).
+// Launches of at least one workgroup per CU do not split: a lone workgroup's whole K loop sets a
+// small launch's time, not a large one's.
+int split_copies(int64_t blocks, int max_copies) {
+  const int64_t cus = device_cu_count();
+  int ks = 1;
+  if (blocks < cus) {
+    double best = 1.0;
+    for (int k = 2; k <= max_copies; ++k) {
+      const double cost = (double)((k * blocks + cus - 1) / cus) / k + 0.15 + 0.02 * k * (double)blocks / cus;
+      if (cost < best) best = cost, ks = k;
+    }
+  }
+  return ks;
+}
+
+// Elements of one partial copy of a launch over `runs`: its output extent, rounded to 64.
+int64_t split_span(const MapRun* runs, int n_runs) {
+  int64_t span = 0;
+  for (int i = 0; i < n_runs; ++i) span = std::max(span, runs[i].out_off + runs[i].n * runs[i].out_stride);
+  return (span + 63) / 64 * 64;
+}
+
 // part / part_bytes: workspace for the partial sums of a split fp32 launch (may be NULL: no split);
 // part_need non-NULL: only report the bytes this launch would use there (0 without a split).
 template <typename T, int R, int BM, int TM, int OCC, int TS, int BMP = BM, int TN = 4>
@@ -1360,27 +1407,12 @@ int run_conv_s1(const T* in, T* out, const T* wp, const T* wstage, const float* 
   });
   if (blocks <= 0) return (int)hipErrorInvalidValue;
   if constexpr (Cf::F32 || (TM != 2 && TM != 3)) {
-    // fp32 launches of fewer workgroups than CUs may split their input channels over ks <= nchunks
-    // copies: a lone workgroup's whole K loop would otherwise set the launch's time.  ks minimises
-    // rounds(ks) / ks + 0.15 [ks > 1] + 0.02 ks blocks / CUs, rounds(ks) = ceil(ks blocks / CUs) (one
-    // fp32 workgroup per CU at a time): the launch's rounds of shorter workgroups, plus the reduction
-    // and the partial sums' traffic, which grows with the copies and the launch's output (fitted to
-    // timed launches of the 227 x 227 and the 8-scale 480 x 640 pyramids).
+    // fp32 launches too small to fill the chip split their input chunks over ks copies
     int ks = 1;
-    int64_t span = 0;  // elements of one partial copy: the launch's output extent
+    int64_t span = 0;  // elements of one partial copy
     if constexpr (Cf::F32) {
-      const int64_t cus = device_cu_count();
-      if (blocks < cus) {
-        double best = 1.0;
-        for (int k = 2; k <= Cg / Cf::CC; ++k) {
-          const double cost =
-              (double)((k * blocks + cus - 1) / cus) / k + 0.15 + 0.02 * k * (double)blocks / cus;
-          if (cost < best) best = cost, ks = k;
-        }
-      }
-      for (int i = 0; i < n_runs; ++i)
-        span = std::max(span, runs[i].out_off + runs[i].n * runs[i].out_stride);
-      span = (span + 63) / 64 * 64;
+      ks = split_copies(blocks, Cg / Cf::CC);
+      span = split_span(runs, n_runs);
     }
     const size_t need = ks > 1 ? (size_t)ks * (size_t)span * sizeof(float) : 0;
     if (part_need) {
@@ -1482,10 +1514,7 @@ int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, c
   const T* ws = L.s_off[layer - 1] ? (const T*)((const char*)d_packed + L.s_off[layer - 1]) : wp;
   const float* bias = (const float*)((const char*)d_packed + L.b_off[layer - 1]);
   if (layer == 1) {
-    if (part_need) {  // conv1 does not split
-      *part_need = 0;
-      return 0;
-    }
+    if (part_need) *part_need = 0;
     KRuns kr;
     auto tiles16 = [](KRun& k) {  // tiles of 16 x 16 output pixels
       k.Ho = (k.H - 11) / 4 + 1, k.Wo = (k.W - 11) / 4 + 1;
@@ -1495,8 +1524,29 @@ int conv_dispatch(int layer, const void* d_in, const MapRun* runs, int n_runs, c
     if constexpr (std::is_same<T, float>::value) {
       const int64_t blocks = fill_kruns(runs, n_runs, kr, tiles16);
       if (blocks <= 0) return (int)hipErrorInvalidValue;
-      conv1_kernel<T><<<(unsigned)blocks, 256, 0, s>>>(in, out, wp, bias, kr);
+      // launches too small to fill the chip split the three input channels (as conv2-5 do)
+      int ks = split_copies(blocks, 3);
+      const int64_t span = split_span(runs, n_runs);
+      const size_t need = ks > 1 ? (size_t)ks * (size_t)span * sizeof(float) : 0;
+      if (part_need) {
+        *part_need = need;
+        return 0;
+      }
+      if (ks > 1 && (!part || part_bytes < need)) ks = 1;
+      conv1_kernel<T><<<(unsigned)(blocks * ks), 256, 0, s>>>(in, out, wp, bias, kr, ks, (int)blocks, part,
+                                                            span);
+      if (ks > 1) {
+        KRuns rr;
+        const int64_t rb = fill_kruns(runs, n_runs, rr, [](KRun& k) {
+          k.Ho = (k.H - 11) / 4 + 1, k.Wo = (k.W - 11) / 4 + 1;
+          k.tiles_x = (int)(((int64_t)k.Ho * k.Wo * 96 / 4 + 255) / 256), k.tiles_y = 1;
+          return (int64_t)k.tiles_x;
+        });
+        if (rb <= 0) return (int)hipErrorInvalidValue;
+        split_reduce_kernel<<<(unsigned)rb, 256, 0, s>>>(part, span, ks, bias, (float*)out, rr, 96);
+      }
     } else {
+      if (part_need) return 0;
       // Direct loads take 16-byte slots of plane rows at 32-bit byte offsets within one plane.
       bool direct = ((uintptr_t)in & 15) == 0;
       for (int i = 0; i < n_runs; ++i) {
