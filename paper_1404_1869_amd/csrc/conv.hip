@@ -489,8 +489,14 @@ constexpr int conv_threads() {
 // workgroups; copy ks runs the input-channel chunks [ks nchunks / ksplit, (ks + 1) nchunks / ksplit)
 // and writes its raw sums (no bias, no ReLU) to part + ks part_slice at the output's element offsets;
 // split_reduce_kernel then adds the copies in order.
+// (fp32 instances run one wave per SIMD whatever the configuration asks: their registers need it)
+template <typename T, int OCC>
+constexpr int conv_s1_occ() {
+  return std::is_same<T, float>::value ? 1 : OCC;
+}
+
 template <typename T, int R, int BM, int TM, int OCC, int TS>
-__global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), OCC) void conv_s1_kernel(
+__global__ __launch_bounds__((conv_threads<T, BM, TM, TS>()), (conv_s1_occ<T, OCC>())) void conv_s1_kernel(
     const T* __restrict__ in, T* __restrict__ out, const T* __restrict__ wp,
     const float* __restrict__ bias, KRuns runs, int C, int Cg, int M, int Mg, int mblocks, int ksplit,
     int base, float* __restrict__ part, int64_t part_slice) {

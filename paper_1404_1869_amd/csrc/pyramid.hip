@@ -172,10 +172,6 @@ __device__ inline bool valid_item(const dn_scale_geom& g, const BatchGeom& bg) {
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
-// Keeps the compiler from moving this wave's LDS accesses across it (a wave's own LDS operations
-// execute in order).
-__device__ inline void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
-
 // Horizontal taps of one source row, exact in integers: for the 4-byte pixels q0 (left) and q1
 // (right), channel c gives I0 (Dx - rx) + I1 rx = Dx ((1 - lx) I0 + lx I1), with the column fraction
 // lx = rx / Dx, Dx = 2 w (at most 65535) and the weights packed as u16 pairs (Dx - rx) | rx << 16.

@@ -197,7 +197,6 @@ __global__ __launch_bounds__(256) void region_windows_kernel(const T* __restrict
     const int c0 = lt * VT;
     const uint32_t cb = (uint32_t)(c0 * sizeof(T));
     const __amdgpu_buffer_rsrc_t rf = __builtin_amdgcn_make_buffer_rsrc((void*)F, 0, 0x7fffffff, 0x00020000);
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
     vec_t a[MAXIT][4];
 #pragma unroll
     for (int it = 0; it < MAXIT; ++it) {

@@ -17,6 +17,7 @@ namespace {
 struct Rec {
   std::string name;
   hipEvent_t a, b;
+  bool ok;  // both events recorded
 };
 
 std::mutex g_mu;
@@ -49,16 +50,20 @@ TraceScope::TraceScope(const char* name, void* stream) : idx_(-1), stream_(strea
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on || !wanted(name)) return;
   hipEvent_t a = take_event(), b = take_event();
-  if (!a || !b) return;
-  hipEventRecord(a, (hipStream_t)stream);
-  g_recs.push_back(Rec{name, a, b});
+  if (!a || !b || hipEventRecord(a, (hipStream_t)stream) != hipSuccess) {  // not traced
+    if (a) g_pool.push_back(a);
+    if (b) g_pool.push_back(b);
+    return;
+  }
+  g_recs.push_back(Rec{name, a, b, true});
   idx_ = (int)g_recs.size() - 1;
 }
 
 TraceScope::~TraceScope() {
   if (idx_ < 0) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  if (idx_ < (int)g_recs.size()) hipEventRecord(g_recs[idx_].b, (hipStream_t)stream_);
+  if (idx_ < (int)g_recs.size() && hipEventRecord(g_recs[idx_].b, (hipStream_t)stream_) != hipSuccess)
+    g_recs[idx_].ok = false;
 }
 
 }  // namespace dn
@@ -93,7 +98,8 @@ int densenet_profile_stop(dn_profile_entry* out, int32_t max_entries, int32_t* n
   int status = DN_OK;
   for (Rec& r : g_recs) {
     float ms = 0.f;
-    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess)
+    if (!r.ok || hipEventSynchronize(r.b) != hipSuccess ||
+        hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess)
       status = fail(DN_E_HIP, "event timing failed");
     if (!acc.count(r.name)) order.push_back(r.name);
     acc[r.name].first += 1;
