@@ -112,3 +112,35 @@ def test_fp32_split_launches_match_layer_by_layer(D):
             assert got.shape == ref.shape
             assert torch.allclose(got, ref, rtol=1e-5, atol=1e-5 * float(ref.abs().max())), (d.h, what)
             assert float(ref.abs().max()) > 0
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_large_runs_share_batch_kernels(D, dt):
+    """Two runs large enough for the batch configurations (16 planes of 1200 x 1200, 8 of 1000 x 1000,
+    each run at its own pitch): one call launches conv1-5 and the lrn_pool2 strip kernel with a
+    two-entry run table; each run through the stack alone (single-run kernels, and for the smaller run
+    the per-pixel LRN kernel, which computes the same values) must give the same maps bit for bit."""
+    runs = [(16, 1200, 1216), (8, 1000, 1024)]
+    descs, off = [], 0
+    for n, side, pitch in runs:
+        for _ in range(n):
+            q = D.dn_plane_desc()
+            q.h, q.w, q.pitch, q.offset = side, side, pitch, off
+            descs.append(q)
+            off += 3 * side * pitch
+    g = torch.Generator(device="cuda").manual_seed(11)
+    planes = (torch.rand(off, generator=g, device="cuda") * 200 - 100).to(
+        {"bf16": torch.bfloat16, "f16": torch.float16}[dt])
+    net = D.net_params()
+    both = D.ConvFeatures(descs, DTS[dt], net, device="cuda")
+    both(planes, packed(D, dt))
+    first, i0 = [], 0
+    for n, _, _ in runs:
+        one = D.ConvFeatures(descs[i0:i0 + n], DTS[dt], net, device="cuda")
+        one(planes, packed(D, dt))
+        first += [m.clone() for m in one.conv5_maps()]
+        i0 += n
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(both.conv5_maps(), first)):
+        assert torch.equal(a, b), f"plane {i}"
+    assert float(first[0].float().abs().max()) > 0
