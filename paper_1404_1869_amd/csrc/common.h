@@ -173,12 +173,13 @@ __device__ inline int run_of(const KRuns& t, int b) {
   }
 }
 #endif
-// The kernel table of runs [0, n) (n <= MAX_RUNS): geometry(k) sets k's Ho, Wo, tiles_x and tiles_y
-// from its input size and returns the workgroups (or tiles) of one plane.  Returns the launch's
-// total, or -1 when it is empty or passes 2^31 - 1.
+// The kernel table of runs [0, n) (1 <= n <= MAX_RUNS): geometry(k) sets k's Ho, Wo, tiles_x and
+// tiles_y from its input size and returns the workgroups (or tiles) of one plane.  Returns the
+// launch's total, or -1 when n is out of range, a run is empty or the total passes 2^31 - 1.
 template <typename G>
 inline int64_t fill_kruns(const MapRun* runs, int n, KRuns& t, G&& geometry) {
   t = KRuns{};
+  if (n <= 0 || n > MAX_RUNS) return -1;  // callers issue one launch per MAX_RUNS runs
   t.count = n;
   int64_t total = 0;
   for (int i = 0; i < n; ++i) {
