@@ -262,3 +262,59 @@ def test_region_map_size_limit():
     d[0].h = 2047
     assert L.densenet_region_windows(fake, d, 1, D.DN_BF16, geom, 1, 16, 1, fake, None, 0,
                                      ctypes.c_float(227.0), 6, fake, fake, None, None) == D.DN_OK
+
+
+def _conv_query(L, descs, dt, net):
+    n = len(descs)
+    pd = (D.dn_plane_desc * n)(*descs)
+    c5d, p5d = (D.dn_plane_desc * n)(), (D.dn_plane_desc * n)()
+    ws, c5, p5 = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    st = L.densenet_conv_features(None, pd, n, dt, None, ctypes.byref(net), None, 0, ctypes.byref(ws),
+                                  None, 0, ctypes.byref(c5), c5d, None, 0, ctypes.byref(p5), p5d, None)
+    return st, ws.value, c5.value, list(c5d)
+
+
+def test_conv_features_workspace_for_mixed_plane_sizes():
+    """Planes of several sizes (the 480 x 640 image's 8 per-scale planes, twice: 16 runs of one plane)
+    share one launch per layer: the workspace holds two buffers, each one layer's maps of all planes
+    back to back (plus partial sums where fp32 launches too small for the GPU split), and the conv5
+    maps lie back to back in plane order.  Size queries only: no device (the CU count defaults to
+    256)."""
+    L = D.lib()
+    net = D.net_params()
+    p = D.pyramid_params(8, 4, base_longest_side=1024, pad=16, pad_mode=D.DN_PAD_ZERO)
+    one = list(D.densenet_plan_pyramid(480, 640, p).planes)
+    descs = []
+    for b in range(2):
+        for d in one:
+            q = D.dn_plane_desc()
+            q.h, q.w, q.pitch = d.h, d.w, d.pitch
+            q.offset = b * 10 ** 8 + d.offset
+            descs.append(q)
+    hw = [D.layer_sizes(d.h, d.w) for d in descs]
+    a = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 0), (256, 2), (384, 4)))
+    b = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 1), (256, 3), (384, 5)))
+    for dt, es in ((D.DN_F16, 2), (D.DN_BF16, 2), (D.DN_F32, 4)):
+        st, ws, c5, c5d = _conv_query(L, descs, dt, net)
+        assert st == 0
+        ab = (a * es + 255) // 256 * 256 + (b * es + 255) // 256 * 256
+        assert ws == ab  # 16 planes fill the GPU: no launch splits
+        off = 0
+        for d, h in zip(c5d, hw):
+            assert (d.h, d.w, d.offset) == (h[6][0], h[6][1], off)
+            off += 256 * d.h * d.w
+        assert c5 == off * es
+    # one image's 8 planes in fp32: conv4/conv5 launches too small to fill the GPU split their sums
+    st, ws, _, _ = _conv_query(L, descs[:8], D.DN_F32, net)
+    hw = hw[:8]
+    a = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 0), (256, 2), (384, 4))) * 4
+    b = max(sum(c * h[i][0] * h[i][1] for h in hw) for c, i in ((96, 1), (256, 3), (384, 5))) * 4
+    assert st == 0 and ws > (a + 255) // 256 * 256 + (b + 255) // 256 * 256
+    # one large plane in fp32 fills the GPU: no partial sums
+    q = D.dn_plane_desc()
+    q.h, q.w, q.pitch, q.offset = 1200, 1200, 1216, 0
+    hw = D.layer_sizes(1200, 1200)
+    st, ws, _, _ = _conv_query(L, [q] * 4, D.DN_F32, net)
+    a = max(c * hw[i][0] * hw[i][1] for c, i in ((96, 0), (256, 2), (384, 4))) * 4
+    b = max(c * hw[i][0] * hw[i][1] for c, i in ((96, 1), (256, 3), (384, 5))) * 4
+    assert st == 0 and ws == (4 * a + 255) // 256 * 256 + (4 * b + 255) // 256 * 256
