@@ -144,3 +144,47 @@ def test_large_runs_share_batch_kernels(D, dt):
     for i, (a, b) in enumerate(zip(both.conv5_maps(), first)):
         assert torch.equal(a, b), f"plane {i}"
     assert float(first[0].float().abs().max()) > 0
+
+
+@pytest.mark.parametrize("wname,dt", [("ALEXNET_227", "f32"), ("VGA_8SCALE", "f16")])
+def test_graph_replay_per_scale_planes(D, wname, dt):
+    """Per-scale planes (Sec. 3.1 without stitching) captured once into a graph and replayed several
+    times with eager work in between: the multi-run launches, and for the 227 x 227 fp32 pyramid the
+    split launches with their partial sums and reductions, reproduce the eager conv5 (and pool5) maps
+    bit for bit on every replay (the workspace's partial sums are rewritten in full each time)."""
+    w = getattr(C, wname)
+    img = torch.from_numpy(synth.images(w.seeds, w.H, w.W)).cuda()
+    params = D.params_for(w)
+    planes, plan = D.densenet_build_pyramid(img, params, DTS[dt])
+    cf = D.ConvFeatures(list(plan.planes), DTS[dt], D.net_params(pool5=w.pool5), device="cuda")
+
+    def pyramid():
+        D.densenet_build_pyramid(img, params, DTS[dt], out=planes)
+        cf(planes, packed(D, dt))
+
+    pyramid()
+    torch.cuda.synchronize()
+    ref_c5 = cf.conv5.clone()
+    ref_p5 = cf.pool5.clone() if cf.pool5 is not None else None
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pyramid()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pyramid()
+    other = torch.zeros(1 << 20, device="cuda")
+    for rep in range(3):
+        cf.conv5.zero_()
+        cf.workspace.fill_(0xFF)           # stale partial sums and maps would show
+        if ref_p5 is not None:
+            cf.pool5.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(cf.conv5, ref_c5), f"replay {rep}: conv5"
+        if ref_p5 is not None:
+            assert torch.equal(cf.pool5, ref_p5), f"replay {rep}: pool5"
+        other.add_(1)                       # eager work between replays
+        torch.cuda.synchronize()
