@@ -10,7 +10,9 @@ the same batch with cross-image packing (the scales of all 16 images stitched to
 instead of 96), reported beside the headline, which keeps each image's own planes, and the latency of
 one 25-scale pyramid of one image (fp16), launched eagerly and replayed from a captured graph, and
 the workloads that give each scale its own plane (480 x 640 at 8 scales in fp16 and fp32, 227 x 227
-at 2 scales in fp32), whose planes of different sizes share one launch per layer.
+at 2 scales in fp32), whose planes of different sizes share one launch per layer.  With --ceilings
+it also measures what bounds the kernels on the device: a vendor bf16 GEMM and this library's conv2
+and conv3 on random and on zero operands, and device copy/fill bandwidth.
 The default workload is a batch of 16 images of 768 x 1024, each a 25-scale 2^-0.1 pyramid on
 1200 x 1200 planes (96 planes), bf16 storage with fp32 accumulation.
 
@@ -58,6 +60,10 @@ def parse():
                     help="skip the single-image latency figures (one 25-scale pyramid, fp16)")
     ap.add_argument("--no-per-scale", action="store_true",
                     help="skip the per-scale-plane workloads (480x640 at 8 scales, 227x227 at 2)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="also measure what bounds the kernels on this device: a bf16 GEMM (torch.mm, "
+                         "vendor library) and conv2/conv3 of this library on random and on zero "
+                         "operands, and device copy/fill bandwidth")
     return ap.parse_args()
 
 
@@ -229,6 +235,8 @@ def main():
         result["single_image"] = single_image(D, weights, args.steps, args.warmup)
     if not args.no_per_scale and n_img > 1:
         result["per_scale_planes"] = per_scale_planes(D, weights, args.steps, args.warmup)
+    if args.ceilings:
+        result["ceilings"] = ceilings(D, weights, PH)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_planes)
     print(json.dumps(result), flush=True)
@@ -439,6 +447,78 @@ def per_scale_planes(D, weights, steps, warmup):
                                                            / steps, 2),
                         "conv_mfma_util": round(flops / (conv_ms / 1e3) / 1e12 / PEAK_TFLOPS[dtn], 4)}
         out[w.name] = res
+    return out
+
+
+def ceilings(D, weights, plane_side):
+    """Device ceilings under the same conditions as the kernels (context for the roofline figures).
+
+    * gemm_bf16_tflops: torch.mm of two 8192 x 8192 bf16 matrices (the vendor GEMM library), on
+      N(0, 1) operands and on zeros.  The matrix cores' sustained rate depends on the operand values
+      (the clock falls under the power drawn by toggling data), so the zero-operand figure is the
+      nearest to the 2.5 PF datasheet peak and the random one to what real data allows.
+    * conv_us: this library's conv2 and conv3 over 96 planes of the default workload's map sizes,
+      on N(0, 10)-magnitude inputs with the N(0, 0.01) weights, and on zero inputs and weights.
+    * hbm_tbs: a 1 GiB device-to-device copy (read + write) and a 1 GiB fill.
+    """
+    import numpy as np
+    import torch
+
+    from paper_1404_1869_amd import workmodel
+
+    def timed(fn, reps, warm):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps / 1e3  # seconds
+
+    out = {}
+    g = torch.Generator(device="cuda").manual_seed(11)
+    n = 8192
+    gemm = {}
+    for name, make in (("random", lambda: torch.randn((n, n), device="cuda", generator=g)),
+                       ("zero", lambda: torch.zeros((n, n), device="cuda"))):
+        a = make().to(torch.bfloat16).contiguous()
+        b = make().to(torch.bfloat16).contiguous()
+        c = torch.empty((n, n), device="cuda", dtype=torch.bfloat16)
+        s = timed(lambda: torch.mm(a, b, out=c), 30, 10)
+        gemm[name] = round(2.0 * n ** 3 / s / 1e12, 1)
+        del a, b, c
+    out["gemm_bf16_tflops"] = gemm
+
+    bf = D.DTYPES["bf16"]
+    zero_w = [(torch.zeros_like(wt), bs) for wt, bs in weights]
+    packs = {"real": D.densenet_pack_weights(weights, bf), "zero": D.densenet_pack_weights(zero_w, bf)}
+    sd = workmodel.sides(plane_side)
+    fl = workmodel.conv_flops(plane_side, plane_side)
+    conv = {}
+    for layer, C, H in ((2, 96, sd[1]), (3, 256, sd[3])):
+        shp = (96, H, H, C)
+        xs = {"random": (torch.randn(shp, device="cuda", generator=g) * 10).abs().to(torch.bfloat16),
+              "zero": torch.zeros(shp, device="cuda", dtype=torch.bfloat16)}
+        for name in ("random", "zero"):
+            x, p = xs[name], packs["real" if name == "random" else "zero"]
+            s = timed(lambda: D.densenet_conv_layer(layer, x, 96, H, H, bf, p), 10, 3)
+            conv[f"conv{layer}_{name}_us"] = round(s * 1e6, 1)
+            conv[f"conv{layer}_{name}_tflops"] = round(fl[layer - 1] * 96 / s / 1e12, 1)
+        del xs
+    out["conv_96_planes"] = conv
+    torch.cuda.empty_cache()
+
+    nb = 1 << 30
+    src = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    out["hbm_tbs"] = {"copy": round(2.0 * nb / timed(lambda: dst.copy_(src), 10, 3) / 1e12, 2),
+                      "fill": round(nb / timed(lambda: dst.fill_(2), 10, 3) / 1e12, 2)}
+    del src, dst
+    torch.cuda.empty_cache()
     return out
 
 
