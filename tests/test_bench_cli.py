@@ -1,0 +1,62 @@
+"""Host-side pieces of bench.py: the one-GPU guard, the counter summary it reads for
+`roofline.traffic`, and the source digest that ties that summary to the library it was taken on."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr or "single MI355X" in r.stderr
+    assert r.stdout == ""
+
+
+def test_source_digest_is_stable_and_short():
+    a, b = bench.source_digest(), bench.source_digest()
+    assert a == b and len(a) == 16
+    int(a, 16)
+
+
+def _summary(tmp_path, kernel, workload, digest, value):
+    d = tmp_path / "profiles"
+    d.mkdir(exist_ok=True)
+    (d / f"{kernel}_{workload}_hbm_traffic.txt").write_text(
+        "# test summary\n"
+        f"kernel: {kernel}\n"
+        f"hbm_bytes_per_launch: {value}\n"
+        f"source_digest: {digest}\n")
+
+
+def test_traffic_read_only_for_matching_digest(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    _summary(tmp_path, "conv2", "w", "0123456789abcdef", 1507518290)
+    assert bench.load_traffic("conv2", "w", "0123456789abcdef") == 1507518290.0
+    assert bench.load_traffic("conv2", "w", "fedcba9876543210") is None   # other source
+    assert bench.load_traffic("conv3", "w", "0123456789abcdef") is None   # no summary
+
+
+def test_committed_traffic_summary_parses():
+    """The committed summary of the dominant kernel names a digest and a byte count that the bench
+    can read (it reports them only when the digest matches the library's sources)."""
+    path = os.path.join(ROOT, "profiles",
+                        "conv2_xga768x1024_25scale_1200plane_batch16_hbm_traffic.txt")
+    if not os.path.exists(path):
+        pytest.skip("no committed traffic summary")
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    assert len(vals["source_digest"]) == 16
+    assert float(vals["hbm_bytes_per_launch"]) > 0
+    got = bench.load_traffic("conv2", "xga768x1024_25scale_1200plane_batch16", vals["source_digest"])
+    assert got == float(vals["hbm_bytes_per_launch"])
