@@ -450,9 +450,44 @@ def per_scale_planes(D, weights, steps, warmup):
     return out
 
 
+def mfma_chain(timed):
+    """Sustained rate of independent v_mfma_f32_32x32x16_bf16 chains with no memory traffic
+    (libprobe.so), two waves per SIMD on every SIMD: every MFMA reading the same registers of smooth
+    values (the most favourable case), and random bit patterns.  The matrix cores' ceiling on this
+    device and how far it moves with the operand values."""
+    import ctypes
+
+    import torch
+
+    path = os.path.join(ROOT, "paper_1404_1869_amd", "libprobe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    fn = lib.densenet_probe_mfma_bf16
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    n_out = 2 * torch.cuda.get_device_properties(0).multi_processor_count * 256
+    buf = torch.empty(n_out, dtype=torch.float32, device="cuda")
+    flop = ctypes.c_double()
+    res = {}
+    for mode, name in ((0, "repeated_registers_smooth_values"), (1, "random")):
+        def launch(k):
+            st = fn(mode, k, buf.data_ptr(), n_out, ctypes.byref(flop),
+                    ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            if st != 0:
+                raise RuntimeError("MFMA probe launch failed")
+        launches = 100
+        s = timed(lambda: launch(launches), 1, 1)
+        res[name] = round(flop.value * launches / s / 1e12, 1)
+    del buf
+    return res
+
+
 def ceilings(D, weights, plane_side):
     """Device ceilings under the same conditions as the kernels (context for the roofline figures).
 
+    * mfma_chain_bf16_tflops: chains of dense bf16 MFMAs with no memory traffic (see mfma_chain).
     * gemm_bf16_tflops: torch.mm of two 8192 x 8192 bf16 matrices (the vendor GEMM library), on
       N(0, 1) operands and on zeros.  The matrix cores' sustained rate depends on the operand values
       (the clock falls under the power drawn by toggling data), so the zero-operand figure is the
@@ -491,6 +526,7 @@ def ceilings(D, weights, plane_side):
         gemm[name] = round(2.0 * n ** 3 / s / 1e12, 1)
         del a, b, c
     out["gemm_bf16_tflops"] = gemm
+    out["mfma_chain_bf16_tflops"] = mfma_chain(timed)
 
     bf = D.DTYPES["bf16"]
     zero_w = [(torch.zeros_like(wt), bs) for wt, bs in weights]

@@ -60,3 +60,21 @@ def test_committed_traffic_summary_parses():
     assert float(vals["hbm_bytes_per_launch"]) > 0
     got = bench.load_traffic("conv2", "xga768x1024_25scale_1200plane_batch16", vals["source_digest"])
     assert got == float(vals["hbm_bytes_per_launch"])
+
+
+def test_probe_library_exports_its_entry_point():
+    """libprobe.so (the matrix-core rate probe behind `bench.py --ceilings`) loads without a GPU and
+    exports its one entry point; argument checks run before any device call."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_1404_1869_amd", "libprobe.so")
+    if not os.path.exists(path):
+        pytest.skip("libprobe.so not built")
+    lib = ctypes.CDLL(path)
+    fn = lib.densenet_probe_mfma_bf16
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    flop = ctypes.c_double()
+    assert fn(2, 1, 1, 1 << 20, ctypes.byref(flop), None) == -1      # unknown mode
+    assert fn(0, 0, 1, 1 << 20, ctypes.byref(flop), None) == -1      # no launches
+    assert fn(0, 1, None, 1 << 20, ctypes.byref(flop), None) == -1   # no buffer
