@@ -559,14 +559,26 @@ def ceilings(D, weights, plane_side):
 
 
 def cpu_model() -> str:
+    """The host CPU as /proc/cpuinfo names it (model name, family / model / stepping of the first
+    processor entry) and the logical CPUs this process may run on."""
+    fields = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if not line.strip():
+                    break  # first processor entry only
+                if ":" in line:
+                    k, v = line.split(":", 1)
+                    fields.setdefault(k.strip(), v.strip())
     except OSError:
         pass
-    return "unknown"
+    name = fields.get("model name", "unknown")
+    fam = [f"{k} {fields[k]}" for k in ("cpu family", "model", "stepping") if k in fields]
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 0
+    return f"{name} ({', '.join(fam)}; {usable} logical CPUs usable)" if fam else f"{name} ({usable} logical CPUs usable)"
 
 
 def cpu_baseline(w, n_planes_sample):

@@ -78,3 +78,8 @@ def test_probe_library_exports_its_entry_point():
     assert fn(2, 1, 1, 1 << 20, ctypes.byref(flop), None) == -1      # unknown mode
     assert fn(0, 0, 1, 1 << 20, ctypes.byref(flop), None) == -1      # no launches
     assert fn(0, 1, None, 1 << 20, ctypes.byref(flop), None) == -1   # no buffer
+
+
+def test_cpu_model_names_the_host():
+    s = bench.cpu_model()
+    assert "logical CPUs usable" in s and s[0] != "("
