@@ -492,8 +492,9 @@ def ceilings(D, weights, plane_side):
       N(0, 1) operands and on zeros.  The matrix cores' sustained rate depends on the operand values
       (the clock falls under the power drawn by toggling data), so the zero-operand figure is the
       nearest to the 2.5 PF datasheet peak and the random one to what real data allows.
-    * conv_us: this library's conv2 and conv3 over 96 planes of the default workload's map sizes,
-      on N(0, 10)-magnitude inputs with the N(0, 0.01) weights, and on zero inputs and weights.
+    * conv_96_planes: this library's conv2 and conv3 over 96 planes of the default workload's map
+      sizes, on N(0, 10)-magnitude inputs with the N(0, 0.01) weights and on zero inputs and weights;
+      conv1 over 96 planes of uniform +-128 values with those weights and with zero weights.
     * hbm_tbs: a 1 GiB device-to-device copy (read + write) and a 1 GiB fill.
     """
     import numpy as np
@@ -544,6 +545,15 @@ def ceilings(D, weights, plane_side):
             conv[f"conv{layer}_{name}_us"] = round(s * 1e6, 1)
             conv[f"conv{layer}_{name}_tflops"] = round(fl[layer - 1] * 96 / s / 1e12, 1)
         del xs
+    # conv1 over 96 planes of 1200 x 1200 (channel-major, rows a multiple of 8: the direct-load
+    # kernel): uniform +-128 planes with the N(0, 0.01) weights, and the same planes with zero weights
+    xp = ((torch.rand((96, 3, plane_side, plane_side), device="cuda", generator=g) - 0.5) * 256).to(torch.bfloat16)
+    for name in ("random", "zero_weights"):
+        p = packs["real" if name == "random" else "zero"]
+        s = timed(lambda: D.densenet_conv_layer(1, xp, 96, plane_side, plane_side, bf, p), 10, 3)
+        conv[f"conv1_{name}_us"] = round(s * 1e6, 1)
+        conv[f"conv1_{name}_tflops"] = round(fl[0] * 96 / s / 1e12, 1)
+    del xp
     out["conv_96_planes"] = conv
     torch.cuda.empty_cache()
 
