@@ -453,8 +453,9 @@ def per_scale_planes(D, weights, steps, warmup):
 def mfma_chain(timed):
     """Sustained rate of independent v_mfma_f32_32x32x16_bf16 chains with no memory traffic
     (libprobe.so), two waves per SIMD on every SIMD: every MFMA reading the same registers of smooth
-    values (the most favourable case), and random bit patterns.  The matrix cores' ceiling on this
-    device and how far it moves with the operand values."""
+    values (the most favourable case), random bit patterns in four register sets read in turn, and
+    the smooth values copied into four register sets read in turn.  The matrix cores' ceiling on
+    this device and how far it moves with the operands."""
     import ctypes
 
     import torch
@@ -471,7 +472,8 @@ def mfma_chain(timed):
     buf = torch.empty(n_out, dtype=torch.float32, device="cuda")
     flop = ctypes.c_double()
     res = {}
-    for mode, name in ((0, "repeated_registers_smooth_values"), (1, "random")):
+    for mode, name in ((0, "repeated_registers_smooth_values"), (1, "random"),
+                       (2, "rotated_registers_smooth_values")):
         def launch(k):
             st = fn(mode, k, buf.data_ptr(), n_out, ctypes.byref(flop),
                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))

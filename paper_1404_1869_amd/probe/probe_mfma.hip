@@ -8,9 +8,10 @@
 //   mode 0: every MFMA reads the same A and B registers, A varying smoothly across lanes and B the
 //           same on every lane (the most favourable case: near the datasheet peak);
 //   mode 1: A and B are hashed bit patterns (random sign, exponent 2^-8..2^7 and mantissa), four
-//           register sets used in turn.
-// With random operands the rate is the same whether consecutive MFMAs reuse their registers or
-// not; it is the operand values that lower it.
+//           register sets used in turn;
+//   mode 2: the values of mode 0, copied into four register sets used in turn as in mode 1.
+// Modes 0 and 2 run at the same rate and mode 1 at well under half of it: the operand values, not
+// the registers read, set the clock.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -57,9 +58,15 @@ __global__ __launch_bounds__(THREADS, 2) void mfma_chain_kernel(float* out, uint
     bf16x8 a[4], b[4];
     for (int v = 0; v < 4; ++v)
       for (int i = 0; i < 8; ++i) {
-        const uint32_t key = t * 64u + (uint32_t)(v * 8 + i);
-        a[v][i] = hashed_bf16(mix32(seed ^ key));
-        b[v][i] = hashed_bf16(mix32(~seed ^ key));
+        if constexpr (MODE == 1) {
+          const uint32_t key = t * 64u + (uint32_t)(v * 8 + i);
+          a[v][i] = hashed_bf16(mix32(seed ^ key));
+          b[v][i] = hashed_bf16(mix32(~seed ^ key));
+        } else {
+          // the same values in every set; seed (never 0 here) keeps the compiler from merging the sets
+          a[v][i] = (__bf16)(1e-3f * (float)(threadIdx.x + i) + (seed == 0u ? (float)v : 0.f));
+          b[v][i] = (__bf16)(1e-3f * (float)(i + 1) + (seed == 0u ? (float)v : 0.f));
+        }
       }
     for (int it = 0; it < ITERS; it += 4) {
 #pragma unroll
@@ -86,7 +93,7 @@ extern "C" {
 int densenet_probe_mfma_bf16(int mode, int launches, float* d_out, int64_t out_floats,
                              double* flop_per_launch, void* stream) {
   int dev = 0, cus = 0;
-  if (mode < 0 || mode > 1 || launches < 1 || !d_out || !flop_per_launch) return -1;
+  if (mode < 0 || mode > 2 || launches < 1 || !d_out || !flop_per_launch) return -1;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     return -1;
@@ -98,8 +105,10 @@ int densenet_probe_mfma_bf16(int mode, int launches, float* d_out, int64_t out_f
     const uint32_t seed = 12345u + (uint32_t)l;
     if (mode == 0)
       mfma_chain_kernel<0><<<grid, THREADS, 0, s>>>(d_out, seed);
-    else
+    else if (mode == 1)
       mfma_chain_kernel<1><<<grid, THREADS, 0, s>>>(d_out, seed);
+    else
+      mfma_chain_kernel<2><<<grid, THREADS, 0, s>>>(d_out, seed);
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -75,7 +75,7 @@ def test_probe_library_exports_its_entry_point():
     fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
                    ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
     flop = ctypes.c_double()
-    assert fn(2, 1, 1, 1 << 20, ctypes.byref(flop), None) == -1      # unknown mode
+    assert fn(3, 1, 1, 1 << 20, ctypes.byref(flop), None) == -1      # unknown mode
     assert fn(0, 0, 1, 1 << 20, ctypes.byref(flop), None) == -1      # no launches
     assert fn(0, 1, None, 1 << 20, ctypes.byref(flop), None) == -1   # no buffer
 
