@@ -397,16 +397,15 @@ __global__ __launch_bounds__(256) void conv1_persistent_kernel(
   }
 }
 
+// Compute units of the device current at the first call (256 if the query fails), queried once;
+// the initialisation is thread-safe.
 int device_cu_count() {
-  static int n = 0;
-  if (!n) {
+  static const int n = [] {
     int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-      n = v;
-    else
-      n = 256;
-  }
+    const bool ok = hipGetDevice(&dev) == hipSuccess &&
+                    hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess;
+    return ok && v > 0 ? v : 256;
+  }();
   return n;
 }
 

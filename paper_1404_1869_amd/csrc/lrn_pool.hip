@@ -55,16 +55,15 @@ constexpr int VECB = 16;  // bytes per channel vector
 #ifndef DN_STRIP256
 #define DN_STRIP256 32, 7, 8, 4
 #endif
+// Compute units of the device current at the first call (256 if the query fails), queried once;
+// the initialisation is thread-safe.
 int device_cus() {
-  static int n = 0;
-  if (!n) {
+  static const int n = [] {
     int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-      n = v;
-    else
-      n = 256;
-  }
+    const bool ok = hipGetDevice(&dev) == hipSuccess &&
+                    hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess;
+    return ok && v > 0 ? v : 256;
+  }();
   return n;
 }
 constexpr int MAX_HALF = 8;

@@ -318,3 +318,48 @@ def test_conv_features_workspace_for_mixed_plane_sizes():
     a = max(c * hw[i][0] * hw[i][1] for c, i in ((96, 0), (256, 2), (384, 4))) * 4
     b = max(c * hw[i][0] * hw[i][1] for c, i in ((96, 1), (256, 3), (384, 5))) * 4
     assert st == 0 and ws == (4 * a + 255) // 256 * 256 + (4 * b + 255) // 256 * 256
+
+
+def test_host_threads_call_concurrently():
+    """Eight host threads plan pyramids at once (valid and invalid parameters in turn): every plan
+    equals the one made alone, and each thread's error message is the one its own call left
+    (densenet_last_error is per thread)."""
+    import threading
+
+    good = D.pyramid_params(25, 10, pad=16, plane_h=1200, plane_w=1200)
+    ref = [(g.plane, g.y, g.x, g.rh, g.rw) for g in D.densenet_plan_pyramid(768, 1024, good).geom]
+    failures = []
+    own_msg = {}
+    for t in range(8):  # each thread's invalid call, made alone first
+        with pytest.raises(D.DenseNetError):
+            D.densenet_plan_pyramid(100 * (1 + t), 100, D.pyramid_params(2, 2, plane_h=8 + t, plane_w=8 + t))
+        own_msg[t] = D.last_error()
+    assert len(set(own_msg.values())) == 8
+
+    def worker(t):
+        try:
+            for i in range(40):
+                if (i + t) % 2:
+                    got = [(g.plane, g.y, g.x, g.rh, g.rw)
+                           for g in D.densenet_plan_pyramid(768, 1024, good).geom]
+                    if got != ref:
+                        failures.append(f"thread {t}: plan differs")
+                else:
+                    H = 1 + t  # a different invalid call per thread: the plane is too small
+                    bad = D.pyramid_params(2, 2, plane_h=8 + t, plane_w=8 + t)
+                    try:
+                        D.densenet_plan_pyramid(100 * H, 100, bad)
+                        failures.append(f"thread {t}: invalid plan accepted")
+                    except D.DenseNetError:
+                        msg = D.last_error()
+                        if msg != own_msg[t]:
+                            failures.append(f"thread {t}: error message {msg!r} is not its own")
+        except Exception as e:  # noqa: BLE001
+            failures.append(f"thread {t}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(8)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not failures, failures[:5]
